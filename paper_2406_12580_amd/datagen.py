@@ -1,0 +1,192 @@
+"""Seeded synthetic inputs for the BD-LRU scan.
+
+This module is shared by the parity tests, the benchmark and the smoke check:
+it feeds the same numbers to the HIP library and to the fp64 oracle.  It holds
+none of the method's arithmetic, only the input recipe:
+
+* x, the gate pre-activations z_r, z_i and the upstream gradient dL/dh are
+  standard normal draws.  Drawing z directly stands in for W x with
+  W ~ N(0, 1/D) and x ~ N(0, 1), whose entries have unit variance.
+* The decay parameter follows the paper's initialisation (section 3.2): a
+  per-channel base a_d ~ U[lo, hi] and Lambda_d = ln(1/a_d - 1), so that
+  exp(-softplus(Lambda_d)) = a_d.
+* For bf16 I/O every tensor the kernel reads in bf16 is rounded to nearest
+  even from its fp32 draw; the arrays stay float32 but hold bf16 values.
+
+Every generator draws from numpy's PCG64 with an explicit seed.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+def round_bf16(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    bits = a.view(np.uint32).astype(np.uint64)
+    rounded = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
+    nan = np.isnan(a)
+    out = rounded.astype(np.uint32).view(np.float32).copy()
+    out[nan] = np.float32("nan")
+    return out
+
+
+def bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Upper 16 bits of float32 values that are already bf16-representable."""
+    return (np.ascontiguousarray(a, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def bf16_from_bits(bits: np.ndarray) -> np.ndarray:
+    """Widen raw bfloat16 bit patterns to float32 (exact)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def lambda_from_base(a: np.ndarray) -> np.ndarray:
+    """Lambda such that exp(-softplus(Lambda)) equals the decay base a (0 < a < 1)."""
+    a = np.asarray(a, dtype=np.float64)
+    return np.log(1.0 / a - 1.0).astype(np.float32)
+
+
+@dataclass
+class Config:
+    name: str
+    B: int
+    L: int
+    D: int
+    io: str            # "f32" or "bf16": the dtype of x, z and h in HBM
+    a_range: tuple     # per-channel decay base range
+    seed: int
+    ops: tuple         # "fwd", "bwd", "step"
+    note: str = ""
+
+
+# The synthetic workloads: typical next-item training batches (D = 64, L = 200,
+# batch 2048), long user histories (L = 2048, D = 128) and very long histories
+# in bf16 (L = 16384, D = 256) plus a one-step decode over 65536 users.
+CONFIGS = {
+    "c1": Config("c1", 4, 50, 64, "f32", (0.9, 0.999), 1, ("fwd",), "small case"),
+    "c2": Config("c2", 256, 200, 64, "f32", (0.9, 0.999), 2, ("fwd",), "training batch"),
+    "c3": Config("c3", 2048, 200, 64, "f32", (0.9, 0.999), 3, ("fwd", "bwd"), "batch 2048"),
+    "c4": Config("c4", 256, 2048, 128, "f32", (0.99, 0.9999), 4, ("fwd", "bwd"),
+                 "long histories"),
+    "c5": Config("c5", 16, 16384, 256, "bf16", (0.99, 0.9999), 5, ("fwd", "bwd"),
+                 "very long histories, bf16 I/O"),
+    "c5dec": Config("c5dec", 65536, 1, 256, "bf16", (0.99, 0.9999), 6, ("step",),
+                    "single-step decode"),
+}
+
+
+@dataclass
+class ScanInputs:
+    x: np.ndarray
+    zr: np.ndarray
+    zi: np.ndarray
+    lam: np.ndarray
+    h0: np.ndarray | None = None
+    dh: np.ndarray | None = None
+    dhT: np.ndarray | None = None
+    io: str = "f32"
+    extra: dict = field(default_factory=dict)
+
+
+def _normal(rng, shape, io):
+    a = rng.standard_normal(shape, dtype=np.float32)
+    return round_bf16(a) if io == "bf16" else a
+
+
+def scan_inputs(B, L, D, seed, io="f32", a_range=(0.9, 0.999), h0=False, grad=False,
+                dhT=False, silu_x=False, pad_rows=False) -> ScanInputs:
+    """Inputs of the scan-level entry points (pre-activations given).
+
+    h0: draw the initial state from N(0, 1) (fp32), else None (zero state).
+    grad: also draw dL/dh ~ N(0, 1) in the I/O dtype.
+    dhT: also draw dL/dh_T ~ N(0, 1) (fp32).
+    silu_x: pass x through SiLU, as the BD-LRU input comes out of a SiLU.
+    pad_rows: left-pad every row with zeros to a random valid length in [1, L].
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = rng.standard_normal((B, L, D), dtype=np.float32)
+    if silu_x:
+        x = (x / (1.0 + np.exp(-x.astype(np.float64)))).astype(np.float32)
+    lengths = None
+    if pad_rows:
+        lengths = rng.integers(1, L + 1, size=B) if L > 0 else np.zeros(B, dtype=np.int64)
+        for b in range(B):
+            x[b, : L - lengths[b]] = 0.0
+    if io == "bf16":
+        x = round_bf16(x)
+    zr = _normal(rng, (B, L, D), io)
+    zi = _normal(rng, (B, L, D), io)
+    lam = lambda_from_base(rng.uniform(a_range[0], a_range[1], size=D))
+    out = ScanInputs(x, zr, zi, lam, io=io)
+    if h0:
+        out.h0 = rng.standard_normal((B, D), dtype=np.float32)
+    if grad:
+        out.dh = _normal(rng, (B, L, D), io)
+    if dhT:
+        out.dhT = rng.standard_normal((B, D), dtype=np.float32)
+    if lengths is not None:
+        out.extra["lengths"] = lengths
+    return out
+
+
+def config_inputs(cfg: Config, grad=None) -> ScanInputs:
+    """Inputs of a named workload at its full size (h0 = 0, as the workload states)."""
+    want_grad = ("bwd" in cfg.ops) if grad is None else grad
+    return scan_inputs(cfg.B, cfg.L, cfg.D, cfg.seed, cfg.io, cfg.a_range, grad=want_grad)
+
+
+@dataclass
+class FullInputs:
+    x: np.ndarray
+    Wr: np.ndarray
+    br: np.ndarray
+    Wi: np.ndarray
+    bi: np.ndarray
+    lam: np.ndarray
+    h0: np.ndarray | None = None
+    dh: np.ndarray | None = None
+    dhT: np.ndarray | None = None
+    io: str = "f32"
+
+
+def full_inputs(B, L, D, seed, io="f32", a_range=(0.9, 0.999), bias=False, h0=False,
+                grad=False, dhT=False) -> FullInputs:
+    """Inputs of the entry points that take gate parameters: W ~ N(0, 1/D), b = 0 or U[-1, 1]."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = _normal(rng, (B, L, D), io)
+    scale = np.float32(1.0 / np.sqrt(D)) if D > 0 else np.float32(1.0)
+    Wr = rng.standard_normal((D, D), dtype=np.float32) * scale
+    Wi = rng.standard_normal((D, D), dtype=np.float32) * scale
+    if io == "bf16":
+        Wr, Wi = round_bf16(Wr), round_bf16(Wi)
+    if bias:
+        br = rng.uniform(-1.0, 1.0, size=D).astype(np.float32)
+        bi = rng.uniform(-1.0, 1.0, size=D).astype(np.float32)
+    else:
+        br = np.zeros(D, np.float32)
+        bi = np.zeros(D, np.float32)
+    if io == "bf16":
+        br, bi = round_bf16(br), round_bf16(bi)
+    lam = lambda_from_base(rng.uniform(a_range[0], a_range[1], size=D))
+    out = FullInputs(x, Wr, br, Wi, bi, lam, io=io)
+    if h0:
+        out.h0 = rng.standard_normal((B, D), dtype=np.float32)
+    if grad:
+        out.dh = _normal(rng, (B, L, D), io)
+    if dhT:
+        out.dhT = rng.standard_normal((B, D), dtype=np.float32)
+    return out
+
+
+def step_inputs(B, D, seed, io="bf16", a_range=(0.99, 0.9999)):
+    """Inputs of one recurrent step: x_t, z_r, z_i in the I/O dtype, h_prev ~ N(0, 1) fp32."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = _normal(rng, (B, D), io)
+    zr = _normal(rng, (B, D), io)
+    zi = _normal(rng, (B, D), io)
+    lam = lambda_from_base(rng.uniform(a_range[0], a_range[1], size=D))
+    h_prev = rng.standard_normal((B, D), dtype=np.float32)
+    return ScanInputs(x, zr, zi, lam, h0=h_prev, io=io)
