@@ -1,0 +1,177 @@
+"""Benchmark of the BD-LRU scan on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+
+A step is one pass of the hot path over one batch: the gated scan forward
+(recblr_bdlru_scan_forward) followed by its backward
+(recblr_bdlru_scan_backward), on synthetic inputs already resident in HBM.
+The default workload is the long-history batch B=256, L=2048, D=128 in fp32.
+Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
+fp64 CPU oracle timed on a bounded sample of the same workload).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+# Algorithmic HBM bytes per element (B*L*D) of each call, by I/O element size.
+# forward: read x, z_r, z_i; write h.  backward: read dh, x, z_r, z_i, h; write dx, dz_r, dz_i.
+FWD_ARRAYS, BWD_ARRAYS = 4, 8
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(cfg, target_s=12.0):
+    """fp64 oracle (forward + backward) on a bounded sample of the workload's rows."""
+    import oracle
+    from paper_2406_12580_amd import datagen as dg
+    inp = dg.config_inputs(cfg, grad=True)
+    per_row = cfg.L * cfg.D
+
+    def run(rows):
+        s = slice(0, rows)
+        t0 = time.perf_counter()
+        oracle.scan_forward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam)
+        oracle.scan_backward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam, inp.dh[s])
+        return time.perf_counter() - t0
+
+    rows = 1
+    dt = run(rows)
+    while dt < target_s / 4 and rows < cfg.B:
+        rows = min(cfg.B, max(rows * 2, int(rows * (target_s / 2) / max(dt, 1e-3))))
+        dt = run(rows)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": rows * per_row / dt, "unit": "elements/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"fp64 oracle forward+backward over {rows} of {cfg.B} batch rows "
+                      f"(L={cfg.L}, D={cfg.D}), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the BD-LRU path is "
+              "built and measured on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2406_12580_amd import datagen as dg
+    from paper_2406_12580_amd import recblr as rb
+
+    cfg = dg.CONFIGS[args.workload]
+    if "bwd" not in cfg.ops:
+        sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")
+    dev = torch.device("cuda:0")
+    dtype = torch.float32 if cfg.io == "f32" else torch.bfloat16
+    log(f"generating {cfg.name}: B={cfg.B} L={cfg.L} D={cfg.D} {cfg.io}")
+    inp = dg.config_inputs(cfg, grad=True)
+    X, ZR, ZI, DH = (torch.from_numpy(a).to(dev).to(dtype) for a in (inp.x, inp.zr, inp.zi, inp.dh))
+    lam = torch.from_numpy(inp.lam).to(dev)
+    del inp
+    B, L, D = cfg.B, cfg.L, cfg.D
+    N = B * L * D
+    io = rb.io_code(dtype)
+    esz = 4 if cfg.io == "f32" else 2
+    h = torch.empty_like(X)
+    hT = torch.empty((B, D), dtype=torch.float32, device=dev)
+    dx, dzr, dzi = torch.empty_like(X), torch.empty_like(X), torch.empty_like(X)
+    dlam = torch.empty(D, dtype=torch.float32, device=dev)
+    dh0 = torch.empty((B, D), dtype=torch.float32, device=dev)
+    nf = rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, B, L, D, io)
+    nb = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, B, L, D, io)
+    wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    s = stream.cuda_stream
+    p = lambda t: t.data_ptr()
+
+    def fwd():
+        st = rb.recblr_bdlru_scan_forward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(hT), B, L, D,
+                                          io, p(wsf), nf, s)
+        assert st == 0, st
+
+    def bwd():
+        st = rb.recblr_bdlru_scan_backward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(DH), None,
+                                           p(dx), p(dzr), p(dzi), p(dlam), p(dh0), B, L, D, io,
+                                           p(wsb), nb, s)
+        assert st == 0, st
+
+    for _ in range(args.warmup):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        ev[k][0].record(stream)
+        fwd()
+        ev[k][1].record(stream)
+        bwd()
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_fwd = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e-3
+    t_bwd = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
+    step_s = wall / K
+    fb_s = float(np.mean(t_fwd + t_bwd))
+    fwd_bytes = FWD_ARRAYS * esz * N
+    bwd_bytes = BWD_ARRAYS * esz * N
+    fwd_gbs = fwd_bytes / float(np.mean(t_fwd)) / 1e9
+    bwd_gbs = bwd_bytes / float(np.mean(t_bwd)) / 1e9
+    dom = "bwd" if np.mean(t_bwd) >= np.mean(t_fwd) else "fwd"
+    ach = bwd_gbs if dom == "bwd" else fwd_gbs
+    log(f"fwd {np.mean(t_fwd)*1e6:.1f} us ({fwd_gbs:.0f} GB/s)  bwd {np.mean(t_bwd)*1e6:.1f} us "
+        f"({bwd_gbs:.0f} GB/s)  wall/step {step_s*1e6:.1f} us")
+
+    out = {
+        "metric": "BD-LRU scan elements/sec (B*L*D), forward+backward",
+        "value": N / step_s,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.io,
+        "data": "synthetic (seeded normal x, z, dL/dh; decay bases per the paper's initialisation)",
+        "config": {"workload": f"{cfg.name}: BD-LRU scan forward+backward, {cfg.note}",
+                   "B": B, "L": L, "D": D, "io": cfg.io, "elements": N},
+        "fwd_elements_per_s": N / float(np.mean(t_fwd)),
+        "fwd_bwd_elements_per_s_events": N / fb_s,
+        "us_fwd": float(np.mean(t_fwd)) * 1e6,
+        "us_bwd": float(np.mean(t_bwd)) * 1e6,
+        "fwd_hbm_gbs": fwd_gbs,
+        "bwd_hbm_gbs": bwd_gbs,
+        "roofline": {"bound": "hbm", "kernel": "scan_bwd" if dom == "bwd" else "scan_fwd",
+                     "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ach / PEAK_HBM_GBS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 CPU oracle on a bounded sample ...")
+        out["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

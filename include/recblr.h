@@ -1,0 +1,177 @@
+/*
+ * recblr.h - C ABI of librecblr.so, the MI355X (gfx950) BD-LRU scan library.
+ *
+ * The behavior-dependent linear recurrent unit of RecBLR ("Behavior-Dependent
+ * Linear Recurrent Units for Efficient Sequential Recommendation", CIKM 2024,
+ * arXiv 2406.12580), section 3.2:
+ *
+ *     r_t = sigmoid(W_r x_t + b_r)            recurrence gate
+ *     i_t = sigmoid(W_i x_t + b_i)            input gate
+ *     alpha_t = exp(-softplus(Lambda) * r_t)
+ *     beta_t  = sqrt(1 - alpha_t^2) * i_t
+ *     h_t     = alpha_t * h_{t-1} + beta_t * x_t        (eq:linrnn)
+ *
+ * computed for every channel (b, d) of a [B, L, D] batch of behavior
+ * sequences.  Section 3.3 evaluates the recurrence as a parallel scan with the
+ * associative operator (a2, b2) . (a1, b1) = (a2 a1, a2 b1 + b2); the library
+ * does the same on the GPU with a chunked scan, and its results equal the
+ * sequential recurrence up to floating-point rounding order.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are dense and row-major: [B][L][D] with D fastest, [B][D], [D],
+ *    and gate weights [D][D] stored [out][in], so z[d] = sum_k W[d][k] x[k] + b[d].
+ *  - Tensor pointers are DEVICE pointers (hipMalloc'ed or equivalent) and must
+ *    be aligned to their element size.  `io` selects the element type of
+ *    the sequence tensors: RECBLR_F32 (float) or RECBLR_BF16 (bfloat16, stored
+ *    as its 16-bit pattern).  Lambda, h0, hT, dh0, dLambda, h_prev, h_next and
+ *    the weight gradients are always float.  Gate weights and biases use `io`.
+ *  - All arithmetic is fp32; recurrent state and carries are fp32; bf16 outputs
+ *    are rounded to nearest even.
+ *  - h0 == NULL means a zero initial state (the paper's c_1 = beta'_1).
+ *    Optional outputs (hT, dh0) may be NULL.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *    enqueues work on it and returns; results are valid once the stream has
+ *    been synchronised.  The library never synchronises, never allocates and
+ *    keeps no state between calls, so concurrent calls on different streams
+ *    with disjoint buffers are safe.
+ *  - `ws`/`ws_bytes`: caller-owned device scratch of at least
+ *    recblr_workspace_size(...) bytes, 256-byte aligned (NULL is accepted when
+ *    that size is 0).  Its contents need no initialisation and are garbage
+ *    after the call.  Two calls in flight at once must not share it.
+ *  - Validation happens on the host, before anything is enqueued; a call that
+ *    returns an error has enqueued nothing.  Output buffers must not overlap
+ *    inputs or each other (recblr_bdlru_scan_step and recblr_bdlru_step allow
+ *    h_next == h_prev exactly).  B == 0 or D == 0 is a no-op; L == 0 writes only
+ *    hT := h0 (forward) and dh0 := dhT, dLambda := 0 (backward).
+ *  - NaN and Inf inputs propagate; they are not checked.  Results are
+ *    deterministic: the same inputs give bitwise identical outputs.
+ */
+#ifndef RECBLR_H_
+#define RECBLR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+enum {
+    RECBLR_OK = 0,
+    RECBLR_ERR_INVALID_ARGUMENT = -1, /* NULL/misaligned/overlapping pointer, negative size */
+    RECBLR_ERR_UNSUPPORTED = -2,      /* unknown dtype or op, size beyond the supported range */
+    RECBLR_ERR_WORKSPACE = -3,        /* ws NULL, too small or not 256-byte aligned */
+    RECBLR_ERR_HIP = -4               /* a kernel launch failed (hipGetLastError) */
+};
+
+/* Element type of the sequence tensors. */
+enum { RECBLR_F32 = 0, RECBLR_BF16 = 1 };
+
+/* Operations, for recblr_workspace_size. */
+enum {
+    RECBLR_OP_SCAN_FORWARD = 0,
+    RECBLR_OP_SCAN_BACKWARD = 1,
+    RECBLR_OP_FORWARD = 2,
+    RECBLR_OP_BACKWARD = 3,
+    RECBLR_OP_STEP = 4
+};
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* recblr_status_string(int status);
+
+/* Bytes of workspace `op` needs for this problem; 0 means none (ws may be NULL).
+ * For RECBLR_OP_STEP, L is ignored.  Returns 0 for invalid arguments too, which
+ * the entry point then reports. */
+size_t recblr_workspace_size(int op, int64_t B, int64_t L, int64_t D, int io);
+
+/*
+ * Gated scan forward from given gate pre-activations (section 3.2 with
+ * z_r = W_r x + b_r and z_i = W_i x + b_i already computed).  This is the
+ * hot path: the gate activation is fused into the scan's loads.
+ *   x, z_r, z_i : [B][L][D] io        inputs
+ *   lambda      : [D] float           decay parameter Lambda
+ *   h0          : [B][D] float|NULL   initial state
+ *   h           : [B][L][D] io        output, h_t for every step
+ *   hT          : [B][D] float|NULL   output, final state h_L (kept in fp32)
+ */
+int recblr_bdlru_scan_forward(const void* x, const void* z_r, const void* z_i,
+                              const float* lambda, const float* h0, void* h, float* hT,
+                              int64_t B, int64_t L, int64_t D, int io, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * Backward of recblr_bdlru_scan_forward: the exact adjoint of the recurrence
+ * of eq:linrnn and of the gate equations of section 3.2 (the paper states no
+ * backward pass; see the derivation in scan_bwd.hip).
+ *   h    : [B][L][D] io    the forward output (saved activations)
+ *   dh   : [B][L][D] io    dLoss/dh_t for every step
+ *   dhT  : [B][D] float|NULL  dLoss/dh_L of the final-state output
+ * Outputs:
+ *   dx   : [B][L][D] io    dLoss/dx through beta'_t = beta_t x_t only (the
+ *                          z inputs are independent here)
+ *   dz_r, dz_i : [B][L][D] io
+ *   dlambda    : [D] float  summed over b and t in a fixed order (fp64 final stage)
+ *   dh0        : [B][D] float|NULL
+ */
+int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
+                               const float* lambda, const float* h0, const void* h,
+                               const void* dh, const float* dhT, void* dx, void* dz_r,
+                               void* dz_i, float* dlambda, float* dh0, int64_t B, int64_t L,
+                               int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One recurrent step for inference (eq:linrnn applied once; the paper's
+ * low-cost recurrent inference):  h_next = alpha(z_r) h_prev + beta(z_r, z_i) x.
+ *   x, z_r, z_i : [B][D] io;  h_prev, h_next : [B][D] float (h_next may == h_prev)
+ */
+int recblr_bdlru_scan_step(const void* x, const void* z_r, const void* z_i,
+                           const float* lambda, const float* h_prev, float* h_next, int64_t B,
+                           int64_t D, int io, void* stream);
+
+/*
+ * Full forward with the gate projections (section 3.2): z_r = x W_r^T + b_r and
+ * z_i = x W_i^T + b_i on the matrix cores, then the gated scan.
+ *   W_r, W_i : [D][D] io;  b_r, b_i : [D] io or NULL (zero bias)
+ * Other arguments as recblr_bdlru_scan_forward.  Supports 1 <= D <= 1024.
+ */
+int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                         const void* b_i, const float* lambda, const float* h0, void* h,
+                         float* hT, int64_t B, int64_t L, int64_t D, int io, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/*
+ * Full backward: scan backward, then the projection backward
+ *   dx += dz_r W_r + dz_i W_i,  dW = sum_rows dz^T x,  db = sum_rows dz.
+ *   dx : [B][L][D] io, the TOTAL gradient with respect to x
+ *   dW_r, dW_i : [D][D] float;  db_r, db_i : [D] float;  dlambda : [D] float
+ *   dh0 : [B][D] float|NULL
+ */
+int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                          const void* b_i, const float* lambda, const float* h0, const void* h,
+                          const void* dh, const float* dhT, void* dx, float* dW_r, float* db_r,
+                          float* dW_i, float* db_i, float* dlambda, float* dh0, int64_t B,
+                          int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Full single step: projections of x_t, then one recurrent step.
+ *   x : [B][D] io;  h_prev, h_next : [B][D] float (h_next may == h_prev) */
+int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                      const void* b_i, const float* lambda, const float* h_prev, float* h_next,
+                      int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Raw first-order recurrence h_t = a_t h_{t-1} + u_t (eq:linrnn with the
+ * coefficients given directly), float only.  Same kernel as the gated scan
+ * with the gate stage removed; used to check the scan against closed forms.
+ *   a, u, h : [B][L][D] float;  h0, hT : [B][D] float|NULL
+ */
+int recblr_linear_scan_forward(const float* a, const float* u, const float* h0, float* h,
+                               float* hT, int64_t B, int64_t L, int64_t D, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RECBLR_H_ */

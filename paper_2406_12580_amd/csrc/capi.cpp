@@ -1,0 +1,345 @@
+// C ABI of librecblr.so (declared in include/recblr.h): argument validation,
+// workspace carving and dispatch to the HIP kernels.  Validation runs entirely
+// on the host and before any HIP call, so a rejected call has enqueued nothing.
+#include "recblr.h"
+
+#include <hip/hip_runtime.h>
+
+#include <initializer_list>
+
+#include "gemm.hpp"
+#include "launch.hpp"
+
+using namespace recblr;
+
+namespace {
+
+constexpr size_t kWsAlign = 256;
+constexpr int64_t kMaxDim = (int64_t)1 << 31;       // each of B, L, D
+constexpr int64_t kMaxElems = (int64_t)1 << 40;     // B*L*D
+constexpr int64_t kMaxChannels = (int64_t)1 << 36;  // B*D (grid of B*D/64 workgroups)
+constexpr int64_t kMaxProjD = 1024;
+constexpr int64_t kMaxD = (int64_t)65535 * 64;        // channel groups of the dLambda reduction
+
+inline size_t align_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+struct Buf {
+    const void* p;
+    size_t bytes;
+};
+
+bool overlaps(Buf a, Buf b) {
+    if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+    uintptr_t a0 = (uintptr_t)a.p, b0 = (uintptr_t)b.p;
+    return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+bool aligned(const void* p, size_t a) { return p == nullptr || ((uintptr_t)p % a) == 0; }
+
+// Outputs must not overlap inputs or each other.
+bool disjoint(std::initializer_list<Buf> outs, std::initializer_list<Buf> ins) {
+    for (auto o = outs.begin(); o != outs.end(); ++o) {
+        for (const Buf& i : ins)
+            if (overlaps(*o, i)) return false;
+        for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+            if (overlaps(*o, *o2)) return false;
+    }
+    return true;
+}
+
+int check_dims(int64_t B, int64_t L, int64_t D, int io) {
+    if (io != RECBLR_F32 && io != RECBLR_BF16) return RECBLR_ERR_UNSUPPORTED;
+    if (B < 0 || L < 0 || D < 0) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (B >= kMaxDim || L >= kMaxDim || D > kMaxD) return RECBLR_ERR_UNSUPPORTED;
+    if (B * D > kMaxChannels) return RECBLR_ERR_UNSUPPORTED;
+    if (B * D > 0 && L > kMaxElems / (B * D)) return RECBLR_ERR_UNSUPPORTED;
+    return RECBLR_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+    if (need == 0) return RECBLR_OK;
+    if (ws == nullptr || ws_bytes < need || !aligned(ws, kWsAlign)) return RECBLR_ERR_WORKSPACE;
+    return RECBLR_OK;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? RECBLR_OK : RECBLR_ERR_HIP; }
+
+IoType io_of(int io) { return io == RECBLR_BF16 ? IoType::kBf16 : IoType::kF32; }
+
+size_t esz(int io) { return io == RECBLR_BF16 ? 2 : 4; }
+
+// ---- workspace layouts of the entry points with gate parameters
+struct FullFwdLayout {
+    size_t zr, zi, scan, total;
+};
+// z and dz scratch is fp32 whatever the I/O type.
+FullFwdLayout full_fwd_layout(int64_t B, int64_t L, int64_t D, int io) {
+    size_t zbytes = align_up((size_t)(B * L * D) * sizeof(float));
+    FullFwdLayout l;
+    l.zr = 0;
+    l.zi = zbytes;
+    l.scan = 2 * zbytes;
+    l.total = l.scan + align_up(scan_forward_workspace(B, L, D, io_of(io)));
+    return l;
+}
+
+struct FullBwdLayout {
+    size_t zr, zi, dzr, dzi, scan, dw, total;
+};
+FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
+    size_t zbytes = align_up((size_t)(B * L * D) * sizeof(float));
+    FullBwdLayout l;
+    l.zr = 0;
+    l.zi = zbytes;
+    l.dzr = 2 * zbytes;
+    l.dzi = 3 * zbytes;
+    l.scan = 4 * zbytes;
+    l.dw = l.scan + align_up(scan_backward_workspace(B, L, D, io_of(io)));
+    l.total = l.dw + align_up(project_dw_workspace(B * L, D));
+    return l;
+}
+
+size_t step_ws(int64_t B, int64_t D, int) { return 2 * align_up((size_t)(B * D) * sizeof(float)); }
+
+char* at(void* ws, size_t off) { return (char*)ws + off; }
+
+}  // namespace
+
+extern "C" {
+
+const char* recblr_status_string(int status) {
+    switch (status) {
+        case RECBLR_OK: return "ok";
+        case RECBLR_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case RECBLR_ERR_UNSUPPORTED: return "unsupported";
+        case RECBLR_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+        case RECBLR_ERR_HIP: return "HIP launch failure";
+        default: return "unknown status";
+    }
+}
+
+size_t recblr_workspace_size(int op, int64_t B, int64_t L, int64_t D, int io) {
+    if (op == RECBLR_OP_STEP) L = 1;
+    if (check_dims(B, L, D, io) != RECBLR_OK) return 0;
+    switch (op) {
+        case RECBLR_OP_SCAN_FORWARD: return scan_forward_workspace(B, L, D, io_of(io));
+        case RECBLR_OP_SCAN_BACKWARD: return scan_backward_workspace(B, L, D, io_of(io));
+        case RECBLR_OP_FORWARD: return full_fwd_layout(B, L, D, io).total;
+        case RECBLR_OP_BACKWARD: return full_bwd_layout(B, L, D, io).total;
+        case RECBLR_OP_STEP: return step_ws(B, D, io);
+        default: return 0;
+    }
+}
+
+int recblr_bdlru_scan_forward(const void* x, const void* z_r, const void* z_i,
+                              const float* lambda, const float* h0, void* h, float* hT,
+                              int64_t B, int64_t L, int64_t D, int io, void* ws,
+                              size_t ws_bytes, void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4;
+    if (L > 0 && (!x || !z_r || !z_i || !h)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!lambda) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i, (const void*)h})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)hT})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{h, n}, {hT, s}},
+                  {{x, n}, {z_r, n}, {z_i, n}, {lambda, (size_t)D * 4}, {h0, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    st = check_ws(ws, ws_bytes, scan_forward_workspace(B, L, D, io_of(io)));
+    if (st) return st;
+    ScanFwdArgs a{x, z_r, z_i, lambda, h0, h, hT, B, L, D, io_of(io), io_of(io), ws, ws_bytes};
+    return status_of(launch_scan_forward(a, (hipStream_t)stream));
+}
+
+int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
+                               const float* lambda, const float* h0, const void* h,
+                               const void* dh, const float* dhT, void* dx, void* dz_r,
+                               void* dz_i, float* dlambda, float* dh0, int64_t B, int64_t L,
+                               int64_t D, int io, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D == 0) return RECBLR_OK;
+    if (!lambda || !dlambda) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 dl = (size_t)D * 4;
+    if (B > 0 && L > 0 && (!x || !z_r || !z_i || !h || !dh || !dx || !dz_r || !dz_i))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i, h, dh, (const void*)dx, (const void*)dz_r,
+                          (const void*)dz_i})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)dhT,
+                          (const void*)dlambda, (const void*)dh0})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{dx, n}, {dz_r, n}, {dz_i, n}, {dlambda, dl}, {dh0, s}},
+                  {{x, n}, {z_r, n}, {z_i, n}, {lambda, dl}, {h0, s}, {h, n}, {dh, n},
+                   {dhT, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    if (B == 0) return status_of(launch_fill(dlambda, 0.0f, D, strm));
+    st = check_ws(ws, ws_bytes, scan_backward_workspace(B, L, D, io_of(io)));
+    if (st) return st;
+    ScanBwdArgs a{x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
+                  B, L, D, io_of(io), io_of(io), ws, ws_bytes};
+    return status_of(launch_scan_backward(a, strm));
+}
+
+int recblr_bdlru_scan_step(const void* x, const void* z_r, const void* z_i,
+                           const float* lambda, const float* h_prev, float* h_next, int64_t B,
+                           int64_t D, int io, void* stream) {
+    int st = check_dims(B, 1, D, io);
+    if (st) return st;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    if (!x || !z_r || !z_i || !lambda || !h_prev || !h_next) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h_prev, (const void*)h_next})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * D) * esz(io), s = (size_t)(B * D) * 4;
+    // h_next may be h_prev exactly (in-place update) but must not partly overlap it.
+    if (h_next != h_prev && overlaps({h_next, s}, {h_prev, s})) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{h_next, s}}, {{x, n}, {z_r, n}, {z_i, n}, {lambda, (size_t)D * 4}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    return status_of(launch_scan_step(x, z_r, z_i, lambda, h_prev, h_next, B, D, io_of(io),
+                                      io_of(io), (hipStream_t)stream));
+}
+
+int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                         const void* b_i, const float* lambda, const float* h0, void* h,
+                         float* hT, int64_t B, int64_t L, int64_t D, int io, void* ws,
+                         size_t ws_bytes, void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D > kMaxProjD) return RECBLR_ERR_UNSUPPORTED;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    if (!lambda || !W_r || !W_i || (L > 0 && (!x || !h))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, W_r, W_i, b_r, b_i, (const void*)h})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)hT})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 w = (size_t)(D * D) * esz(io), bb = (size_t)D * esz(io);
+    if (!disjoint({{h, n}, {hT, s}}, {{x, n}, {W_r, w}, {W_i, w}, {b_r, bb}, {b_i, bb},
+                                      {lambda, (size_t)D * 4}, {h0, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    FullFwdLayout lay = full_fwd_layout(B, L, D, io);
+    st = check_ws(ws, ws_bytes, lay.total);
+    if (st) return st;
+    if (!disjoint({{ws, lay.total}}, {{x, n}, {h, n}, {hT, s}, {lambda, (size_t)D * 4}, {h0, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    void* zr = at(ws, lay.zr);
+    void* zi = at(ws, lay.zi);
+    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B * L, D, io_of(io), strm);
+    if (e != hipSuccess) return RECBLR_ERR_HIP;
+    ScanFwdArgs a{x, zr, zi, lambda, h0, h, hT, B, L, D, io_of(io), IoType::kF32,
+                  at(ws, lay.scan), lay.total - lay.scan};
+    return status_of(launch_scan_forward(a, strm));
+}
+
+int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                          const void* b_i, const float* lambda, const float* h0, const void* h,
+                          const void* dh, const float* dhT, void* dx, float* dW_r, float* db_r,
+                          float* dW_i, float* db_i, float* dlambda, float* dh0, int64_t B,
+                          int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
+                          void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D > kMaxProjD) return RECBLR_ERR_UNSUPPORTED;
+    if (D == 0) return RECBLR_OK;
+    if (!lambda || !W_r || !W_i || !dlambda || !dW_r || !dW_i || !db_r || !db_i)
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    if (B > 0 && L > 0 && (!x || !h || !dh || !dx)) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, W_r, W_i, b_r, b_i, h, dh, (const void*)dx})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)dhT,
+                          (const void*)dW_r, (const void*)db_r, (const void*)dW_i,
+                          (const void*)db_i, (const void*)dlambda, (const void*)dh0})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 w = (size_t)(D * D) * esz(io), bb = (size_t)D * esz(io), wf = (size_t)(D * D) * 4,
+                 df = (size_t)D * 4;
+    if (!disjoint({{dx, n}, {dW_r, wf}, {db_r, df}, {dW_i, wf}, {db_i, df}, {dlambda, df},
+                   {dh0, s}},
+                  {{x, n}, {W_r, w}, {W_i, w}, {b_r, bb}, {b_i, bb}, {lambda, df}, {h0, s},
+                   {h, n}, {dh, n}, {dhT, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    FullBwdLayout lay = full_bwd_layout(B, L, D, io);
+    st = check_ws(ws, ws_bytes, lay.total);
+    if (st) return st;
+    void* zr = at(ws, lay.zr);
+    void* zi = at(ws, lay.zi);
+    void* dzr = at(ws, lay.dzr);
+    void* dzi = at(ws, lay.dzi);
+    hipError_t e = hipSuccess;
+    if (B == 0) {
+        // Sums over an empty batch: every parameter gradient is zero.
+        for (float* p : {dW_r, dW_i})
+            if ((e = launch_fill(p, 0.0f, D * D, strm)) != hipSuccess) return RECBLR_ERR_HIP;
+        for (float* p : {db_r, db_i, dlambda})
+            if ((e = launch_fill(p, 0.0f, D, strm)) != hipSuccess) return RECBLR_ERR_HIP;
+        return RECBLR_OK;
+    }
+    const int64_t M = B * L;
+    e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, M, D, io_of(io), strm);
+    if (e != hipSuccess) return RECBLR_ERR_HIP;
+    ScanBwdArgs a{x, zr, zi, lambda, h0, h, dh, dhT, dx, dzr, dzi, dlambda, dh0,
+                  B, L, D, io_of(io), IoType::kF32, at(ws, lay.scan), lay.dw - lay.scan};
+    e = launch_scan_backward(a, strm);
+    if (e != hipSuccess) return RECBLR_ERR_HIP;
+    e = launch_project_backward_data(dzr, dzi, W_r, W_i, dx, M, D, io_of(io), strm);
+    if (e != hipSuccess) return RECBLR_ERR_HIP;
+    e = launch_project_backward_weights(dzr, dzi, x, dW_r, db_r, dW_i, db_i, M, D, io_of(io),
+                                        at(ws, lay.dw), strm);
+    return status_of(e);
+}
+
+int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const void* W_i,
+                      const void* b_i, const float* lambda, const float* h_prev, float* h_next,
+                      int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_dims(B, 1, D, io);
+    if (st) return st;
+    if (D > kMaxProjD) return RECBLR_ERR_UNSUPPORTED;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    if (!x || !W_r || !W_i || !lambda || !h_prev || !h_next) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, W_r, W_i, b_r, b_i})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h_prev, (const void*)h_next})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * D) * esz(io), s = (size_t)(B * D) * 4,
+                 w = (size_t)(D * D) * esz(io), bb = (size_t)D * esz(io);
+    if (h_next != h_prev && overlaps({h_next, s}, {h_prev, s})) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{h_next, s}}, {{x, n}, {W_r, w}, {W_i, w}, {b_r, bb}, {b_i, bb},
+                                  {lambda, (size_t)D * 4}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t need = step_ws(B, D, io);
+    st = check_ws(ws, ws_bytes, need);
+    if (st) return st;
+    hipStream_t strm = (hipStream_t)stream;
+    void* zr = ws;
+    void* zi = at(ws, need / 2);
+    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B, D, io_of(io), strm);
+    if (e != hipSuccess) return RECBLR_ERR_HIP;
+    return status_of(
+        launch_scan_step(x, zr, zi, lambda, h_prev, h_next, B, D, io_of(io), IoType::kF32, strm));
+}
+
+int recblr_linear_scan_forward(const float* a, const float* u, const float* h0, float* h,
+                               float* hT, int64_t B, int64_t L, int64_t D, void* stream) {
+    int st = check_dims(B, L, D, RECBLR_F32);
+    if (st) return st;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    if (L > 0 && (!a || !u || !h)) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)a, (const void*)u, (const void*)h0, (const void*)h,
+                          (const void*)hT})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * 4, s = (size_t)(B * D) * 4;
+    if (!disjoint({{h, n}, {hT, s}}, {{a, n}, {u, n}, {h0, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    return status_of(launch_linear_scan(a, u, h0, h, hT, B, L, D, (hipStream_t)stream));
+}
+
+}  // extern "C"

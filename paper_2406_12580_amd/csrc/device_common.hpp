@@ -1,0 +1,143 @@
+// Device-side helpers shared by the BD-LRU kernels (gfx950 / CDNA4, wave64).
+//
+// Gate arithmetic of the behavior-dependent linear recurrent unit
+// (RecBLR, arXiv 2406.12580, section 3.2):
+//   r = sigmoid(z_r), i = sigmoid(z_i), q = softplus(Lambda) * r
+//   alpha = exp(-q), beta = sqrt(1 - alpha^2) * i
+// evaluated in fp32 with the hardware transcendental units (v_exp, v_rcp,
+// v_sqrt, v_rsq), and 1 - alpha^2 = 1 - exp(-2q) evaluated without
+// cancellation when q is small (see one_minus_exp_neg).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace recblr {
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ------------------------------------------------------------------ I/O types
+struct bf16 {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return __uint_as_float((uint32_t)v.bits << 16); }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float v);
+
+template <>
+__device__ __forceinline__ float from_f32<float>(float v) { return v; }
+
+// Round to nearest, ties to even; NaN stays a quiet NaN.
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float v) {
+    uint32_t u = __float_as_uint(v);
+    uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    bf16 out;
+    out.bits = (v != v) ? (uint16_t)((u >> 16) | 0x40u) : (uint16_t)r;
+    return out;
+}
+
+template <typename T>
+__device__ __forceinline__ float load(const T* p) { return to_f32(*p); }
+
+// Load/store at a byte offset from a kernel-argument base pointer.  With a
+// 32-bit offset the compiler emits the scalar-base + 32-bit-vector-offset
+// form of global_load/global_store, so one VGPR addresses every tensor that
+// shares the element offset (x, z_r, z_i, h, dh all do).
+template <typename T, typename Off>
+__device__ __forceinline__ float load_at(const T* p, Off off_bytes) {
+    return to_f32(*(const T*)((const char*)p + off_bytes));
+}
+
+template <typename T, typename Off>
+__device__ __forceinline__ void store_at(T* p, Off off_bytes, float v) {
+    *(T*)((char*)p + off_bytes) = from_f32<T>(v);
+}
+
+template <typename T>
+__device__ __forceinline__ void store(T* p, float v) { *p = from_f32<T>(v); }
+
+// Byte offset into a TZ tensor from the byte offset of the same element in a
+// TX tensor (TZ is never narrower than TX).
+template <typename TX, typename TZ, typename Off>
+__device__ __forceinline__ Off z_offset(Off off_x) {
+    static_assert(sizeof(TZ) >= sizeof(TX), "z tensors are at least as wide as x");
+    return sizeof(TZ) == sizeof(TX) ? off_x : off_x * (Off)(sizeof(TZ) / sizeof(TX));
+}
+
+// ------------------------------------------------------------------ gate math
+__device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
+__device__ __forceinline__ float fast_rcp(float v) { return __builtin_amdgcn_rcpf(v); }
+__device__ __forceinline__ float fast_sqrt(float v) { return __builtin_amdgcn_sqrtf(v); }
+__device__ __forceinline__ float fast_rsq(float v) { return __builtin_amdgcn_rsqf(v); }
+
+// sigmoid(z) = 1 / (1 + e^-z); saturates cleanly to 0 and 1 for large |z|.
+__device__ __forceinline__ float sigmoid(float z) {
+    return fast_rcp(1.0f + fast_exp2(-z * kLog2e));
+}
+
+// softplus(v) = log(1 + e^v) = max(v, 0) + log1p(e^-|v|); once per channel.
+__device__ __forceinline__ float softplus(float v) {
+    return fmaxf(v, 0.0f) + log1pf(expf(-fabsf(v)));
+}
+
+// 1 - e^-y for y >= 0.  For y < 1/4 the Maclaurin series of 1 - e^-y,
+// y * sum_{n>=0} (-y)^n / (n+1)!, truncated after the y^8 term (relative
+// truncation error below (1/4)^8 / 9! < 5e-11), in Horner form; above 1/4
+// the direct form 1 - a^2 with a = e^-(y/2) has no harmful cancellation
+// (a^2 <= e^-1/4, so the relative error stays within a few ulp).
+__device__ __forceinline__ float one_minus_exp_neg(float y, float a) {
+    float p = 1.0f / 40320.0f;
+    p = fmaf(p, -y, 1.0f / 5040.0f);
+    p = fmaf(p, -y, 1.0f / 720.0f);
+    p = fmaf(p, -y, 1.0f / 120.0f);
+    p = fmaf(p, -y, 1.0f / 24.0f);
+    p = fmaf(p, -y, 1.0f / 6.0f);
+    p = fmaf(p, -y, 0.5f);
+    p = fmaf(p, -y, 1.0f);
+    float series = y * p;
+    float direct = fmaf(-a, a, 1.0f);
+    return y < 0.25f ? series : direct;
+}
+
+// Per-channel constants derived from Lambda.
+struct ChannelConst {
+    float s;        // softplus(Lambda)
+    float neg_s_l2; // -softplus(Lambda) * log2(e): alpha = exp2(r * neg_s_l2)
+    float two_s;    // 2 softplus(Lambda): 2q = r * two_s
+};
+
+__device__ __forceinline__ ChannelConst channel_const(float lam) {
+    ChannelConst c;
+    c.s = softplus(lam);
+    c.neg_s_l2 = -c.s * kLog2e;
+    c.two_s = 2.0f * c.s;
+    return c;
+}
+
+// alpha and beta' = beta * x of one element (forward path).
+__device__ __forceinline__ void gate_forward(float x, float zr, float zi, const ChannelConst& cc,
+                                             float& alpha, float& u) {
+    float r = sigmoid(zr);
+    float i = sigmoid(zi);
+    alpha = fast_exp2(r * cc.neg_s_l2);
+    float m = one_minus_exp_neg(r * cc.two_s, alpha);
+    u = fast_sqrt(m) * i * x;
+}
+
+// (A, H) pair of the scan operator: a segment maps a state h to A h + H.
+// Composing an earlier segment e with a later segment l gives
+// (A_l A_e, A_l H_e + H_l) (section 3.3, operator "bullet").
+struct Seg {
+    float A, H;
+};
+
+__device__ __forceinline__ Seg compose(Seg later, Seg earlier) {
+    return Seg{later.A * earlier.A, fmaf(later.A, earlier.H, later.H)};
+}
+
+}  // namespace recblr

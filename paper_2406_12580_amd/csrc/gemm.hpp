@@ -1,0 +1,29 @@
+// Host launchers of the gate-projection products (internal to librecblr.so).
+#pragma once
+
+#include "launch.hpp"
+
+namespace recblr {
+
+// z_r = x W_r^T + b_r, z_i = x W_i^T + b_i over M = B*L rows (b may be null).
+// x, W, b and dx use the I/O type; z and dz are always fp32.
+hipError_t launch_project_forward(const void* x, const void* wr, const void* br, const void* wi,
+                                  const void* bi, void* zr, void* zi, int64_t M, int64_t D,
+                                  IoType io, hipStream_t stream);
+
+// dx += dz_r W_r + dz_i W_i (dx holds the direct term on entry).
+hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const void* wr,
+                                        const void* wi, void* dx, int64_t M, int64_t D,
+                                        IoType io, hipStream_t stream);
+
+// dW_r, dW_i = dz^T x and db_r, db_i = column sums of dz; uses
+// project_dw_workspace(M, D) bytes of scratch at `ws`.
+hipError_t launch_project_backward_weights(const void* dzr, const void* dzi, const void* x,
+                                           float* dwr, float* dbr, float* dwi, float* dbi,
+                                           int64_t M, int64_t D, IoType io, void* ws,
+                                           hipStream_t stream);
+
+int64_t project_dw_splits(int64_t M, int64_t D);
+size_t project_dw_workspace(int64_t M, int64_t D);
+
+}  // namespace recblr

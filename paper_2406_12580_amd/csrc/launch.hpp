@@ -1,0 +1,66 @@
+// Host-side launchers of the BD-LRU kernels.  Internal to librecblr.so: the
+// C ABI in capi.cpp validates every argument and then calls these.  Every
+// launcher enqueues work on `stream` and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace recblr {
+
+enum class IoType : int { kF32 = 0, kBf16 = 1 };
+
+inline size_t io_bytes(IoType t) { return t == IoType::kF32 ? 4 : 2; }
+
+struct ScanFwdArgs {
+    const void* x;
+    const void* zr;
+    const void* zi;
+    const float* lambda;
+    const float* h0;  // may be null (zero state)
+    void* h;
+    float* hT;        // may be null
+    int64_t B, L, D;
+    IoType io;        // element type of x and h
+    IoType zio;       // element type of z_r, z_i (fp32 scratch in the entry points with weights)
+    void* ws;         // look-back state, when the launcher uses it
+    size_t ws_bytes;
+};
+
+struct ScanBwdArgs {
+    const void* x;
+    const void* zr;
+    const void* zi;
+    const float* lambda;
+    const float* h0;   // may be null
+    const void* h;     // forward output
+    const void* dh;
+    const float* dhT;  // may be null
+    void* dx;
+    void* dzr;
+    void* dzi;
+    float* dlambda;
+    float* dh0;        // may be null
+    int64_t B, L, D;
+    IoType io;        // element type of x, h, dh, dx
+    IoType zio;       // element type of z_r, z_i, dz_r, dz_i
+    void* ws;
+    size_t ws_bytes;
+};
+
+// Workspace (bytes) the scan launchers need for a given problem.
+size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io);
+size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType io);
+
+hipError_t launch_scan_forward(const ScanFwdArgs& a, hipStream_t stream);
+hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream);
+hipError_t launch_linear_scan(const float* a, const float* u, const float* h0, float* h,
+                              float* hT, int64_t B, int64_t L, int64_t D, hipStream_t stream);
+hipError_t launch_scan_step(const void* x, const void* zr, const void* zi, const float* lambda,
+                            const float* h_prev, float* h_next, int64_t B, int64_t D, IoType io,
+                            IoType zio, hipStream_t stream);
+hipError_t launch_copy_state(const float* src, float* dst, int64_t n, hipStream_t stream);
+hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream);
+
+}  // namespace recblr

@@ -1,0 +1,224 @@
+"""Thin ctypes binding of librecblr.so (the C ABI in include/recblr.h).
+
+Two layers, both pure argument marshalling (every step of the computation runs
+in the HIP kernels of librecblr.so):
+
+* ``recblr_*`` functions mirror the C entry points one to one: they take raw
+  device pointers (ints) and sizes and return the C status code.
+* ``bdlru_scan_forward`` and friends take torch tensors that live on the GPU,
+  check their shapes and dtypes, allocate outputs and workspace with torch,
+  call the C entry point on the current HIP stream and raise on a non-zero
+  status.
+
+There is no fallback: if the library is missing or fails to load, importing
+this module raises.  Build it first with ``python -m paper_2406_12580_amd.build``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librecblr.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing; build it with `python -m paper_2406_12580_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP = range(5)
+
+EXPORTS = (
+    "recblr_status_string", "recblr_workspace_size", "recblr_bdlru_scan_forward",
+    "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
+    "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
+)
+
+_p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+_SIGS = {
+    "recblr_status_string": ([_int], ctypes.c_char_p),
+    "recblr_workspace_size": ([_int, _i64, _i64, _i64, _int], _sz),
+    "recblr_bdlru_scan_forward": ([_p] * 7 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_bdlru_scan_backward": ([_p] * 13 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_bdlru_scan_step": ([_p] * 6 + [_i64] * 2 + [_int, _p], _int),
+    "recblr_bdlru_forward": ([_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_bdlru_backward": ([_p] * 17 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_bdlru_step": ([_p] * 8 + [_i64] * 2 + [_int, _p, _sz, _p], _int),
+    "recblr_linear_scan_forward": ([_p] * 5 + [_i64] * 3 + [_p], _int),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = _res
+    globals()[_name] = _fn
+
+
+class RecblrError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {recblr_status_string(status).decode()} ({status})")
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise RecblrError(status, where)
+
+
+# ------------------------------------------------------------------ torch-level helpers
+
+def io_code(dtype: torch.dtype) -> int:
+    if dtype == torch.float32:
+        return F32
+    if dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported I/O dtype {dtype}; use float32 or bfloat16")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _workspace(op: int, B: int, L: int, D: int, io: int, device):
+    n = recblr_workspace_size(op, B, L, D, io)
+    if n == 0:
+        return None, 0
+    return torch.empty(n, dtype=torch.uint8, device=device), n
+
+
+def _f32(t, shape, name):
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be float32 of shape {tuple(shape)}")
+    return t
+
+
+def _io(t, shape, dtype, name):
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be {dtype} of shape {tuple(shape)}")
+    return t
+
+
+def bdlru_scan_forward(x, zr, zi, lam, h0=None, stream=None):
+    """Gated BD-LRU scan from pre-activations. Returns (h [B,L,D] io, hT [B,D] float32)."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    _io(zr, x.shape, x.dtype, "zr"), _io(zi, x.shape, x.dtype, "zi")
+    _f32(lam, (D,), "lambda"), _f32(h0, (B, D), "h0")
+    h = torch.empty_like(x)
+    hT = torch.empty((B, D), dtype=torch.float32, device=x.device)
+    ws, nws = _workspace(OP_SCAN_FORWARD, B, L, D, io, x.device)
+    _check(recblr_bdlru_scan_forward(_ptr(x), _ptr(zr), _ptr(zi), _ptr(lam), _ptr(h0), _ptr(h),
+                                     _ptr(hT), B, L, D, io, _ptr(ws), nws, _stream(stream)),
+           "recblr_bdlru_scan_forward")
+    return h, hT
+
+
+def bdlru_scan_backward(x, zr, zi, lam, h, dh, h0=None, dhT=None, stream=None):
+    """Backward of bdlru_scan_forward. Returns dict dx, dzr, dzi, dlambda, dh0."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    for t, n in ((zr, "zr"), (zi, "zi"), (h, "h"), (dh, "dh")):
+        _io(t, x.shape, x.dtype, n)
+    _f32(lam, (D,), "lambda"), _f32(h0, (B, D), "h0"), _f32(dhT, (B, D), "dhT")
+    out = {k: torch.empty_like(x) for k in ("dx", "dzr", "dzi")}
+    out["dlambda"] = torch.empty(D, dtype=torch.float32, device=x.device)
+    out["dh0"] = torch.empty((B, D), dtype=torch.float32, device=x.device)
+    ws, nws = _workspace(OP_SCAN_BACKWARD, B, L, D, io, x.device)
+    _check(recblr_bdlru_scan_backward(
+        _ptr(x), _ptr(zr), _ptr(zi), _ptr(lam), _ptr(h0), _ptr(h), _ptr(dh), _ptr(dhT),
+        _ptr(out["dx"]), _ptr(out["dzr"]), _ptr(out["dzi"]), _ptr(out["dlambda"]),
+        _ptr(out["dh0"]), B, L, D, io, _ptr(ws), nws, _stream(stream)),
+        "recblr_bdlru_scan_backward")
+    return out
+
+
+def bdlru_scan_step(x, zr, zi, lam, h_prev, out=None, stream=None):
+    """One recurrent step over [B, D]; returns h_next (float32). out may be h_prev."""
+    B, D = x.shape
+    io = io_code(x.dtype)
+    _io(zr, x.shape, x.dtype, "zr"), _io(zi, x.shape, x.dtype, "zi")
+    _f32(lam, (D,), "lambda"), _f32(h_prev, (B, D), "h_prev")
+    h_next = torch.empty((B, D), dtype=torch.float32, device=x.device) if out is None else out
+    _check(recblr_bdlru_scan_step(_ptr(x), _ptr(zr), _ptr(zi), _ptr(lam), _ptr(h_prev),
+                                  _ptr(h_next), B, D, io, _stream(stream)),
+           "recblr_bdlru_scan_step")
+    return h_next
+
+
+def bdlru_forward(x, Wr, br, Wi, bi, lam, h0=None, stream=None):
+    """Full forward with gate projections. Returns (h, hT)."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    for t, n in ((Wr, "Wr"), (Wi, "Wi")):
+        _io(t, (D, D), x.dtype, n)
+    for t, n in ((br, "br"), (bi, "bi")):
+        if t is not None:
+            _io(t, (D,), x.dtype, n)
+    _f32(lam, (D,), "lambda"), _f32(h0, (B, D), "h0")
+    h = torch.empty_like(x)
+    hT = torch.empty((B, D), dtype=torch.float32, device=x.device)
+    ws, nws = _workspace(OP_FORWARD, B, L, D, io, x.device)
+    _check(recblr_bdlru_forward(_ptr(x), _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam),
+                                _ptr(h0), _ptr(h), _ptr(hT), B, L, D, io, _ptr(ws), nws,
+                                _stream(stream)), "recblr_bdlru_forward")
+    return h, hT
+
+
+def bdlru_backward(x, Wr, br, Wi, bi, lam, h, dh, h0=None, dhT=None, stream=None):
+    """Full backward. Returns dict dx, dWr, dbr, dWi, dbi, dlambda, dh0."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    for t, n in ((Wr, "Wr"), (Wi, "Wi")):
+        _io(t, (D, D), x.dtype, n)
+    _io(h, x.shape, x.dtype, "h"), _io(dh, x.shape, x.dtype, "dh")
+    _f32(lam, (D,), "lambda"), _f32(h0, (B, D), "h0"), _f32(dhT, (B, D), "dhT")
+    f32 = dict(dtype=torch.float32, device=x.device)
+    out = {"dx": torch.empty_like(x), "dWr": torch.empty((D, D), **f32),
+           "dbr": torch.empty(D, **f32), "dWi": torch.empty((D, D), **f32),
+           "dbi": torch.empty(D, **f32), "dlambda": torch.empty(D, **f32),
+           "dh0": torch.empty((B, D), **f32)}
+    ws, nws = _workspace(OP_BACKWARD, B, L, D, io, x.device)
+    _check(recblr_bdlru_backward(
+        _ptr(x), _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam), _ptr(h0), _ptr(h), _ptr(dh),
+        _ptr(dhT), _ptr(out["dx"]), _ptr(out["dWr"]), _ptr(out["dbr"]), _ptr(out["dWi"]),
+        _ptr(out["dbi"]), _ptr(out["dlambda"]), _ptr(out["dh0"]), B, L, D, io, _ptr(ws), nws,
+        _stream(stream)), "recblr_bdlru_backward")
+    return out
+
+
+def bdlru_step(x, Wr, br, Wi, bi, lam, h_prev, out=None, stream=None):
+    """Full single step with gate projections; returns h_next (float32)."""
+    B, D = x.shape
+    io = io_code(x.dtype)
+    _f32(lam, (D,), "lambda"), _f32(h_prev, (B, D), "h_prev")
+    h_next = torch.empty((B, D), dtype=torch.float32, device=x.device) if out is None else out
+    ws, nws = _workspace(OP_STEP, B, 1, D, io, x.device)
+    _check(recblr_bdlru_step(_ptr(x), _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam),
+                             _ptr(h_prev), _ptr(h_next), B, D, io, _ptr(ws), nws,
+                             _stream(stream)), "recblr_bdlru_step")
+    return h_next
+
+
+def linear_scan_forward(a, u, h0=None, stream=None):
+    """Raw recurrence h_t = a_t h_{t-1} + u_t (float32). Returns (h, hT)."""
+    B, L, D = a.shape
+    h = torch.empty_like(a)
+    hT = torch.empty((B, D), dtype=torch.float32, device=a.device)
+    _check(recblr_linear_scan_forward(_ptr(a), _ptr(u), _ptr(h0), _ptr(h), _ptr(hT), B, L, D,
+                                      _stream(stream)), "recblr_linear_scan_forward")
+    return h, hT

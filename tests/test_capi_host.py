@@ -1,0 +1,140 @@
+"""Host-only checks of the C ABI (no GPU needed).
+
+The library must load and export every entry point include/recblr.h declares,
+and every validation error must be reported before anything reaches the GPU.
+Pointers here are fake addresses: every call below is rejected by host-side
+validation, so no HIP call is made.
+"""
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "recblr.h")
+
+
+@pytest.fixture(scope="module")
+def rb():
+    from paper_2406_12580_amd import recblr
+    return recblr
+
+
+def header_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(recblr_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    syms = header_symbols()
+    assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
+    assert len(syms) == 9
+
+
+def test_library_exports_every_declared_symbol(rb):
+    import ctypes
+    lib = ctypes.CDLL(rb.LIB_PATH)
+    for s in header_symbols():
+        assert hasattr(lib, s), s
+    assert set(header_symbols()) == set(rb.EXPORTS)
+
+
+def test_status_strings(rb):
+    for code in (0, -1, -2, -3, -4):
+        assert rb.recblr_status_string(code)
+    assert rb.recblr_status_string(99) == b"unknown status"
+
+
+def test_workspace_sizes(rb):
+    assert rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, 256, 2048, 128, rb.F32) == 0
+    bwd = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, 256, 2048, 128, rb.F32)
+    assert bwd >= 256 * 128 * 4
+    full = rb.recblr_workspace_size(rb.OP_FORWARD, 4, 50, 64, rb.BF16)
+    assert full >= 2 * 4 * 50 * 64 * 2
+    assert rb.recblr_workspace_size(rb.OP_STEP, 8, 123, 64, rb.F32) >= 2 * 8 * 64 * 4
+    assert rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, -1, 5, 5, rb.F32) == 0
+    assert rb.recblr_workspace_size(rb.OP_FORWARD, 1, 5, 5, 9) == 0
+    assert rb.recblr_workspace_size(17, 1, 5, 5, rb.F32) == 0
+
+
+A = 0x10000000  # fake, well aligned device addresses, 64 MiB apart
+def addr(k):
+    return A + k * (64 << 20)
+
+
+def scan_fwd(rb, x=addr(0), zr=addr(1), zi=addr(2), lam=addr(3), h0=None, h=addr(4), hT=addr(5),
+             B=2, L=3, D=4, io=0, ws=None, nws=0):
+    return rb.recblr_bdlru_scan_forward(x, zr, zi, lam, h0, h, hT, B, L, D, io, ws, nws, None)
+
+
+def test_scan_forward_validation(rb):
+    assert scan_fwd(rb, B=-1) == rb.ERR_INVALID_ARGUMENT
+    assert scan_fwd(rb, L=-5) == rb.ERR_INVALID_ARGUMENT
+    assert scan_fwd(rb, io=2) == rb.ERR_UNSUPPORTED
+    assert scan_fwd(rb, x=None) == rb.ERR_INVALID_ARGUMENT
+    assert scan_fwd(rb, lam=None) == rb.ERR_INVALID_ARGUMENT
+    assert scan_fwd(rb, zr=addr(1) + 2) == rb.ERR_INVALID_ARGUMENT          # misaligned f32
+    assert scan_fwd(rb, h=addr(0) + 8) == rb.ERR_INVALID_ARGUMENT            # h overlaps x
+    assert scan_fwd(rb, hT=addr(4) + 4) == rb.ERR_INVALID_ARGUMENT           # hT inside h
+    assert scan_fwd(rb, B=1 << 31) == rb.ERR_UNSUPPORTED
+    # empty problems are accepted without touching anything
+    assert scan_fwd(rb, B=0, x=None, zr=None, zi=None, lam=None, h=None) == rb.OK
+    assert scan_fwd(rb, D=0, x=None, zr=None, zi=None, lam=None, h=None) == rb.OK
+
+
+def test_scan_backward_validation(rb):
+    def call(**kw):
+        a = dict(x=addr(0), zr=addr(1), zi=addr(2), lam=addr(3), h0=None, h=addr(4),
+                 dh=addr(5), dhT=None, dx=addr(6), dzr=addr(7), dzi=addr(8), dlam=addr(9),
+                 dh0=None, B=2, L=3, D=4, io=0, ws=addr(10), nws=1 << 20)
+        a.update(kw)
+        return rb.recblr_bdlru_scan_backward(
+            a["x"], a["zr"], a["zi"], a["lam"], a["h0"], a["h"], a["dh"], a["dhT"], a["dx"],
+            a["dzr"], a["dzi"], a["dlam"], a["dh0"], a["B"], a["L"], a["D"], a["io"], a["ws"],
+            a["nws"], None)
+    assert call(dlam=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(dh=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(dzr=addr(6)) == rb.ERR_INVALID_ARGUMENT                     # dzr == dx
+    assert call(dx=addr(4)) == rb.ERR_INVALID_ARGUMENT                      # dx over h
+    assert call(ws=None) == rb.ERR_WORKSPACE
+    assert call(nws=16) == rb.ERR_WORKSPACE
+    assert call(ws=addr(10) + 64) == rb.ERR_WORKSPACE                       # not 256-aligned
+    assert call(io=5) == rb.ERR_UNSUPPORTED
+
+
+def test_step_validation(rb):
+    def call(h_prev=addr(4), h_next=addr(5), **kw):
+        a = dict(x=addr(0), zr=addr(1), zi=addr(2), lam=addr(3), B=8, D=16, io=1)
+        a.update(kw)
+        return rb.recblr_bdlru_scan_step(a["x"], a["zr"], a["zi"], a["lam"], h_prev, h_next,
+                                         a["B"], a["D"], a["io"], None)
+    assert call(h_next=addr(4) + 4) == rb.ERR_INVALID_ARGUMENT              # partial overlap
+    assert call(h_next=addr(0)) == rb.ERR_INVALID_ARGUMENT                  # over x
+    assert call(h_prev=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(x=addr(0) + 1) == rb.ERR_INVALID_ARGUMENT                   # misaligned bf16
+    assert call(io=3) == rb.ERR_UNSUPPORTED
+
+
+def test_full_api_validation(rb):
+    def fwd(**kw):
+        a = dict(x=addr(0), Wr=addr(1), br=None, Wi=addr(2), bi=None, lam=addr(3), h0=None,
+                 h=addr(4), hT=None, B=2, L=3, D=4, io=0, ws=addr(6), nws=1 << 20)
+        a.update(kw)
+        return rb.recblr_bdlru_forward(a["x"], a["Wr"], a["br"], a["Wi"], a["bi"], a["lam"],
+                                       a["h0"], a["h"], a["hT"], a["B"], a["L"], a["D"], a["io"],
+                                       a["ws"], a["nws"], None)
+    assert fwd(D=1025) == rb.ERR_UNSUPPORTED
+    assert fwd(Wr=None) == rb.ERR_INVALID_ARGUMENT
+    assert fwd(nws=8) == rb.ERR_WORKSPACE
+    assert fwd(ws=addr(4)) == rb.ERR_INVALID_ARGUMENT                      # ws over h
+    B, D = 3, 8
+    need = rb.recblr_workspace_size(rb.OP_STEP, B, 1, D, rb.F32)
+    assert rb.recblr_bdlru_step(addr(0), addr(1), None, addr(2), None, addr(3), addr(4), addr(5),
+                                B, D, rb.F32, addr(6), need - 1, None) == rb.ERR_WORKSPACE
+
+
+def test_linear_scan_validation(rb):
+    assert rb.recblr_linear_scan_forward(None, addr(1), None, addr(2), None, 2, 3, 4,
+                                         None) == rb.ERR_INVALID_ARGUMENT
+    assert rb.recblr_linear_scan_forward(addr(0), addr(1), None, addr(1), None, 2, 3, 4,
+                                         None) == rb.ERR_INVALID_ARGUMENT

@@ -1,0 +1,278 @@
+"""GPU parity of every librecblr.so entry point against the fp64 oracle.
+
+All inputs come from paper_2406_12580_amd.datagen (seeded); the GPU path is
+called through the C ABI (ctypes binding) and compared element by element with
+the oracle under the floored relative error of tests/helpers.py
+(1e-4 for fp32 I/O, 1e-2 for bf16 I/O).  Shapes cover several macro-chunks of
+the scan kernels with ragged tails, channel groups that span batch rows
+(D < 64 and D not a multiple of 64), L = 1, D = 1 and the degenerate L = 0 and
+B = 0 cases; the named workloads run at full size with sampled rows (and the
+full dLambda reduction).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import TOL, assert_close, dev, dev32, floored_rel_err, host
+from paper_2406_12580_amd import datagen as dg
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def rb():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2406_12580_amd import recblr
+    return recblr
+
+
+SHAPES = [(4, 50, 64), (3, 131, 48), (2, 1, 64), (1, 2, 1), (5, 257, 72), (2, 97, 3),
+          (3, 513, 130), (1, 64, 128)]
+
+
+def _run_fwd(rb, inp):
+    return rb.bdlru_scan_forward(dev(inp.x, inp.io), dev(inp.zr, inp.io), dev(inp.zi, inp.io),
+                                 dev32(inp.lam), dev32(inp.h0))
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_scan_forward(rb, shape, io):
+    B, L, D = shape
+    seed = 1000 + B * 7 + L * 13 + D
+    for with_h0 in (False, True):
+        inp = dg.scan_inputs(B, L, D, seed, io=io, h0=with_h0)
+        h, hT = _run_fwd(rb, inp)
+        oh, ohT = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+        print(f"scan_forward {shape} {io} h0={with_h0}", flush=True)
+        assert_close(host(h), oh, io, "h")
+        assert_close(host(hT), ohT, "f32", "hT")  # the fp32 state: fp32 bar for both I/O types
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_scan_backward(rb, shape, io):
+    B, L, D = shape
+    inp = dg.scan_inputs(B, L, D, 2000 + B + L + D, io=io, h0=True, grad=True, dhT=True)
+    X, ZR, ZI = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io)
+    lam, h0 = dev32(inp.lam), dev32(inp.h0)
+    h, _ = rb.bdlru_scan_forward(X, ZR, ZI, lam, h0)
+    got = rb.bdlru_scan_backward(X, ZR, ZI, lam, h, dev(inp.dh, io), h0, dev32(inp.dhT))
+    want = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh, inp.h0, inp.dhT)
+    print(f"scan_backward {shape} {io}", flush=True)
+    for k in ("dx", "dzr", "dzi", "dlambda"):
+        assert_close(host(got[k]), want[k], io, k)
+    assert_close(host(got["dh0"]), want["dh0"], "f32", "dh0")  # fp32 adjoint state
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_scan_variants(rb, io):
+    """SiLU-shaped x, nonzero h0, extreme decay bases and left-zero-padded rows."""
+    cases = [dict(silu_x=True, h0=True), dict(a_range=(0.5, 0.9)),
+             dict(a_range=(0.9999, 0.99999)), dict(pad_rows=True)]
+    for k, kw in enumerate(cases):
+        inp = dg.scan_inputs(6, 300, 64, 3000 + k, io=io, **kw)
+        h, hT = _run_fwd(rb, inp)
+        oh, ohT = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+        assert_close(host(h), oh, io, f"h {kw}")
+        if kw.get("pad_rows"):
+            lengths = inp.extra["lengths"]
+            hh = host(h)
+            for b in range(6):
+                assert np.all(hh[b, : 300 - lengths[b]] == 0.0)  # exact zeros before the row starts
+
+
+def test_alpha_to_zero_gives_gated_input(rb):
+    inp = dg.scan_inputs(3, 70, 64, 3100, h0=True)
+    inp.lam[:] = 1000.0
+    inp.zr[:] = 40.0
+    h, _ = _run_fwd(rb, inp)
+    i = 1.0 / (1.0 + np.exp(-inp.zi.astype(np.float64)))
+    assert_close(host(h), i * inp.x, "f32", "h")
+
+
+def test_linear_scan_closed_forms(rb):
+    import torch
+    rng = np.random.Generator(np.random.PCG64(3200))
+    B, L, D = 3, 333, 70
+    u = rng.standard_normal((B, L, D), dtype=np.float32)
+    h0 = rng.standard_normal((B, D), dtype=np.float32)
+    h, hT = rb.linear_scan_forward(dev32(np.zeros_like(u)), dev32(u), dev32(h0))
+    np.testing.assert_array_equal(host(h), u)                     # a = 0: h = u exactly
+    h, hT = rb.linear_scan_forward(dev32(np.ones_like(u)), dev32(u), dev32(h0))
+    want = h0[:, None, :].astype(np.float64) + np.cumsum(u.astype(np.float64), axis=1)
+    assert_close(host(h), want, "f32", "prefix sum")
+    a = np.broadcast_to(np.float32(0.9), (B, L, D)).copy()
+    c = np.full((B, L, D), 0.5, np.float32)
+    h, hT = rb.linear_scan_forward(dev32(a), dev32(c), dev32(h0))
+    t = np.arange(1, L + 1)[None, :, None]
+    aa = np.float64(np.float32(0.9))
+    want = aa ** t * h0[:, None, :] + 0.5 * (1 - aa ** t) / (1 - aa)
+    assert_close(host(h), want, "f32", "geometric")
+    a = rng.uniform(0, 1.1, (B, L, D)).astype(np.float32)
+    h, hT = rb.linear_scan_forward(dev32(a), dev32(u), dev32(h0))
+    oh, ohT = oracle.linear_scan(a, u, h0)
+    assert_close(host(h), oh, "f32", "raw")
+    assert_close(host(hT), ohT, "f32", "raw hT")
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("B,D", [(65, 256), (7, 3), (3, 2056), (33, 64)])
+def test_scan_step(rb, io, B, D):
+    inp = dg.step_inputs(B, D, 3300 + B + D, io=io)
+    got = rb.bdlru_scan_step(dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io), dev32(inp.lam),
+                             dev32(inp.h0))
+    want = oracle.scan_step(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(host(got), want, io, "h_next")
+    # in place: h_next aliases h_prev
+    hp = dev32(inp.h0)
+    rb.bdlru_scan_step(dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io), dev32(inp.lam), hp,
+                       out=hp)
+    assert_close(host(hp), want, io, "h_next in place")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_steps_equal_scan(rb, io):
+    inp = dg.scan_inputs(5, 40, 96, 3400, io=io, h0=True)
+    h, _ = _run_fwd(rb, inp)
+    import torch
+    state = dev32(inp.h0)
+    X, ZR, ZI = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io)
+    lam = dev32(inp.lam)
+    for t in range(40):
+        state = rb.bdlru_scan_step(X[:, t].contiguous(), ZR[:, t].contiguous(),
+                                   ZI[:, t].contiguous(), lam, state)
+    torch.cuda.synchronize()
+    oh, _ = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(host(state), oh[:, -1], io, "stepped state")
+
+
+def test_split_and_continue(rb):
+    inp = dg.scan_inputs(4, 700, 64, 3500, h0=True)
+    m = 333
+    X, ZR, ZI, lam = dev(inp.x), dev(inp.zr), dev(inp.zi), dev32(inp.lam)
+    h, hT = rb.bdlru_scan_forward(X, ZR, ZI, lam, dev32(inp.h0))
+    h1, hm = rb.bdlru_scan_forward(X[:, :m].contiguous(), ZR[:, :m].contiguous(),
+                                   ZI[:, :m].contiguous(), lam, dev32(inp.h0))
+    h2, hT2 = rb.bdlru_scan_forward(X[:, m:].contiguous(), ZR[:, m:].contiguous(),
+                                    ZI[:, m:].contiguous(), lam, hm)
+    oh, _ = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(np.concatenate([host(h1), host(h2)], axis=1), oh, "f32", "split")
+    assert floored_rel_err(host(hT2), host(hT)) <= 1e-5
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_empty_and_degenerate(rb, io):
+    import torch
+    inp = dg.scan_inputs(3, 0, 8, 3600, io=io, h0=True, grad=True, dhT=True)
+    h, hT = _run_fwd(rb, inp)
+    assert h.shape == (3, 0, 8)
+    np.testing.assert_array_equal(host(hT), inp.h0)                   # L = 0: hT = h0
+    X, ZR, ZI = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io)
+    got = rb.bdlru_scan_backward(X, ZR, ZI, dev32(inp.lam), dev(inp.x, io), dev(inp.x, io),
+                                 dev32(inp.h0), dev32(inp.dhT))
+    np.testing.assert_array_equal(host(got["dh0"]), inp.dhT)
+    np.testing.assert_array_equal(host(got["dlambda"]), 0.0)
+    # B = 0: nothing to compute; dLambda is an empty sum
+    inp0 = dg.scan_inputs(0, 5, 8, 3601, io=io, grad=True)
+    h, hT = _run_fwd(rb, inp0)
+    assert h.shape == (0, 5, 8)
+    X0 = dev(inp0.x, io)
+    got = rb.bdlru_scan_backward(X0, X0, X0, dev32(inp0.lam), X0, X0)
+    np.testing.assert_array_equal(host(got["dlambda"]), 0.0)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_deterministic(rb, io):
+    inp = dg.scan_inputs(16, 300, 64, 3700, io=io, h0=True, grad=True, dhT=True)
+    X, ZR, ZI, lam, h0 = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io), dev32(inp.lam), \
+        dev32(inp.h0)
+    outs = []
+    for _ in range(2):
+        h, hT = rb.bdlru_scan_forward(X, ZR, ZI, lam, h0)
+        g = rb.bdlru_scan_backward(X, ZR, ZI, lam, h, dev(inp.dh, io), h0, dev32(inp.dhT))
+        outs.append([host(h), host(hT)] + [host(g[k]) for k in sorted(g)])
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
+
+
+# ------------------------------------------------------------------ entry points with gate parameters
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 37, 64), (3, 70, 48), (1, 5, 130), (2, 130, 256)])
+def test_full_forward_backward(rb, shape, io):
+    B, L, D = shape
+    f = dg.full_inputs(B, L, D, 4000 + B + L + D, io=io, bias=True, h0=True, grad=True, dhT=True)
+    X, Wr, br, Wi, bi = (dev(a, io) for a in (f.x, f.Wr, f.br, f.Wi, f.bi))
+    lam, h0 = dev32(f.lam), dev32(f.h0)
+    h, hT = rb.bdlru_forward(X, Wr, br, Wi, bi, lam, h0)
+    oh, ohT = oracle.forward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    print(f"full {shape} {io}", flush=True)
+    assert_close(host(h), oh, io, "h")
+    assert_close(host(hT), ohT, io, "hT")
+    got = rb.bdlru_backward(X, Wr, br, Wi, bi, lam, h, dev(f.dh, io), h0, dev32(f.dhT))
+    want = oracle.backward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh, f.h0, f.dhT)
+    for k in ("dx", "dWr", "dbr", "dWi", "dbi", "dlambda", "dh0"):
+        assert_close(host(got[k]), want[k], io, k)
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_full_step(rb, io):
+    B, D = 50, 64
+    f = dg.full_inputs(B, 1, D, 4100, io=io, bias=True, h0=True)
+    x = f.x[:, 0]
+    got = rb.bdlru_step(dev(x, io), dev(f.Wr, io), dev(f.br, io), dev(f.Wi, io), dev(f.bi, io),
+                        dev32(f.lam), dev32(f.h0))
+    want = oracle.step(x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    assert_close(host(got), want, io, "h_next")
+
+
+def test_full_forward_without_bias(rb):
+    f = dg.full_inputs(2, 20, 64, 4200)
+    X, Wr, Wi = dev(f.x), dev(f.Wr), dev(f.Wi)
+    h, hT = rb.bdlru_forward(X, Wr, None, Wi, None, dev32(f.lam))
+    oh, _ = oracle.forward(f.x, f.Wr, None, f.Wi, None, f.lam)
+    assert_close(host(h), oh, "f32", "h")
+
+
+# ------------------------------------------------------------------ named workloads at full size
+
+def _sample_rows(B, k=3):
+    return sorted(set([0, B // 2, B - 1][:k]))
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_config_full_size(rb, name):
+    import torch
+    cfg = dg.CONFIGS[name]
+    inp = dg.config_inputs(cfg, grad=True)
+    io = cfg.io
+    X, ZR, ZI, lam = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io), dev32(inp.lam)
+    h, hT = rb.bdlru_scan_forward(X, ZR, ZI, lam)
+    g = rb.bdlru_scan_backward(X, ZR, ZI, lam, h, dev(inp.dh, io))
+    torch.cuda.synchronize()
+    print(f"config {name}: GPU done", flush=True)
+    rows = _sample_rows(cfg.B)
+    sub = lambda a: a[rows]
+    oh, ohT = oracle.scan_forward(sub(inp.x), sub(inp.zr), sub(inp.zi), inp.lam)
+    assert_close(host(h[rows]), oh, io, f"{name} h")
+    assert_close(host(hT[rows]), ohT, io, f"{name} hT")
+    ob = oracle.scan_backward(sub(inp.x), sub(inp.zr), sub(inp.zi), inp.lam, sub(inp.dh))
+    for k in ("dx", "dzr", "dzi", "dh0"):
+        assert_close(host(g[k][rows]), ob[k], io, f"{name} {k}")
+    # dLambda sums over every row: compare with the oracle over the whole batch.
+    full = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh)
+    assert_close(host(g["dlambda"]), full["dlambda"], io, f"{name} dlambda")
+
+
+def test_config_decode_full_size(rb):
+    cfg = dg.CONFIGS["c5dec"]
+    inp = dg.step_inputs(cfg.B, cfg.D, cfg.seed, io=cfg.io, a_range=cfg.a_range)
+    got = rb.bdlru_scan_step(dev(inp.x, cfg.io), dev(inp.zr, cfg.io), dev(inp.zi, cfg.io),
+                             dev32(inp.lam), dev32(inp.h0))
+    want = oracle.scan_step(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(host(got), want, cfg.io, "decode h_next")
