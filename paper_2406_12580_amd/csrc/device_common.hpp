@@ -48,14 +48,68 @@ __device__ __forceinline__ float load(const T* p) { return to_f32(*p); }
 // 32-bit offset the compiler emits the scalar-base + 32-bit-vector-offset
 // form of global_load/global_store, so one VGPR addresses every tensor that
 // shares the element offset (x, z_r, z_i, h, dh all do).
-template <typename T, typename Off>
-__device__ __forceinline__ float load_at(const T* p, Off off_bytes) {
-    return to_f32(*(const T*)((const char*)p + off_bytes));
+// ------------------------------------------------------------------ vector I/O
+// A lane owns VEC consecutive channels; their VEC elements of one time step
+// are one contiguous load or store of VEC * sizeof(T) bytes.  The sequence
+// tensors are streamed exactly once, so every access carries the
+// non-temporal hint.
+template <typename T, int VEC>
+struct VecT;
+template <> struct VecT<float, 1> { using type = float; };
+template <> struct VecT<float, 2> { using type = float __attribute__((ext_vector_type(2))); };
+template <> struct VecT<float, 4> { using type = float __attribute__((ext_vector_type(4))); };
+template <> struct VecT<bf16, 1> { using type = uint16_t; };
+template <> struct VecT<bf16, 2> { using type = uint32_t; };
+template <> struct VecT<bf16, 4> { using type = uint32_t __attribute__((ext_vector_type(2))); };
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+    return (uint32_t)from_f32<bf16>(lo).bits | ((uint32_t)from_f32<bf16>(hi).bits << 16);
 }
 
-template <typename T, typename Off>
-__device__ __forceinline__ void store_at(T* p, Off off_bytes, float v) {
-    *(T*)((char*)p + off_bytes) = from_f32<T>(v);
+template <typename T, int VEC, typename Off>
+__device__ __forceinline__ void load_vec(const T* p, Off off_bytes, float (&out)[VEC]) {
+    using V = typename VecT<T, VEC>::type;
+    V v = __builtin_nontemporal_load((const V*)((const char*)p + off_bytes));
+    if constexpr (sizeof(T) == 4) {
+        if constexpr (VEC == 1) out[0] = v;
+        else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) out[k] = v[k];
+        }
+    } else if constexpr (VEC == 1) {
+        out[0] = __uint_as_float((uint32_t)v << 16);
+    } else if constexpr (VEC == 2) {
+        out[0] = bf16_lo(v);
+        out[1] = bf16_hi(v);
+    } else {
+        out[0] = bf16_lo(v[0]);
+        out[1] = bf16_hi(v[0]);
+        out[2] = bf16_lo(v[1]);
+        out[3] = bf16_hi(v[1]);
+    }
+}
+
+template <typename T, int VEC, typename Off>
+__device__ __forceinline__ void store_vec(T* p, Off off_bytes, const float (&in)[VEC]) {
+    using V = typename VecT<T, VEC>::type;
+    V v;
+    if constexpr (sizeof(T) == 4) {
+        if constexpr (VEC == 1) v = in[0];
+        else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) v[k] = in[k];
+        }
+    } else if constexpr (VEC == 1) {
+        v = from_f32<bf16>(in[0]).bits;
+    } else if constexpr (VEC == 2) {
+        v = bf16_pair(in[0], in[1]);
+    } else {
+        v[0] = bf16_pair(in[0], in[1]);
+        v[1] = bf16_pair(in[2], in[3]);
+    }
+    __builtin_nontemporal_store(v, (V*)((char*)p + off_bytes));
 }
 
 template <typename T>

@@ -17,11 +17,14 @@
 // The paper gives no backward pass; these are the exact derivatives of its
 // forward equations.
 //
-// Decomposition mirrors the forward chain kernel: lane = channel, workgroup =
-// 64 channels x the whole sequence, W waves per macro-chunk of W*C steps,
-// macro-chunks visited from the end of the sequence to its start.
+// Decomposition mirrors the forward kernels (lane = VEC channels, W waves per
+// macro-chunk of W*C steps): the chain kernel walks the macro-chunks from the
+// end of the sequence to its start; the look-back kernel hands out tiles from
+// the end too, so that tile index r in processing order is macro-chunk
+// nseg-1-r and the forward look-back code applies unchanged.
 #include "device_common.hpp"
 #include "launch.hpp"
+#include "lookback.hpp"
 
 namespace recblr {
 
@@ -33,225 +36,383 @@ inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // Rows of the per-channel dLambda partials are reduced in blocks of this many.
 constexpr int kReduceRows = 64;
 
-struct BwdWorkspace {
-    unsigned* counter;  // arrival counter of the reduction's last-block step
-    float* partial;     // [rows][D] per-channel sums of dLoss/dq * r
-    double* partial2;   // [ceil(rows / kReduceRows)][D]
-};
-
-inline size_t bwd_ws_bytes(int64_t rows, int64_t D) {
-    int64_t nb = (rows + kReduceRows - 1) / kReduceRows;
-    return kAlign + align_up((size_t)(rows * D) * sizeof(float)) +
-           align_up((size_t)(nb * D) * sizeof(double));
-}
-
-inline BwdWorkspace bwd_ws_carve(void* ws, int64_t rows, int64_t D) {
-    char* p = (char*)ws;
-    BwdWorkspace w;
-    w.counter = (unsigned*)p;
-    p += kAlign;
-    w.partial = (float*)p;
-    p += align_up((size_t)(rows * D) * sizeof(float));
-    w.partial2 = (double*)p;
-    return w;
-}
-
 }  // namespace
 
-template <typename T, typename TZ, int C, typename Off>
-struct BwdRegs {
-    float g[C], x[C], zr[C], zi[C], hp[C];
-    float zr_after;  // z_r of the step just after this wave's chunk
+struct BwdParams {
+    const void* x;
+    const void* zr;
+    const void* zi;
+    const float* lam;
+    const float* h0;
+    const void* h;
+    const void* dh;
+    const float* dhT;
+    void* dx;
+    void* dzr;
+    void* dzi;
+    float* dh0;
+    float* partial;  // [nseg][B*D] per-tile sums of dLoss/dq * r
+    int64_t L, D, nch;
+    int64_t ngroups, nseg;
+    LookbackWs lb;
+};
 
-    // Loads steps [t_first, t_first + C) (clamped to L-1; the caller masks) and
-    // h_{t-1} for each of them (h0 at t = 0).
-    __device__ __forceinline__ void fetch(const T* __restrict__ G, const T* __restrict__ X,
-                                          const TZ* __restrict__ ZR, const TZ* __restrict__ ZI,
-                                          const T* __restrict__ H, float h0v, Off base, Off row,
-                                          int64_t t_first, int64_t L) {
+template <typename TX, int VEC, typename Off>
+struct BwdLane {
+    bool valid;
+    int64_t c0, d0;
+    Off base, row;
+    __device__ __forceinline__ void init(int64_t group, int lane, int64_t L, int64_t D,
+                                         int64_t nch) {
+        const int64_t c = (group * kWave + lane) * VEC;
+        valid = c < nch;
+        c0 = valid ? c : 0;  // idle lanes shadow channel 0 and store nothing
+        const int64_t b = c0 / D;
+        d0 = c0 - b * D;
+        base = (Off)((b * L * D + d0) * (int64_t)sizeof(TX));
+        row = (Off)(D * (int64_t)sizeof(TX));
+    }
+    __device__ __forceinline__ Off at(int64_t t) const { return base + (Off)t * row; }
+};
+
+// Raw inputs of C steps (clamped to L-1; masked later), h_{t-1} for each of
+// them (h0 at t = 0) and z_r of the step right after the chunk.
+template <typename TX, typename TZ, int C, int VEC, typename Off>
+struct BwdIn {
+    float g[C][VEC], x[C][VEC], zr[C][VEC], zi[C][VEC], hp[C][VEC];
+    float zr_after[VEC];
+
+    __device__ __forceinline__ void fetch(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
+                                          const float (&h0v)[VEC], int64_t t_first) {
 #pragma unroll
         for (int j = 0; j < C; ++j) {
-            int64_t t = t_first + j < L ? t_first + j : L - 1;
-            Off off = base + (Off)t * row;
-            g[j] = load_at(G, off);
-            x[j] = load_at(X, off);
-            zr[j] = load_at(ZR, z_offset<T, TZ>(off));
-            zi[j] = load_at(ZI, z_offset<T, TZ>(off));
-            float hv = load_at(H, t > 0 ? off - row : off);
-            hp[j] = t > 0 ? hv : h0v;
+            const int64_t t = t_first + j < P.L ? t_first + j : P.L - 1;
+            const Off off = ln.at(t);
+            load_vec<TX, VEC>((const TX*)P.dh, off, g[j]);
+            load_vec<TX, VEC>((const TX*)P.x, off, x[j]);
+            load_vec<TZ, VEC>((const TZ*)P.zr, z_offset<TX, TZ>(off), zr[j]);
+            load_vec<TZ, VEC>((const TZ*)P.zi, z_offset<TX, TZ>(off), zi[j]);
+            load_vec<TX, VEC>((const TX*)P.h, t > 0 ? off - ln.row : off, hp[j]);
+            if (t == 0) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) hp[j][k] = h0v[k];
+            }
         }
-        int64_t ta = t_first + C < L ? t_first + C : L - 1;
-        zr_after = load_at(ZR, z_offset<T, TZ>(base + (Off)ta * row));
+        const int64_t ta = t_first + C < P.L ? t_first + C : P.L - 1;
+        load_vec<TZ, VEC>((const TZ*)P.zr, z_offset<TX, TZ>(ln.at(ta)), zr_after);
     }
 };
 
-template <typename T, typename TZ, int W, int C, typename Off>
-__global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(
-    const T* __restrict__ X, const TZ* __restrict__ ZR, const TZ* __restrict__ ZI,
-    const float* __restrict__ lam, const float* __restrict__ h0, const T* __restrict__ H,
-    const T* __restrict__ G, const float* __restrict__ dhT, T* __restrict__ DX,
-    TZ* __restrict__ DZR, TZ* __restrict__ DZI, float* __restrict__ dh0,
-    float* __restrict__ partial, unsigned* __restrict__ counter, int64_t L, int64_t D,
-    int64_t nch) {
-    __shared__ Seg agg[2][W][kWave];
-    __shared__ float red[W][kWave];
-    if (blockIdx.x == 0 && threadIdx.x == 0) *counter = 0u;  // consumed by the reduction
+// Per-step pieces of the reverse recurrence: r_t, alpha_t, and the pair
+// (alpha_{t+1}, G_t) (identity (1, 0) past the end; alpha_{L+1} = 0).
+template <int C, int VEC>
+struct BwdSteps {
+    float r[C][VEC], al[C][VEC], ap[C][VEC], gg[C][VEC];
+};
 
+template <typename TX, typename TZ, int C, int VEC, typename Off>
+__device__ __forceinline__ void form_bwd(const BwdIn<TX, TZ, C, VEC, Off>& in,
+                                         const ChannelConst (&cc)[VEC], const float (&dhTv)[VEC],
+                                         int64_t t_first, int64_t L, BwdSteps<C, VEC>& st) {
+#pragma unroll
+    for (int j = 0; j < C; ++j)
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            st.r[j][k] = sigmoid(in.zr[j][k]);
+            st.al[j][k] = fast_exp2(st.r[j][k] * cc[k].neg_s_l2);
+        }
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        const int64_t t = t_first + j;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            float nxt = j + 1 < C ? st.al[j + 1 < C ? j + 1 : j][k]
+                                  : fast_exp2(sigmoid(in.zr_after[k]) * cc[k].neg_s_l2);
+            if (t + 1 >= L) nxt = 0.0f;
+            const float gj = in.g[j][k] + (t == L - 1 ? dhTv[k] : 0.0f);
+            st.ap[j][k] = t < L ? nxt : 1.0f;
+            st.gg[j][k] = t < L ? gj : 0.0f;
+        }
+    }
+}
+
+template <int C, int VEC>
+__device__ __forceinline__ void local_reverse(const BwdSteps<C, VEC>& st, Seg (&s)[VEC]) {
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        s[k] = Seg{1.0f, 0.0f};
+#pragma unroll
+        for (int j = C - 1; j >= 0; --j) s[k] = compose(Seg{st.ap[j][k], st.gg[j][k]}, s[k]);
+    }
+}
+
+// Run the chunk backwards from delta (the adjoint right after the chunk) and
+// apply the gate-gradient epilogue to every step before L.
+template <typename TX, typename TZ, int C, int VEC, typename Off>
+__device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
+                                         const BwdIn<TX, TZ, C, VEC, Off>& in,
+                                         const BwdSteps<C, VEC>& st,
+                                         const ChannelConst (&cc)[VEC], int64_t t_first,
+                                         float (&delta)[VEC], float (&dsum)[VEC]) {
+#pragma unroll
+    for (int j = C - 1; j >= 0; --j) {
+        const int64_t t = t_first + j;
+        float dxv[VEC], dzrv[VEC], dziv[VEC];
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            delta[k] = fmaf(st.ap[j][k], delta[k], st.gg[j][k]);
+            const float r = st.r[j][k], al = st.al[j][k];
+            const float i = sigmoid(in.zi[j][k]);
+            const float q = r * cc[k].s;
+            const float mm = one_minus_exp_neg(r * cc[k].two_s, al);
+            const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
+            const float sq = mm * rs;  // sqrt(1 - alpha^2)
+            const float g_alpha = delta[k] * in.hp[j][k];
+            const float g_beta = delta[k] * in.x[j][k];
+            const float g1 = -al * g_alpha;
+            const float g2 = g_beta * i * al * al;
+            if (t < P.L) dsum[k] = fmaf(g1, r, fmaf(g2, r * rs, dsum[k]));
+            dxv[k] = delta[k] * sq * i;
+            dzrv[k] = fmaf(g1, q, g2 * (q * rs)) * (1.0f - r);
+            dziv[k] = g_beta * sq * i * (1.0f - i);
+        }
+        if (ln.valid && t < P.L) {
+            const Off off = ln.at(t);
+            store_vec<TX, VEC>((TX*)P.dx, off, dxv);
+            store_vec<TZ, VEC>((TZ*)P.dzr, z_offset<TX, TZ>(off), dzrv);
+            store_vec<TZ, VEC>((TZ*)P.dzi, z_offset<TX, TZ>(off), dziv);
+            if (t == 0 && P.dh0) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) P.dh0[ln.c0 + k] = st.al[j][k] * delta[k];
+            }
+        }
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void bwd_lane_consts(const BwdParams& P, int64_t c0, int64_t d0,
+                                                ChannelConst (&cc)[VEC], float (&h0v)[VEC],
+                                                float (&dhTv)[VEC]) {
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        cc[k] = channel_const(P.lam[d0 + k]);
+        h0v[k] = P.h0 ? P.h0[c0 + k] : 0.0f;
+        dhTv[k] = P.dhT ? P.dhT[c0 + k] : 0.0f;
+    }
+}
+
+// Sum the waves' dLambda partials of this workgroup in a fixed order.
+template <int W, int VEC>
+__device__ __forceinline__ void write_partial(float (&red)[W][kWave][VEC],
+                                              const float (&dsum)[VEC], float* out, bool valid,
+                                              int w, int lane) {
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) red[w][lane][k] = dsum[k];
+    __syncthreads();
+    if (w == 0 && valid) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int q = 0; q < W; ++q) acc += red[q][lane][k];
+            out[k] = acc;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ chain kernel
+template <typename TX, typename TZ, int W, int C, int VEC, typename Off>
+__global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(BwdParams P) {
+    __shared__ Seg agg[2][W][kWave][VEC];
+    __shared__ float red[W][kWave][VEC];
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
-    const int64_t c = (int64_t)blockIdx.x * kWave + lane;
-    const bool valid = c < nch;
-    const int64_t cs = valid ? c : 0;  // idle lanes shadow channel 0 and store nothing
-    const int64_t b = cs / D;
-    const int64_t d = cs - b * D;
-    const Off base = (Off)((b * L * D + d) * (int64_t)sizeof(T));
-    const Off row = (Off)(D * (int64_t)sizeof(T));
-    const ChannelConst cc = channel_const(lam[d]);
-    const float h0v = h0 ? h0[cs] : 0.0f;
-    const float dhTv = dhT ? dhT[cs] : 0.0f;
+    BwdLane<TX, VEC, Off> ln;
+    ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
+    ChannelConst cc[VEC];
+    float h0v[VEC], dhTv[VEC], carry[VEC], dsum[VEC];
+    bwd_lane_consts<VEC>(P, ln.c0, ln.d0, cc, h0v, dhTv);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) carry[k] = dsum[k] = 0.0f;
 
     constexpr int64_t kMacro = (int64_t)W * C;
-    const int64_t nmacro = (L + kMacro - 1) / kMacro;
-    float carry = 0.0f;   // delta flowing in from later steps
-    float dsum = 0.0f;    // sum of dLoss/dq * r over this lane's steps
-
-    BwdRegs<T, TZ, C, Off> cur, nxt;
-    if (nmacro > 0)
-        cur.fetch(G, X, ZR, ZI, H, h0v, base, row, (nmacro - 1) * kMacro + (int64_t)w * C, L);
+    const int64_t nmacro = (P.L + kMacro - 1) / kMacro;
+    BwdIn<TX, TZ, C, VEC, Off> cur, nxt;
+    if (nmacro > 0) cur.fetch(P, ln, h0v, (nmacro - 1) * kMacro + (int64_t)w * C);
     int buf = 0;
     for (int64_t m = nmacro - 1; m >= 0; --m, buf ^= 1) {
         const int64_t tw = m * kMacro + (int64_t)w * C;
-        if (m > 0) nxt.fetch(G, X, ZR, ZI, H, h0v, base, row, tw - kMacro, L);
-
-        // alpha_t and r_t of this chunk; alpha of the step after it.
-        float r[C], al[C], ap[C], gg[C];
+        if (m > 0) nxt.fetch(P, ln, h0v, tw - kMacro);
+        BwdSteps<C, VEC> st;
+        form_bwd(cur, cc, dhTv, tw, P.L, st);
+        Seg s[VEC];
+        local_reverse(st, s);
 #pragma unroll
-        for (int j = 0; j < C; ++j) {
-            r[j] = sigmoid(cur.zr[j]);
-            al[j] = fast_exp2(r[j] * cc.neg_s_l2);
-        }
-        const float al_after = fast_exp2(sigmoid(cur.zr_after) * cc.neg_s_l2);
-#pragma unroll
-        for (int j = 0; j < C; ++j) {
-            const int64_t t = tw + j;
-            const bool ok = t < L;
-            float nxt_alpha = (j + 1 < C) ? al[j + 1 < C ? j + 1 : j] : al_after;
-            if (t + 1 >= L) nxt_alpha = 0.0f;    // delta_{L+1} = 0
-            const float gj = cur.g[j] + (t == L - 1 ? dhTv : 0.0f);
-            ap[j] = ok ? nxt_alpha : 1.0f;       // steps past the end are the identity (1, 0)
-            gg[j] = ok ? gj : 0.0f;
-        }
-        // Local aggregate of the reverse recurrence over this wave's chunk.
-        Seg s{1.0f, 0.0f};
-#pragma unroll
-        for (int j = C - 1; j >= 0; --j) s = compose(Seg{ap[j], gg[j]}, s);
-        agg[buf][w][lane] = s;
+        for (int k = 0; k < VEC; ++k) agg[buf][w][lane][k] = s[k];
         __syncthreads();
-
-        // Carry into this wave: fold the later waves, last one first.
-        float cin = carry;
+        // Carry into this wave: the later waves, last one first.
+        float delta[VEC], cout[VEC];
 #pragma unroll
-        for (int k = W - 1; k >= 0; --k) {
-            if (k > w) {
-                Seg e = agg[buf][k][lane];
-                cin = fmaf(e.A, cin, e.H);
-            }
-        }
-        // Re-run the chunk backwards from the true carry; gate-gradient epilogue.
-        float delta = cin;
+        for (int k = 0; k < VEC; ++k) delta[k] = carry[k];
 #pragma unroll
-        for (int j = C - 1; j >= 0; --j) {
-            delta = fmaf(ap[j], delta, gg[j]);
-            const int64_t t = tw + j;
-            if (t < L) {
-                const float i = sigmoid(cur.zi[j]);
-                const float q = r[j] * cc.s;
-                const float mm = one_minus_exp_neg(r[j] * cc.two_s, al[j]);
-                const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
-                const float sq = mm * rs;  // sqrt(1 - alpha^2)
-                const float g_alpha = delta * cur.hp[j];
-                const float g_beta = delta * cur.x[j];
-                const float g1 = -al[j] * g_alpha;
-                const float g2 = g_beta * i * al[j] * al[j];
-                dsum = fmaf(g1, r[j], fmaf(g2, r[j] * rs, dsum));
-                if (valid) {
-                    const Off off = base + (Off)t * row;
-                    store_at(DX, off, delta * sq * i);
-                    const Off zoff = z_offset<T, TZ>(off);
-                    store_at(DZR, zoff, fmaf(g1, q, g2 * (q * rs)) * (1.0f - r[j]));
-                    store_at(DZI, zoff, g_beta * sq * i * (1.0f - i));
-                    if (t == 0 && dh0) dh0[cs] = al[j] * delta;
+        for (int q = W - 1; q >= 0; --q) {
+            if (q > w) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const Seg e = agg[buf][q][lane][k];
+                    delta[k] = fmaf(e.A, delta[k], e.H);
                 }
             }
         }
-        // Carry out of the macro-chunk (towards earlier steps).
-        float cout = cin;
 #pragma unroll
-        for (int k = W - 1; k >= 0; --k) {
-            if (k <= w) {
-                Seg e = agg[buf][k][lane];
-                cout = fmaf(e.A, cout, e.H);
+        for (int k = 0; k < VEC; ++k) cout[k] = delta[k];
+        emit_bwd(P, ln, cur, st, cc, tw, delta, dsum);
+        // Carry out of the macro-chunk, towards earlier steps.
+#pragma unroll
+        for (int q = W - 1; q >= 0; --q) {
+            if (q <= w) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const Seg e = agg[buf][q][lane][k];
+                    cout[k] = fmaf(e.A, cout[k], e.H);
+                }
             }
         }
-        carry = cout;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
         cur = nxt;
     }
-    if (L == 0 && w == 0 && valid && dh0) dh0[cs] = dhTv;
-
-    // Per-channel partial of dLoss/dLambda: waves combined in a fixed order.
-    red[w][lane] = dsum;
-    __syncthreads();
-    if (w == 0 && valid) {
-        float acc = 0.0f;
+    if (P.L == 0 && w == 0 && ln.valid && P.dh0) {
 #pragma unroll
-        for (int k = 0; k < W; ++k) acc += red[k][lane];
-        partial[cs] = acc;
+        for (int k = 0; k < VEC; ++k) P.dh0[ln.c0 + k] = dhTv[k];
     }
+    write_partial<W, VEC>(red, dsum, P.partial + ln.c0, ln.valid, w, lane);
 }
 
-// dLambda[d] = sigmoid(Lambda_d) * sum_rows partial[row][d], in double, in a
-// fixed order.  Block (nb, dg) sums rows [nb*64, nb*64 + 64) of channels
-// [dg*64, dg*64 + 64); the last block to arrive adds the block sums in
-// row-block order.
-__global__ __launch_bounds__(256) void dlambda_reduce_kernel(
-    const float* __restrict__ partial, double* __restrict__ partial2, unsigned* counter,
-    const float* __restrict__ lam, float* __restrict__ dlambda, int64_t rows, int64_t D) {
+// ------------------------------------------------------------------ look-back kernel
+template <typename TX, typename TZ, int W, int C, int VEC, int K, typename Off>
+__global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P) {
+    __shared__ Seg agg[W][kWave][VEC];
+    __shared__ uint64_t win_sh[W * K][kWave][VEC];
+    __shared__ float carry_sh[kWave][VEC];
+    __shared__ float red[W][kWave][VEC];
+    __shared__ int64_t tile_sh;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    if (threadIdx.x == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
+    __syncthreads();
+    const int64_t tile = tile_sh;
+    if (tile >= P.ngroups * P.nseg) return;  // only if the workspace was shared by two calls
+    const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
+    const int64_t g = tile - r * P.ngroups;
+    const int64_t s = P.nseg - 1 - r;    // macro-chunk of this tile
+
+    BwdLane<TX, VEC, Off> ln;
+    ln.init(g, lane, P.L, P.D, P.nch);
+    ChannelConst cc[VEC];
+    float h0v[VEC], dhTv[VEC], dsum[VEC], zero[VEC];
+    bwd_lane_consts<VEC>(P, ln.c0, ln.d0, cc, h0v, dhTv);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) dsum[k] = zero[k] = 0.0f;
+
+    const int64_t tw = s * W * C + (int64_t)w * C;
+    BwdIn<TX, TZ, C, VEC, Off> in;
+    in.fetch(P, ln, h0v, tw);
+    BwdSteps<C, VEC> st;
+    form_bwd(in, cc, dhTv, tw, P.L, st);
+    {
+        Seg sg[VEC];
+        local_reverse(st, sg);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) agg[w][lane][k] = sg[k];
+    }
+    __syncthreads();
+    // pre: the waves after this one (applied first); tot: the whole tile.
+    Seg pre[VEC], tot[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) pre[k] = tot[k] = Seg{1.0f, 0.0f};
+#pragma unroll
+    for (int q = W - 1; q >= 0; --q) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            const Seg e = agg[q][lane][k];
+            if (q > w) pre[k] = compose(e, pre[k]);
+            tot[k] = compose(e, tot[k]);
+        }
+    }
+    __syncthreads();  // agg is reused below
+
+    uint64_t* const own = P.lb.states + r * P.nch + ln.c0;
+    if (r == 0) {
+        if (w == 0) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                carry_sh[lane][k] = 0.0f;
+                if (ln.valid) publish(own + k, pack_inclusive(tot[k].H));
+            }
+        }
+    } else {
+        if (w == 0 && ln.valid) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) publish(own + k, pack_aggregate(tot[k]));
+        }
+        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, r, zero, win_sh, carry_sh, w, lane);
+        if (w == 0 && ln.valid) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+                publish(own + k, pack_inclusive(fmaf(tot[k].A, carry_sh[lane][k], tot[k].H)));
+        }
+    }
+    __syncthreads();
+    float delta[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) delta[k] = fmaf(pre[k].A, carry_sh[lane][k], pre[k].H);
+    emit_bwd(P, ln, in, st, cc, tw, delta, dsum);
+    write_partial<W, VEC>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
+}
+
+// ------------------------------------------------------------------ dLambda reduction
+// dLambda[d] = sigmoid(Lambda_d) * sum_rows partial[row][d], in double and in a
+// fixed order, in two fence-free launches: block (nb, dg) of the first sums
+// rows [nb*64, nb*64 + 64) of channels [dg*64, dg*64 + 64) into partial2[nb];
+// the second adds the row blocks in order.  (A single launch with a
+// last-block-done counter would need an agent-scope release fence, which on
+// this GPU writes back every dirty line of the L2 right after the scan has
+// filled it with outputs.)
+__global__ __launch_bounds__(256) void dlambda_rows_kernel(const float* __restrict__ partial,
+                                                           double* __restrict__ partial2,
+                                                           int64_t rows, int64_t D) {
     __shared__ double red[4][kWave];
-    __shared__ bool last;
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
     const int64_t d = (int64_t)blockIdx.y * kWave + lane;
     const int64_t nb = blockIdx.x;
     double acc = 0.0;
     if (d < D) {
-        int64_t r0 = nb * kReduceRows + w * (kReduceRows / 4);
+        const int64_t r0 = nb * kReduceRows + w * (kReduceRows / 4);
 #pragma unroll
         for (int k = 0; k < kReduceRows / 4; ++k) {
-            int64_t row = r0 + k;
+            const int64_t row = r0 + k;
             if (row < rows) acc += (double)partial[row * D + d];
         }
     }
     red[w][lane] = acc;
     __syncthreads();
-    if (w == 0 && d < D) partial2[nb * D + d] = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned total = gridDim.x * gridDim.y;
-        last = atomicAdd(counter, 1u) == total - 1;
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    const int64_t nblk = gridDim.x;
-    for (int64_t dd = threadIdx.x; dd < D; dd += blockDim.x) {
-        double s = 0.0;
-        for (int64_t k = 0; k < nblk; ++k) s += partial2[k * D + dd];
-        double lv = (double)lam[dd];
-        double sig = 1.0 / (1.0 + exp(-lv));
-        dlambda[dd] = (float)(sig * s);
-    }
-    if (threadIdx.x == 0) *counter = 0u;
+    if (w == 0 && d < D)
+        partial2[nb * D + d] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+__global__ __launch_bounds__(256) void dlambda_final_kernel(const double* __restrict__ partial2,
+                                                            int64_t nblk,
+                                                            const float* __restrict__ lam,
+                                                            float* __restrict__ dlambda,
+                                                            int64_t D) {
+    const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (d >= D) return;
+    double s = 0.0;
+    for (int64_t k = 0; k < nblk; ++k) s += partial2[k * D + d];
+    const double lv = (double)lam[d];
+    dlambda[d] = (float)(s / (1.0 + exp(-lv)));
 }
 
 __global__ void fill_kernel(float* __restrict__ dst, float v, int64_t n) {
@@ -266,39 +427,166 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
     return hipGetLastError();
 }
 
-size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType) {
-    (void)L;
-    return bwd_ws_bytes(B, D);
+// ------------------------------------------------------------------ launch plan
+// Tile shapes: W waves per workgroup and E elements per lane per macro-chunk
+// (C = E / VEC steps per wave), so a wave moves the same bytes per
+// macro-chunk whatever VEC is.
+#ifndef RECBLR_BWD_CHAIN_W
+#define RECBLR_BWD_CHAIN_W 16
+#endif
+#ifndef RECBLR_BWD_CHAIN_E
+#define RECBLR_BWD_CHAIN_E 4
+#endif
+#ifndef RECBLR_BWD_LB_W
+#define RECBLR_BWD_LB_W 8
+#endif
+#ifndef RECBLR_BWD_LB_E
+#define RECBLR_BWD_LB_E 8
+#endif
+// Channels per lane at most, per kernel (measured best on MI355X).
+#ifndef RECBLR_BWD_CHAIN_MAX_VEC
+#define RECBLR_BWD_CHAIN_MAX_VEC 1
+#endif
+#ifndef RECBLR_BWD_LB_MAX_VEC
+#define RECBLR_BWD_LB_MAX_VEC 1
+#endif
+constexpr int kChainW = RECBLR_BWD_CHAIN_W, kChainE = RECBLR_BWD_CHAIN_E;
+constexpr int kLbW = RECBLR_BWD_LB_W, kLbE = RECBLR_BWD_LB_E;
+// Look-back window per wave: K tiles, K * VEC = 8 state words per lane.
+template <int VEC>
+constexpr int lb_window() { return 8 / VEC; }
+template <int E, int VEC>
+constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
+// Steps of one look-back tile for a given VEC.
+constexpr int64_t lb_tile_steps(int vec) { return (int64_t)kLbW * (kLbE / vec > 0 ? kLbE / vec : 1); }
+// The chain kernel is used when its workgroups alone fill the GPU (one
+// workgroup per compute unit at least); lanes then take as many channels as
+// keep that many workgroups.
+constexpr int64_t kChainMinGroups = 256;
+// Largest channels-per-lane of a kernel for an element size (8-byte accesses
+// per lane at most).
+constexpr int max_vec(size_t esz, bool lookback, int64_t nch = INT64_MAX) {
+    const int cap = lookback ? RECBLR_BWD_LB_MAX_VEC : RECBLR_BWD_CHAIN_MAX_VEC;
+    int v = (int)(8 / esz) < cap ? (int)(8 / esz) : cap;
+    while (v > 1 && !lookback && nch / (kWave * v) < kChainMinGroups) v /= 2;
+    return v;
 }
 
-template <typename T, typename TZ, int W, int C>
-static hipError_t launch_bwd_chain(const ScanBwdArgs& a, hipStream_t stream) {
-    const int64_t nch = a.B * a.D;
-    BwdWorkspace ws = bwd_ws_carve(a.ws, a.B, a.D);
-    dim3 grid((unsigned)((nch + kWave - 1) / kWave));
-    if ((uint64_t)(nch * a.L) * sizeof(TZ) < (1ull << 32))
-        hipLaunchKernelGGL((scan_bwd_chain_kernel<T, TZ, W, C, uint32_t>), grid, dim3(W * kWave),
-                           0, stream, (const T*)a.x, (const TZ*)a.zr, (const TZ*)a.zi, a.lambda,
-                           a.h0, (const T*)a.h, (const T*)a.dh, a.dhT, (T*)a.dx, (TZ*)a.dzr,
-                           (TZ*)a.dzi, a.dh0, ws.partial, ws.counter, a.L, a.D, nch);
-    else
-        hipLaunchKernelGGL((scan_bwd_chain_kernel<T, TZ, W, C, uint64_t>), grid, dim3(W * kWave),
-                           0, stream, (const T*)a.x, (const TZ*)a.zr, (const TZ*)a.zi, a.lambda,
-                           a.h0, (const T*)a.h, (const T*)a.dh, a.dhT, (T*)a.dx, (TZ*)a.dzr,
-                           (TZ*)a.dzi, a.dh0, ws.partial, ws.counter, a.L, a.D, nch);
-    hipError_t e = hipGetLastError();
+struct BwdPlan {
+    bool lookback;
+    int vec;
+    int64_t ngroups, nseg;
+};
+
+// The mode depends only on (B, L, D); the tile count also on VEC (see the
+// forward launcher).
+static bool backward_uses_lookback(int64_t B, int64_t L, int64_t D, size_t esz) {
+    const int64_t groups_one = (B * D + kWave - 1) / kWave;
+    return groups_one < kChainMinGroups && L > lb_tile_steps(max_vec(esz, true));
+}
+
+static BwdPlan plan_backward(int64_t B, int64_t L, int64_t D, size_t esz, int vec) {
+    BwdPlan p;
+    p.vec = vec;
+    p.lookback = backward_uses_lookback(B, L, D, esz);
+    p.ngroups = (B * D / vec + kWave - 1) / kWave;
+    p.nseg = p.lookback ? (L + lb_tile_steps(vec) - 1) / lb_tile_steps(vec) : 1;
+    return p;
+}
+
+static int pick_vec_bwd(const ScanBwdArgs& a) {
+    const size_t esz = io_bytes(a.io), zsz = io_bytes(a.zio);
+    const uintptr_t xm = (uintptr_t)a.x | (uintptr_t)a.h | (uintptr_t)a.dh | (uintptr_t)a.dx;
+    const uintptr_t zm = (uintptr_t)a.zr | (uintptr_t)a.zi | (uintptr_t)a.dzr | (uintptr_t)a.dzi;
+    const uintptr_t sm = (uintptr_t)a.h0 | (uintptr_t)a.dhT | (uintptr_t)a.dh0;
+    for (int v = max_vec(esz, backward_uses_lookback(a.B, a.L, a.D, esz), a.B * a.D); v > 1;
+         v /= 2)
+        if (a.D % v == 0 && xm % (v * esz) == 0 && zm % (v * zsz) == 0 && sm % (v * 4) == 0)
+            return v;
+    return 1;
+}
+
+// Workspace: [look-back states][dLambda partials (nseg rows of B*D)][row-block sums].
+struct BwdLayout {
+    size_t lb, partial, partial2, total;
+};
+
+static BwdLayout bwd_layout(int64_t B, int64_t D, const BwdPlan& p) {
+    BwdLayout l;
+    const int64_t rows = p.nseg * B;
+    const int64_t nb = (rows + kReduceRows - 1) / kReduceRows;
+    l.lb = 0;
+    l.partial = p.lookback ? align_up(lookback_ws_bytes(p.nseg, B * D)) : 0;
+    l.partial2 = l.partial + align_up((size_t)(rows * D) * sizeof(float));
+    l.total = l.partial2 + align_up((size_t)(nb * D) * sizeof(double));
+    return l;
+}
+
+size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
+    const size_t esz = io_bytes(io);
+    const bool lb = backward_uses_lookback(B, L, D, esz);
+    return bwd_layout(B, D, plan_backward(B, L, D, esz, max_vec(esz, lb))).total;
+}
+
+template <typename TX, typename TZ, typename Off, int VEC>
+static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStream_t stream) {
+    if (!plan.lookback) {
+        hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, steps_per_wave<kChainE, VEC>(),
+                                                  VEC, Off>),
+                           dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
+        return hipGetLastError();
+    }
+    hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
-    dim3 rgrid((unsigned)((a.B + kReduceRows - 1) / kReduceRows),
-               (unsigned)((a.D + kWave - 1) / kWave));
-    hipLaunchKernelGGL(dlambda_reduce_kernel, rgrid, dim3(256), 0, stream, ws.partial,
-                       ws.partial2, ws.counter, a.lambda, a.dlambda, a.B, a.D);
+    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(), VEC,
+                                                 lb_window<VEC>(), Off>),
+                       dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0, stream,
+                       P);
     return hipGetLastError();
 }
 
+template <typename TX, typename TZ>
+static hipError_t launch_bwd_typed(const BwdParams& P, const BwdPlan& plan, hipStream_t stream) {
+    // 32-bit byte offsets whenever a whole [B, L, D] tensor spans less than 4 GiB.
+    const bool small = (uint64_t)(P.nch * P.L) * sizeof(TZ) < (1ull << 32);
+    // VEC = 4 only exists for 2-byte x (8-byte accesses per lane).
+    if (small) {
+        if constexpr (sizeof(TX) == 2)
+            if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint32_t, 4>(P, plan, stream);
+        if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint32_t, 2>(P, plan, stream);
+        return launch_bwd_vec<TX, TZ, uint32_t, 1>(P, plan, stream);
+    }
+    if constexpr (sizeof(TX) == 2)
+        if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint64_t, 4>(P, plan, stream);
+    if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint64_t, 2>(P, plan, stream);
+    return launch_bwd_vec<TX, TZ, uint64_t, 1>(P, plan, stream);
+}
+
 hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
-    if (a.io == IoType::kF32) return launch_bwd_chain<float, float, 8, 8>(a, stream);
-    if (a.zio == IoType::kF32) return launch_bwd_chain<bf16, float, 8, 8>(a, stream);
-    return launch_bwd_chain<bf16, bf16, 8, 8>(a, stream);
+    const BwdPlan plan = plan_backward(a.B, a.L, a.D, io_bytes(a.io), pick_vec_bwd(a));
+    const BwdLayout lay = bwd_layout(a.B, a.D, plan);
+    char* ws = (char*)a.ws;
+    float* partial = (float*)(ws + lay.partial);
+    double* partial2 = (double*)(ws + lay.partial2);
+    const BwdParams P{a.x,   a.zr,    a.zi,  a.lambda, a.h0, a.h,   a.dh,  a.dhT,
+                      a.dx,  a.dzr,   a.dzi, a.dh0,    partial, a.L, a.D,  a.B * a.D,
+                      plan.ngroups, plan.nseg,
+                      plan.lookback ? lookback_ws(ws + lay.lb) : LookbackWs{}};
+    hipError_t e;
+    if (a.io == IoType::kF32) e = launch_bwd_typed<float, float>(P, plan, stream);
+    else if (a.zio == IoType::kF32) e = launch_bwd_typed<bf16, float>(P, plan, stream);
+    else e = launch_bwd_typed<bf16, bf16>(P, plan, stream);
+    if (e != hipSuccess) return e;
+    const int64_t rows = plan.nseg * a.B;
+    const int64_t nblk = (rows + kReduceRows - 1) / kReduceRows;
+    dim3 rgrid((unsigned)nblk, (unsigned)((a.D + kWave - 1) / kWave));
+    hipLaunchKernelGGL(dlambda_rows_kernel, rgrid, dim3(256), 0, stream, partial, partial2, rows,
+                       a.D);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((a.D + 255) / 256)), dim3(256), 0,
+                       stream, partial2, nblk, a.lambda, a.dlambda, a.D);
+    return hipGetLastError();
 }
 
 }  // namespace recblr

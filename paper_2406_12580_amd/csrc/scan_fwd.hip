@@ -1,5 +1,6 @@
 // Forward BD-LRU scan for gfx950: gate activation fused into the load,
-// chunked along the sequence, carries combined through LDS.
+// chunked along the sequence, carries combined through LDS and, for long
+// sequences over few channels, across workgroups by decoupled look-back.
 //
 // Recurrence (RecBLR, arXiv 2406.12580, eq:linrnn):  h_t = alpha_t h_{t-1} + beta'_t,
 // beta'_t = beta_t x_t, with alpha, beta from the gate equations of section 3.2.
@@ -7,171 +8,434 @@
 // pair, pairs compose with the associative operator "bullet", and the state at
 // any step is the composition of all earlier segments applied to h0.
 //
-// Work decomposition ("chain" kernel):
-//   * one lane owns one channel (b, d); the 64 lanes of a wave own 64
-//     consecutive flattened channels c = b*D + d, so every load and store of
-//     a time step is one contiguous run of 64 elements;
-//   * a workgroup of W waves owns those 64 channels for the whole sequence and
-//     walks it in macro-chunks of W*C steps; wave w scans steps
-//     [w*C, w*C + C) of the macro-chunk sequentially in registers;
-//   * the W wave aggregates (A, H) go through LDS; every wave folds the ones
-//     before it onto the carry, re-runs its C steps from there and stores h;
-//   * the carry after the macro-chunk stays in registers for the next one,
-//     whose loads are already in flight (register double buffer).
+// Work decomposition:
+//   * a lane owns VEC consecutive channels (b, d..d+VEC-1); the 64 lanes of a
+//     wave own 64*VEC consecutive flattened channels c = b*D + d, so the loads
+//     and stores of one time step are one contiguous run of 64*VEC elements;
+//   * a workgroup of W waves owns one channel group; its macro-chunk of W*C
+//     steps is split so that wave w scans steps [w*C, w*C + C) sequentially
+//     in registers and publishes its aggregate (A, H) in LDS;
+//   * chain kernel: the workgroup walks the whole sequence, macro-chunk after
+//     macro-chunk, keeping the carry in registers and the next macro-chunk's
+//     loads in flight (register double buffer);
+//   * look-back kernel: every workgroup takes one (group, macro-chunk) tile in
+//     ticket order, publishes the tile aggregate, reads the state words of the
+//     preceding tiles (each wave a window of K of them, in parallel) and
+//     publishes its inclusive state (lookback.hpp).
 // Each input element is read once and each output element written once.
 #include "device_common.hpp"
 #include "launch.hpp"
+#include "lookback.hpp"
 
 namespace recblr {
 
-template <typename T, typename TZ, int C, bool RAW, typename Off>
-struct ChunkRegs {
-    float v0[C], v1[C], v2[C];  // gated: x, z_r, z_i;  raw: a, u (v2 unused)
+struct FwdParams {
+    const void* p0;  // gated: x;    raw: a
+    const void* p1;  // gated: z_r;  raw: u
+    const void* p2;  // gated: z_i
+    const float* lam;
+    const float* h0;
+    void* h;
+    float* hT;
+    int64_t L, D, nch;      // nch = B * D
+    int64_t ngroups, nseg;  // channel groups; tiles along L (look-back kernel)
+    LookbackWs lb;
+};
 
-    // Loads steps [t_first, t_first + C); steps past the end re-read step L-1
-    // (always in bounds) and are masked by the caller.
-    __device__ __forceinline__ void fetch(const T* __restrict__ p0, const TZ* __restrict__ p1,
-                                          const TZ* __restrict__ p2, Off base, Off row,
-                                          int64_t t_first, int64_t L) {
+// One lane's channels and addressing.
+template <typename TX, int VEC, typename Off>
+struct LaneChannels {
+    bool valid;
+    int64_t c0;  // first channel (valid lanes) or 0 (idle lanes shadow channel 0)
+    int64_t d0;
+    Off base;    // byte offset of (b, 0, d) in an x-typed tensor
+    Off row;     // bytes between consecutive time steps
+
+    __device__ __forceinline__ void init(int64_t group, int lane, int64_t L, int64_t D,
+                                         int64_t nch) {
+        const int64_t c = (group * kWave + lane) * VEC;
+        valid = c < nch;
+        c0 = valid ? c : 0;
+        const int64_t b = c0 / D;
+        d0 = c0 - b * D;
+        base = (Off)((b * L * D + d0) * (int64_t)sizeof(TX));
+        row = (Off)(D * (int64_t)sizeof(TX));
+    }
+    __device__ __forceinline__ Off at(int64_t t) const { return base + (Off)t * row; }
+};
+
+// Raw inputs of C steps; steps past the end re-read step L-1 (in bounds) and
+// are masked when the gates are formed.
+template <typename TX, typename TZ, int C, int VEC, bool RAW, typename Off>
+struct ChunkIn {
+    float v0[C][VEC], v1[C][VEC], v2[C][VEC];
+
+    __device__ __forceinline__ void fetch(const FwdParams& P, const LaneChannels<TX, VEC, Off>& ln,
+                                          int64_t t_first) {
 #pragma unroll
         for (int j = 0; j < C; ++j) {
-            int64_t t = t_first + j < L ? t_first + j : L - 1;
-            Off off = base + (Off)t * row;
-            v0[j] = load_at(p0, off);
-            v1[j] = load_at(p1, z_offset<T, TZ>(off));
-            if (!RAW) v2[j] = load_at(p2, z_offset<T, TZ>(off));
+            const int64_t t = t_first + j < P.L ? t_first + j : P.L - 1;
+            const Off off = ln.at(t);
+            load_vec<TX, VEC>((const TX*)P.p0, off, v0[j]);
+            load_vec<TZ, VEC>((const TZ*)P.p1, z_offset<TX, TZ>(off), v1[j]);
+            if (!RAW) load_vec<TZ, VEC>((const TZ*)P.p2, z_offset<TX, TZ>(off), v2[j]);
         }
     }
 };
 
-template <typename T, typename TZ, int W, int C, bool RAW, typename Off>
-__global__ __launch_bounds__(W* kWave) void scan_fwd_chain_kernel(
-    const T* __restrict__ p0, const TZ* __restrict__ p1, const TZ* __restrict__ p2,
-    const float* __restrict__ lam, const float* __restrict__ h0, T* __restrict__ h,
-    float* __restrict__ hT, int64_t L, int64_t D, int64_t nch) {
-    __shared__ Seg agg[2][W][kWave];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
-    const int64_t c = (int64_t)blockIdx.x * kWave + lane;
-    const bool valid = c < nch;
-    const int64_t cs = valid ? c : 0;  // idle lanes shadow channel 0 and store nothing
-    const int64_t b = cs / D;
-    const int64_t d = cs - b * D;
-    const Off base = (Off)((b * L * D + d) * (int64_t)sizeof(T));
-    const Off row = (Off)(D * (int64_t)sizeof(T));
-    ChannelConst cc{};
-    if (!RAW) cc = channel_const(lam[d]);
-    float carry = (valid && h0) ? h0[cs] : 0.0f;
-
-    constexpr int64_t kMacro = (int64_t)W * C;
-    ChunkRegs<T, TZ, C, RAW, Off> cur, nxt;
-    if (L > 0) cur.fetch(p0, p1, p2, base, row, (int64_t)w * C, L);
-    int buf = 0;
-    for (int64_t t0 = 0; t0 < L; t0 += kMacro, buf ^= 1) {
-        const int64_t tw = t0 + (int64_t)w * C;
-        if (t0 + kMacro < L) nxt.fetch(p0, p1, p2, base, row, tw + kMacro, L);
-
-        float a[C], u[C];
+// (alpha_t, beta'_t) of C steps from the raw inputs; masked steps are the
+// identity (1, 0).
+template <typename TX, typename TZ, int C, int VEC, bool RAW, typename Off>
+__device__ __forceinline__ void form_steps(const ChunkIn<TX, TZ, C, VEC, RAW, Off>& in,
+                                           const ChannelConst (&cc)[VEC], int64_t t_first,
+                                           int64_t L, float (&a)[C][VEC], float (&u)[C][VEC]) {
 #pragma unroll
-        for (int j = 0; j < C; ++j) {
-            bool ok = (tw + j) < L;
+    for (int j = 0; j < C; ++j) {
+        const bool ok = t_first + j < L;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
             float aj, uj;
             if (RAW) {
-                aj = cur.v0[j];
-                uj = cur.v1[j];
+                aj = in.v0[j][k];
+                uj = in.v1[j][k];
             } else {
-                gate_forward(cur.v0[j], cur.v1[j], cur.v2[j], cc, aj, uj);
+                gate_forward(in.v0[j][k], in.v1[j][k], in.v2[j][k], cc[k], aj, uj);
             }
-            a[j] = ok ? aj : 1.0f;  // steps past the end are the identity (1, 0)
-            u[j] = ok ? uj : 0.0f;
+            a[j][k] = ok ? aj : 1.0f;
+            u[j][k] = ok ? uj : 0.0f;
         }
-        // Local aggregate of this wave's C steps.
-        Seg s{1.0f, 0.0f};
+    }
+}
+
+// Run C steps on from the states hv and store h (steps before L only).
+template <typename TX, int C, int VEC, typename Off>
+__device__ __forceinline__ void emit_steps(const FwdParams& P, const LaneChannels<TX, VEC, Off>& ln,
+                                           int64_t t_first, const float (&a)[C][VEC],
+                                           const float (&u)[C][VEC], float (&hv)[VEC]) {
 #pragma unroll
-        for (int j = 0; j < C; ++j) s = compose(Seg{a[j], u[j]}, s);
-        agg[buf][w][lane] = s;
+    for (int j = 0; j < C; ++j) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) hv[k] = fmaf(a[j][k], hv[k], u[j][k]);
+        if (ln.valid && t_first + j < P.L) store_vec<TX, VEC>((TX*)P.h, ln.at(t_first + j), hv);
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void load_consts(const float* lam, int64_t d0,
+                                            ChannelConst (&cc)[VEC]) {
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) cc[k] = channel_const(lam[d0 + k]);
+}
+
+// ------------------------------------------------------------------ chain kernel
+template <typename TX, typename TZ, int W, int C, int VEC, bool RAW, typename Off>
+__global__ __launch_bounds__(W* kWave) void scan_fwd_chain_kernel(FwdParams P) {
+    __shared__ Seg agg[2][W][kWave][VEC];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    LaneChannels<TX, VEC, Off> ln;
+    ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
+    ChannelConst cc[VEC];
+    if (!RAW) load_consts<VEC>(P.lam, ln.d0, cc);
+    float carry[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) carry[k] = P.h0 ? P.h0[ln.c0 + k] : 0.0f;
+
+    constexpr int64_t kMacro = (int64_t)W * C;
+    ChunkIn<TX, TZ, C, VEC, RAW, Off> cur, nxt;
+    if (P.L > 0) cur.fetch(P, ln, (int64_t)w * C);
+    int buf = 0;
+    for (int64_t t0 = 0; t0 < P.L; t0 += kMacro, buf ^= 1) {
+        const int64_t tw = t0 + (int64_t)w * C;
+        if (t0 + kMacro < P.L) nxt.fetch(P, ln, tw + kMacro);
+
+        float a[C][VEC], u[C][VEC];
+        form_steps(cur, cc, tw, P.L, a, u);
+        // Local aggregate of this wave's C steps.
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            Seg s{1.0f, 0.0f};
+#pragma unroll
+            for (int j = 0; j < C; ++j) s = compose(Seg{a[j][k], u[j][k]}, s);
+            agg[buf][w][lane][k] = s;
+        }
         __syncthreads();
 
-        // Carry into this wave: fold the aggregates of the earlier waves.
-        float cin = carry;
+        // Carry into this wave: fold the earlier waves' aggregates onto the carry.
+        float hv[VEC], cout[VEC];
 #pragma unroll
-        for (int k = 0; k < W; ++k) {
-            if (k < w) {
-                Seg e = agg[buf][k][lane];
-                cin = fmaf(e.A, cin, e.H);
+        for (int k = 0; k < VEC; ++k) hv[k] = carry[k];
+#pragma unroll
+        for (int q = 0; q < W; ++q) {
+            if (q < w) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const Seg e = agg[buf][q][lane][k];
+                    hv[k] = fmaf(e.A, hv[k], e.H);
+                }
             }
         }
-        // Re-run the C steps from the true carry and store h.
-        float hv = cin;
 #pragma unroll
-        for (int j = 0; j < C; ++j) {
-            hv = fmaf(a[j], hv, u[j]);
-            if (valid && (tw + j) < L) store_at(h, base + (Off)(tw + j) * row, hv);
-        }
-        // Carry out of the macro-chunk: continue the fold through the last wave.
-        float cout = cin;
+        for (int k = 0; k < VEC; ++k) cout[k] = hv[k];
+        emit_steps<TX, C, VEC, Off>(P, ln, tw, a, u, hv);
+        // Carry out of the macro-chunk: the fold continued through the last wave.
 #pragma unroll
-        for (int k = 0; k < W; ++k) {
-            if (k >= w) {
-                Seg e = agg[buf][k][lane];
-                cout = fmaf(e.A, cout, e.H);
+        for (int q = 0; q < W; ++q) {
+            if (q >= w) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const Seg e = agg[buf][q][lane][k];
+                    cout[k] = fmaf(e.A, cout[k], e.H);
+                }
             }
         }
-        carry = cout;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
         cur = nxt;
     }
-    if (w == 0 && valid && hT) hT[cs] = carry;
+    if (w == 0 && ln.valid && P.hT) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) P.hT[ln.c0 + k] = carry[k];
+    }
 }
 
-// Copy h0 (or zeros) into hT: the L = 0 case.
-__global__ void copy_state_kernel(const float* __restrict__ src, float* __restrict__ dst,
-                                  int64_t n) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) dst[i] = src ? src[i] : 0.0f;
+// ------------------------------------------------------------------ look-back kernel
+template <typename TX, typename TZ, int W, int C, int VEC, int K, typename Off>
+__global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P) {
+    __shared__ Seg agg[W][kWave][VEC];
+    __shared__ uint64_t win_sh[W * K][kWave][VEC];
+    __shared__ float carry_sh[kWave][VEC];
+    __shared__ int64_t tile_sh;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    if (threadIdx.x == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
+    __syncthreads();
+    const int64_t tile = tile_sh;
+    if (tile >= P.ngroups * P.nseg) return;  // only if the workspace was shared by two calls
+    const int64_t s = tile / P.ngroups;  // tiles are handed out one tile-row at a time
+    const int64_t g = tile - s * P.ngroups;
+
+    LaneChannels<TX, VEC, Off> ln;
+    ln.init(g, lane, P.L, P.D, P.nch);
+    ChannelConst cc[VEC];
+    load_consts<VEC>(P.lam, ln.d0, cc);
+    float h0v[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) h0v[k] = P.h0 ? P.h0[ln.c0 + k] : 0.0f;
+
+    const int64_t tw = s * W * C + (int64_t)w * C;
+    float a[C][VEC], u[C][VEC];
+    {
+        ChunkIn<TX, TZ, C, VEC, false, Off> in;
+        in.fetch(P, ln, tw);
+        form_steps(in, cc, tw, P.L, a, u);
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        Seg sg{1.0f, 0.0f};
+#pragma unroll
+        for (int j = 0; j < C; ++j) sg = compose(Seg{a[j][k], u[j][k]}, sg);
+        agg[w][lane][k] = sg;
+    }
+    __syncthreads();
+    // pre: the waves before this one; tot: the whole tile.
+    Seg pre[VEC], tot[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) pre[k] = tot[k] = Seg{1.0f, 0.0f};
+#pragma unroll
+    for (int q = 0; q < W; ++q) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            const Seg e = agg[q][lane][k];
+            if (q < w) pre[k] = compose(e, pre[k]);
+            tot[k] = compose(e, tot[k]);
+        }
+    }
+    __syncthreads();  // agg is reused below
+
+    uint64_t* const own = P.lb.states + s * P.nch + ln.c0;
+    if (s == 0) {
+        if (w == 0) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                carry_sh[lane][k] = h0v[k];
+                if (ln.valid) publish(own + k, pack_inclusive(fmaf(tot[k].A, h0v[k], tot[k].H)));
+            }
+        }
+    } else {
+        if (w == 0 && ln.valid) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) publish(own + k, pack_aggregate(tot[k]));
+        }
+        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, s, h0v, win_sh, carry_sh, w, lane);
+        if (w == 0 && ln.valid) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+                publish(own + k, pack_inclusive(fmaf(tot[k].A, carry_sh[lane][k], tot[k].H)));
+        }
+    }
+    __syncthreads();
+    float hv[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) hv[k] = fmaf(pre[k].A, carry_sh[lane][k], pre[k].H);
+    emit_steps<TX, C, VEC, Off>(P, ln, tw, a, u, hv);
+    if (s == P.nseg - 1 && w == W - 1 && ln.valid && P.hT) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) P.hT[ln.c0 + k] = hv[k];
+    }
 }
 
-template <typename T, typename TZ, int W, int C, bool RAW>
-static hipError_t launch_chain(const void* p0, const void* p1, const void* p2, const float* lam,
-                               const float* h0, void* h, float* hT, int64_t B, int64_t L,
-                               int64_t D, hipStream_t stream) {
-    int64_t nch = B * D;
-    dim3 grid((unsigned)((nch + kWave - 1) / kWave));
+// ------------------------------------------------------------------ launch plan
+// Tile shapes: W waves per workgroup and E elements per lane per macro-chunk
+// (C = E / VEC steps per wave), so a wave moves the same bytes per
+// macro-chunk whatever VEC is.
+#ifndef RECBLR_FWD_CHAIN_W
+#define RECBLR_FWD_CHAIN_W 8
+#endif
+#ifndef RECBLR_FWD_CHAIN_E
+#define RECBLR_FWD_CHAIN_E 8
+#endif
+#ifndef RECBLR_FWD_LB_W
+#define RECBLR_FWD_LB_W 8
+#endif
+#ifndef RECBLR_FWD_LB_E
+#define RECBLR_FWD_LB_E 16
+#endif
+// Channels per lane at most, per kernel (measured best on MI355X).
+#ifndef RECBLR_FWD_CHAIN_MAX_VEC
+#define RECBLR_FWD_CHAIN_MAX_VEC 4
+#endif
+#ifndef RECBLR_FWD_LB_MAX_VEC
+#define RECBLR_FWD_LB_MAX_VEC 1
+#endif
+constexpr int kChainW = RECBLR_FWD_CHAIN_W, kChainE = RECBLR_FWD_CHAIN_E;
+constexpr int kLbW = RECBLR_FWD_LB_W, kLbE = RECBLR_FWD_LB_E;
+// Look-back window per wave: K tiles, K * VEC = 8 state words per lane.
+template <int VEC>
+constexpr int lb_window() { return 8 / VEC; }
+template <int E, int VEC>
+constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
+// Steps of one look-back tile for a given VEC.
+constexpr int64_t lb_tile_steps(int vec) { return (int64_t)kLbW * (kLbE / vec > 0 ? kLbE / vec : 1); }
+// The chain kernel is used when its workgroups alone fill the GPU.
+// The chain kernel is used when its workgroups alone fill the GPU (one
+// workgroup per compute unit at least); lanes then take as many channels as
+// keep that many workgroups.
+constexpr int64_t kChainMinGroups = 256;
+// Largest channels-per-lane of a kernel for an element size (8-byte accesses
+// per lane at most).
+constexpr int max_vec(size_t esz, bool lookback, int64_t nch = INT64_MAX) {
+    const int cap = lookback ? RECBLR_FWD_LB_MAX_VEC : RECBLR_FWD_CHAIN_MAX_VEC;
+    int v = (int)(8 / esz) < cap ? (int)(8 / esz) : cap;
+    while (v > 1 && !lookback && nch / (kWave * v) < kChainMinGroups) v /= 2;
+    return v;
+}
+
+// Channels per lane: up to max_vec, when D and the pointers allow (x-typed
+// tensors aligned to VEC * esz, z-typed ones to VEC * zsz, fp32 states to
+// VEC * 4).
+static int pick_vec(int maxv, uintptr_t xmask, uintptr_t zmask, const float* h0, const float* hT,
+                    int64_t D, size_t esz, size_t zsz) {
+    const uintptr_t smask = (uintptr_t)h0 | (uintptr_t)hT;
+    for (int v = maxv; v > 1; v /= 2)
+        if (D % v == 0 && xmask % (v * esz) == 0 && zmask % (v * zsz) == 0 &&
+            smask % (v * 4) == 0)
+            return v;
+    return 1;
+}
+
+struct FwdPlan {
+    bool lookback;
+    int vec;
+    int64_t ngroups, nseg;
+};
+
+// The mode depends only on (B, L, D): the look-back kernel runs when there are
+// too few channel groups for the chain kernel to fill the GPU.  The tile count
+// depends on VEC (hence on pointer alignment); the workspace is sized for the
+// largest VEC the mode allows (shortest tiles).
+static bool forward_uses_lookback(int64_t B, int64_t L, int64_t D, size_t esz) {
+    const int64_t groups_one = (B * D + kWave - 1) / kWave;
+    return groups_one < kChainMinGroups && L > lb_tile_steps(max_vec(esz, true));
+}
+
+static FwdPlan plan_forward(int64_t B, int64_t L, int64_t D, size_t esz, int vec) {
+    FwdPlan p;
+    p.vec = vec;
+    p.lookback = forward_uses_lookback(B, L, D, esz);
+    p.ngroups = (B * D / vec + kWave - 1) / kWave;
+    p.nseg = p.lookback ? (L + lb_tile_steps(vec) - 1) / lb_tile_steps(vec) : 1;
+    return p;
+}
+
+size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
+    const size_t esz = io_bytes(io);
+    if (!forward_uses_lookback(B, L, D, esz)) return 0;
+    return lookback_ws_bytes(plan_forward(B, L, D, esz, max_vec(esz, true)).nseg, B * D);
+}
+
+template <typename TX, typename TZ, bool RAW, typename Off, int VEC>
+static hipError_t launch_vec(const FwdParams& P, const FwdPlan& plan, hipStream_t stream) {
+    if (!plan.lookback) {
+        hipLaunchKernelGGL((scan_fwd_chain_kernel<TX, TZ, kChainW,
+                                                  steps_per_wave<kChainE, VEC>(), VEC, RAW, Off>),
+                           dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
+        return hipGetLastError();
+    }
+    if constexpr (RAW) {
+        return hipErrorInvalidValue;  // the raw scan always runs the chain kernel
+    } else {
+        hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((scan_fwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(),
+                                                     VEC, lb_window<VEC>(), Off>),
+                           dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0,
+                           stream, P);
+        return hipGetLastError();
+    }
+}
+
+template <typename TX, typename TZ, bool RAW>
+static hipError_t launch_typed(const FwdParams& P, const FwdPlan& plan, hipStream_t stream) {
     // 32-bit byte offsets whenever a whole [B, L, D] tensor spans less than 4 GiB.
-    if ((uint64_t)(nch * L) * sizeof(TZ) < (1ull << 32))
-        hipLaunchKernelGGL((scan_fwd_chain_kernel<T, TZ, W, C, RAW, uint32_t>), grid,
-                           dim3(W * kWave), 0, stream, (const T*)p0, (const TZ*)p1,
-                           (const TZ*)p2, lam, h0, (T*)h, hT, L, D, nch);
-    else
-        hipLaunchKernelGGL((scan_fwd_chain_kernel<T, TZ, W, C, RAW, uint64_t>), grid,
-                           dim3(W * kWave), 0, stream, (const T*)p0, (const TZ*)p1,
-                           (const TZ*)p2, lam, h0, (T*)h, hT, L, D, nch);
-    return hipGetLastError();
+    const bool small = (uint64_t)(P.nch * P.L) * sizeof(TZ) < (1ull << 32);
+    // VEC = 4 only exists for 2-byte x (8-byte accesses per lane).
+    if (small) {
+        if constexpr (sizeof(TX) == 2)
+            if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint32_t, 4>(P, plan, stream);
+        if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint32_t, 2>(P, plan, stream);
+        return launch_vec<TX, TZ, RAW, uint32_t, 1>(P, plan, stream);
+    }
+    if constexpr (sizeof(TX) == 2)
+        if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint64_t, 4>(P, plan, stream);
+    if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint64_t, 2>(P, plan, stream);
+    return launch_vec<TX, TZ, RAW, uint64_t, 1>(P, plan, stream);
 }
-
-hipError_t launch_copy_state(const float* src, float* dst, int64_t n, hipStream_t stream) {
-    if (n <= 0 || dst == nullptr) return hipSuccess;
-    hipLaunchKernelGGL(copy_state_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                       stream, src, dst, n);
-    return hipGetLastError();
-}
-
-size_t scan_forward_workspace(int64_t, int64_t, int64_t, IoType) { return 0; }
 
 hipError_t launch_scan_forward(const ScanFwdArgs& a, hipStream_t stream) {
-    if (a.io == IoType::kF32)
-        return launch_chain<float, float, 8, 8, false>(a.x, a.zr, a.zi, a.lambda, a.h0, a.h,
-                                                       a.hT, a.B, a.L, a.D, stream);
-    if (a.zio == IoType::kF32)
-        return launch_chain<bf16, float, 8, 8, false>(a.x, a.zr, a.zi, a.lambda, a.h0, a.h, a.hT,
-                                                      a.B, a.L, a.D, stream);
-    return launch_chain<bf16, bf16, 8, 8, false>(a.x, a.zr, a.zi, a.lambda, a.h0, a.h, a.hT,
-                                                 a.B, a.L, a.D, stream);
+    const size_t esz = io_bytes(a.io);
+    const int maxv = max_vec(esz, forward_uses_lookback(a.B, a.L, a.D, esz), a.B * a.D);
+    const int vec = pick_vec(maxv, (uintptr_t)a.x | (uintptr_t)a.h,
+                             (uintptr_t)a.zr | (uintptr_t)a.zi, a.h0, a.hT, a.D, esz,
+                             io_bytes(a.zio));
+    const FwdPlan plan = plan_forward(a.B, a.L, a.D, esz, vec);
+    FwdParams P{a.x, a.zr, a.zi, a.lambda, a.h0, a.h, a.hT, a.L, a.D, a.B * a.D,
+                plan.ngroups, plan.nseg, plan.lookback ? lookback_ws(a.ws) : LookbackWs{}};
+    if (a.io == IoType::kF32) return launch_typed<float, float, false>(P, plan, stream);
+    if (a.zio == IoType::kF32) return launch_typed<bf16, float, false>(P, plan, stream);
+    return launch_typed<bf16, bf16, false>(P, plan, stream);
 }
 
 hipError_t launch_linear_scan(const float* a, const float* u, const float* h0, float* h,
                               float* hT, int64_t B, int64_t L, int64_t D, hipStream_t stream) {
-    return launch_chain<float, float, 8, 8, true>(a, u, nullptr, nullptr, h0, h, hT, B, L, D,
-                                                  stream);
+    FwdPlan plan;
+    plan.lookback = false;
+    plan.vec = pick_vec(max_vec(4, false, B * D), (uintptr_t)a | (uintptr_t)h, (uintptr_t)u, h0, hT,
+                        D, 4, 4);
+    plan.ngroups = (B * D / plan.vec + kWave - 1) / kWave;
+    plan.nseg = 1;
+    FwdParams P{a, u, nullptr, nullptr, h0, h, hT, L, D, B * D, plan.ngroups, 1, LookbackWs{}};
+    return launch_typed<float, float, true>(P, plan, stream);
 }
 
 }  // namespace recblr

@@ -276,3 +276,62 @@ def test_config_decode_full_size(rb):
                              dev32(inp.lam), dev32(inp.h0))
     want = oracle.scan_step(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
     assert_close(host(got), want, cfg.io, "decode h_next")
+
+
+# ------------------------------------------------------------------ kernel modes
+# Few channel groups and long sequences run the look-back kernels; many
+# channel groups run the chain kernels.  Forward chain lanes carry 1, 2 or 4
+# channels depending on D, the I/O type and pointer alignment.
+MODE_CASES = [
+    ((1, 5000, 64), "f32"),    # look-back, one channel group
+    ((2, 3000, 256), "bf16"),  # look-back, 8 groups
+    ((1, 2000, 3), "f32"),     # look-back, mostly idle lanes
+    ((3, 1000, 40), "f32"),    # look-back, partially idle group
+    ((64, 300, 512), "f32"),   # chain, 2 channels per lane forward
+    ((64, 130, 1024), "bf16"), # chain, 4 channels per lane forward
+    ((11000, 70, 3), "f32"),   # chain, 1 channel per lane, ragged last group
+]
+
+
+@pytest.mark.parametrize("shape,io", MODE_CASES)
+def test_kernel_modes(rb, shape, io):
+    B, L, D = shape
+    inp = dg.scan_inputs(B, L, D, 5000 + B + L + D, io=io, h0=True, grad=True, dhT=True)
+    X, ZR, ZI = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io)
+    lam, h0 = dev32(inp.lam), dev32(inp.h0)
+    h, hT = rb.bdlru_scan_forward(X, ZR, ZI, lam, h0)
+    got = rb.bdlru_scan_backward(X, ZR, ZI, lam, h, dev(inp.dh, io), h0, dev32(inp.dhT))
+    print(f"mode case {shape} {io}: GPU done", flush=True)
+    oh, ohT = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(host(h), oh, io, "h")
+    assert_close(host(hT), ohT, "f32", "hT")
+    want = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh, inp.h0, inp.dhT)
+    for k in ("dx", "dzr", "dzi", "dlambda"):
+        assert_close(host(got[k]), want[k], io, k)
+    assert_close(host(got["dh0"]), want["dh0"], "f32", "dh0")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_misaligned_pointers(rb, io):
+    """Tensors that start one element past an aligned address take the 1-channel lanes."""
+    import torch
+    B, L, D = 2, 700, 64
+    inp = dg.scan_inputs(B, L, D, 5100, io=io, h0=True, grad=True)
+    n = B * L * D
+
+    def shifted(a, iot):
+        t = dev(a.reshape(-1), iot)
+        buf = torch.empty(n + 1, dtype=t.dtype, device=t.device)
+        buf[1:] = t
+        return buf[1:].view(B, L, D)
+
+    X, ZR, ZI, DH = (shifted(a, io) for a in (inp.x, inp.zr, inp.zi, inp.dh))
+    assert X.data_ptr() % 8 != 0
+    lam, h0 = dev32(inp.lam), dev32(inp.h0)
+    h, hT = rb.bdlru_scan_forward(X, ZR, ZI, lam, h0)
+    got = rb.bdlru_scan_backward(X, ZR, ZI, lam, h, DH, h0)
+    oh, ohT = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam, inp.h0)
+    assert_close(host(h), oh, io, "h")
+    want = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh, inp.h0)
+    for k in ("dx", "dzr", "dzi", "dlambda"):
+        assert_close(host(got[k]), want[k], io, k)
