@@ -28,6 +28,28 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 FWD_ARRAYS, BWD_ARRAYS = 4, 8
 
 
+# HBM traffic per launch from rocprofv3 counters (FETCH_SIZE scaled by 2.0 and
+# WRITE_SIZE by 1.0, the factors a plain 1 GiB device copy reads for them),
+# valid only for the kernel sources they were taken on: the sha256 prefix of
+# the listed files must match, else the traffic is reported as null.
+TRAFFIC = {
+    ("c4", "scan_bwd"): {"bytes": 2_158_210_000, "sha": "264345cf7aebe3aa",
+                         "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
+}
+
+
+def traffic_bytes(workload, kernel):
+    import hashlib
+    rec = TRAFFIC.get((workload, kernel))
+    if rec is None:
+        return None
+    h = hashlib.sha256()
+    for f in rec["sources"]:
+        with open(os.path.join(ROOT, "paper_2406_12580_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return rec["bytes"] if h.hexdigest()[:16] == rec["sha"] else None
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -74,6 +96,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
+                    help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the BD-LRU path is "
@@ -83,6 +107,16 @@ def main():
     import torch
     from paper_2406_12580_amd import datagen as dg
     from paper_2406_12580_amd import recblr as rb
+
+    if args.copy_reference:
+        n = args.copy_reference * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_reference_bytes_each_way": 4 * n, "copies": args.warmup + args.steps}))
+        return
 
     cfg = dg.CONFIGS[args.workload]
     if "bwd" not in cfg.ops:
@@ -174,7 +208,8 @@ def main():
         "bwd_hbm_gbs": bwd_gbs,
         "roofline": {"bound": "hbm", "kernel": "scan_bwd" if dom == "bwd" else "scan_fwd",
                      "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": ach / PEAK_HBM_GBS, "traffic": None},
+                     "frac": ach / PEAK_HBM_GBS,
+                     "traffic": traffic_bytes(cfg.name, "scan_bwd" if dom == "bwd" else "scan_fwd")},
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 CPU oracle on a bounded sample ...")
