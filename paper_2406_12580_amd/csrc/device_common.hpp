@@ -15,6 +15,11 @@
 namespace recblr {
 
 constexpr int kWave = 64;
+
+// Index of the calling wave within its workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ I/O types
@@ -31,13 +36,11 @@ __device__ __forceinline__ T from_f32(float v);
 template <>
 __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 
-// Round to nearest, ties to even; NaN stays a quiet NaN.
+// Round to nearest, ties to even (NaN stays NaN): the hardware conversion.
 template <>
 __device__ __forceinline__ bf16 from_f32<bf16>(float v) {
-    uint32_t u = __float_as_uint(v);
-    uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
     bf16 out;
-    out.bits = (v != v) ? (uint16_t)((u >> 16) | 0x40u) : (uint16_t)r;
+    out.bits = __builtin_bit_cast(uint16_t, (__bf16)v);
     return out;
 }
 
@@ -64,8 +67,12 @@ template <> struct VecT<bf16, 4> { using type = uint32_t __attribute__((ext_vect
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+// Two floats to a packed bf16 pair (one v_cvt_pk_bf16_f32, round to nearest even).
 __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
-    return (uint32_t)from_f32<bf16>(lo).bits | ((uint32_t)from_f32<bf16>(hi).bits << 16);
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    const f2 v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
 }
 
 template <typename T, int VEC, typename Off>
@@ -139,23 +146,20 @@ __device__ __forceinline__ float softplus(float v) {
     return fmaxf(v, 0.0f) + log1pf(expf(-fabsf(v)));
 }
 
-// 1 - e^-y for y >= 0.  For y < 1/4 the Maclaurin series of 1 - e^-y,
-// y * sum_{n>=0} (-y)^n / (n+1)!, truncated after the y^8 term (relative
-// truncation error below (1/4)^8 / 9! < 5e-11), in Horner form; above 1/4
-// the direct form 1 - a^2 with a = e^-(y/2) has no harmful cancellation
-// (a^2 <= e^-1/4, so the relative error stays within a few ulp).
+// 1 - e^-y for y >= 0.  For y < 1/8 the Maclaurin series of 1 - e^-y,
+// y * sum_{n>=0} (-y)^n / (n+1)!, truncated after the y^5 term: the first
+// omitted term bounds the relative error by (1/8)^5 / 6! < 4.3e-8.  From 1/8
+// on, the direct form 1 - a^2 with a = e^-(y/2) has a^2 <= e^-1/8 = 0.8825,
+// so a few ulp of error in a^2 stay below 1e-6 relative to 1 - a^2 >= 0.1175.
 __device__ __forceinline__ float one_minus_exp_neg(float y, float a) {
-    float p = 1.0f / 40320.0f;
-    p = fmaf(p, -y, 1.0f / 5040.0f);
-    p = fmaf(p, -y, 1.0f / 720.0f);
-    p = fmaf(p, -y, 1.0f / 120.0f);
+    float p = 1.0f / 120.0f;
     p = fmaf(p, -y, 1.0f / 24.0f);
     p = fmaf(p, -y, 1.0f / 6.0f);
     p = fmaf(p, -y, 0.5f);
     p = fmaf(p, -y, 1.0f);
-    float series = y * p;
-    float direct = fmaf(-a, a, 1.0f);
-    return y < 0.25f ? series : direct;
+    const float series = y * p;
+    const float direct = fmaf(-a, a, 1.0f);
+    return y < 0.125f ? series : direct;
 }
 
 // Per-channel constants derived from Lambda.

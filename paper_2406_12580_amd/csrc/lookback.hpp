@@ -93,17 +93,22 @@ __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ stat
                                                int64_t c0, int64_t r, const float (&init)[VEC],
                                                uint64_t (&win_sh)[W * K][kWave][VEC],
                                                float (&carry_sh)[kWave][VEC], int w, int lane) {
+    // Issue all K*VEC loads of the window first, then wait on any not ready.
+    uint64_t wv[K][VEC];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const int64_t p = r - 1 - (int64_t)w * K - j;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k)
+            wv[j][k] = p >= 0 ? peek(states + p * nch + c0 + k) : pack_inclusive(init[k]);
+    }
 #pragma unroll
     for (int j = 0; j < K; ++j) {
         const int64_t p = r - 1 - (int64_t)w * K - j;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
-            uint64_t wd = pack_inclusive(init[k]);
-            if (p >= 0) {
-                const uint64_t* src = states + p * nch + c0 + k;
-                wd = wait_ready(src, peek(src));
-            }
-            win_sh[w * K + j][lane][k] = wd;
+            if (p >= 0) wv[j][k] = wait_ready(states + p * nch + c0 + k, wv[j][k]);
+            win_sh[w * K + j][lane][k] = wv[j][k];
         }
     }
     __syncthreads();

@@ -82,23 +82,25 @@ struct BwdIn {
     float g[C][VEC], x[C][VEC], zr[C][VEC], zi[C][VEC], hp[C][VEC];
     float zr_after[VEC];
 
+    // FULL: 0 < t and t + 1 < L for every step of the chunk (no clamping, no h0).
+    template <bool FULL>
     __device__ __forceinline__ void fetch(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
                                           const float (&h0v)[VEC], int64_t t_first) {
 #pragma unroll
         for (int j = 0; j < C; ++j) {
-            const int64_t t = t_first + j < P.L ? t_first + j : P.L - 1;
+            const int64_t t = FULL || t_first + j < P.L ? t_first + j : P.L - 1;
             const Off off = ln.at(t);
             load_vec<TX, VEC>((const TX*)P.dh, off, g[j]);
             load_vec<TX, VEC>((const TX*)P.x, off, x[j]);
             load_vec<TZ, VEC>((const TZ*)P.zr, z_offset<TX, TZ>(off), zr[j]);
             load_vec<TZ, VEC>((const TZ*)P.zi, z_offset<TX, TZ>(off), zi[j]);
-            load_vec<TX, VEC>((const TX*)P.h, t > 0 ? off - ln.row : off, hp[j]);
-            if (t == 0) {
+            load_vec<TX, VEC>((const TX*)P.h, FULL || t > 0 ? off - ln.row : off, hp[j]);
+            if (!FULL && t == 0) {
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) hp[j][k] = h0v[k];
             }
         }
-        const int64_t ta = t_first + C < P.L ? t_first + C : P.L - 1;
+        const int64_t ta = FULL || t_first + C < P.L ? t_first + C : P.L - 1;
         load_vec<TZ, VEC>((const TZ*)P.zr, z_offset<TX, TZ>(ln.at(ta)), zr_after);
     }
 };
@@ -110,7 +112,7 @@ struct BwdSteps {
     float r[C][VEC], al[C][VEC], ap[C][VEC], gg[C][VEC];
 };
 
-template <typename TX, typename TZ, int C, int VEC, typename Off>
+template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off>
 __device__ __forceinline__ void form_bwd(const BwdIn<TX, TZ, C, VEC, Off>& in,
                                          const ChannelConst (&cc)[VEC], const float (&dhTv)[VEC],
                                          int64_t t_first, int64_t L, BwdSteps<C, VEC>& st) {
@@ -128,10 +130,15 @@ __device__ __forceinline__ void form_bwd(const BwdIn<TX, TZ, C, VEC, Off>& in,
         for (int k = 0; k < VEC; ++k) {
             float nxt = j + 1 < C ? st.al[j + 1 < C ? j + 1 : j][k]
                                   : fast_exp2(sigmoid(in.zr_after[k]) * cc[k].neg_s_l2);
-            if (t + 1 >= L) nxt = 0.0f;
-            const float gj = in.g[j][k] + (t == L - 1 ? dhTv[k] : 0.0f);
-            st.ap[j][k] = t < L ? nxt : 1.0f;
-            st.gg[j][k] = t < L ? gj : 0.0f;
+            if (FULL) {
+                st.ap[j][k] = nxt;
+                st.gg[j][k] = in.g[j][k];
+            } else {
+                if (t + 1 >= L) nxt = 0.0f;
+                const float gj = in.g[j][k] + (t == L - 1 ? dhTv[k] : 0.0f);
+                st.ap[j][k] = t < L ? nxt : 1.0f;
+                st.gg[j][k] = t < L ? gj : 0.0f;
+            }
         }
     }
 }
@@ -148,7 +155,7 @@ __device__ __forceinline__ void local_reverse(const BwdSteps<C, VEC>& st, Seg (&
 
 // Run the chunk backwards from delta (the adjoint right after the chunk) and
 // apply the gate-gradient epilogue to every step before L.
-template <typename TX, typename TZ, int C, int VEC, typename Off>
+template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off>
 __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
                                          const BwdIn<TX, TZ, C, VEC, Off>& in,
                                          const BwdSteps<C, VEC>& st,
@@ -171,17 +178,17 @@ __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, V
             const float g_beta = delta[k] * in.x[j][k];
             const float g1 = -al * g_alpha;
             const float g2 = g_beta * i * al * al;
-            if (t < P.L) dsum[k] = fmaf(g1, r, fmaf(g2, r * rs, dsum[k]));
+            if (FULL || t < P.L) dsum[k] = fmaf(g1, r, fmaf(g2, r * rs, dsum[k]));
             dxv[k] = delta[k] * sq * i;
             dzrv[k] = fmaf(g1, q, g2 * (q * rs)) * (1.0f - r);
             dziv[k] = g_beta * sq * i * (1.0f - i);
         }
-        if (ln.valid && t < P.L) {
+        if (ln.valid && (FULL || t < P.L)) {
             const Off off = ln.at(t);
             store_vec<TX, VEC>((TX*)P.dx, off, dxv);
             store_vec<TZ, VEC>((TZ*)P.dzr, z_offset<TX, TZ>(off), dzrv);
             store_vec<TZ, VEC>((TZ*)P.dzi, z_offset<TX, TZ>(off), dziv);
-            if (t == 0 && P.dh0) {
+            if (!FULL && t == 0 && P.dh0) {
 #pragma unroll
                 for (int k = 0; k < VEC; ++k) P.dh0[ln.c0 + k] = st.al[j][k] * delta[k];
             }
@@ -221,12 +228,66 @@ __device__ __forceinline__ void write_partial(float (&red)[W][kWave][VEC],
 }
 
 // ------------------------------------------------------------------ chain kernel
+// One macro-chunk, backwards: reverse local aggregates through LDS, carry fold
+// from the later waves, gate-gradient epilogue and stores.
+template <bool FULL, typename TX, typename TZ, int W, int C, int VEC, typename Off>
+__device__ __forceinline__ void chain_bwd_step(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
+                                               const BwdIn<TX, TZ, C, VEC, Off>& cur,
+                                               const ChannelConst (&cc)[VEC],
+                                               const float (&dhTv)[VEC],
+                                               Seg (&agg)[W][kWave][VEC], int64_t tw, int w,
+                                               int lane, float (&carry)[VEC],
+                                               float (&dsum)[VEC]) {
+    BwdSteps<C, VEC> st;
+    form_bwd<FULL>(cur, cc, dhTv, tw, P.L, st);
+    Seg s[VEC];
+    local_reverse(st, s);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) agg[w][lane][k] = s[k];
+    __syncthreads();
+    // Carry into this wave: the later waves, last one first.
+    float delta[VEC], cout[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) delta[k] = carry[k];
+#pragma unroll
+    for (int q = W - 1; q >= 0; --q) {
+        if (q > w) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const Seg e = agg[q][lane][k];
+                delta[k] = fmaf(e.A, delta[k], e.H);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) cout[k] = delta[k];
+    emit_bwd<FULL>(P, ln, cur, st, cc, tw, delta, dsum);
+    // Carry out of the macro-chunk, towards earlier steps.
+#pragma unroll
+    for (int q = W - 1; q >= 0; --q) {
+        if (q <= w) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const Seg e = agg[q][lane][k];
+                cout[k] = fmaf(e.A, cout[k], e.H);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
+}
+
+// Macro-chunks are walked from the end of the sequence.  The first one
+// processed (holding t = L-1) and the last (holding t = 0) take the masked
+// path; the steady-state loop in between has no branch around a memory
+// instruction (see the forward chain kernel) and always prefetches the next
+// chunk.
 template <typename TX, typename TZ, int W, int C, int VEC, typename Off>
 __global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(BwdParams P) {
     __shared__ Seg agg[2][W][kWave][VEC];
     __shared__ float red[W][kWave][VEC];
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
+    const int w = wave_id();
     BwdLane<TX, VEC, Off> ln;
     ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
     ChannelConst cc[VEC];
@@ -237,50 +298,39 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(BwdParams P) {
 
     constexpr int64_t kMacro = (int64_t)W * C;
     const int64_t nmacro = (P.L + kMacro - 1) / kMacro;
-    BwdIn<TX, TZ, C, VEC, Off> cur, nxt;
-    if (nmacro > 0) cur.fetch(P, ln, h0v, (nmacro - 1) * kMacro + (int64_t)w * C);
-    int buf = 0;
-    for (int64_t m = nmacro - 1; m >= 0; --m, buf ^= 1) {
-        const int64_t tw = m * kMacro + (int64_t)w * C;
-        if (m > 0) nxt.fetch(P, ln, h0v, tw - kMacro);
-        BwdSteps<C, VEC> st;
-        form_bwd(cur, cc, dhTv, tw, P.L, st);
-        Seg s[VEC];
-        local_reverse(st, s);
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) agg[buf][w][lane][k] = s[k];
-        __syncthreads();
-        // Carry into this wave: the later waves, last one first.
-        float delta[VEC], cout[VEC];
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) delta[k] = carry[k];
-#pragma unroll
-        for (int q = W - 1; q >= 0; --q) {
-            if (q > w) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const Seg e = agg[buf][q][lane][k];
-                    delta[k] = fmaf(e.A, delta[k], e.H);
+    const int64_t woff = (int64_t)w * C;
+    // Two buffers alternate roles (loop unrolled by two), so no register copy
+    // ties the prefetched chunk to the one being consumed.
+    BwdIn<TX, TZ, C, VEC, Off> bufA, bufB;
+    if (nmacro > 0) {
+        int64_t m = nmacro - 1;
+        bufA.template fetch<false>(P, ln, h0v, m * kMacro + woff);
+        if (m == 0) {
+            chain_bwd_step<false>(P, ln, bufA, cc, dhTv, agg[0], woff, w, lane, carry, dsum);
+        } else {
+            bufB.template fetch<false>(P, ln, h0v, (m - 1) * kMacro + woff);
+            chain_bwd_step<false>(P, ln, bufA, cc, dhTv, agg[m & 1], m * kMacro + woff, w, lane,
+                                  carry, dsum);
+            --m;
+            for (;;) {
+                if (m == 0) {
+                    chain_bwd_step<false>(P, ln, bufB, cc, dhTv, agg[0], woff, w, lane, carry, dsum);
+                    break;
                 }
+                bufA.template fetch<false>(P, ln, h0v, (m - 1) * kMacro + woff);
+                chain_bwd_step<true>(P, ln, bufB, cc, dhTv, agg[m & 1], m * kMacro + woff, w,
+                                     lane, carry, dsum);
+                --m;
+                if (m == 0) {
+                    chain_bwd_step<false>(P, ln, bufA, cc, dhTv, agg[0], woff, w, lane, carry, dsum);
+                    break;
+                }
+                bufB.template fetch<false>(P, ln, h0v, (m - 1) * kMacro + woff);
+                chain_bwd_step<true>(P, ln, bufA, cc, dhTv, agg[m & 1], m * kMacro + woff, w,
+                                     lane, carry, dsum);
+                --m;
             }
         }
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) cout[k] = delta[k];
-        emit_bwd(P, ln, cur, st, cc, tw, delta, dsum);
-        // Carry out of the macro-chunk, towards earlier steps.
-#pragma unroll
-        for (int q = W - 1; q >= 0; --q) {
-            if (q <= w) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const Seg e = agg[buf][q][lane][k];
-                    cout[k] = fmaf(e.A, cout[k], e.H);
-                }
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
-        cur = nxt;
     }
     if (P.L == 0 && w == 0 && ln.valid && P.dh0) {
 #pragma unroll
@@ -298,7 +348,7 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     __shared__ float red[W][kWave][VEC];
     __shared__ int64_t tile_sh;
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
+    const int w = wave_id();
     if (threadIdx.x == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
     __syncthreads();
     const int64_t tile = tile_sh;
@@ -316,10 +366,16 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     for (int k = 0; k < VEC; ++k) dsum[k] = zero[k] = 0.0f;
 
     const int64_t tw = s * W * C + (int64_t)w * C;
+    const bool full = s > 0 && (s + 1) * W * C < P.L;  // workgroup-uniform
     BwdIn<TX, TZ, C, VEC, Off> in;
-    in.fetch(P, ln, h0v, tw);
     BwdSteps<C, VEC> st;
-    form_bwd(in, cc, dhTv, tw, P.L, st);
+    if (full) {
+        in.template fetch<true>(P, ln, h0v, tw);
+        form_bwd<true>(in, cc, dhTv, tw, P.L, st);
+    } else {
+        in.template fetch<false>(P, ln, h0v, tw);
+        form_bwd<false>(in, cc, dhTv, tw, P.L, st);
+    }
     {
         Seg sg[VEC];
         local_reverse(st, sg);
@@ -367,7 +423,8 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     float delta[VEC];
 #pragma unroll
     for (int k = 0; k < VEC; ++k) delta[k] = fmaf(pre[k].A, carry_sh[lane][k], pre[k].H);
-    emit_bwd(P, ln, in, st, cc, tw, delta, dsum);
+    if (full) emit_bwd<true>(P, ln, in, st, cc, tw, delta, dsum);
+    else emit_bwd<false>(P, ln, in, st, cc, tw, delta, dsum);
     write_partial<W, VEC>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
 }
 
@@ -452,9 +509,12 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
 #endif
 constexpr int kChainW = RECBLR_BWD_CHAIN_W, kChainE = RECBLR_BWD_CHAIN_E;
 constexpr int kLbW = RECBLR_BWD_LB_W, kLbE = RECBLR_BWD_LB_E;
-// Look-back window per wave: K tiles, K * VEC = 8 state words per lane.
+// Look-back window per wave: K tiles, K * VEC state words per lane.
+#ifndef RECBLR_BWD_LB_WORDS
+#define RECBLR_BWD_LB_WORDS 1
+#endif
 template <int VEC>
-constexpr int lb_window() { return 8 / VEC; }
+constexpr int lb_window() { return RECBLR_BWD_LB_WORDS / VEC > 0 ? RECBLR_BWD_LB_WORDS / VEC : 1; }
 template <int E, int VEC>
 constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
 // Steps of one look-back tile for a given VEC.

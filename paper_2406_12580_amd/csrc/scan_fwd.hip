@@ -70,11 +70,13 @@ template <typename TX, typename TZ, int C, int VEC, bool RAW, typename Off>
 struct ChunkIn {
     float v0[C][VEC], v1[C][VEC], v2[C][VEC];
 
+    // FULL: every step is before L (no clamping needed).
+    template <bool FULL>
     __device__ __forceinline__ void fetch(const FwdParams& P, const LaneChannels<TX, VEC, Off>& ln,
                                           int64_t t_first) {
 #pragma unroll
         for (int j = 0; j < C; ++j) {
-            const int64_t t = t_first + j < P.L ? t_first + j : P.L - 1;
+            const int64_t t = FULL || t_first + j < P.L ? t_first + j : P.L - 1;
             const Off off = ln.at(t);
             load_vec<TX, VEC>((const TX*)P.p0, off, v0[j]);
             load_vec<TZ, VEC>((const TZ*)P.p1, z_offset<TX, TZ>(off), v1[j]);
@@ -84,14 +86,14 @@ struct ChunkIn {
 };
 
 // (alpha_t, beta'_t) of C steps from the raw inputs; masked steps are the
-// identity (1, 0).
-template <typename TX, typename TZ, int C, int VEC, bool RAW, typename Off>
+// identity (1, 0).  FULL: no step is masked.
+template <bool FULL, typename TX, typename TZ, int C, int VEC, bool RAW, typename Off>
 __device__ __forceinline__ void form_steps(const ChunkIn<TX, TZ, C, VEC, RAW, Off>& in,
                                            const ChannelConst (&cc)[VEC], int64_t t_first,
                                            int64_t L, float (&a)[C][VEC], float (&u)[C][VEC]) {
 #pragma unroll
     for (int j = 0; j < C; ++j) {
-        const bool ok = t_first + j < L;
+        const bool ok = FULL || t_first + j < L;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
             float aj, uj;
@@ -108,7 +110,7 @@ __device__ __forceinline__ void form_steps(const ChunkIn<TX, TZ, C, VEC, RAW, Of
 }
 
 // Run C steps on from the states hv and store h (steps before L only).
-template <typename TX, int C, int VEC, typename Off>
+template <bool FULL, typename TX, int C, int VEC, typename Off>
 __device__ __forceinline__ void emit_steps(const FwdParams& P, const LaneChannels<TX, VEC, Off>& ln,
                                            int64_t t_first, const float (&a)[C][VEC],
                                            const float (&u)[C][VEC], float (&hv)[VEC]) {
@@ -116,7 +118,8 @@ __device__ __forceinline__ void emit_steps(const FwdParams& P, const LaneChannel
     for (int j = 0; j < C; ++j) {
 #pragma unroll
         for (int k = 0; k < VEC; ++k) hv[k] = fmaf(a[j][k], hv[k], u[j][k]);
-        if (ln.valid && t_first + j < P.L) store_vec<TX, VEC>((TX*)P.h, ln.at(t_first + j), hv);
+        if (ln.valid && (FULL || t_first + j < P.L))
+            store_vec<TX, VEC>((TX*)P.h, ln.at(t_first + j), hv);
     }
 }
 
@@ -128,11 +131,67 @@ __device__ __forceinline__ void load_consts(const float* lam, int64_t d0,
 }
 
 // ------------------------------------------------------------------ chain kernel
+// One macro-chunk: gates, local aggregates through LDS, carry fold, store.
+template <bool FULL, typename TX, typename TZ, int W, int C, int VEC, bool RAW, typename Off>
+__device__ __forceinline__ void chain_fwd_step(const FwdParams& P,
+                                               const LaneChannels<TX, VEC, Off>& ln,
+                                               const ChunkIn<TX, TZ, C, VEC, RAW, Off>& cur,
+                                               const ChannelConst (&cc)[VEC],
+                                               Seg (&agg)[W][kWave][VEC], int64_t tw, int w,
+                                               int lane, float (&carry)[VEC]) {
+    float a[C][VEC], u[C][VEC];
+    form_steps<FULL>(cur, cc, tw, P.L, a, u);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        Seg s{1.0f, 0.0f};
+#pragma unroll
+        for (int j = 0; j < C; ++j) s = compose(Seg{a[j][k], u[j][k]}, s);
+        agg[w][lane][k] = s;
+    }
+    __syncthreads();
+    // Carry into this wave: fold the earlier waves' aggregates onto the carry.
+    float hv[VEC], cout[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) hv[k] = carry[k];
+#pragma unroll
+    for (int q = 0; q < W; ++q) {
+        if (q < w) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const Seg e = agg[q][lane][k];
+                hv[k] = fmaf(e.A, hv[k], e.H);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) cout[k] = hv[k];
+    emit_steps<FULL, TX, C, VEC, Off>(P, ln, tw, a, u, hv);
+    // Carry out of the macro-chunk: the fold continued through the last wave.
+#pragma unroll
+    for (int q = 0; q < W; ++q) {
+        if (q >= w) {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const Seg e = agg[q][lane][k];
+                cout[k] = fmaf(e.A, cout[k], e.H);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
+}
+
+// The steady-state loop covers the full macro-chunks and has no branch
+// around a memory instruction: on this GPU loads and stores share one
+// in-order counter, and a branch that issues a different number of them
+// makes the compiler wait for every outstanding load, including the
+// prefetched next chunk.  The next chunk's loads are always issued (clamped
+// to step L-1 past the end); a partial last macro-chunk runs after the loop.
 template <typename TX, typename TZ, int W, int C, int VEC, bool RAW, typename Off>
 __global__ __launch_bounds__(W* kWave) void scan_fwd_chain_kernel(FwdParams P) {
     __shared__ Seg agg[2][W][kWave][VEC];
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
+    const int w = wave_id();
     LaneChannels<TX, VEC, Off> ln;
     ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
     ChannelConst cc[VEC];
@@ -142,56 +201,28 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_chain_kernel(FwdParams P) {
     for (int k = 0; k < VEC; ++k) carry[k] = P.h0 ? P.h0[ln.c0 + k] : 0.0f;
 
     constexpr int64_t kMacro = (int64_t)W * C;
-    ChunkIn<TX, TZ, C, VEC, RAW, Off> cur, nxt;
-    if (P.L > 0) cur.fetch(P, ln, (int64_t)w * C);
-    int buf = 0;
-    for (int64_t t0 = 0; t0 < P.L; t0 += kMacro, buf ^= 1) {
-        const int64_t tw = t0 + (int64_t)w * C;
-        if (t0 + kMacro < P.L) nxt.fetch(P, ln, tw + kMacro);
-
-        float a[C][VEC], u[C][VEC];
-        form_steps(cur, cc, tw, P.L, a, u);
-        // Local aggregate of this wave's C steps.
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            Seg s{1.0f, 0.0f};
-#pragma unroll
-            for (int j = 0; j < C; ++j) s = compose(Seg{a[j][k], u[j][k]}, s);
-            agg[buf][w][lane][k] = s;
+    const int64_t nfull = P.L / kMacro;
+    const bool tail = nfull * kMacro < P.L;
+    // Two buffers alternate roles (loop unrolled by two), so no register copy
+    // ties the prefetched chunk to the one being consumed.
+    ChunkIn<TX, TZ, C, VEC, RAW, Off> bufA, bufB;
+    const int64_t woff = (int64_t)w * C;
+    if (P.L > 0) bufA.template fetch<false>(P, ln, woff);
+    for (int64_t m = 0;;) {
+        if (m >= nfull) {
+            if (tail) chain_fwd_step<false>(P, ln, bufA, cc, agg[m & 1], m * kMacro + woff, w, lane, carry);
+            break;
         }
-        __syncthreads();
-
-        // Carry into this wave: fold the earlier waves' aggregates onto the carry.
-        float hv[VEC], cout[VEC];
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) hv[k] = carry[k];
-#pragma unroll
-        for (int q = 0; q < W; ++q) {
-            if (q < w) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const Seg e = agg[buf][q][lane][k];
-                    hv[k] = fmaf(e.A, hv[k], e.H);
-                }
-            }
+        bufB.template fetch<false>(P, ln, (m + 1) * kMacro + woff);
+        chain_fwd_step<true>(P, ln, bufA, cc, agg[m & 1], m * kMacro + woff, w, lane, carry);
+        ++m;
+        if (m >= nfull) {
+            if (tail) chain_fwd_step<false>(P, ln, bufB, cc, agg[m & 1], m * kMacro + woff, w, lane, carry);
+            break;
         }
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) cout[k] = hv[k];
-        emit_steps<TX, C, VEC, Off>(P, ln, tw, a, u, hv);
-        // Carry out of the macro-chunk: the fold continued through the last wave.
-#pragma unroll
-        for (int q = 0; q < W; ++q) {
-            if (q >= w) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const Seg e = agg[buf][q][lane][k];
-                    cout[k] = fmaf(e.A, cout[k], e.H);
-                }
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) carry[k] = cout[k];
-        cur = nxt;
+        bufA.template fetch<false>(P, ln, (m + 1) * kMacro + woff);
+        chain_fwd_step<true>(P, ln, bufB, cc, agg[m & 1], m * kMacro + woff, w, lane, carry);
+        ++m;
     }
     if (w == 0 && ln.valid && P.hT) {
 #pragma unroll
@@ -207,7 +238,7 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
     __shared__ float carry_sh[kWave][VEC];
     __shared__ int64_t tile_sh;
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
+    const int w = wave_id();
     if (threadIdx.x == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
     __syncthreads();
     const int64_t tile = tile_sh;
@@ -224,11 +255,17 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
     for (int k = 0; k < VEC; ++k) h0v[k] = P.h0 ? P.h0[ln.c0 + k] : 0.0f;
 
     const int64_t tw = s * W * C + (int64_t)w * C;
+    const bool full = (s + 1) * W * C <= P.L;  // workgroup-uniform
     float a[C][VEC], u[C][VEC];
     {
         ChunkIn<TX, TZ, C, VEC, false, Off> in;
-        in.fetch(P, ln, tw);
-        form_steps(in, cc, tw, P.L, a, u);
+        if (full) {
+            in.template fetch<true>(P, ln, tw);
+            form_steps<true>(in, cc, tw, P.L, a, u);
+        } else {
+            in.template fetch<false>(P, ln, tw);
+            form_steps<false>(in, cc, tw, P.L, a, u);
+        }
     }
 #pragma unroll
     for (int k = 0; k < VEC; ++k) {
@@ -278,7 +315,8 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
     float hv[VEC];
 #pragma unroll
     for (int k = 0; k < VEC; ++k) hv[k] = fmaf(pre[k].A, carry_sh[lane][k], pre[k].H);
-    emit_steps<TX, C, VEC, Off>(P, ln, tw, a, u, hv);
+    if (full) emit_steps<true, TX, C, VEC, Off>(P, ln, tw, a, u, hv);
+    else emit_steps<false, TX, C, VEC, Off>(P, ln, tw, a, u, hv);
     if (s == P.nseg - 1 && w == W - 1 && ln.valid && P.hT) {
 #pragma unroll
         for (int k = 0; k < VEC; ++k) P.hT[ln.c0 + k] = hv[k];
@@ -310,9 +348,12 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
 #endif
 constexpr int kChainW = RECBLR_FWD_CHAIN_W, kChainE = RECBLR_FWD_CHAIN_E;
 constexpr int kLbW = RECBLR_FWD_LB_W, kLbE = RECBLR_FWD_LB_E;
-// Look-back window per wave: K tiles, K * VEC = 8 state words per lane.
+// Look-back window per wave: K tiles, K * VEC state words per lane.
+#ifndef RECBLR_FWD_LB_WORDS
+#define RECBLR_FWD_LB_WORDS 1
+#endif
 template <int VEC>
-constexpr int lb_window() { return 8 / VEC; }
+constexpr int lb_window() { return RECBLR_FWD_LB_WORDS / VEC > 0 ? RECBLR_FWD_LB_WORDS / VEC : 1; }
 template <int E, int VEC>
 constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
 // Steps of one look-back tile for a given VEC.
