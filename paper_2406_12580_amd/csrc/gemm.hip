@@ -7,25 +7,37 @@
 // weights use the I/O type; z and dz are fp32 scratch (rounding them to bf16
 // would cost about 1e-2 of relative accuracy in dW).
 //
-// Tiling: a 256-thread workgroup computes a 64 x 64 tile of C = A B, staging
-// 64 x 16 slices of A and 16 x 64 slices of B through LDS; each thread owns a
-// 4 x 4 register micro-tile, accumulated in fp32.  The weight-gradient product
-// reduces over all B*L rows and is split across workgroups (split-K); its fp32
-// partial tiles are summed afterwards in a fixed order, so results are
-// deterministic.
+// Tiling: a 256-thread workgroup (4 waves) computes a 64 x 64 tile of C = A B
+// on the matrix cores; each wave owns a 32 x 32 quarter as 2 x 2 MFMA blocks of
+// 16 x 16 (v_mfma_f32_16x16x4_f32, or v_mfma_f32_16x16x32_bf16 when both
+// operands are bf16 inputs), accumulating in fp32.  K-slices of A and B are
+// staged through LDS in a K-contiguous layout; each operand is read from
+// global memory in the order that is contiguous for it.  The weight-gradient
+// product reduces over all B*L rows and is split across workgroups
+// (split-K); its fp32 partial tiles are summed afterwards in a fixed order,
+// so results are deterministic.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "gemm.hpp"
 
 namespace recblr {
 
 namespace {
-constexpr int kTM = 64, kTN = 64, kTK = 16, kThreads = 256;
+constexpr int kTM = 64, kTN = 64, kThreads = 256;
 }
 
-// ------------------------------------------------------------------ accessors
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------------ operand accessors
+// a(i, k) and b(k, n) read one element; kAKFast / kBKFast say whether k is the
+// contiguous index of the operand in memory (then k runs fastest across
+// threads when staging, else i / n does).
 // Forward: A = x [M x D], B(k, n) = Wcat[n][k] with Wcat = [W_r; W_i] ([2D x D]).
 template <typename T>
 struct FwdOps {
+    static constexpr bool kAKFast = true, kBKFast = true;
     const T* x;
     const T* wr;
     const T* wi;
@@ -39,13 +51,14 @@ struct FwdOps {
 // Backward data: A(i, k) = [dz_r | dz_i][i][k] ([M x 2D]), B(k, n) = Wcat[k][n].
 template <typename T>
 struct DxOps {
+    static constexpr bool kAKFast = true, kBKFast = false;
     const float* dzr;
     const float* dzi;
     const T* wr;
     const T* wi;
     int64_t D;
     __device__ float a(int64_t i, int64_t k) const {
-        return k < D ? load(dzr + i * D + k) : load(dzi + i * D + (k - D));
+        return k < D ? dzr[i * D + k] : dzi[i * D + (k - D)];
     }
     __device__ float b(int64_t k, int64_t n) const {
         return k < D ? load(wr + k * D + n) : load(wi + (k - D) * D + n);
@@ -56,62 +69,103 @@ struct DxOps {
 // B(row, k) = x[row][k] for k < D and 1 for k = D (so column D yields db).
 template <typename T>
 struct DwOps {
+    static constexpr bool kAKFast = false, kBKFast = false;
     const float* dzr;
     const float* dzi;
     const T* x;
     int64_t D;
     __device__ float a(int64_t o, int64_t row) const {
-        return o < D ? load(dzr + row * D + o) : load(dzi + row * D + (o - D));
+        return o < D ? dzr[row * D + o] : dzi[row * D + (o - D)];
     }
     __device__ float b(int64_t row, int64_t k) const {
         return k < D ? load(x + row * D + k) : 1.0f;
     }
 };
 
-// C tile = sum over k in [k_begin, k_end) of A(i, k) B(k, n), for the tile at
-// (blockIdx.x * 64, blockIdx.y * 64).  Result handed to `epi(i, n, value)`.
-template <class Ops, class Epi>
-__device__ __forceinline__ void tile_product(const Ops& ops, int64_t M, int64_t N,
-                                             int64_t k_begin, int64_t k_end, Epi epi) {
-    __shared__ float As[kTK][kTM + 1];
-    __shared__ float Bs[kTK][kTN + 1];
+// C tile = sum over k in [k_begin, k_end) of A(i, k) B(k, n) for the 64 x 64
+// tile at (blockIdx.x * 64, blockIdx.y * 64); each result goes to
+// epi(i, n, value).  BF16: both operands are bf16 values (exact in bf16) and
+// the bf16 MFMA is used; otherwise fp32 MFMA.
+template <bool BF16, class Ops, class Epi>
+__device__ __forceinline__ void mfma_tile(const Ops& ops, int64_t M, int64_t N, int64_t k_begin,
+                                          int64_t k_end, Epi epi) {
+    using E = typename std::conditional<BF16, __bf16, float>::type;
+    constexpr int kBK = BF16 ? 32 : 16;       // K-slice staged per iteration
+    constexpr int kPad = BF16 ? 8 : 1;        // keeps 16-byte rows (bf16) / spreads banks (fp32)
+    __shared__ __attribute__((aligned(16))) E As[kTM][kBK + kPad];
+    __shared__ __attribute__((aligned(16))) E Bs[kTN][kBK + kPad];
     const int tid = threadIdx.x;
-    const int tr = tid / 16, tc = tid % 16;  // 16 x 16 threads, 4 x 4 outputs each
+    const int lane = tid & 63;
+    const int wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1;      // this wave's 32 x 32 quarter
     const int64_t i0 = (int64_t)blockIdx.x * kTM, n0 = (int64_t)blockIdx.y * kTN;
-    float acc[4][4] = {};
-    for (int64_t k0 = k_begin; k0 < k_end; k0 += kTK) {
-        for (int e = tid; e < kTM * kTK; e += kThreads) {
-            int ii = e / kTK, kk = e % kTK;
-            int64_t i = i0 + ii, k = k0 + kk;
-            As[kk][ii] = (i < M && k < k_end) ? ops.a(i, k) : 0.0f;
+    f4v acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int64_t k0 = k_begin; k0 < k_end; k0 += kBK) {
+        for (int e = tid; e < kTM * kBK; e += kThreads) {
+            const int ii = Ops::kAKFast ? e / kBK : e % kTM;
+            const int kk = Ops::kAKFast ? e % kBK : e / kTM;
+            const int64_t i = i0 + ii, k = k0 + kk;
+            As[ii][kk] = (E)((i < M && k < k_end) ? ops.a(i, k) : 0.0f);
         }
-        for (int e = tid; e < kTK * kTN; e += kThreads) {
-            int kk = e / kTN, nn = e % kTN;
-            int64_t k = k0 + kk, n = n0 + nn;
-            Bs[kk][nn] = (n < N && k < k_end) ? ops.b(k, n) : 0.0f;
+        for (int e = tid; e < kTN * kBK; e += kThreads) {
+            const int nn = Ops::kBKFast ? e / kBK : e % kTN;
+            const int kk = Ops::kBKFast ? e % kBK : e / kTN;
+            const int64_t n = n0 + nn, k = k0 + kk;
+            Bs[nn][kk] = (E)((n < N && k < k_end) ? ops.b(k, n) : 0.0f);
         }
         __syncthreads();
+        if constexpr (BF16) {
+            // v_mfma_f32_16x16x32_bf16: lane l supplies row l%16, k = 8*(l/16)..+7.
+            bf8v av[2], bv[2];
 #pragma unroll
-        for (int kk = 0; kk < kTK; ++kk) {
-            float av[4], bv[4];
+            for (int i = 0; i < 2; ++i)
+                av[i] = *(const bf8v*)&As[wm * 32 + i * 16 + (lane & 15)][8 * (lane >> 4)];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) av[r] = As[kk][tr * 4 + r];
+            for (int j = 0; j < 2; ++j)
+                bv[j] = *(const bf8v*)&Bs[wn * 32 + j * 16 + (lane & 15)][8 * (lane >> 4)];
 #pragma unroll
-            for (int s = 0; s < 4; ++s) bv[s] = Bs[kk][tc * 4 + s];
+            for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv[j], acc[i][j],
+                                                                         0, 0, 0);
+        } else {
+            // v_mfma_f32_16x16x4_f32: lane l supplies row l%16, k = l/16.
 #pragma unroll
-                for (int s = 0; s < 4; ++s) acc[r][s] = fmaf(av[r], bv[s], acc[r][s]);
+            for (int ks = 0; ks < kBK; ks += 4) {
+                float av[2], bv[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    av[i] = As[wm * 32 + i * 16 + (lane & 15)][ks + (lane >> 4)];
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    bv[j] = Bs[wn * 32 + j * 16 + (lane & 15)][ks + (lane >> 4)];
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j],
+                                                                          acc[i][j], 0, 0, 0);
+            }
         }
         __syncthreads();
     }
+    // D[r][c] of a 16 x 16 block: lane l holds rows 4*(l/16)+v, column l%16.
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            int64_t i = i0 + tr * 4 + r, n = n0 + tc * 4 + s;
-            if (i < M && n < N) epi(i, n, acc[r][s]);
-        }
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t r = i0 + wm * 32 + i * 16 + 4 * (lane >> 4) + v;
+                const int64_t c = n0 + wn * 32 + j * 16 + (lane & 15);
+                if (r < M && c < N) epi(r, c, acc[i][j][v]);
+            }
 }
 
 template <typename T>
@@ -120,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void proj_fwd_kernel(const T* x, const T*
                                                             const T* bi, float* zr, float* zi,
                                                             int64_t M, int64_t D) {
     FwdOps<T> ops{x, wr, wi, D};
-    tile_product(ops, M, 2 * D, 0, D, [&](int64_t i, int64_t n, float v) {
+    mfma_tile<sizeof(T) == 2>(ops, M, 2 * D, 0, D, [&](int64_t i, int64_t n, float v) {
         if (n < D) {
             store(zr + i * D + n, v + (br ? load(br + n) : 0.0f));
         } else {
@@ -135,7 +189,7 @@ __global__ __launch_bounds__(kThreads) void proj_dx_kernel(const float* dzr, con
                                                            const T* wr, const T* wi, T* dx,
                                                            int64_t M, int64_t D) {
     DxOps<T> ops{dzr, dzi, wr, wi, D};
-    tile_product(ops, M, D, 0, 2 * D, [&](int64_t i, int64_t n, float v) {
+    mfma_tile<false>(ops, M, D, 0, 2 * D, [&](int64_t i, int64_t n, float v) {
         T* p = dx + i * D + n;
         store(p, load(p) + v);  // dx already holds the direct term delta * beta
     });
@@ -154,8 +208,8 @@ __global__ __launch_bounds__(kThreads) void proj_dw_kernel(const float* dzr, con
     if (k_end > M) k_end = M;
     const int64_t N = D + 1;
     float* out = partial + split * (2 * D) * N;
-    tile_product(ops, 2 * D, N, k_begin, k_end,
-                 [&](int64_t o, int64_t k, float v) { out[o * N + k] = v; });
+    mfma_tile<false>(ops, 2 * D, N, k_begin, k_end,
+                     [&](int64_t o, int64_t k, float v) { out[o * N + k] = v; });
 }
 
 // Sum the split-K partials in split order (fp64) into dW_r, dW_i, db_r, db_i.
