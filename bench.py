@@ -33,8 +33,10 @@ FWD_ARRAYS, BWD_ARRAYS = 4, 8
 # valid only for the kernel sources they were taken on: the sha256 prefix of
 # the listed files must match, else the traffic is reported as null.
 TRAFFIC = {
-    ("c4", "scan_bwd"): {"bytes": 2_158_210_000, "sha": "264345cf7aebe3aa",
+    ("c4", "scan_bwd"): {"bytes": 2_169_439_232, "sha": "d383609ee17df598",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
+    ("c4", "scan_fwd"): {"bytes": 1_074_286_592, "sha": "a6622ab36a98d29c",
+                         "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
 }
 
 
