@@ -224,21 +224,26 @@ void oracle_backward(int64_t B, int64_t L, int64_t D, const double* x, const dou
                 acc += dzr[row * D + o] * Wr[o * D + k] + dzi[row * D + o] * Wi[o * D + k];
             dx[row * D + k] += acc;
         }
+    /* dW[o][k] = sum over rows (ascending) of dz[row][o] x[row][k]; the row loop
+     * sits outside the k loop only so that x is read along its rows. */
 #pragma omp parallel for schedule(static)
     for (int64_t o = 0; o < D; ++o) {
+        double* wr = dWr + o * D;
+        double* wi = dWi + o * D;
         for (int64_t k = 0; k < D; ++k) {
-            double ar = 0.0, ai = 0.0;
-            for (int64_t row = 0; row < M; ++row) {
-                ar += dzr[row * D + o] * x[row * D + k];
-                ai += dzi[row * D + o] * x[row * D + k];
-            }
-            dWr[o * D + k] = ar;
-            dWi[o * D + k] = ai;
+            wr[k] = 0.0;
+            wi[k] = 0.0;
         }
         double sr = 0.0, si = 0.0;
         for (int64_t row = 0; row < M; ++row) {
-            sr += dzr[row * D + o];
-            si += dzi[row * D + o];
+            const double gr = dzr[row * D + o], gi = dzi[row * D + o];
+            const double* xr = x + row * D;
+            for (int64_t k = 0; k < D; ++k) {
+                wr[k] += gr * xr[k];
+                wi[k] += gi * xr[k];
+            }
+            sr += gr;
+            si += gi;
         }
         dbr[o] = sr;
         dbi[o] = si;
