@@ -1,12 +1,15 @@
 """Benchmark of the BD-LRU scan on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--api scan|full]
 
 A step is one pass of the hot path over one batch: the gated scan forward
 (recblr_bdlru_scan_forward) followed by its backward
 (recblr_bdlru_scan_backward), on synthetic inputs already resident in HBM.
 The default workload is the long-history batch B=256, L=2048, D=128 in fp32.
-Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
+With --api full the step is the whole layer instead: the gate projections and
+the scan, forward (recblr_bdlru_forward) and backward (recblr_bdlru_backward,
+which recomputes the projections and returns dx, dW, db, dLambda).
+Prints ONE JSON line (metric, value, roofline of the dominant call, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).
 """
 from __future__ import annotations
@@ -23,9 +26,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E peak, GB/s
-# Algorithmic HBM bytes per element (B*L*D) of each call, by I/O element size.
-# forward: read x, z_r, z_i; write h.  backward: read dh, x, z_r, z_i, h; write dx, dz_r, dz_i.
-FWD_ARRAYS, BWD_ARRAYS = 4, 8
+# Algorithmic HBM bytes per element (B*L*D) of each call, in units of the I/O
+# element size.  Scan level -- forward: read x, z_r, z_i; write h.  backward:
+# read dh, x, z_r, z_i, h; write dx, dz_r, dz_i.  Full layer (gate projections
+# included; the weights are negligible) -- forward: read x; write h.
+# backward: read x, h, dh; write dx.
+ARRAYS = {"scan": (4, 8), "full": (2, 4)}
 
 
 # HBM traffic per launch from rocprofv3 counters (FETCH_SIZE scaled by 2.0 and
@@ -56,7 +62,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(cfg, target_s=10.0):
+def cpu_baseline(cfg, api="scan", target_s=10.0):
     """fp64 oracle (forward + backward) on a bounded sample of the workload.
 
     The sample is the first `rows` batch rows (each row is independent), grown
@@ -65,15 +71,26 @@ def cpu_baseline(cfg, target_s=10.0):
     """
     import oracle
     from paper_2406_12580_amd import datagen as dg
-    inp = dg.config_inputs(cfg, grad=True)
     per_row = cfg.L * cfg.D
+    if api == "full":
+        f = dg.full_inputs(cfg.B, cfg.L, cfg.D, cfg.seed, io=cfg.io, a_range=cfg.a_range,
+                           bias=True, grad=True)
 
-    def run(rows):
-        s = slice(0, rows)
-        t0 = time.perf_counter()
-        oracle.scan_forward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam)
-        oracle.scan_backward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam, inp.dh[s])
-        return time.perf_counter() - t0
+        def run(rows):
+            s = slice(0, rows)
+            t0 = time.perf_counter()
+            oracle.forward(f.x[s], f.Wr, f.br, f.Wi, f.bi, f.lam)
+            oracle.backward(f.x[s], f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh[s])
+            return time.perf_counter() - t0
+    else:
+        inp = dg.config_inputs(cfg, grad=True)
+
+        def run(rows):
+            s = slice(0, rows)
+            t0 = time.perf_counter()
+            oracle.scan_forward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam)
+            oracle.scan_backward(inp.x[s], inp.zr[s], inp.zi[s], inp.lam, inp.dh[s])
+            return time.perf_counter() - t0
 
     rows = 1
     dt = run(rows)
@@ -87,7 +104,8 @@ def cpu_baseline(cfg, target_s=10.0):
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": passes * rows * per_row / total, "unit": "elements/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"fp64 oracle forward+backward over {rows} of {cfg.B} batch rows "
+            "sample": f"fp64 oracle {'layer' if api == 'full' else 'scan'} forward+backward "
+                      f"over {rows} of {cfg.B} batch rows "
                       f"(L={cfg.L}, D={cfg.D}), {passes} passes, {total:.1f} s"}
 
 
@@ -97,6 +115,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c4")
+    ap.add_argument("--api", choices=["scan", "full"], default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
                     help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
@@ -125,38 +144,65 @@ def main():
         sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")
     dev = torch.device("cuda:0")
     dtype = torch.float32 if cfg.io == "f32" else torch.bfloat16
-    log(f"generating {cfg.name}: B={cfg.B} L={cfg.L} D={cfg.D} {cfg.io}")
-    inp = dg.config_inputs(cfg, grad=True)
-    X, ZR, ZI, DH = (torch.from_numpy(a).to(dev).to(dtype) for a in (inp.x, inp.zr, inp.zi, inp.dh))
-    lam = torch.from_numpy(inp.lam).to(dev)
-    del inp
+    log(f"generating {cfg.name}: B={cfg.B} L={cfg.L} D={cfg.D} {cfg.io} ({args.api} API)")
     B, L, D = cfg.B, cfg.L, cfg.D
     N = B * L * D
     io = rb.io_code(dtype)
     esz = 4 if cfg.io == "f32" else 2
-    h = torch.empty_like(X)
-    hT = torch.empty((B, D), dtype=torch.float32, device=dev)
-    dx, dzr, dzi = torch.empty_like(X), torch.empty_like(X), torch.empty_like(X)
-    dlam = torch.empty(D, dtype=torch.float32, device=dev)
-    dh0 = torch.empty((B, D), dtype=torch.float32, device=dev)
-    nf = rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, B, L, D, io)
-    nb = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, B, L, D, io)
-    wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
-    wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
     s = stream.cuda_stream
     p = lambda t: t.data_ptr()
+    hT = torch.empty((B, D), dtype=torch.float32, device=dev)
+    dlam = torch.empty(D, dtype=torch.float32, device=dev)
+    dh0 = torch.empty((B, D), dtype=torch.float32, device=dev)
+    if args.api == "scan":
+        inp = dg.config_inputs(cfg, grad=True)
+        X, ZR, ZI, DH = (torch.from_numpy(a).to(dev).to(dtype)
+                         for a in (inp.x, inp.zr, inp.zi, inp.dh))
+        lam = torch.from_numpy(inp.lam).to(dev)
+        del inp
+        h = torch.empty_like(X)
+        dx, dzr, dzi = torch.empty_like(X), torch.empty_like(X), torch.empty_like(X)
+        nf = rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, B, L, D, io)
+        nb = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, B, L, D, io)
+        wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
+        wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
 
-    def fwd():
-        st = rb.recblr_bdlru_scan_forward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(hT), B, L, D,
-                                          io, p(wsf), nf, s)
-        assert st == 0, st
+        def fwd():
+            st = rb.recblr_bdlru_scan_forward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(hT), B, L,
+                                              D, io, p(wsf), nf, s)
+            assert st == 0, st
 
-    def bwd():
-        st = rb.recblr_bdlru_scan_backward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(DH), None,
-                                           p(dx), p(dzr), p(dzi), p(dlam), p(dh0), B, L, D, io,
-                                           p(wsb), nb, s)
-        assert st == 0, st
+        def bwd():
+            st = rb.recblr_bdlru_scan_backward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(DH), None,
+                                               p(dx), p(dzr), p(dzi), p(dlam), p(dh0), B, L, D,
+                                               io, p(wsb), nb, s)
+            assert st == 0, st
+    else:
+        f = dg.full_inputs(B, L, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True,
+                           grad=True)
+        X, Wr, br, Wi, bi, DH = (torch.from_numpy(a).to(dev).to(dtype)
+                                 for a in (f.x, f.Wr, f.br, f.Wi, f.bi, f.dh))
+        lam = torch.from_numpy(f.lam).to(dev)
+        del f
+        h, dx = torch.empty_like(X), torch.empty_like(X)
+        dWr, dWi = (torch.empty((D, D), dtype=torch.float32, device=dev) for _ in range(2))
+        dbr, dbi = (torch.empty(D, dtype=torch.float32, device=dev) for _ in range(2))
+        nf = rb.recblr_workspace_size(rb.OP_FORWARD, B, L, D, io)
+        nb = rb.recblr_workspace_size(rb.OP_BACKWARD, B, L, D, io)
+        wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
+        wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+
+        def fwd():
+            st = rb.recblr_bdlru_forward(p(X), p(Wr), p(br), p(Wi), p(bi), p(lam), None, p(h),
+                                         p(hT), B, L, D, io, p(wsf), nf, s)
+            assert st == 0, st
+
+        def bwd():
+            st = rb.recblr_bdlru_backward(p(X), p(Wr), p(br), p(Wi), p(bi), p(lam), None, p(h),
+                                          p(DH), None, p(dx), p(dWr), p(dbr), p(dWi), p(dbi),
+                                          p(dlam), p(dh0), B, L, D, io, p(wsb), nb, s)
+            assert st == 0, st
 
     for _ in range(args.warmup):
         fwd()
@@ -178,8 +224,9 @@ def main():
     t_bwd = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
     step_s = wall / K
     fb_s = float(np.mean(t_fwd + t_bwd))
-    fwd_bytes = FWD_ARRAYS * esz * N
-    bwd_bytes = BWD_ARRAYS * esz * N
+    fwd_arrays, bwd_arrays = ARRAYS[args.api]
+    fwd_bytes = fwd_arrays * esz * N
+    bwd_bytes = bwd_arrays * esz * N
     fwd_gbs = fwd_bytes / float(np.mean(t_fwd)) / 1e9
     bwd_gbs = bwd_bytes / float(np.mean(t_bwd)) / 1e9
     dom = "bwd" if np.mean(t_bwd) >= np.mean(t_fwd) else "fwd"
@@ -187,8 +234,11 @@ def main():
     log(f"fwd {np.mean(t_fwd)*1e6:.1f} us ({fwd_gbs:.0f} GB/s)  bwd {np.mean(t_bwd)*1e6:.1f} us "
         f"({bwd_gbs:.0f} GB/s)  wall/step {step_s*1e6:.1f} us")
 
+    full = args.api == "full"
+    kname = ("layer_" if full else "scan_") + dom
     out = {
-        "metric": "BD-LRU scan elements/sec (B*L*D), forward+backward",
+        "metric": ("BD-LRU layer (gate projections + scan)" if full else "BD-LRU scan")
+                  + " elements/sec (B*L*D), forward+backward",
         "value": N / step_s,
         "unit": "elements/s",
         "n_gpus": 1,
@@ -200,7 +250,8 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.io,
         "data": "synthetic (seeded normal x, z, dL/dh; decay bases per the paper's initialisation)",
-        "config": {"workload": f"{cfg.name}: BD-LRU scan forward+backward, {cfg.note}",
+        "config": {"workload": f"{cfg.name}: BD-LRU {'layer' if full else 'scan'} "
+                               f"forward+backward, {cfg.note}",
                    "B": B, "L": L, "D": D, "io": cfg.io, "elements": N},
         "fwd_elements_per_s": N / float(np.mean(t_fwd)),
         "fwd_bwd_elements_per_s_events": N / fb_s,
@@ -208,14 +259,14 @@ def main():
         "us_bwd": float(np.mean(t_bwd)) * 1e6,
         "fwd_hbm_gbs": fwd_gbs,
         "bwd_hbm_gbs": bwd_gbs,
-        "roofline": {"bound": "hbm", "kernel": "scan_bwd" if dom == "bwd" else "scan_fwd",
+        "roofline": {"bound": "hbm", "kernel": kname,
                      "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": ach / PEAK_HBM_GBS,
-                     "traffic": traffic_bytes(cfg.name, "scan_bwd" if dom == "bwd" else "scan_fwd")},
+                     "traffic": traffic_bytes(cfg.name, kname)},
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 CPU oracle on a bounded sample ...")
-        out["cpu_baseline"] = cpu_baseline(cfg)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.api)
     print(json.dumps(out), flush=True)
 
 

@@ -278,6 +278,42 @@ def test_config_decode_full_size(rb):
     assert_close(host(got), want, cfg.io, "decode h_next")
 
 
+@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+def test_config_full_api(rb, name):
+    """Entry points with gate parameters at the workload's full size.
+
+    The forward is checked on sampled batch rows (rows are independent).  The
+    backward runs with dL/dh nonzero only on the sampled rows, so every other
+    row has zero gradient and the weight gradients, summed over all B*L rows by
+    the full launch, equal the oracle's over the sampled rows alone.
+    """
+    import torch
+    cfg = dg.CONFIGS[name]
+    io = cfg.io
+    f = dg.full_inputs(cfg.B, cfg.L, cfg.D, cfg.seed + 100, io=io, a_range=cfg.a_range,
+                       bias=True, grad=True)
+    rows = _sample_rows(cfg.B)
+    mask = np.zeros((cfg.B, 1, 1), np.float32)
+    mask[rows] = 1.0
+    dh = f.dh * mask
+    X, Wr, br, Wi, bi = (dev(a, io) for a in (f.x, f.Wr, f.br, f.Wi, f.bi))
+    lam = dev32(f.lam)
+    h, hT = rb.bdlru_forward(X, Wr, br, Wi, bi, lam)
+    got = rb.bdlru_backward(X, Wr, br, Wi, bi, lam, h, dev(dh, io))
+    torch.cuda.synchronize()
+    print(f"full API {name}: GPU done", flush=True)
+    sub = lambda a: a[rows]
+    oh, ohT = oracle.forward(sub(f.x), f.Wr, f.br, f.Wi, f.bi, f.lam)
+    assert_close(host(h[rows]), oh, io, f"{name} h")
+    assert_close(host(hT[rows]), ohT, io, f"{name} hT")
+    want = oracle.backward(sub(f.x), f.Wr, f.br, f.Wi, f.bi, f.lam, sub(dh))
+    assert_close(host(got["dx"][rows]), want["dx"], io, f"{name} dx")
+    for k in ("dWr", "dbr", "dWi", "dbi", "dlambda"):
+        assert_close(host(got[k]), want[k], io, f"{name} {k}")
+    others = np.setdiff1d(np.arange(cfg.B), rows)
+    assert not host(got["dx"][others]).any(), "rows with zero dL/dh must get dx = 0"
+
+
 # ------------------------------------------------------------------ kernel modes
 # Few channel groups and long sequences run the look-back kernels; many
 # channel groups run the chain kernels.  Forward chain lanes carry 1, 2 or 4
