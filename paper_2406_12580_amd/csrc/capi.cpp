@@ -70,21 +70,23 @@ size_t esz(int io) { return io == RECBLR_BF16 ? 2 : 4; }
 
 // ---- workspace layouts of the entry points with gate parameters
 struct FullFwdLayout {
-    size_t zr, zi, scan, total;
+    size_t zr, zi, pack, scan, total;
 };
-// z and dz scratch is fp32 whatever the I/O type.
+// z and dz scratch is fp32 whatever the I/O type; z_i follows z_r (and dz_i
+// follows dz_r) in the same workspace, which the projection kernels rely on.
 FullFwdLayout full_fwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     size_t zbytes = align_up((size_t)(B * L * D) * sizeof(float));
     FullFwdLayout l;
     l.zr = 0;
     l.zi = zbytes;
-    l.scan = 2 * zbytes;
+    l.pack = 2 * zbytes;
+    l.scan = l.pack + align_up(project_pack_workspace(D, io_of(io)));
     l.total = l.scan + align_up(scan_forward_workspace(B, L, D, io_of(io)));
     return l;
 }
 
 struct FullBwdLayout {
-    size_t zr, zi, dzr, dzi, scan, dw, total;
+    size_t zr, zi, dzr, dzi, pack, scan, dw, total;
 };
 FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     size_t zbytes = align_up((size_t)(B * L * D) * sizeof(float));
@@ -93,13 +95,18 @@ FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     l.zi = zbytes;
     l.dzr = 2 * zbytes;
     l.dzi = 3 * zbytes;
-    l.scan = 4 * zbytes;
+    l.pack = 4 * zbytes;
+    l.scan = l.pack + align_up(project_pack_workspace(D, io_of(io)));
     l.dw = l.scan + align_up(scan_backward_workspace(B, L, D, io_of(io)));
     l.total = l.dw + align_up(project_dw_workspace(B * L, D));
     return l;
 }
 
-size_t step_ws(int64_t B, int64_t D, int) { return 2 * align_up((size_t)(B * D) * sizeof(float)); }
+// Step: z_r, z_i scratch, then the packed weights.
+size_t step_z_bytes(int64_t B, int64_t D) { return align_up((size_t)(B * D) * sizeof(float)); }
+size_t step_ws(int64_t B, int64_t D, int io) {
+    return 2 * step_z_bytes(B, D) + align_up(project_pack_workspace(D, io_of(io)));
+}
 
 char* at(void* ws, size_t off) { return (char*)ws + off; }
 
@@ -232,7 +239,8 @@ int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const 
     hipStream_t strm = (hipStream_t)stream;
     void* zr = at(ws, lay.zr);
     void* zi = at(ws, lay.zi);
-    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B * L, D, io_of(io), strm);
+    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B * L, D, io_of(io),
+                                          at(ws, lay.pack), strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     ScanFwdArgs a{x, zr, zi, lambda, h0, h, hT, B, L, D, io_of(io), IoType::kF32,
                   at(ws, lay.scan), lay.total - lay.scan};
@@ -284,13 +292,15 @@ int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const
         return RECBLR_OK;
     }
     const int64_t M = B * L;
-    e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, M, D, io_of(io), strm);
+    e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, M, D, io_of(io), at(ws, lay.pack),
+                               strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     ScanBwdArgs a{x, zr, zi, lambda, h0, h, dh, dhT, dx, dzr, dzi, dlambda, dh0,
                   B, L, D, io_of(io), IoType::kF32, at(ws, lay.scan), lay.dw - lay.scan};
     e = launch_scan_backward(a, strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
-    e = launch_project_backward_data(dzr, dzi, W_r, W_i, dx, M, D, io_of(io), strm);
+    e = launch_project_backward_data(dzr, dzi, W_r, W_i, dx, M, D, io_of(io), at(ws, lay.pack),
+                                     strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     e = launch_project_backward_weights(dzr, dzi, x, dW_r, db_r, dW_i, db_i, M, D, io_of(io),
                                         at(ws, lay.dw), strm);
@@ -320,8 +330,9 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
     if (st) return st;
     hipStream_t strm = (hipStream_t)stream;
     void* zr = ws;
-    void* zi = at(ws, need / 2);
-    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B, D, io_of(io), strm);
+    void* zi = at(ws, step_z_bytes(B, D));
+    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B, D, io_of(io),
+                                          at(ws, 2 * step_z_bytes(B, D)), strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     return status_of(
         launch_scan_step(x, zr, zi, lambda, h_prev, h_next, B, D, io_of(io), IoType::kF32, strm));

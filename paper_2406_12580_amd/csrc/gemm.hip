@@ -234,123 +234,173 @@ __global__ void proj_dw_reduce_kernel(const float* partial, int64_t splits, int6
 }
 
 // ------------------------------------------------------------------ fast path
-// Taken when D % 8 == 0 and the operands are 16-byte aligned (every workload
-// shape of the paper).  A 256-thread workgroup computes a 128 x 128 tile of
-// C = A B; each wave owns a 64 x 64 quarter as 4 x 4 blocks of
-// v_mfma_f32_16x16x32_bf16.  An fp32 operand is split on load into
-// hi = bf16(v) and lo = bf16(v - hi) and the product is formed from the three
-// terms hi*hi + hi*lo + lo*hi (a bf16 operand is exact and needs one plane):
-// each product then carries a relative error below 3 * 2^-17 against 2^-24
-// for a plain fp32 product, while the matrix cores deliver 16x the fp32 MFMA
-// rate, so the projection stays bound by HBM instead of by fp32 MFMA.
-// Operand quads (4 consecutive elements along the contiguous memory index)
-// are prefetched into registers for the next K-slice while the current slice
-// is multiplied from LDS.  Tiles are ordered so that consecutive tiles of one
-// row block land on the same XCD and share its L2.
+// Taken when D % 8 == 0, the operands are 16-byte aligned and every operand
+// spans less than 2 GiB (all workload shapes of the paper).  A 256-thread
+// workgroup computes a 128 x 128 tile of C = A B^T (A: rows m, B: rows n, both
+// over the contracted index k); each wave owns a 64 x 64 quarter as 4 x 4
+// blocks of v_mfma_f32_16x16x32_bf16.  An fp32 operand is split into
+// hi = bf16(v) and lo = bf16(v - hi) and a product of two fp32 operands is
+// formed from the three terms hi*hi + hi*lo + lo*hi (a bf16 operand is exact
+// and needs one plane): each product then carries a relative error below
+// 3 * 2^-17 against 2^-24 for a plain fp32 product, while the matrix cores
+// deliver 16x the fp32 MFMA rate, so the projection stays bound by HBM
+// instead of by fp32 MFMA.  The weights are packed once per call into bf16
+// planes laid out the way the tiles read them.
+//
+// Operands are read through buffer resources at per-lane 32-bit byte
+// offsets computed once per tile; offsets at or past a resource's size read
+// zero, which masks the contraction tail.  Operand quads (4 consecutive
+// elements along the contiguous memory index) for the next K-slice are
+// loaded into registers while the current slice is multiplied from LDS.
+// Tiles are numbered so that consecutive tiles of one row block land on the
+// same XCD and share its L2.
 namespace fastmm {
-#ifndef RECBLR_GEMM_BK
-#define RECBLR_GEMM_BK 64
-#endif
-constexpr int BM = 128, BN = 128, BK = RECBLR_GEMM_BK;
-static_assert(BK == 32 || BK == 64, "K-slice depth");
+constexpr int BM = 128, BN = 128, BK = 64;
 constexpr int NQ = BK / 8;  // quads per thread and operand in one slice
-// LDS row pitch (bf16 elements): BK + 8 keeps rows 16-byte aligned and the
-// fragment reads of 8 consecutive rows on distinct banks.
-constexpr int KP = BK + 8;
+// LDS tiles hold BK bf16 per row (128 bytes); the 16-byte chunk j of row r is
+// stored at chunk j ^ f(r) with f(r) = (r ^ (r >> 2)) mod 8, so that the
+// fragment reads (8 consecutive rows, one chunk) and the transposed stores
+// (rows 4m + c for consecutive m, one chunk) each touch 8 distinct chunk
+// positions.
+constexpr int KP = BK;
+constexpr uint32_t kOOB = 0x80000000u;  // at or past every resource size: loads return 0
+
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef float f8 __attribute__((ext_vector_type(8)));
 typedef __bf16 b4 __attribute__((ext_vector_type(4)));
 typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
-// A quad (4 consecutive elements) as loaded: fp32 values or raw bf16 bits.
-__device__ __forceinline__ f4 raw_quad(const float* p) { return *(const f4*)p; }
-__device__ __forceinline__ uint2 raw_quad(const bf16* p) { return *(const uint2*)p; }
+// Column (bf16 elements) at which element k of LDS row `row` is stored.
+__device__ __forceinline__ int lds_col(int row, int k) {
+    const int f = (row ^ (row >> 2)) & 7;
+    return (((k >> 3) ^ f) << 3) | (k & 7);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t resource(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
 __device__ __forceinline__ f4 widen(f4 v) { return v; }
-__device__ __forceinline__ f4 widen(uint2 v) {
+__device__ __forceinline__ f4 widen(u2v v) {
     return f4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
               __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u)};
 }
-__device__ __forceinline__ f4 load_quad(const float* p) { return raw_quad(p); }
-__device__ __forceinline__ f4 load_quad(const bf16* p) { return widen(raw_quad(p)); }
-// Element c of a raw quad as 16 bf16 bits.
-__device__ __forceinline__ uint32_t bits16(uint2 v, int c) {
+// Element c of four packed bf16 as 16 bits.
+__device__ __forceinline__ uint32_t bits16(u2v v, int c) {
     const uint32_t w = c < 2 ? v.x : v.y;
     return (c & 1) ? w >> 16 : w & 0xffffu;
 }
 
-// Memory views: at(row, col) points at element (row, col), contiguous along col.
-template <typename T>
-struct PlainMem {
-    const T* p;
-    int64_t ld;
-    __device__ const T* at(int64_t row, int64_t col) const { return p + row * ld + col; }
-};
-// Rows [0, split) come from p0, the rest from p1 (both with pitch ld).
-template <typename T>
-struct RowPairMem {
-    const T* p0;
-    const T* p1;
-    int64_t split, ld;
-    __device__ const T* at(int64_t row, int64_t col) const {
-        return row < split ? p0 + row * ld + col : p1 + (row - split) * ld + col;
-    }
-};
-// Columns [0, split) come from p0, the rest from p1 (both with pitch split).
-template <typename T>
-struct ColPairMem {
-    const T* p0;
-    const T* p1;
-    int64_t split;
-    __device__ const T* at(int64_t row, int64_t col) const {
-        return col < split ? p0 + row * split + col : p1 + row * split + (col - split);
-    }
+// Kinds of operand data.
+enum Kind {
+    kF32,    // fp32 values, split into hi and lo planes on the way to LDS
+    kBf16,   // bf16 values, one plane
+    kPack1,  // packed weights: one bf16 plane
+    kPack2,  // packed weights: bf16 hi and lo planes
 };
 
-// Operand with element (mn, k): mn is the row of A (or column of B), k the
-// contracted index.  KFAST: memory is contiguous along k (element at
-// mem.at(mn, k)); otherwise along mn (element at mem.at(k, mn)).  mn_end is
-// the number of valid mn (a multiple of 4).
-template <typename T, bool KFAST, class Mem>
+template <int KIND>
+struct RawOf {
+    using type = u2v;
+};
+template <>
+struct RawOf<kF32> {
+    using type = f4;
+};
+template <>
+struct RawOf<kPack2> {
+    struct type {
+        u2v p[2];
+    };
+};
+
+// Operand with element (mn, k): mn is the output row (A) or column (B), k the
+// contracted index.  KFAST: memory rows are mn and k runs along them;
+// otherwise memory rows are k.  Byte offset of memory element (row, col):
+// row * pitch + col_off(col), where PAIR operands hold columns [0, half) at
+// byte 0 and [half, 2 half) at byte hoff (the two gates' fp32 scratch).
+template <int KIND, bool KFAST, bool PAIR = false>
 struct Operand {
+    static constexpr int kKind = KIND;
     static constexpr bool kKFast = KFAST;
-    static constexpr int kPlanes = sizeof(T) == 4 ? 2 : 1;
-    using raw_t = decltype(raw_quad((const T*)nullptr));
-    Mem mem;
-    int64_t mn_end;
-    __device__ raw_t quad(int64_t mn, int64_t k) const {
-        return raw_quad(KFAST ? mem.at(mn, k) : mem.at(k, mn));
+    static constexpr int kPlanes = (KIND == kF32 || KIND == kPack2) ? 2 : 1;
+    static constexpr uint32_t kEsz = KIND == kF32 ? 4 : 2;
+    using raw_t = typename RawOf<KIND>::type;
+    __amdgpu_buffer_rsrc_t rsrc;
+    uint32_t pitch;  // bytes per memory row
+    uint32_t half;   // PAIR: columns per half
+    uint32_t hoff;   // PAIR: byte offset of the second half
+    uint32_t plane;  // kPack2: bytes per plane
+    __device__ uint32_t col_off(int64_t c) const {
+        if constexpr (PAIR)
+            return c < half ? (uint32_t)c * 4u : hoff + (uint32_t)(c - half) * 4u;
+        else
+            return (uint32_t)c * kEsz;
+    }
+    __device__ uint32_t row_off(int64_t r) const {
+        const uint64_t o = (uint64_t)r * pitch;
+        return o < kOOB ? (uint32_t)o : kOOB;
+    }
+    __device__ raw_t load(uint32_t off) const {
+        if constexpr (KIND == kF32) {
+            const u4v v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+            return f4{__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                      __uint_as_float(v.w)};
+        } else if constexpr (KIND == kPack2) {
+            raw_t r;
+            r.p[0] = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
+            r.p[1] = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off + plane, 0, 0);
+            return r;
+        } else {
+            return __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
+        }
     }
 };
 
-// Staging of one operand's 128 x BK slice: NQ = BK / 8 quads per thread.
-//   KFAST: quad j covers (mn = e / (BK / 4), k = 4 (e % (BK / 4)) .. +3) with e = tid + 256 j.
+// Per-thread staging of one operand's 128 x BK slices: NQ quads per thread.
+//   KFAST: quad j covers (mn = tid / 16 + 16 j, k = 4 (tid % 16) .. +3).
 //   else : quad j covers (mn = 4 (tid % 32) .. +3, k = NQ (tid / 32) + j).
+// The per-tile part of the byte offsets is fixed at construction; quad j
+// adds j times a uniform stride (16 memory rows, or one memory row).  The
+// launch bounds keep every in-tile row offset below 2^31.
 template <class Op>
-__device__ __forceinline__ void fetch_slice(const Op& op, int64_t mn0, int64_t k0, int64_t k_end,
-                                            int tid, typename Op::raw_t (&r)[NQ]) {
-#pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-        int64_t mn, k;
-        if constexpr (Op::kKFast) {
-            const int e = tid + 256 * j;
-            mn = mn0 + e / (BK / 4);
-            k = k0 + 4 * (e % (BK / 4));
-        } else {
-            mn = mn0 + 4 * (tid & 31);
-            k = k0 + NQ * (tid >> 5) + j;
-        }
-        r[j] = (mn < op.mn_end && k < k_end) ? op.quad(mn, k) : typename Op::raw_t{};
+struct Stager {
+    uint32_t fixed;
+    __device__ Stager(const Op& op, int64_t mn0, int tid) {
+        if constexpr (Op::kKFast)
+            fixed = op.row_off(mn0 + (tid >> 4));
+        else
+            fixed = op.col_off(mn0 + 4 * (tid & 31));
     }
-}
+    // Loads the slice starting at k0 (zeros for k >= k_end).
+    __device__ void fetch(const Op& op, int64_t k0, int64_t k_end, int tid,
+                          typename Op::raw_t (&r)[NQ]) const {
+        if constexpr (Op::kKFast) {
+            const int64_t k = k0 + 4 * (tid & 15);
+            const uint32_t base = fixed + (k < k_end ? op.col_off(k) : kOOB);
+            const uint32_t step = 16 * op.pitch;
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) r[j] = op.load(base + j * step);
+        } else {
+            const int64_t k = k0 + NQ * (tid >> 5);
+            const uint32_t base = op.row_off(k) + fixed;
+            if (k0 + BK <= k_end) {
+#pragma unroll
+                for (int j = 0; j < NQ; ++j) r[j] = op.load(base + j * op.pitch);
+            } else {
+#pragma unroll
+                for (int j = 0; j < NQ; ++j)
+                    r[j] = op.load(k + j < k_end ? base + j * op.pitch : kOOB);
+            }
+        }
+    }
+};
 
 template <int N>
 struct PackT;
-template <>
-struct PackT<4> {
-    using bits = uint2;
-    using fv = f4;
-    using bv = b4;
-};
 template <>
 struct PackT<8> {
     using bits = uint4;
@@ -358,45 +408,50 @@ struct PackT<8> {
     using bv = b8;
 };
 
+// Writes a staged slice to the operand's LDS planes.
 template <class Op>
 __device__ __forceinline__ void store_slice(__bf16 (*lds)[BM][KP], int tid,
                                             const typename Op::raw_t (&r)[NQ]) {
-    constexpr int P = Op::kPlanes;
+    constexpr int KIND = Op::kKind;
     if constexpr (Op::kKFast) {
 #pragma unroll
         for (int j = 0; j < NQ; ++j) {
-            const int e = tid + 256 * j;
-            const int row = e / (BK / 4), kc = 4 * (e % (BK / 4));
-            if constexpr (P == 1) {
-                *(uint2*)&lds[0][row][kc] = r[j];  // bf16 input: store the bits as they are
-            } else {
-                const f4 v = widen(r[j]);
+            const int row = (tid >> 4) + 16 * j, col = lds_col(row, 4 * (tid & 15));
+            if constexpr (KIND == kF32) {
+                const f4 v = r[j];
                 const b4 hi = __builtin_convertvector(v, b4);
-                *(b4*)&lds[0][row][kc] = hi;
-                *(b4*)&lds[1][row][kc] =
+                *(b4*)&lds[0][row][col] = hi;
+                *(b4*)&lds[1][row][col] =
                     __builtin_convertvector(v - __builtin_convertvector(hi, f4), b4);
+            } else if constexpr (KIND == kPack2) {
+                *(u2v*)&lds[0][row][col] = r[j].p[0];
+                *(u2v*)&lds[1][row][col] = r[j].p[1];
+            } else {
+                *(u2v*)&lds[0][row][col] = r[j];  // bf16 bits as they are
             }
         }
     } else {
+        static_assert(KIND == kF32 || KIND == kBf16, "transposed staging of packed weights");
         // Transpose in registers: column c of the thread's quads becomes NQ
         // consecutive k of LDS row 4 mq + c.
         using PK = PackT<NQ>;
         const int mq = tid & 31, kc = NQ * (tid >> 5);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            if constexpr (P == 1) {
+            const int row = 4 * mq + c, col = lds_col(row, kc);
+            if constexpr (KIND == kBf16) {
                 uint32_t w[NQ / 2];
 #pragma unroll
                 for (int j = 0; j < NQ / 2; ++j)
                     w[j] = bits16(r[2 * j], c) | (bits16(r[2 * j + 1], c) << 16);
-                *(typename PK::bits*)&lds[0][4 * mq + c][kc] = *(const typename PK::bits*)w;
+                *(typename PK::bits*)&lds[0][row][col] = *(const typename PK::bits*)w;
             } else {
                 typename PK::fv v;
 #pragma unroll
-                for (int j = 0; j < NQ; ++j) v[j] = widen(r[j])[c];
+                for (int j = 0; j < NQ; ++j) v[j] = r[j][c];
                 const typename PK::bv hi = __builtin_convertvector(v, typename PK::bv);
-                *(typename PK::bv*)&lds[0][4 * mq + c][kc] = hi;
-                *(typename PK::bv*)&lds[1][4 * mq + c][kc] = __builtin_convertvector(
+                *(typename PK::bv*)&lds[0][row][col] = hi;
+                *(typename PK::bv*)&lds[1][row][col] = __builtin_convertvector(
                     v - __builtin_convertvector(hi, typename PK::fv), typename PK::bv);
             }
         }
@@ -422,29 +477,31 @@ __device__ __forceinline__ void mma_slice(__bf16 (*la)[BM][KP], __bf16 (*lb)[BN]
                                           f4 (&acc)[4][4], int wm, int wn, int fr, int fk) {
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 32) {
-        b8 fa[PA][4], fb[PB][4];
+        b8 fa[PA][4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+            const int ra = wm * 64 + i * 16 + fr;
 #pragma unroll
-            for (int p = 0; p < PA; ++p)
-                fa[p][i] = *(const b8*)&la[p][wm * 64 + i * 16 + fr][ks + fk];
-#pragma unroll
-            for (int p = 0; p < PB; ++p)
-                fb[p][i] = *(const b8*)&lb[p][wn * 64 + i * 16 + fr][ks + fk];
+            for (int p = 0; p < PA; ++p) fa[p][i] = *(const b8*)&la[p][ra][lds_col(ra, ks + fk)];
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) {
+            const int rb = wn * 64 + j * 16 + fr;
+            b8 fb[PB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int p = 0; p < PB; ++p) fb[p] = *(const b8*)&lb[p][rb][lds_col(rb, ks + fk)];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
                 if constexpr (PB == 2)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][i], fb[1][j],
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][i], fb[1],
                                                                          acc[i][j], 0, 0, 0);
                 if constexpr (PA == 2)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1][i], fb[0][j],
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1][i], fb[0],
                                                                          acc[i][j], 0, 0, 0);
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][i], fb[0][j],
-                                                                     acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][i], fb[0], acc[i][j],
+                                                                     0, 0, 0);
             }
+        }
     }
 }
 
@@ -494,7 +551,8 @@ __device__ __forceinline__ void tile_epilogue(const f4 (&acc)[4][4], char* smem,
         strip_rows(m0w, i, lane, m);
         f4 val[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) val[q] = *(const f4*)&buf[(4 * q + (lane >> 4)) * EP + 4 * (lane & 15)];
+        for (int q = 0; q < 4; ++q)
+            val[q] = *(const f4*)&buf[(4 * q + (lane >> 4)) * EP + 4 * (lane & 15)];
         typename Epi::pre_t next{};
         if (i < 3) {
             int64_t mn[4];
@@ -507,18 +565,15 @@ __device__ __forceinline__ void tile_epilogue(const f4 (&acc)[4][4], char* smem,
     }
 }
 
-// A run of output tiles: tiles first, first + stride, ... (count of them),
-// tile t at rows (t / ntn) * BM and columns (t % ntn) * BN, each the sum over
-// k in [k_begin, k_end) of A(m, k) B(n, k), handed to epi.  The first
-// K-slice of the next tile is fetched during the last slice of the current
-// one, and so are the epilogue's reads of the destination.  If colsum_out is
-// not null (A not KFAST, count 1), the sums over the same k range of the
-// tile's 128 rows of A are written there.
+// One output tile at (m0, n0): the sum over k in [k_begin, k_end) of
+// A(m, k) B(n, k), handed to epi.  The next K-slice is loaded during the
+// current slice's MFMAs, and during the last slice the epilogue's reads of
+// the destination.  If colsum_out is not null (A not KFAST), the sums over the
+// same k range of the tile's 128 rows of A are written there.
 template <class OpA, class OpB, class Epi>
-__device__ __forceinline__ void tile_stream(const OpA& a, const OpB& b, int64_t k_begin,
-                                            int64_t k_end, int64_t ntn, int64_t first,
-                                            int64_t count, int64_t stride, const Epi& epi,
-                                            char* smem, float* colsum_out = nullptr) {
+__device__ __forceinline__ void tile(const OpA& a, const OpB& b, int64_t m0, int64_t n0,
+                                     int64_t k_begin, int64_t k_end, const Epi& epi, char* smem,
+                                     float* colsum_out = nullptr) {
     constexpr int PA = OpA::kPlanes, PB = OpB::kPlanes;
     __bf16 (*la)[BM][KP] = (__bf16 (*)[BM][KP])smem;
     __bf16 (*lb)[BN][KP] = (__bf16 (*)[BN][KP])(smem + (size_t)PA * BM * KP * 2);
@@ -527,70 +582,65 @@ __device__ __forceinline__ void tile_stream(const OpA& a, const OpB& b, int64_t 
     const int wv = tid >> 6;
     const int wm = wv >> 1, wn = wv & 1;
     const int fr = lane & 15, fk = 8 * (lane >> 4);
+    const int64_t m0w = m0 + wm * 64, n0w = n0 + wn * 64;
     const int64_t nsl = k_end > k_begin ? (k_end - k_begin + BK - 1) / BK : 0;
-    if (count <= 0) return;
 
+    const Stager<OpA> sa(a, m0, tid);
+    const Stager<OpB> sb(b, n0, tid);
     typename OpA::raw_t ra[NQ];
     typename OpB::raw_t rb[NQ];
     f4 cs = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    int64_t t = first;
-    if (nsl > 0) {
-        fetch_slice(a, (t / ntn) * BM, k_begin, k_end, tid, ra);
-        fetch_slice(b, (t % ntn) * BN, k_begin, k_end, tid, rb);
-    }
-    for (int64_t c = 0; c < count; ++c, t += stride) {
-        const int64_t m0 = (t / ntn) * BM, n0 = (t % ntn) * BN;
-        const int64_t m0w = m0 + wm * 64, n0w = n0 + wn * 64;
-        f4 acc[4][4];
+    f4 acc[4][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-        typename Epi::pre_t pre{};
-        if (nsl == 0) {
-            int64_t m[4];
-            strip_rows(m0w, 0, lane, m);
-            epi.load(m, n0w + 4 * (lane & 15), pre);
-        }
-        for (int64_t sl = 0; sl < nsl; ++sl) {
+        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    typename Epi::pre_t pre{};
+    int64_t mr[4];
+    strip_rows(m0w, 0, lane, mr);
+    const int64_t ne = n0w + 4 * (lane & 15);
+
+    if (nsl == 0) {
+        epi.load(mr, ne, pre);
+    } else {
+        sa.fetch(a, k_begin, k_end, tid, ra);
+        sb.fetch(b, k_begin, k_end, tid, rb);
+        for (int64_t sl = 0; sl + 1 < nsl; ++sl) {
             store_slice<OpA>(la, tid, ra);
             store_slice<OpB>(lb, tid, rb);
             if constexpr (!OpA::kKFast)
                 if (colsum_out) add_colsum(cs, ra);
             __syncthreads();
-            if (sl + 1 < nsl) {
-                const int64_t k0 = k_begin + (sl + 1) * BK;
-                fetch_slice(a, m0, k0, k_end, tid, ra);
-                fetch_slice(b, n0, k0, k_end, tid, rb);
-            } else {
-                if (c + 1 < count) {
-                    const int64_t tn = t + stride;
-                    fetch_slice(a, (tn / ntn) * BM, k_begin, k_end, tid, ra);
-                    fetch_slice(b, (tn % ntn) * BN, k_begin, k_end, tid, rb);
-                }
-                int64_t m[4];
-                strip_rows(m0w, 0, lane, m);
-                epi.load(m, n0w + 4 * (lane & 15), pre);
-            }
+            const int64_t k0 = k_begin + (sl + 1) * BK;
+            sa.fetch(a, k0, k_end, tid, ra);
+            sb.fetch(b, k0, k_end, tid, rb);
             mma_slice<PA, PB>(la, lb, acc, wm, wn, fr, fk);
             __syncthreads();
         }
-        if (!OpA::kKFast && colsum_out) {
-            // Reduce the 8 k-groups of each column quad through LDS.
-            f4* red = (f4*)smem;
-            red[tid] = cs;
-            __syncthreads();
-            if (tid < 32) {
-                f4 v = red[tid];
-#pragma unroll
-                for (int g = 1; g < 8; ++g) v += red[tid + 32 * g];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) colsum_out[4 * tid + q] = v[q];
-            }
-            __syncthreads();
-        }
-        tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+        store_slice<OpA>(la, tid, ra);
+        store_slice<OpB>(lb, tid, rb);
+        if constexpr (!OpA::kKFast)
+            if (colsum_out) add_colsum(cs, ra);
+        __syncthreads();
+        epi.load(mr, ne, pre);
+        mma_slice<PA, PB>(la, lb, acc, wm, wn, fr, fk);
+        __syncthreads();
     }
+    if (!OpA::kKFast && colsum_out) {
+        // Reduce the 8 k-groups of each column quad through LDS.
+        f4* red = (f4*)smem;
+        red[tid] = cs;
+        __syncthreads();
+        if (tid < 32) {
+            f4 v = red[tid];
+#pragma unroll
+            for (int g = 1; g < 8; ++g) v += red[tid + 32 * g];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) colsum_out[4 * tid + q] = v[q];
+        }
+        __syncthreads();
+    }
+    tile_epilogue(acc, smem, m0w, n0w, epi, pre);
 }
 
 // Logical tile of this workgroup: the hardware deals consecutive workgroup ids
@@ -604,6 +654,31 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t tiles) {
 }
 
 inline unsigned grid_of(int64_t tiles) { return (unsigned)((tiles + 7) & ~(int64_t)7); }
+
+// ---- weight packing: bf16 planes (hi, and lo = bf16(w - hi) for fp32 weights)
+// of Wcat = [W_r; W_i] ([2D x D]) in the layouts the tiles read:
+//   forward: P[n][k] = Wcat[n][k] (n < 2D, k < D)
+//   dx:      P[n][k] = Wcat[k][n] (n < D, k < 2D)
+template <typename T, bool TRANSPOSED>
+__global__ __launch_bounds__(256) void pack_kernel(const T* wr, const T* wi, __bf16* out,
+                                                   int64_t D) {
+    const int64_t total = 2 * D * D;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= total) return;
+    int64_t row, col;  // element of Wcat
+    if (TRANSPOSED) {
+        const int64_t n = e / (2 * D), k = e % (2 * D);
+        row = k;
+        col = n;
+    } else {
+        row = e / D;
+        col = e % D;
+    }
+    const float v = row < D ? to_f32(wr[row * D + col]) : to_f32(wi[(row - D) * D + col]);
+    const __bf16 hi = (__bf16)v;
+    out[e] = hi;
+    if (sizeof(T) == 4) out[total + e] = (__bf16)(v - (float)hi);
+}
 
 template <typename T>
 struct FwdEpi {
@@ -620,7 +695,8 @@ struct FwdEpi {
         if (n >= 2 * D) return;
         const T* bp = n < D ? br : bi;
         const int64_t o = n < D ? n : n - D;
-        if (bp) pre.bias = f4{recblr::load(bp + o), recblr::load(bp + o + 1), recblr::load(bp + o + 2), recblr::load(bp + o + 3)};
+        if (bp)
+            pre.bias = f4{to_f32(bp[o]), to_f32(bp[o + 1]), to_f32(bp[o + 2]), to_f32(bp[o + 3])};
     }
     __device__ void run(const int64_t (&m)[4], int64_t n, const f4 (&v)[4],
                         const pre_t& pre) const {
@@ -632,19 +708,24 @@ struct FwdEpi {
     }
 };
 
-// One 128 x 128 tile of [z_r | z_i] (M x 2D) per workgroup.
+// One 128 x 128 tile of [z_r | z_i] (M x 2D) per workgroup; pack holds the
+// forward weight planes.
 template <typename T>
-__global__ __launch_bounds__(256, 2) void fwd_kernel(const T* x, const T* wr, const T* br,
-                                                     const T* wi, const T* bi, float* zr,
+__global__ __launch_bounds__(256, 2) void fwd_kernel(const T* x, const __bf16* pack,
+                                                     const T* br, const T* bi, float* zr,
                                                      float* zi, int64_t M, int64_t D) {
-    using OpA = Operand<T, true, PlainMem<T>>;
-    using OpB = Operand<T, true, RowPairMem<T>>;
+    constexpr bool F32 = sizeof(T) == 4;
+    using OpA = Operand<F32 ? kF32 : kBf16, true>;
+    using OpB = Operand<F32 ? kPack2 : kPack1, true>;
     __shared__ __attribute__((aligned(16))) char smem[lds_bytes<OpA::kPlanes, OpB::kPlanes>()];
     const int64_t ntn = (2 * D + BN - 1) / BN;
     const int64_t t = xcd_tile(((M + BM - 1) / BM) * ntn);
     if (t < 0) return;
+    const uint32_t plane = (uint32_t)(2 * D * D * 2);
+    const OpA a{resource(x, (uint32_t)(M * D * sizeof(T))), (uint32_t)(D * sizeof(T)), 0, 0, 0};
+    const OpB b{resource(pack, OpB::kPlanes * plane), (uint32_t)(D * 2), 0, 0, plane};
     const FwdEpi<T> epi{zr, zi, br, bi, M, D};
-    tile_stream(OpA{{x, D}, M}, OpB{{wr, wi, D, D}, 2 * D}, 0, D, ntn, t, 1, 1, epi, smem);
+    tile(a, b, (t / ntn) * BM, (t % ntn) * BN, 0, D, epi, smem);
 }
 
 template <typename T>
@@ -654,21 +735,21 @@ struct DxEpi {
     };
     T* dx;
     int64_t M, D;
+    __device__ static f4 get(const float* p) { return *(const f4*)p; }
+    __device__ static f4 get(const bf16* p) { return widen(*(const u2v*)p); }
     // dx holds the direct term delta * beta on entry.
     __device__ void load(const int64_t (&m)[4], int64_t n, pre_t& pre) const {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            pre.v[q] = (n < D && m[q] < M) ? load_quad(dx + m[q] * D + n)
-                                           : f4{0.0f, 0.0f, 0.0f, 0.0f};
+            pre.v[q] = (n < D && m[q] < M) ? get(dx + m[q] * D + n) : f4{0.0f, 0.0f, 0.0f, 0.0f};
     }
     __device__ void run(const int64_t (&m)[4], int64_t n, const f4 (&v)[4],
                         const pre_t& pre) const {
         if (n >= D) return;
-        const f4(&old)[4] = pre.v;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (m[q] >= M) continue;
-            const f4 r = old[q] + v[q];
+            const f4 r = pre.v[q] + v[q];
             if constexpr (sizeof(T) == 4) {
                 *(f4*)(dx + m[q] * D + n) = r;
             } else {
@@ -681,21 +762,25 @@ struct DxEpi {
     }
 };
 
-// One 128 x 128 tile of dx per workgroup.
+// One 128 x 128 tile of dx per workgroup: dx += [dz_r | dz_i] Wcat, with the
+// two dz halves at dzr and dzr + hoff bytes and pack holding Wcat^T planes.
 template <typename T>
-__global__ __launch_bounds__(256, 2) void dx_kernel(const float* dzr, const float* dzi,
-                                                    const T* wr, const T* wi, T* dx, int64_t M,
+__global__ __launch_bounds__(256, 2) void dx_kernel(const float* dzr, uint32_t hoff,
+                                                    const __bf16* pack, T* dx, int64_t M,
                                                     int64_t D) {
-    // A(m, k) = [dz_r | dz_i][m][k]; B(n, k) = Wcat[k][n], contiguous along n.
-    using OpA = Operand<float, true, ColPairMem<float>>;
-    using OpB = Operand<T, false, RowPairMem<T>>;
+    constexpr bool F32 = sizeof(T) == 4;
+    using OpA = Operand<kF32, true, true>;
+    using OpB = Operand<F32 ? kPack2 : kPack1, true>;
     __shared__ __attribute__((aligned(16))) char smem[lds_bytes<OpA::kPlanes, OpB::kPlanes>()];
     const int64_t ntn = (D + BN - 1) / BN;
     const int64_t t = xcd_tile(((M + BM - 1) / BM) * ntn);
     if (t < 0) return;
+    const uint32_t plane = (uint32_t)(2 * D * D * 2);
+    const OpA a{resource(dzr, hoff + (uint32_t)(M * D * 4)), (uint32_t)(D * 4), (uint32_t)D, hoff,
+                0};
+    const OpB b{resource(pack, OpB::kPlanes * plane), (uint32_t)(2 * D * 2), 0, 0, plane};
     const DxEpi<T> epi{dx, M, D};
-    tile_stream(OpA{{dzr, dzi, D}, M}, OpB{{wr, wi, D, D}, D}, 0, 2 * D, ntn, t, 1, 1, epi,
-                smem);
+    tile(a, b, (t / ntn) * BM, (t % ntn) * BN, 0, 2 * D, epi, smem);
 }
 
 struct DwEpi {
@@ -712,29 +797,32 @@ struct DwEpi {
 };
 
 // Split-K partial of [dW_r; dW_i]: partial[split][o][k] (o < 2D, k < D), and
-// of [db_r; db_i]: dbpart[split][o].
+// of [db_r; db_i]: dbpart[split][o].  The dz halves are at dzr and dzr + hoff
+// bytes.
 template <typename T>
-__global__ __launch_bounds__(256, 2) void dw_kernel(const float* dzr, const float* dzi,
-                                                    const T* x,
-                                                 float* partial, float* dbpart, int64_t M,
-                                                 int64_t D, int64_t splits,
-                                                 int64_t rows_per_split) {
-    // A(o, row) = dz[row][o], B(k, row) = x[row][k]: both contiguous along o / k.
-    using OpA = Operand<float, false, ColPairMem<float>>;
-    using OpB = Operand<T, false, PlainMem<T>>;
+__global__ __launch_bounds__(256, 2) void dw_kernel(const float* dzr, uint32_t hoff, const T* x,
+                                                    float* partial, float* dbpart, int64_t M,
+                                                    int64_t D, int64_t splits,
+                                                    int64_t rows_per_split) {
+    // A(o, row) = dz[row][o], B(k, row) = x[row][k]: memory rows are the
+    // contracted index for both.
+    using OpA = Operand<kF32, false, true>;
+    using OpB = Operand<sizeof(T) == 4 ? kF32 : kBf16, false>;
     __shared__ __attribute__((aligned(16))) char smem[lds_bytes<OpA::kPlanes, OpB::kPlanes>()];
     __shared__ float colsum[BM];
     const int64_t nto = (2 * D + BM - 1) / BM, ntn = (D + BN - 1) / BN;
     const int64_t t = xcd_tile(nto * ntn * splits);
     if (t < 0) return;
-    const int64_t split = t / (nto * ntn), tile = t % (nto * ntn);
-    const int64_t to = tile / ntn, tn = tile % ntn;
+    const int64_t split = t / (nto * ntn), tl = t % (nto * ntn);
+    const int64_t to = tl / ntn, tn = tl % ntn;
     const int64_t k_begin = split * rows_per_split;
     const int64_t k_end = k_begin + rows_per_split < M ? k_begin + rows_per_split : M;
+    const OpA a{resource(dzr, hoff + (uint32_t)(M * D * 4)), (uint32_t)(D * 4), (uint32_t)D, hoff,
+                0};
+    const OpB b{resource(x, (uint32_t)(M * D * sizeof(T))), (uint32_t)(D * sizeof(T)), 0, 0, 0};
     const DwEpi epi{partial + split * (2 * D) * D, 2 * D, D};
     // The tiles of column block 0 also reduce db from the dz rows they stage.
-    tile_stream(OpA{{dzr, dzi, D}, 2 * D}, OpB{{x, D}, D}, k_begin, k_end, ntn, tile, 1, 1, epi,
-                smem, tn == 0 ? colsum : nullptr);
+    tile(a, b, to * BM, tn * BN, k_begin, k_end, epi, smem, tn == 0 ? colsum : nullptr);
     if (tn == 0) {
         const int64_t o = to * BM + threadIdx.x;
         if (threadIdx.x < BM && o < 2 * D) dbpart[split * 2 * D + o] = colsum[threadIdx.x];
@@ -779,43 +867,91 @@ __global__ __launch_bounds__(64 * kRedGroups) void dw_reduce_kernel(
     }
 }
 
-int64_t dw_splits(int64_t M, int64_t D) {
+// Split count and rows per split (a multiple of BK) of the weight gradient:
+// about two workgroups per CU, at least 512 rows per split.
+void dw_split(int64_t M, int64_t D, int64_t* splits, int64_t* rows) {
     const int64_t tiles = ((2 * D + BM - 1) / BM) * ((D + BN - 1) / BN);
-    int64_t splits = 512 / tiles;  // about two workgroups per CU
-    const int64_t by_rows = (M + 511) / 512;  // at least 512 rows per split
-    if (splits > by_rows) splits = by_rows;
-    return splits < 1 ? 1 : splits;
+    int64_t s = 512 / tiles;
+    const int64_t by_rows = (M + 511) / 512;
+    if (s > by_rows) s = by_rows;
+    if (s < 1) s = 1;
+    int64_t r = (M + s - 1) / s;
+    r = (r + BK - 1) / BK * BK;
+    if (r < BK) r = BK;
+    *rows = r;
+    *splits = (M + r - 1) / r;
+    if (*splits < 1) *splits = 1;
 }
 
 }  // namespace fastmm
 
-static bool fast_ok(int64_t D, std::initializer_list<const void*> ptrs) {
-    if (D % 8 != 0) return false;
+namespace {
+constexpr int64_t kFastLimit = (int64_t)1 << 31;  // bytes addressable by one buffer resource here
+
+bool aligned16(std::initializer_list<const void*> ptrs) {
     for (const void* p : ptrs)
         if ((uintptr_t)p % 16 != 0) return false;
     return true;
 }
+
+// Byte distance from lo to hi if the pair [lo, lo + n) and [hi, hi + n) can
+// be addressed as one resource (hi after lo, 16-byte steps), else -1.
+int64_t pair_offset(const void* lo, const void* hi, int64_t n_bytes, int64_t tail_bytes) {
+    const int64_t d = (const char*)hi - (const char*)lo;
+    if (d < n_bytes || d % 16 != 0) return -1;
+    return d + n_bytes + tail_bytes < kFastLimit ? d : -1;
+}
+}  // namespace
 
 // ------------------------------------------------------------------ launchers
 static dim3 tiles(int64_t M, int64_t N, int64_t z = 1) {
     return dim3((unsigned)((M + kTM - 1) / kTM), (unsigned)((N + kTN - 1) / kTN), (unsigned)z);
 }
 
+size_t project_pack_workspace(int64_t D, IoType io) {
+    return (size_t)(io == IoType::kF32 ? 2 : 1) * (size_t)(2 * D * D) * 2;
+}
+
+static hipError_t launch_pack(const void* wr, const void* wi, int64_t D, IoType io,
+                              bool transposed, void* pack, hipStream_t stream) {
+    const dim3 grid((unsigned)((2 * D * D + 255) / 256));
+    if (io == IoType::kF32) {
+        if (transposed)
+            hipLaunchKernelGGL((fastmm::pack_kernel<float, true>), grid, dim3(256), 0, stream,
+                               (const float*)wr, (const float*)wi, (__bf16*)pack, D);
+        else
+            hipLaunchKernelGGL((fastmm::pack_kernel<float, false>), grid, dim3(256), 0, stream,
+                               (const float*)wr, (const float*)wi, (__bf16*)pack, D);
+    } else {
+        if (transposed)
+            hipLaunchKernelGGL((fastmm::pack_kernel<bf16, true>), grid, dim3(256), 0, stream,
+                               (const bf16*)wr, (const bf16*)wi, (__bf16*)pack, D);
+        else
+            hipLaunchKernelGGL((fastmm::pack_kernel<bf16, false>), grid, dim3(256), 0, stream,
+                               (const bf16*)wr, (const bf16*)wi, (__bf16*)pack, D);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_project_forward(const void* x, const void* wr, const void* br, const void* wi,
                                   const void* bi, void* zr, void* zi, int64_t M, int64_t D,
-                                  IoType io, hipStream_t stream) {
+                                  IoType io, void* pack, hipStream_t stream) {
     if (M == 0 || D == 0) return hipSuccess;
-    if (fast_ok(D, {x, wr, wi, zr, zi})) {
+    const int64_t esz = io == IoType::kF32 ? 4 : 2;
+    if (D % 8 == 0 && aligned16({x, zr, zi, pack}) &&
+        (M + fastmm::BM) * D * esz < kFastLimit) {
+        hipError_t e = launch_pack(wr, wi, D, io, false, pack, stream);
+        if (e != hipSuccess) return e;
         const int64_t tiles = ((M + fastmm::BM - 1) / fastmm::BM) *
                               ((2 * D + fastmm::BN - 1) / fastmm::BN);
         if (io == IoType::kF32)
             hipLaunchKernelGGL(fastmm::fwd_kernel<float>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const float*)x, (const float*)wr, (const float*)br,
-                               (const float*)wi, (const float*)bi, (float*)zr, (float*)zi, M, D);
+                               0, stream, (const float*)x, (const __bf16*)pack, (const float*)br,
+                               (const float*)bi, (float*)zr, (float*)zi, M, D);
         else
             hipLaunchKernelGGL(fastmm::fwd_kernel<bf16>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const bf16*)x, (const bf16*)wr, (const bf16*)br,
-                               (const bf16*)wi, (const bf16*)bi, (float*)zr, (float*)zi, M, D);
+                               0, stream, (const bf16*)x, (const __bf16*)pack, (const bf16*)br,
+                               (const bf16*)bi, (float*)zr, (float*)zi, M, D);
         return hipGetLastError();
     }
     if (io == IoType::kF32)
@@ -831,19 +967,22 @@ hipError_t launch_project_forward(const void* x, const void* wr, const void* br,
 
 hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const void* wr,
                                         const void* wi, void* dx, int64_t M, int64_t D,
-                                        IoType io, hipStream_t stream) {
+                                        IoType io, void* pack, hipStream_t stream) {
     if (M == 0 || D == 0) return hipSuccess;
-    if (fast_ok(D, {dzr, dzi, wr, wi, dx})) {
+    const int64_t hoff = pair_offset(dzr, dzi, M * D * 4, fastmm::BM * D * 4);
+    if (D % 8 == 0 && hoff >= 0 && aligned16({dzr, dx, pack})) {
+        hipError_t e = launch_pack(wr, wi, D, io, true, pack, stream);
+        if (e != hipSuccess) return e;
         const int64_t tiles = ((M + fastmm::BM - 1) / fastmm::BM) *
                               ((D + fastmm::BN - 1) / fastmm::BN);
         if (io == IoType::kF32)
             hipLaunchKernelGGL(fastmm::dx_kernel<float>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const float*)dzr, (const float*)dzi, (const float*)wr,
-                               (const float*)wi, (float*)dx, M, D);
+                               0, stream, (const float*)dzr, (uint32_t)hoff, (const __bf16*)pack,
+                               (float*)dx, M, D);
         else
             hipLaunchKernelGGL(fastmm::dx_kernel<bf16>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const float*)dzr, (const float*)dzi, (const bf16*)wr,
-                               (const bf16*)wi, (bf16*)dx, M, D);
+                               0, stream, (const float*)dzr, (uint32_t)hoff, (const __bf16*)pack,
+                               (bf16*)dx, M, D);
         return hipGetLastError();
     }
     if (io == IoType::kF32)
@@ -872,8 +1011,9 @@ size_t project_dw_workspace(int64_t M, int64_t D) {
     // Either path may run (the choice depends on pointer alignment): size for both.
     const size_t generic =
         (size_t)project_dw_splits(M, D) * (size_t)(2 * D) * (size_t)(D + 1) * sizeof(float);
-    const size_t fast =
-        (size_t)fastmm::dw_splits(M, D) * (size_t)(2 * D) * (size_t)(D + 1) * sizeof(float);
+    int64_t splits = 1, rows = 0;
+    fastmm::dw_split(M, D, &splits, &rows);
+    const size_t fast = (size_t)splits * (size_t)(2 * D) * (size_t)(D + 1) * sizeof(float);
     return generic > fast ? generic : fast;
 }
 
@@ -882,27 +1022,30 @@ hipError_t launch_project_backward_weights(const void* dzr, const void* dzi, con
                                            int64_t M, int64_t D, IoType io, void* ws,
                                            hipStream_t stream) {
     if (D == 0) return hipSuccess;
-    if (fast_ok(D, {dzr, dzi, x, ws})) {
-        const int64_t splits = fastmm::dw_splits(M, D);
-        const int64_t rows_per_split = (M + splits - 1) / splits;
+    const int64_t esz = io == IoType::kF32 ? 4 : 2;
+    const int64_t hoff = pair_offset(dzr, dzi, M * D * 4, fastmm::BK * D * 4);
+    if (D % 8 == 0 && M > 0 && hoff >= 0 && aligned16({dzr, x, ws}) &&
+        (M + fastmm::BK) * D * esz < kFastLimit) {
+        int64_t splits = 1, rows_per_split = 0;
+        fastmm::dw_split(M, D, &splits, &rows_per_split);
         const int64_t tiles = ((2 * D + fastmm::BM - 1) / fastmm::BM) *
                               ((D + fastmm::BN - 1) / fastmm::BN) * splits;
         float* partial = (float*)ws;
         float* dbpart = partial + splits * 2 * D * D;
         if (io == IoType::kF32)
             hipLaunchKernelGGL(fastmm::dw_kernel<float>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const float*)dzr, (const float*)dzi, (const float*)x,
+                               0, stream, (const float*)dzr, (uint32_t)hoff, (const float*)x,
                                partial, dbpart, M, D, splits, rows_per_split);
         else
             hipLaunchKernelGGL(fastmm::dw_kernel<bf16>, dim3(fastmm::grid_of(tiles)), dim3(256),
-                               0, stream, (const float*)dzr, (const float*)dzi, (const bf16*)x,
+                               0, stream, (const float*)dzr, (uint32_t)hoff, (const bf16*)x,
                                partial, dbpart, M, D, splits, rows_per_split);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t total = 2 * D * D + 2 * D;
         hipLaunchKernelGGL(fastmm::dw_reduce_kernel, dim3((unsigned)((total + 63) / 64)),
-                           dim3(64 * fastmm::kRedGroups), 0, stream, (const float*)partial, (const float*)dbpart,
-                           splits, D, dwr, dbr, dwi, dbi);
+                           dim3(64 * fastmm::kRedGroups), 0, stream, (const float*)partial,
+                           (const float*)dbpart, splits, D, dwr, dbr, dwi, dbi);
         return hipGetLastError();
     }
     const int64_t splits = project_dw_splits(M, D);

@@ -5,16 +5,22 @@
 
 namespace recblr {
 
+// Bytes of the packed-weight scratch that launch_project_forward and
+// launch_project_backward_data take (16-byte aligned).
+size_t project_pack_workspace(int64_t D, IoType io);
+
 // z_r = x W_r^T + b_r, z_i = x W_i^T + b_i over M = B*L rows (b may be null).
-// x, W, b and dx use the I/O type; z and dz are always fp32.
+// x, W, b and dx use the I/O type; z and dz are always fp32.  The fast path
+// needs zi, dzi after zr, dzr in one allocation (their byte distance is used
+// as an offset from zr, dzr).
 hipError_t launch_project_forward(const void* x, const void* wr, const void* br, const void* wi,
                                   const void* bi, void* zr, void* zi, int64_t M, int64_t D,
-                                  IoType io, hipStream_t stream);
+                                  IoType io, void* pack, hipStream_t stream);
 
 // dx += dz_r W_r + dz_i W_i (dx holds the direct term on entry).
 hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const void* wr,
                                         const void* wi, void* dx, int64_t M, int64_t D,
-                                        IoType io, hipStream_t stream);
+                                        IoType io, void* pack, hipStream_t stream);
 
 // dW_r, dW_i = dz^T x and db_r, db_i = column sums of dz; uses
 // project_dw_workspace(M, D) bytes of scratch at `ws`.
