@@ -1,6 +1,7 @@
 """Benchmark of the BD-LRU scan on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--api scan|full]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+                    [--api scan|full|step|scan_step]
 
 A step is one pass of the hot path over one batch: the gated scan forward
 (recblr_bdlru_scan_forward) followed by its backward
@@ -8,7 +9,11 @@ A step is one pass of the hot path over one batch: the gated scan forward
 The default workload is the long-history batch B=256, L=2048, D=128 in fp32.
 With --api full the step is the whole layer instead: the gate projections and
 the scan, forward (recblr_bdlru_forward) and backward (recblr_bdlru_backward,
-which recomputes the projections and returns dx, dW, db, dLambda).
+which recomputes the projections and returns dx, dW, db, dLambda).  With
+--api step (default workload c5dec) a step is one recurrent decode step over
+the batch with the gate projections fused in (recblr_bdlru_step, state
+updated in place); --api scan_step times the same step from precomputed
+pre-activations (recblr_bdlru_scan_step).
 Prints ONE JSON line (metric, value, roofline of the dominant call, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).
 """
@@ -109,13 +114,104 @@ def cpu_baseline(cfg, api="scan", target_s=10.0):
                       f"(L={cfg.L}, D={cfg.D}), {passes} passes, {total:.1f} s"}
 
 
+def decode_main(args, torch, dg, rb):
+    """One recurrent step over a decode batch per timed step (state updated in place)."""
+    cfg = dg.CONFIGS[args.workload or "c5dec"]
+    B, D = cfg.B, cfg.D
+    dev = torch.device("cuda:0")
+    dtype = torch.float32 if cfg.io == "f32" else torch.bfloat16
+    io = rb.io_code(dtype)
+    esz = 4 if cfg.io == "f32" else 2
+    fused = args.api == "step"
+    log(f"generating {cfg.name}: B={B} D={D} {cfg.io} ({args.api})")
+    f = dg.full_inputs(B, 1, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True, h0=True)
+    x = torch.from_numpy(np.ascontiguousarray(f.x[:, 0])).to(dev).to(dtype)
+    lam = torch.from_numpy(f.lam).to(dev)
+    h = torch.from_numpy(f.h0).to(dev)
+    s = torch.cuda.current_stream().cuda_stream
+    p = lambda t: t.data_ptr()
+    if fused:
+        Wr, br, Wi, bi = (torch.from_numpy(a).to(dev).to(dtype) for a in (f.Wr, f.br, f.Wi, f.bi))
+        nws = rb.recblr_workspace_size(rb.OP_STEP, B, 1, D, io)
+        ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+
+        def step():
+            st = rb.recblr_bdlru_step(p(x), p(Wr), p(br), p(Wi), p(bi), p(lam), p(h), p(h), B, D,
+                                      io, p(ws), nws, s)
+            assert st == 0, st
+        arrays_bytes = esz + 8  # x; h read and written (fp32)
+    else:
+        si = dg.step_inputs(B, D, cfg.seed, io=cfg.io, a_range=cfg.a_range)
+        x, zr, zi = (torch.from_numpy(a).to(dev).to(dtype) for a in (si.x, si.zr, si.zi))
+        lam = torch.from_numpy(si.lam).to(dev)
+        h = torch.from_numpy(si.h0).to(dev)
+
+        def step():
+            st = rb.recblr_bdlru_scan_step(p(x), p(zr), p(zi), p(lam), p(h), p(h), B, D, io, s)
+            assert st == 0, st
+        arrays_bytes = 3 * esz + 8  # x, z_r, z_i; h read and written (fp32)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    stream = torch.cuda.current_stream()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for k in range(K):
+        step()
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    N = B * D
+    ach = arrays_bytes * N / float(np.mean(dts)) / 1e9
+    log(f"step {np.mean(dts)*1e6:.1f} us ({ach:.0f} GB/s)  wall/step {wall/K*1e6:.1f} us")
+    out = {
+        "metric": "BD-LRU decode elements/sec (B*D per step)"
+                  + (", gate projections fused" if fused else ", pre-activations given"),
+        "value": N * K / wall, "unit": "elements/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": wall / K * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.io,
+        "data": "synthetic (seeded normal x, state; decay bases per the paper's initialisation)",
+        "config": {"workload": f"{cfg.name}: one recurrent step, {cfg.note}", "B": B, "D": D,
+                   "io": cfg.io, "elements": N},
+        "us_step": float(np.mean(dts)) * 1e6,
+        "roofline": {"bound": "hbm", "kernel": "step_fused" if fused else "scan_step",
+                     "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ach / PEAK_HBM_GBS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = min(B, 4096)
+        t0 = time.perf_counter()
+        passes = 0
+        if fused:
+            xs, hs = f.x[:rows, 0], f.h0[:rows].astype(np.float64)
+        else:
+            xs, hs = si.x[:rows], si.h0[:rows].astype(np.float64)
+        while time.perf_counter() - t0 < 10.0:
+            if fused:
+                hs = oracle.step(xs, f.Wr, f.br, f.Wi, f.bi, f.lam, hs)
+            else:
+                hs = oracle.scan_step(xs, si.zr[:rows], si.zi[:rows], si.lam, hs)
+            passes += 1
+        total = time.perf_counter() - t0
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        out["cpu_baseline"] = {"value": passes * rows * D / total, "unit": "elements/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"fp64 oracle step over {rows} of {B} batch rows "
+                                         f"(D={D}), {passes} steps, {total:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c4")
-    ap.add_argument("--api", choices=["scan", "full"], default="scan")
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step"], default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
                     help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
@@ -139,7 +235,9 @@ def main():
         print(json.dumps({"copy_reference_bytes_each_way": 4 * n, "copies": args.warmup + args.steps}))
         return
 
-    cfg = dg.CONFIGS[args.workload]
+    if args.api in ("step", "scan_step"):
+        return decode_main(args, torch, dg, rb)
+    cfg = dg.CONFIGS[args.workload or "c4"]
     if "bwd" not in cfg.ops:
         sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")
     dev = torch.device("cuda:0")

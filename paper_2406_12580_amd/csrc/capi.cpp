@@ -104,8 +104,12 @@ FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
 
 // Step: z_r, z_i scratch, then the packed weights.
 size_t step_z_bytes(int64_t B, int64_t D) { return align_up((size_t)(B * D) * sizeof(float)); }
+size_t step_pack_bytes(int64_t D, int io) {
+    const size_t a = project_pack_workspace(D, io_of(io)), b = step_pack_workspace(D, io_of(io));
+    return align_up(a > b ? a : b);
+}
 size_t step_ws(int64_t B, int64_t D, int io) {
-    return 2 * step_z_bytes(B, D) + align_up(project_pack_workspace(D, io_of(io)));
+    return 2 * step_z_bytes(B, D) + step_pack_bytes(D, io);
 }
 
 char* at(void* ws, size_t off) { return (char*)ws + off; }
@@ -331,8 +335,12 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
     hipStream_t strm = (hipStream_t)stream;
     void* zr = ws;
     void* zi = at(ws, step_z_bytes(B, D));
-    hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B, D, io_of(io),
-                                          at(ws, 2 * step_z_bytes(B, D)), strm);
+    void* pack = at(ws, 2 * step_z_bytes(B, D));
+    hipError_t e = hipSuccess;
+    if (launch_fused_step(x, W_r, b_r, W_i, b_i, lambda, h_prev, h_next, B, D, io_of(io), pack,
+                          strm, &e))
+        return status_of(e);
+    e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B, D, io_of(io), pack, strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     return status_of(
         launch_scan_step(x, zr, zi, lambda, h_prev, h_next, B, D, io_of(io), IoType::kF32, strm));

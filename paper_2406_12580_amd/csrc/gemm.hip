@@ -528,8 +528,9 @@ struct NoPre {};
 
 // Passes the wave's 64 x 64 accumulator block (rows m0w.., columns n0w..)
 // to epi.run(m[4], n, v[4], pre): four row indices, the first of four columns,
-// the four float4 values, and what epi.load fetched for those rows (strip 0's
-// comes in as `pre`; strip i + 1's is fetched while strip i is stored).
+// the four float4 values, and what epi.load fetched.  With kStripLoads,
+// epi.load fetches per strip (strip 0's comes in as `pre`, strip i + 1's is
+// fetched before strip i is stored); otherwise `pre` serves every strip.
 // Every thread of the workgroup must call it.
 template <class Epi>
 __device__ __forceinline__ void tile_epilogue(const f4 (&acc)[4][4], char* smem, int64_t m0w,
@@ -553,14 +554,21 @@ __device__ __forceinline__ void tile_epilogue(const f4 (&acc)[4][4], char* smem,
 #pragma unroll
         for (int q = 0; q < 4; ++q)
             val[q] = *(const f4*)&buf[(4 * q + (lane >> 4)) * EP + 4 * (lane & 15)];
-        typename Epi::pre_t next{};
-        if (i < 3) {
-            int64_t mn[4];
-            strip_rows(m0w, i + 1, lane, mn);
-            epi.load(mn, n, next);
+        if constexpr (Epi::kStripLoads) {
+            // The next strip's reads go out before this strip's stores: vector
+            // memory operations complete in issue order, so a read issued
+            // after a store could only be waited for together with the store.
+            typename Epi::pre_t next{};
+            if (i < 3) {
+                int64_t mn[4];
+                strip_rows(m0w, i + 1, lane, mn);
+                epi.load(mn, n, next);
+            }
+            epi.run(m, n, val, pre);
+            pre = next;
+        } else {
+            epi.run(m, n, val, pre);
         }
-        epi.run(m, n, val, pre);
-        pre = next;
         __syncthreads();
     }
 }
@@ -614,6 +622,11 @@ __device__ __forceinline__ void tile(const OpA& a, const OpB& b, int64_t m0, int
             const int64_t k0 = k_begin + (sl + 1) * BK;
             sa.fetch(a, k0, k_end, tid, ra);
             sb.fetch(b, k0, k_end, tid, rb);
+            // Keep the loads ahead of the MFMAs: left to itself the scheduler
+            // sinks them below the multiplications (reusing fragment
+            // registers), and the next slice then waits for a full memory
+            // round trip.
+            __builtin_amdgcn_sched_barrier(0);
             mma_slice<PA, PB>(la, lb, acc, wm, wn, fr, fk);
             __syncthreads();
         }
@@ -623,6 +636,7 @@ __device__ __forceinline__ void tile(const OpA& a, const OpB& b, int64_t m0, int
             if (colsum_out) add_colsum(cs, ra);
         __syncthreads();
         epi.load(mr, ne, pre);
+        __builtin_amdgcn_sched_barrier(0);
         mma_slice<PA, PB>(la, lb, acc, wm, wn, fr, fk);
         __syncthreads();
     }
@@ -640,7 +654,10 @@ __device__ __forceinline__ void tile(const OpA& a, const OpB& b, int64_t m0, int
         }
         __syncthreads();
     }
-    tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+    if constexpr (Epi::kOwnStore)
+        epi.store_tile(acc, m0w, n0w, pre);
+    else
+        tile_epilogue(acc, smem, m0w, n0w, epi, pre);
 }
 
 // Logical tile of this workgroup: the hardware deals consecutive workgroup ids
@@ -680,10 +697,32 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* wr, const T* wi, __b
     if (sizeof(T) == 4) out[total + e] = (__bf16)(v - (float)hi);
 }
 
+// Reads element i of a length-n array through a buffer resource (a null
+// array reads as zeros, as does any i past its end): no branch, so the
+// compiler need not wait for it early.
+template <typename T>
+struct ElemReader {
+    __amdgpu_buffer_rsrc_t rsrc;
+    __device__ ElemReader(const T* p, int64_t n)
+        : rsrc(resource(p, p ? (uint32_t)(n * sizeof(T)) : 0u)) {}
+    __device__ float operator()(int64_t i) const {
+        const uint32_t off = i >= 0 && i < (int64_t)(kOOB / sizeof(T)) ? (uint32_t)(i * sizeof(T))
+                                                                       : kOOB;
+        if constexpr (sizeof(T) == 4) {
+            return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, off, 0, 0));
+        } else {
+            const uint32_t b = __builtin_amdgcn_raw_buffer_load_b16(rsrc, off, 0, 0);
+            return __uint_as_float(b << 16);
+        }
+    }
+};
+
 template <typename T>
 struct FwdEpi {
+    static constexpr bool kOwnStore = false;
+    static constexpr bool kStripLoads = false;
     struct pre_t {
-        f4 bias;  // bias of the lane's four columns
+        float br[4], bi[4];  // the lane's four columns in both biases (one of them is 0)
     };
     float* zr;
     float* zi;
@@ -691,20 +730,25 @@ struct FwdEpi {
     const T* bi;
     int64_t M, D;
     __device__ void load(const int64_t (&)[4], int64_t n, pre_t& pre) const {
-        pre.bias = f4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (n >= 2 * D) return;
-        const T* bp = n < D ? br : bi;
-        const int64_t o = n < D ? n : n - D;
-        if (bp)
-            pre.bias = f4{to_f32(bp[o]), to_f32(bp[o + 1]), to_f32(bp[o + 2]), to_f32(bp[o + 3])};
+        const ElemReader<T> rr(br, D), ri(bi, D);
+        const bool g = n < D;  // the four columns are in one gate (D % 4 == 0)
+        const int64_t o = g ? n : n - D;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            pre.br[c] = rr(g ? o + c : -1);
+            pre.bi[c] = ri(g ? -1 : o + c);
+        }
     }
     __device__ void run(const int64_t (&m)[4], int64_t n, const f4 (&v)[4],
                         const pre_t& pre) const {
         if (n >= 2 * D) return;
         float* base = n < D ? zr + n : zi + (n - D);
+        f4 bias;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bias[c] = pre.br[c] + pre.bi[c];
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (m[q] < M) *(f4*)(base + m[q] * D) = v[q] + pre.bias;
+            if (m[q] < M) *(f4*)(base + m[q] * D) = v[q] + bias;
     }
 };
 
@@ -730,18 +774,30 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(const T* x, const __bf16* p
 
 template <typename T>
 struct DxEpi {
+    static constexpr bool kOwnStore = false;
+    static constexpr bool kStripLoads = true;
     struct pre_t {
         f4 v[4];
     };
     T* dx;
     int64_t M, D;
-    __device__ static f4 get(const float* p) { return *(const f4*)p; }
-    __device__ static f4 get(const bf16* p) { return widen(*(const u2v*)p); }
-    // dx holds the direct term delta * beta on entry.
+    // Reads dx, which holds the direct term delta * beta on entry, through a
+    // buffer resource (rows past M and columns past D read zero): no branch
+    // around the loads.
     __device__ void load(const int64_t (&m)[4], int64_t n, pre_t& pre) const {
+        const __amdgpu_buffer_rsrc_t r = resource(dx, (uint32_t)(M * D * sizeof(T)));
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            pre.v[q] = (n < D && m[q] < M) ? get(dx + m[q] * D + n) : f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t off =
+                (n < D && m[q] < M) ? (uint32_t)((m[q] * D + n) * sizeof(T)) : kOOB;
+            if constexpr (sizeof(T) == 4) {
+                const u4v w = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+                pre.v[q] = f4{__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z),
+                              __uint_as_float(w.w)};
+            } else {
+                pre.v[q] = widen(__builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+            }
+        }
     }
     __device__ void run(const int64_t (&m)[4], int64_t n, const f4 (&v)[4],
                         const pre_t& pre) const {
@@ -784,6 +840,8 @@ __global__ __launch_bounds__(256, 2) void dx_kernel(const float* dzr, uint32_t h
 }
 
 struct DwEpi {
+    static constexpr bool kOwnStore = false;
+    static constexpr bool kStripLoads = false;
     using pre_t = NoPre;
     float* out;
     int64_t O, D;
@@ -827,6 +885,122 @@ __global__ __launch_bounds__(256, 2) void dw_kernel(const float* dzr, uint32_t h
         const int64_t o = to * BM + threadIdx.x;
         if (threadIdx.x < BM && o < 2 * D) dbpart[split * 2 * D + o] = colsum[threadIdx.x];
     }
+}
+
+// ---- fused recurrent step with the gate projections (decode)
+// One tile covers 64 channels: with the weights packed so that each wave's 64
+// columns are [z_r of 32 channels | z_i of the same 32 channels], MFMA block
+// j < 2 of a lane holds z_r and block j + 2 holds z_i of the same (row,
+// channel), and the step h_next = alpha h_prev + beta x runs on the
+// accumulators directly: z never leaves the registers.
+// Packed row n (of ceil(D / 64) * 128): channel block n / 128, wave half
+// w = (n / 64) % 2, gate (n / 32) % 2, channel (n / 128) * 64 + 32 w + n % 32.
+__host__ __device__ inline int64_t step_pack_rows(int64_t D) { return (D + 63) / 64 * 128; }
+
+template <typename T>
+__global__ __launch_bounds__(256) void pack_step_kernel(const T* wr, const T* wi, __bf16* out,
+                                                        int64_t D) {
+    const int64_t rows = step_pack_rows(D), total = rows * D;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= total) return;
+    const int64_t n = e / D, k = e % D;
+    const int64_t ch = (n / 128) * 64 + 32 * ((n / 64) % 2) + n % 32;
+    const bool gate_i = (n / 32) % 2 == 1;
+    float v = 0.0f;
+    if (ch < D) v = gate_i ? to_f32(wi[ch * D + k]) : to_f32(wr[ch * D + k]);
+    const __bf16 hi = (__bf16)v;
+    out[e] = hi;
+    if (sizeof(T) == 4) out[total + e] = (__bf16)(v - (float)hi);
+}
+
+template <typename T>
+struct StepEpi {
+    static constexpr bool kOwnStore = true;
+    static constexpr bool kStripLoads = false;
+    // Everything the step reads besides z, for the lane's 2 x 4 x 4 elements
+    // (channel block j, strip i, row v): loaded before any store.
+    struct pre_t {
+        float x[2][4][4], hp[2][4][4];
+        ChannelConst cc[2];
+        float bzr[2], bzi[2];
+    };
+    const T* x;
+    const T* br;
+    const T* bi;
+    const float* lam;
+    const float* h_prev;
+    float* h_next;
+    int64_t B, D;
+    // m[0] is the lane's first row of strip 0; n is the tile column of the
+    // lane's first output (n0w + 4 (lane % 16)), unused here.
+    __device__ void load(const int64_t (&m)[4], int64_t, pre_t& pre) const {
+        const int lane = threadIdx.x & 63;
+        const int64_t m0w = m[0] - (lane >> 4);
+        const int64_t ch0 = chan0();
+        const ElemReader<T> rx(x, B * D), rbr(br, D), rbi(bi, D);
+        const ElemReader<float> rh(h_prev, B * D), rl(lam, D);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t ch = ch0 + 16 * j;
+            const bool okc = ch < D;
+            pre.cc[j] = channel_const(rl(okc ? ch : -1));
+            pre.bzr[j] = rbr(okc ? ch : -1);
+            pre.bzi[j] = rbi(okc ? ch : -1);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t b = m0w + i * 16 + 4 * (lane >> 4) + v;
+                    const int64_t e = (okc && b < B) ? b * D + ch : -1;
+                    pre.x[j][i][v] = rx(e);
+                    pre.hp[j][i][v] = rh(e);
+                }
+        }
+    }
+    __device__ int64_t chan0() const { return ch_base + (threadIdx.x & 15); }
+    int64_t ch_base = 0;  // first channel of this wave's 32 (set per tile)
+    __device__ void store_tile(const f4 (&acc)[4][4], int64_t m0w, int64_t, const pre_t& pre) const {
+        const int lane = threadIdx.x & 63;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t ch = chan0() + 16 * j;
+            if (ch >= D) continue;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t b = m0w + i * 16 + 4 * (lane >> 4) + v;
+                    if (b >= B) continue;
+                    float a, u;
+                    gate_forward(pre.x[j][i][v], acc[i][j][v] + pre.bzr[j],
+                                 acc[i][j + 2][v] + pre.bzi[j], pre.cc[j], a, u);
+                    h_next[b * D + ch] = fmaf(a, pre.hp[j][i][v], u);
+                }
+        }
+    }
+};
+
+// One tile of 128 batch rows x 64 channels per workgroup; pack holds the
+// step-ordered weight planes.  h_next may equal h_prev.
+template <typename T>
+__global__ __launch_bounds__(256, 2) void step_kernel(const T* x, const __bf16* pack,
+                                                      const T* br, const T* bi, const float* lam,
+                                                      const float* h_prev, float* h_next,
+                                                      int64_t B, int64_t D) {
+    constexpr bool F32 = sizeof(T) == 4;
+    using OpA = Operand<F32 ? kF32 : kBf16, true>;
+    using OpB = Operand<F32 ? kPack2 : kPack1, true>;
+    __shared__ __attribute__((aligned(16))) char smem[lds_bytes<OpA::kPlanes, OpB::kPlanes>()];
+    const int64_t ntn = step_pack_rows(D) / BN;
+    const int64_t t = xcd_tile(((B + BM - 1) / BM) * ntn);
+    if (t < 0) return;
+    const uint32_t plane = (uint32_t)(step_pack_rows(D) * D * 2);
+    const OpA a{resource(x, (uint32_t)(B * D * sizeof(T))), (uint32_t)(D * sizeof(T)), 0, 0, 0};
+    const OpB b{resource(pack, OpB::kPlanes * plane), (uint32_t)(D * 2), 0, 0, plane};
+    StepEpi<T> epi{x, br, bi, lam, h_prev, h_next, B, D};
+    // Columns n0w.. of wave half wn hold channels (n0w / 2).. (see the packing).
+    epi.ch_base = ((t % ntn) * BN + ((threadIdx.x >> 6) & 1) * 64) / 2;
+    tile(a, b, (t / ntn) * BM, (t % ntn) * BN, 0, D, epi, smem);
 }
 
 // Sums the split-K partials (fp64) in a fixed order: block column g of 8 sums
@@ -994,6 +1168,37 @@ hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const 
                            (const float*)dzr, (const float*)dzi, (const bf16*)wr, (const bf16*)wi,
                            (bf16*)dx, M, D);
     return hipGetLastError();
+}
+
+size_t step_pack_workspace(int64_t D, IoType io) {
+    return (size_t)(io == IoType::kF32 ? 2 : 1) * (size_t)(fastmm::step_pack_rows(D) * D) * 2;
+}
+
+bool launch_fused_step(const void* x, const void* wr, const void* br, const void* wi,
+                       const void* bi, const float* lambda, const float* h_prev, float* h_next,
+                       int64_t B, int64_t D, IoType io, void* pack, hipStream_t stream,
+                       hipError_t* err) {
+    const int64_t esz = io == IoType::kF32 ? 4 : 2;
+    if (B == 0 || D % 8 != 0 || !aligned16({x, pack}) || (B + fastmm::BM) * D * esz >= kFastLimit)
+        return false;
+    const int64_t rows = fastmm::step_pack_rows(D);
+    const dim3 pgrid((unsigned)((rows * D + 255) / 256));
+    const int64_t tiles = ((B + fastmm::BM - 1) / fastmm::BM) * (rows / fastmm::BN);
+    if (io == IoType::kF32) {
+        hipLaunchKernelGGL(fastmm::pack_step_kernel<float>, pgrid, dim3(256), 0, stream,
+                           (const float*)wr, (const float*)wi, (__bf16*)pack, D);
+        hipLaunchKernelGGL(fastmm::step_kernel<float>, dim3(fastmm::grid_of(tiles)), dim3(256), 0,
+                           stream, (const float*)x, (const __bf16*)pack, (const float*)br,
+                           (const float*)bi, lambda, h_prev, h_next, B, D);
+    } else {
+        hipLaunchKernelGGL(fastmm::pack_step_kernel<bf16>, pgrid, dim3(256), 0, stream,
+                           (const bf16*)wr, (const bf16*)wi, (__bf16*)pack, D);
+        hipLaunchKernelGGL(fastmm::step_kernel<bf16>, dim3(fastmm::grid_of(tiles)), dim3(256), 0,
+                           stream, (const bf16*)x, (const __bf16*)pack, (const bf16*)br,
+                           (const bf16*)bi, lambda, h_prev, h_next, B, D);
+    }
+    *err = hipGetLastError();
+    return true;
 }
 
 int64_t project_dw_splits(int64_t M, int64_t D) {

@@ -29,6 +29,17 @@ hipError_t launch_project_backward_weights(const void* dzr, const void* dzi, con
                                            int64_t M, int64_t D, IoType io, void* ws,
                                            hipStream_t stream);
 
+// Recurrent step with the gate projections fused in (z stays in registers):
+// h_next = alpha h_prev + beta x with z = x W^T + b.  Returns false, having
+// launched nothing, where the fused path does not apply (D % 8 != 0, x or
+// pack not 16-byte aligned, or x too large); else launches and stores the
+// launch status in *err.  pack takes step_pack_workspace(D, io) bytes.
+size_t step_pack_workspace(int64_t D, IoType io);
+bool launch_fused_step(const void* x, const void* wr, const void* br, const void* wi,
+                       const void* bi, const float* lambda, const float* h_prev, float* h_next,
+                       int64_t B, int64_t D, IoType io, void* pack, hipStream_t stream,
+                       hipError_t* err);
+
 int64_t project_dw_splits(int64_t M, int64_t D);
 size_t project_dw_workspace(int64_t M, int64_t D);
 

@@ -220,15 +220,42 @@ def test_full_forward_backward(rb, shape, io):
         assert_close(host(got[k]), want[k], io, k)
 
 
+# (B, D): D % 8 == 0 runs the step fused with the projection (z in registers),
+# with a partial channel block for D = 72; D = 130 takes the two-kernel path.
 @pytest.mark.parametrize("io", ["f32", "bf16"])
-def test_full_step(rb, io):
-    B, D = 50, 64
-    f = dg.full_inputs(B, 1, D, 4100, io=io, bias=True, h0=True)
+@pytest.mark.parametrize("shape", [(50, 64), (300, 72), (129, 256), (7, 130)])
+def test_full_step(rb, io, shape):
+    B, D = shape
+    f = dg.full_inputs(B, 1, D, 4100 + B + D, io=io, bias=True, h0=True)
     x = f.x[:, 0]
     got = rb.bdlru_step(dev(x, io), dev(f.Wr, io), dev(f.br, io), dev(f.Wi, io), dev(f.bi, io),
                         dev32(f.lam), dev32(f.h0))
     want = oracle.step(x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
     assert_close(host(got), want, io, "h_next")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_full_step_in_place(rb, io):
+    """h_next may be h_prev; two steps in a row match two oracle steps."""
+    import torch
+    B, D = 200, 128
+    f = dg.full_inputs(B, 2, D, 4150, io=io, bias=True, h0=True)
+    W = [dev(a, io) for a in (f.Wr, f.br, f.Wi, f.bi)]
+    lam = dev32(f.lam)
+    h = dev32(f.h0)
+    io_code = rb.io_code(torch.float32 if io == "f32" else torch.bfloat16)
+    nws = rb.recblr_workspace_size(rb.OP_STEP, B, 1, D, io_code)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=h.device)
+    want = f.h0.astype(np.float64)
+    for t in range(2):
+        xt = dev(np.ascontiguousarray(f.x[:, t]), io)
+        st = rb.recblr_bdlru_step(xt.data_ptr(), W[0].data_ptr(), W[1].data_ptr(),
+                                  W[2].data_ptr(), W[3].data_ptr(), lam.data_ptr(),
+                                  h.data_ptr(), h.data_ptr(), B, D, io_code, ws.data_ptr(), nws,
+                                  torch.cuda.current_stream().cuda_stream)
+        assert st == 0, st
+        want = oracle.step(f.x[:, t], f.Wr, f.br, f.Wi, f.bi, f.lam, want)
+    assert_close(host(h), want, "f32" if io == "f32" else "bf16", "h after two in-place steps")
 
 
 def test_full_forward_without_bias(rb):
@@ -267,6 +294,19 @@ def test_config_full_size(rb, name):
     # dLambda sums over every row: compare with the oracle over the whole batch.
     full = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh)
     assert_close(host(g["dlambda"]), full["dlambda"], io, f"{name} dlambda")
+
+
+def test_config_decode_full_api(rb):
+    """The decode workload through the entry point with gate weights (fused path)."""
+    cfg = dg.CONFIGS["c5dec"]
+    f = dg.full_inputs(cfg.B, 1, cfg.D, cfg.seed + 100, io=cfg.io, a_range=cfg.a_range,
+                       bias=True, h0=True)
+    x = f.x[:, 0]
+    got = rb.bdlru_step(dev(x, cfg.io), dev(f.Wr, cfg.io), dev(f.br, cfg.io), dev(f.Wi, cfg.io),
+                        dev(f.bi, cfg.io), dev32(f.lam), dev32(f.h0))
+    rows = np.array(sorted(set([0, 1, 4095, cfg.B // 2, cfg.B - 1])))
+    want = oracle.step(x[rows], f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0[rows])
+    assert_close(host(got)[rows], want, cfg.io, "decode h_next (full API)")
 
 
 def test_config_decode_full_size(rb):
