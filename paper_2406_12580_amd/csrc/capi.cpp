@@ -243,8 +243,15 @@ int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const 
     hipStream_t strm = (hipStream_t)stream;
     void* zr = at(ws, lay.zr);
     void* zi = at(ws, lay.zi);
+    void* pack = at(ws, lay.pack);
+    if (L > 0 && fused_forward_applies(B, L, D, io_of(io), x, pack)) {
+        hipError_t e = launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm);
+        if (e != hipSuccess) return RECBLR_ERR_HIP;
+        return status_of(launch_fused_forward(x, pack, b_r, b_i, lambda, h0, h, hT, B, L, D,
+                                              io_of(io), at(ws, lay.scan), strm));
+    }
     hipError_t e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, B * L, D, io_of(io),
-                                          at(ws, lay.pack), strm);
+                                          pack, strm);
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     ScanFwdArgs a{x, zr, zi, lambda, h0, h, hT, B, L, D, io_of(io), IoType::kF32,
                   at(ws, lay.scan), lay.total - lay.scan};

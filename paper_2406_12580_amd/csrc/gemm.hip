@@ -21,6 +21,7 @@
 
 #include "device_common.hpp"
 #include "gemm.hpp"
+#include "mfma_tile.hpp"
 
 namespace recblr {
 
@@ -255,218 +256,6 @@ __global__ void proj_dw_reduce_kernel(const float* partial, int64_t splits, int6
 // Tiles are numbered so that consecutive tiles of one row block land on the
 // same XCD and share its L2.
 namespace fastmm {
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int NQ = BK / 8;  // quads per thread and operand in one slice
-// LDS tiles hold BK bf16 per row (128 bytes); the 16-byte chunk j of row r is
-// stored at chunk j ^ f(r) with f(r) = (r ^ (r >> 2)) mod 8, so that the
-// fragment reads (8 consecutive rows, one chunk) and the transposed stores
-// (rows 4m + c for consecutive m, one chunk) each touch 8 distinct chunk
-// positions.
-constexpr int KP = BK;
-constexpr uint32_t kOOB = 0x80000000u;  // at or past every resource size: loads return 0
-
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef float f8 __attribute__((ext_vector_type(8)));
-typedef __bf16 b4 __attribute__((ext_vector_type(4)));
-typedef __bf16 b8 __attribute__((ext_vector_type(8)));
-typedef uint32_t u2v __attribute__((ext_vector_type(2)));
-typedef uint32_t u4v __attribute__((ext_vector_type(4)));
-
-// Column (bf16 elements) at which element k of LDS row `row` is stored.
-__device__ __forceinline__ int lds_col(int row, int k) {
-    const int f = (row ^ (row >> 2)) & 7;
-    return (((k >> 3) ^ f) << 3) | (k & 7);
-}
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t resource(const void* p, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
-                                             0x00020000);
-}
-
-__device__ __forceinline__ f4 widen(f4 v) { return v; }
-__device__ __forceinline__ f4 widen(u2v v) {
-    return f4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
-              __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u)};
-}
-// Element c of four packed bf16 as 16 bits.
-__device__ __forceinline__ uint32_t bits16(u2v v, int c) {
-    const uint32_t w = c < 2 ? v.x : v.y;
-    return (c & 1) ? w >> 16 : w & 0xffffu;
-}
-
-// Kinds of operand data.
-enum Kind {
-    kF32,    // fp32 values, split into hi and lo planes on the way to LDS
-    kBf16,   // bf16 values, one plane
-    kPack1,  // packed weights: one bf16 plane
-    kPack2,  // packed weights: bf16 hi and lo planes
-};
-
-template <int KIND>
-struct RawOf {
-    using type = u2v;
-};
-template <>
-struct RawOf<kF32> {
-    using type = f4;
-};
-template <>
-struct RawOf<kPack2> {
-    struct type {
-        u2v p[2];
-    };
-};
-
-// Operand with element (mn, k): mn is the output row (A) or column (B), k the
-// contracted index.  KFAST: memory rows are mn and k runs along them;
-// otherwise memory rows are k.  Byte offset of memory element (row, col):
-// row * pitch + col_off(col), where PAIR operands hold columns [0, half) at
-// byte 0 and [half, 2 half) at byte hoff (the two gates' fp32 scratch).
-template <int KIND, bool KFAST, bool PAIR = false>
-struct Operand {
-    static constexpr int kKind = KIND;
-    static constexpr bool kKFast = KFAST;
-    static constexpr int kPlanes = (KIND == kF32 || KIND == kPack2) ? 2 : 1;
-    static constexpr uint32_t kEsz = KIND == kF32 ? 4 : 2;
-    using raw_t = typename RawOf<KIND>::type;
-    __amdgpu_buffer_rsrc_t rsrc;
-    uint32_t pitch;  // bytes per memory row
-    uint32_t half;   // PAIR: columns per half
-    uint32_t hoff;   // PAIR: byte offset of the second half
-    uint32_t plane;  // kPack2: bytes per plane
-    __device__ uint32_t col_off(int64_t c) const {
-        if constexpr (PAIR)
-            return c < half ? (uint32_t)c * 4u : hoff + (uint32_t)(c - half) * 4u;
-        else
-            return (uint32_t)c * kEsz;
-    }
-    __device__ uint32_t row_off(int64_t r) const {
-        const uint64_t o = (uint64_t)r * pitch;
-        return o < kOOB ? (uint32_t)o : kOOB;
-    }
-    __device__ raw_t load(uint32_t off) const {
-        if constexpr (KIND == kF32) {
-            const u4v v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
-            return f4{__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
-                      __uint_as_float(v.w)};
-        } else if constexpr (KIND == kPack2) {
-            raw_t r;
-            r.p[0] = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
-            r.p[1] = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off + plane, 0, 0);
-            return r;
-        } else {
-            return __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
-        }
-    }
-};
-
-// Per-thread staging of one operand's 128 x BK slices: NQ quads per thread.
-//   KFAST: quad j covers (mn = tid / 16 + 16 j, k = 4 (tid % 16) .. +3).
-//   else : quad j covers (mn = 4 (tid % 32) .. +3, k = NQ (tid / 32) + j).
-// The per-tile part of the byte offsets is fixed at construction; quad j
-// adds j times a uniform stride (16 memory rows, or one memory row).  The
-// launch bounds keep every in-tile row offset below 2^31.
-template <class Op>
-struct Stager {
-    uint32_t fixed;
-    __device__ Stager(const Op& op, int64_t mn0, int tid) {
-        if constexpr (Op::kKFast)
-            fixed = op.row_off(mn0 + (tid >> 4));
-        else
-            fixed = op.col_off(mn0 + 4 * (tid & 31));
-    }
-    // Loads the slice starting at k0 (zeros for k >= k_end).
-    __device__ void fetch(const Op& op, int64_t k0, int64_t k_end, int tid,
-                          typename Op::raw_t (&r)[NQ]) const {
-        if constexpr (Op::kKFast) {
-            const int64_t k = k0 + 4 * (tid & 15);
-            const uint32_t base = fixed + (k < k_end ? op.col_off(k) : kOOB);
-            const uint32_t step = 16 * op.pitch;
-#pragma unroll
-            for (int j = 0; j < NQ; ++j) r[j] = op.load(base + j * step);
-        } else {
-            const int64_t k = k0 + NQ * (tid >> 5);
-            const uint32_t base = op.row_off(k) + fixed;
-            if (k0 + BK <= k_end) {
-#pragma unroll
-                for (int j = 0; j < NQ; ++j) r[j] = op.load(base + j * op.pitch);
-            } else {
-#pragma unroll
-                for (int j = 0; j < NQ; ++j)
-                    r[j] = op.load(k + j < k_end ? base + j * op.pitch : kOOB);
-            }
-        }
-    }
-};
-
-template <int N>
-struct PackT;
-template <>
-struct PackT<8> {
-    using bits = uint4;
-    using fv = f8;
-    using bv = b8;
-};
-
-// Writes a staged slice to the operand's LDS planes.
-template <class Op>
-__device__ __forceinline__ void store_slice(__bf16 (*lds)[BM][KP], int tid,
-                                            const typename Op::raw_t (&r)[NQ]) {
-    constexpr int KIND = Op::kKind;
-    if constexpr (Op::kKFast) {
-#pragma unroll
-        for (int j = 0; j < NQ; ++j) {
-            const int row = (tid >> 4) + 16 * j, col = lds_col(row, 4 * (tid & 15));
-            if constexpr (KIND == kF32) {
-                const f4 v = r[j];
-                const b4 hi = __builtin_convertvector(v, b4);
-                *(b4*)&lds[0][row][col] = hi;
-                *(b4*)&lds[1][row][col] =
-                    __builtin_convertvector(v - __builtin_convertvector(hi, f4), b4);
-            } else if constexpr (KIND == kPack2) {
-                *(u2v*)&lds[0][row][col] = r[j].p[0];
-                *(u2v*)&lds[1][row][col] = r[j].p[1];
-            } else {
-                *(u2v*)&lds[0][row][col] = r[j];  // bf16 bits as they are
-            }
-        }
-    } else {
-        static_assert(KIND == kF32 || KIND == kBf16, "transposed staging of packed weights");
-        // Transpose in registers: column c of the thread's quads becomes NQ
-        // consecutive k of LDS row 4 mq + c.
-        using PK = PackT<NQ>;
-        const int mq = tid & 31, kc = NQ * (tid >> 5);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int row = 4 * mq + c, col = lds_col(row, kc);
-            if constexpr (KIND == kBf16) {
-                uint32_t w[NQ / 2];
-#pragma unroll
-                for (int j = 0; j < NQ / 2; ++j)
-                    w[j] = bits16(r[2 * j], c) | (bits16(r[2 * j + 1], c) << 16);
-                *(typename PK::bits*)&lds[0][row][col] = *(const typename PK::bits*)w;
-            } else {
-                typename PK::fv v;
-#pragma unroll
-                for (int j = 0; j < NQ; ++j) v[j] = r[j][c];
-                const typename PK::bv hi = __builtin_convertvector(v, typename PK::bv);
-                *(typename PK::bv*)&lds[0][row][col] = hi;
-                *(typename PK::bv*)&lds[1][row][col] = __builtin_convertvector(
-                    v - __builtin_convertvector(hi, typename PK::fv), typename PK::bv);
-            }
-        }
-    }
-}
-
-// Column sums over k of a non-KFAST operand's staged slice (used for db):
-// thread (mq, kg) adds its NQ k values of each of its four columns.
-template <class Raw>
-__device__ __forceinline__ void add_colsum(f4& cs, const Raw (&r)[NQ]) {
-    f4 t = widen(r[0]);
-#pragma unroll
-    for (int j = 1; j < NQ; ++j) t += widen(r[j]);
-    cs += t;
-}
 
 // Multiplies the staged 128 x BK slices: the wave's 4 x 4 blocks of 16 x 16,
 // k-steps of 32.  Lane l supplies row l % 16 and k = 8 (l / 16) .. +7 of
@@ -697,25 +486,22 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* wr, const T* wi, __b
     if (sizeof(T) == 4) out[total + e] = (__bf16)(v - (float)hi);
 }
 
-// Reads element i of a length-n array through a buffer resource (a null
-// array reads as zeros, as does any i past its end): no branch, so the
-// compiler need not wait for it early.
+// Weights ordered by channel group for the scan forward with the projections
+// fused in: rows 128 g .. 128 g + 63 are W_r rows of channels 64 g .. 64 g + 63,
+// the next 64 rows the W_i rows of the same channels (D % 64 == 0).
 template <typename T>
-struct ElemReader {
-    __amdgpu_buffer_rsrc_t rsrc;
-    __device__ ElemReader(const T* p, int64_t n)
-        : rsrc(resource(p, p ? (uint32_t)(n * sizeof(T)) : 0u)) {}
-    __device__ float operator()(int64_t i) const {
-        const uint32_t off = i >= 0 && i < (int64_t)(kOOB / sizeof(T)) ? (uint32_t)(i * sizeof(T))
-                                                                       : kOOB;
-        if constexpr (sizeof(T) == 4) {
-            return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, off, 0, 0));
-        } else {
-            const uint32_t b = __builtin_amdgcn_raw_buffer_load_b16(rsrc, off, 0, 0);
-            return __uint_as_float(b << 16);
-        }
-    }
-};
+__global__ __launch_bounds__(256) void pack_group_kernel(const T* wr, const T* wi, __bf16* out,
+                                                         int64_t D) {
+    const int64_t total = 2 * D * D;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= total) return;
+    const int64_t n = e / D, k = e % D;
+    const int64_t ch = (n / 128) * 64 + n % 64;
+    const float v = (n / 64) % 2 == 0 ? to_f32(wr[ch * D + k]) : to_f32(wi[ch * D + k]);
+    const __bf16 hi = (__bf16)v;
+    out[e] = hi;
+    if (sizeof(T) == 4) out[total + e] = (__bf16)(v - (float)hi);
+}
 
 template <typename T>
 struct FwdEpi {
@@ -1167,6 +953,18 @@ hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const 
         hipLaunchKernelGGL(proj_dx_kernel<bf16>, tiles(M, D), dim3(kThreads), 0, stream,
                            (const float*)dzr, (const float*)dzi, (const bf16*)wr, (const bf16*)wi,
                            (bf16*)dx, M, D);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_groups(const void* wr, const void* wi, int64_t D, IoType io, void* pack,
+                              hipStream_t stream) {
+    const dim3 grid((unsigned)((2 * D * D + 255) / 256));
+    if (io == IoType::kF32)
+        hipLaunchKernelGGL(fastmm::pack_group_kernel<float>, grid, dim3(256), 0, stream,
+                           (const float*)wr, (const float*)wi, (__bf16*)pack, D);
+    else
+        hipLaunchKernelGGL(fastmm::pack_group_kernel<bf16>, grid, dim3(256), 0, stream,
+                           (const bf16*)wr, (const bf16*)wi, (__bf16*)pack, D);
     return hipGetLastError();
 }
 

@@ -29,6 +29,12 @@ hipError_t launch_project_backward_weights(const void* dzr, const void* dzi, con
                                            int64_t M, int64_t D, IoType io, void* ws,
                                            hipStream_t stream);
 
+// Packs [W_r; W_i] by channel group of 64 (rows 128 g.. : W_r rows of the
+// group's channels, then their W_i rows) into project_pack_workspace(D, io)
+// bytes of bf16 planes, for the scan forward with the projections fused in.
+hipError_t launch_pack_groups(const void* wr, const void* wi, int64_t D, IoType io, void* pack,
+                              hipStream_t stream);
+
 // Recurrent step with the gate projections fused in (z stays in registers):
 // h_next = alpha h_prev + beta x with z = x W^T + b.  Returns false, having
 // launched nothing, where the fused path does not apply (D % 8 != 0, x or

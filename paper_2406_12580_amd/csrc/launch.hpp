@@ -63,4 +63,16 @@ hipError_t launch_scan_step(const void* x, const void* zr, const void* zi, const
 hipError_t launch_copy_state(const float* src, float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream);
 
+// Scan forward with the gate projections computed per tile on the matrix
+// cores (z never reaches HBM).  Applies when the look-back kernel runs,
+// D % 64 == 0 and x and pack are 16-byte aligned; pack holds the weights
+// ordered by channel group (launch_pack_groups); ws is the scan-forward
+// workspace.
+bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
+                           const void* pack);
+hipError_t launch_fused_forward(const void* x, const void* pack, const void* br, const void* bi,
+                                const float* lambda, const float* h0, void* h, float* hT,
+                                int64_t B, int64_t L, int64_t D, IoType io, void* ws,
+                                hipStream_t stream);
+
 }  // namespace recblr

@@ -220,6 +220,26 @@ def test_full_forward_backward(rb, shape, io):
         assert_close(host(got[k]), want[k], io, k)
 
 
+# Few channel groups and sequences longer than one look-back tile (128 steps)
+# with D % 64 == 0 run the forward with the projections fused into the
+# look-back scan; D = 72 takes the two-kernel path.
+FUSED_FWD = [(1, 1000, 64), (3, 700, 128), (2, 257, 192), (1, 129, 256), (2, 1000, 72)]
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", FUSED_FWD)
+def test_full_forward_fused(rb, shape, io):
+    B, L, D = shape
+    f = dg.full_inputs(B, L, D, 4300 + B + L + D, io=io, a_range=(0.99, 0.9999), bias=True,
+                       h0=True)
+    h, hT = rb.bdlru_forward(*(dev(a, io) for a in (f.x, f.Wr, f.br, f.Wi, f.bi)),
+                             dev32(f.lam), dev32(f.h0))
+    print(f"fused forward {shape} {io}: GPU done", flush=True)
+    oh, ohT = oracle.forward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    assert_close(host(h), oh, io, "h")
+    assert_close(host(hT), ohT, "f32" if io == "f32" else "bf16", "hT")
+
+
 # (B, D): D % 8 == 0 runs the step fused with the projection (z in registers),
 # with a partial channel block for D = 72; D = 130 takes the two-kernel path.
 @pytest.mark.parametrize("io", ["f32", "bf16"])
