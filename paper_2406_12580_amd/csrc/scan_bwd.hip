@@ -459,17 +459,32 @@ __global__ __launch_bounds__(256) void dlambda_rows_kernel(const float* __restri
         partial2[nb * D + d] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
-__global__ __launch_bounds__(256) void dlambda_final_kernel(const double* __restrict__ partial2,
-                                                            int64_t nblk,
-                                                            const float* __restrict__ lam,
-                                                            float* __restrict__ dlambda,
-                                                            int64_t D) {
-    const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (d >= D) return;
+// dLambda_d = sigmoid(Lambda_d) * sum of the row-block sums, in a fixed order:
+// thread group g of 8 (64 channels per workgroup) sums its contiguous run of
+// row blocks in ascending order, then the 8 runs are added in order.
+constexpr int kFinalGroups = 8;
+__global__ __launch_bounds__(64 * kFinalGroups) void dlambda_final_kernel(
+    const double* __restrict__ partial2, int64_t nblk, const float* __restrict__ lam,
+    float* __restrict__ dlambda, int64_t D) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int g = threadIdx.x / kWave;
+    const int64_t d = (int64_t)blockIdx.x * kWave + lane;
+    const int64_t per = (nblk + kFinalGroups - 1) / kFinalGroups;
+    const int64_t k0 = g * per, k1 = k0 + per < nblk ? k0 + per : nblk;
     double s = 0.0;
-    for (int64_t k = 0; k < nblk; ++k) s += partial2[k * D + d];
+    if (d < D) {
+#pragma unroll 8
+        for (int64_t k = k0; k < k1; ++k) s += partial2[k * D + d];
+    }
+    __shared__ double red[kFinalGroups][kWave];
+    red[g][lane] = s;
+    __syncthreads();
+    if (g != 0 || d >= D) return;
+    double t = red[0][lane];
+#pragma unroll
+    for (int q = 1; q < kFinalGroups; ++q) t += red[q][lane];
     const double lv = (double)lam[d];
-    dlambda[d] = (float)(s / (1.0 + exp(-lv)));
+    dlambda[d] = (float)(t / (1.0 + exp(-lv)));
 }
 
 __global__ void fill_kernel(float* __restrict__ dst, float v, int64_t n) {
@@ -644,8 +659,9 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
                        a.D);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((a.D + 255) / 256)), dim3(256), 0,
-                       stream, partial2, nblk, a.lambda, a.dlambda, a.D);
+    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((a.D + kWave - 1) / kWave)),
+                       dim3(kWave * kFinalGroups), 0, stream, partial2, nblk, a.lambda, a.dlambda,
+                       a.D);
     return hipGetLastError();
 }
 
