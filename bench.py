@@ -1,7 +1,7 @@
 """Benchmark of the BD-LRU scan on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
-                    [--api scan|full|step|scan_step]
+                    [--api scan|full|step|scan_step|ablation]
 
 A step is one pass of the hot path over one batch: the gated scan forward
 (recblr_bdlru_scan_forward) followed by its backward
@@ -13,7 +13,11 @@ which recomputes the projections and returns dx, dW, db, dLambda).  With
 --api step (default workload c5dec) a step is one recurrent decode step over
 the batch with the gate projections fused in (recblr_bdlru_step, state
 updated in place); --api scan_step times the same step from precomputed
-pre-activations (recblr_bdlru_scan_step).
+pre-activations (recblr_bdlru_scan_step).  --api ablation times the layer
+forward (gate projections + scan) with the scan algorithms of the paper's
+efficiency ablation (serial scan; two-tree scan with sequence padding or with
+embedding padding; the production chunked scan) at the paper's three
+sequence lengths.
 Prints ONE JSON line (metric, value, roofline of the dominant call, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).
 """
@@ -114,6 +118,87 @@ def cpu_baseline(cfg, api="scan", target_s=10.0):
                       f"(L={cfg.L}, D={cfg.D}), {passes} passes, {total:.1f} s"}
 
 
+# Shapes of the paper's efficiency ablation: sequence lengths 200, 100 and 257
+# (padded to 256, 128 and 512 for the tree scan), training batches 2048, 2048
+# and 512, BD-LRU width E * D = 2 * 64; plus a long-history shape.
+ABLATION_WORKLOADS = [("ml1m-like", 2048, 200, 128), ("gowalla-like", 2048, 100, 128),
+                      ("xlong-like", 512, 257, 128),
+                      # few channels, long histories: where parallelism along the
+                      # sequence matters (4096 channels, one wave each for the serial scan)
+                      ("long-history", 16, 4096, 256)]
+
+
+def ablation_main(args, torch, dg, rb):
+    """Layer forward (projections + scan) per scan algorithm.
+
+    proj(len) is measured as recblr_bdlru_forward minus the production scan at
+    that length; each scheme's time is proj(its length) + its scan:
+      serial:   proj(L)  + serial scan(L)
+      tree_sp:  proj(P)  + tree scan of inputs left-padded to P (sequence padding)
+      tree_ep:  proj(L)  + tree scan padding to P inside (embedding padding)
+      chunked:  proj(L)  + production scan(L)          (P = power of two >= L)
+    """
+    dev = torch.device("cuda:0")
+    s = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(s)
+        for k in range(reps):
+            fn()
+            ev[k + 1].record(s)
+        torch.cuda.synchronize()
+        return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(reps)])) * 1e3
+
+    rows = []
+    for name, B, L, D in ABLATION_WORKLOADS:
+        P = 1 << (L - 1).bit_length()
+        log(f"{name}: B={B} L={L} (padded {P}) D={D} fp32")
+        f = dg.full_inputs(B, L, D, 7000 + L, io="f32", bias=True)
+        zr = np.einsum("bld,ed->ble", f.x, f.Wr, optimize=True).astype(np.float32) + f.br
+        zi = np.einsum("bld,ed->ble", f.x, f.Wi, optimize=True).astype(np.float32) + f.bi
+        T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        padw = ((0, 0), (P - L, 0), (0, 0))
+        X, ZR, ZI = T(f.x), T(zr), T(zi)
+        XP, ZRP, ZIP = T(np.pad(f.x, padw)), T(np.pad(zr, padw) + 0), T(np.pad(zi, padw) + 0)
+        Wr, br, Wi, bi, lam = T(f.Wr), T(f.br), T(f.Wi), T(f.bi), T(f.lam)
+        reps = max(args.steps, 5)
+        t = {}
+        t["layer_L"] = timed(lambda: rb.bdlru_forward(X, Wr, br, Wi, bi, lam), reps)
+        t["layer_P"] = timed(lambda: rb.bdlru_forward(XP, Wr, br, Wi, bi, lam), reps)
+        t["chunked_L"] = timed(lambda: rb.scan_forward_method(rb.SCAN_CHUNKED, X, ZR, ZI, lam), reps)
+        t["chunked_P"] = timed(lambda: rb.scan_forward_method(rb.SCAN_CHUNKED, XP, ZRP, ZIP, lam),
+                               reps)
+        t["serial"] = timed(lambda: rb.scan_forward_method(rb.SCAN_SERIAL, X, ZR, ZI, lam), reps)
+        t["tree_sp"] = timed(lambda: rb.scan_forward_method(rb.SCAN_TREE, XP, ZRP, ZIP, lam), reps)
+        t["tree_ep"] = timed(lambda: rb.scan_forward_method(rb.SCAN_TREE, X, ZR, ZI, lam), reps)
+        proj_L, proj_P = t["layer_L"] - t["chunked_L"], t["layer_P"] - t["chunked_P"]
+        row = {"workload": name, "B": B, "L": L, "padded": P, "D": D,
+               "us_scan": {k: round(t[k], 1) for k in ("serial", "tree_sp", "tree_ep", "chunked_L")},
+               "us_projection": {"L": round(proj_L, 1), "padded": round(proj_P, 1)},
+               "us_layer_forward": {"serial": round(proj_L + t["serial"], 1),
+                                    "tree_sp": round(proj_P + t["tree_sp"], 1),
+                                    "tree_ep": round(proj_L + t["tree_ep"], 1),
+                                    "chunked": round(t["layer_L"], 1)}}
+        log(json.dumps(row))
+        rows.append(row)
+    first = rows[0]["us_layer_forward"]
+    out = {"metric": "BD-LRU layer forward, serial-scan time over chunked-scan time "
+                     "(efficiency-ablation analogue, ml1m-like)",
+           "value": first["serial"] / first["chunked"], "unit": "x", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (seeded normal x, weights N(0, 1/D), decay bases per the paper's "
+                   "initialisation)",
+           "config": {"workload": "efficiency ablation analogue: ml1m-like, gowalla-like, "
+                                  "xlong-like shapes"},
+           "table": rows}
+    print(json.dumps(out), flush=True)
+
+
 def decode_main(args, torch, dg, rb):
     """One recurrent step over a decode batch per timed step (state updated in place)."""
     cfg = dg.CONFIGS[args.workload or "c5dec"]
@@ -211,7 +296,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step"], default="scan")
+    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation"],
+                    default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
                     help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
@@ -237,6 +323,8 @@ def main():
 
     if args.api in ("step", "scan_step"):
         return decode_main(args, torch, dg, rb)
+    if args.api == "ablation":
+        return ablation_main(args, torch, dg, rb)
     cfg = dg.CONFIGS[args.workload or "c4"]
     if "bwd" not in cfg.ops:
         sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")

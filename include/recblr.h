@@ -162,6 +162,28 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
                       int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Scan algorithms of the efficiency ablation (section 4, Table tab:efficiency;
+ * the two-tree scan of section 3.3, figure fig:scan): the gated scan forward
+ * from a zero initial state by one of
+ *   RECBLR_SCAN_CHUNKED  the production kernels (recblr_bdlru_scan_forward;
+ *                        workspace as for RECBLR_OP_SCAN_FORWARD);
+ *   RECBLR_SCAN_SERIAL   one wave per 64 channels walks the whole sequence,
+ *                        no parallelism along it (no workspace);
+ *   RECBLR_SCAN_TREE     up-sweep / down-sweep over the power of two >= L,
+ *                        the leading positions padded with the identity,
+ *                        i.e. left zero padding applied inside the scan
+ *                        (embedding padding); L <= 4096 (no workspace).
+ * Sequence padding is the caller's: pass inputs already left-padded to the
+ * power of two.  Arguments as recblr_bdlru_scan_forward (h0 = 0, no hT).
+ * Errors: INVALID_ARGUMENT for an unknown method; UNSUPPORTED for a tree
+ * scan longer than 4096 steps.
+ */
+enum { RECBLR_SCAN_CHUNKED = 0, RECBLR_SCAN_SERIAL = 1, RECBLR_SCAN_TREE = 2 };
+int recblr_scan_forward_method(int method, const void* x, const void* z_r, const void* z_i,
+                               const float* lambda, void* h, int64_t B, int64_t L, int64_t D,
+                               int io, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Raw first-order recurrence h_t = a_t h_{t-1} + u_t (eq:linrnn with the
  * coefficients given directly), float only.  Same kernel as the gated scan
  * with the gate stage removed; used to check the scan against closed forms.

@@ -165,6 +165,31 @@ int recblr_bdlru_scan_forward(const void* x, const void* z_r, const void* z_i,
     return status_of(launch_scan_forward(a, (hipStream_t)stream));
 }
 
+int recblr_scan_forward_method(int method, const void* x, const void* z_r, const void* z_i,
+                               const float* lambda, void* h, int64_t B, int64_t L, int64_t D,
+                               int io, void* ws, size_t ws_bytes, void* stream) {
+    if (method == RECBLR_SCAN_CHUNKED)
+        return recblr_bdlru_scan_forward(x, z_r, z_i, lambda, nullptr, h, nullptr, B, L, D, io,
+                                         ws, ws_bytes, stream);
+    if (method != RECBLR_SCAN_SERIAL && method != RECBLR_SCAN_TREE)
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (method == RECBLR_SCAN_TREE && !tree_scan_supported(L)) return RECBLR_ERR_UNSUPPORTED;
+    if (B == 0 || D == 0 || L == 0) return RECBLR_OK;
+    const size_t n = (size_t)(B * L * D) * esz(io);
+    if (!x || !z_r || !z_i || !h || !lambda) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i, (const void*)h})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!aligned(lambda, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{h, n}}, {{x, n}, {z_r, n}, {z_i, n}, {lambda, (size_t)D * 4}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    ScanFwdArgs a{x, z_r, z_i, lambda, nullptr, h, nullptr, B, L, D, io_of(io), io_of(io),
+                  nullptr, 0};
+    return status_of(method == RECBLR_SCAN_SERIAL ? launch_scan_forward_serial(a, (hipStream_t)stream)
+                                                  : launch_scan_forward_tree(a, (hipStream_t)stream));
+}
+
 int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
                                const float* lambda, const float* h0, const void* h,
                                const void* dh, const float* dhT, void* dx, void* dz_r,

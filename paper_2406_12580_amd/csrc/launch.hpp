@@ -75,4 +75,12 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
                                 int64_t B, int64_t L, int64_t D, IoType io, void* ws,
                                 hipStream_t stream);
 
+// Scan-algorithm variants for the efficiency ablation (zero initial state;
+// x, z, h share the I/O type): a serial scan (one wave per 64 channels walks
+// the sequence) and the two-tree scan over the power of two >= L with the
+// leading positions as identity (embedding padding), L <= 4096.
+hipError_t launch_scan_forward_serial(const ScanFwdArgs& a, hipStream_t stream);
+hipError_t launch_scan_forward_tree(const ScanFwdArgs& a, hipStream_t stream);
+bool tree_scan_supported(int64_t L);
+
 }  // namespace recblr

@@ -702,6 +702,36 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
     return hipGetLastError();
 }
 
+// Serial scan of the efficiency ablation: one wave per 64 channels walks the
+// whole sequence with the state in registers (the chain kernel with a single
+// wave, one channel per lane): no parallelism along the sequence.
+hipError_t launch_scan_forward_serial(const ScanFwdArgs& a, hipStream_t stream) {
+    const int64_t nch = a.B * a.D;
+    if (nch == 0) return hipSuccess;
+    const int64_t groups = (nch + kWave - 1) / kWave;
+    FwdParams P{a.x, a.zr, a.zi, a.lambda, a.h0, a.h, a.hT, a.L, a.D, nch, groups, 1,
+                LookbackWs{}};
+    const bool small = (uint64_t)(nch * a.L) * io_bytes(a.io) < (1ull << 32);
+    const dim3 grid((unsigned)groups), block(kWave);
+    constexpr int C = 8;
+    if (a.io == IoType::kF32) {
+        if (small)
+            hipLaunchKernelGGL((scan_fwd_chain_kernel<float, float, 1, C, 1, false, uint32_t>),
+                               grid, block, 0, stream, P);
+        else
+            hipLaunchKernelGGL((scan_fwd_chain_kernel<float, float, 1, C, 1, false, uint64_t>),
+                               grid, block, 0, stream, P);
+    } else {
+        if (small)
+            hipLaunchKernelGGL((scan_fwd_chain_kernel<bf16, bf16, 1, C, 1, false, uint32_t>),
+                               grid, block, 0, stream, P);
+        else
+            hipLaunchKernelGGL((scan_fwd_chain_kernel<bf16, bf16, 1, C, 1, false, uint64_t>),
+                               grid, block, 0, stream, P);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_linear_scan(const float* a, const float* u, const float* h0, float* h,
                               float* hT, int64_t B, int64_t L, int64_t D, hipStream_t stream) {
     FwdPlan plan;

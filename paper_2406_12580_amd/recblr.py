@@ -30,11 +30,13 @@ _lib = ctypes.CDLL(LIB_PATH)
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
 OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP = range(5)
+SCAN_CHUNKED, SCAN_SERIAL, SCAN_TREE = range(3)
 
 EXPORTS = (
     "recblr_status_string", "recblr_workspace_size", "recblr_bdlru_scan_forward",
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
+    "recblr_scan_forward_method",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
@@ -48,6 +50,7 @@ _SIGS = {
     "recblr_bdlru_backward": ([_p] * 17 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
     "recblr_bdlru_step": ([_p] * 8 + [_i64] * 2 + [_int, _p, _sz, _p], _int),
     "recblr_linear_scan_forward": ([_p] * 5 + [_i64] * 3 + [_p], _int),
+    "recblr_scan_forward_method": ([_int] + [_p] * 5 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -222,3 +225,16 @@ def linear_scan_forward(a, u, h0=None, stream=None):
     _check(recblr_linear_scan_forward(_ptr(a), _ptr(u), _ptr(h0), _ptr(h), _ptr(hT), B, L, D,
                                       _stream(stream)), "recblr_linear_scan_forward")
     return h, hT
+
+
+def scan_forward_method(method, x, zr, zi, lam, stream=None):
+    """Gated scan forward (zero initial state) by one of SCAN_CHUNKED, SCAN_SERIAL,
+    SCAN_TREE (the efficiency-ablation variants). Returns h."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    h = torch.empty_like(x)
+    ws, nws = _workspace(OP_SCAN_FORWARD, B, L, D, io, x.device)
+    _check(recblr_scan_forward_method(method, _ptr(x), _ptr(zr), _ptr(zi), _ptr(lam), _ptr(h),
+                                      B, L, D, io, _ptr(ws), nws, _stream(stream)),
+           "recblr_scan_forward_method")
+    return h

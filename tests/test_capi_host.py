@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 9
+    assert len(syms) == 10
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -138,3 +138,20 @@ def test_linear_scan_validation(rb):
                                          None) == rb.ERR_INVALID_ARGUMENT
     assert rb.recblr_linear_scan_forward(addr(0), addr(1), None, addr(1), None, 2, 3, 4,
                                          None) == rb.ERR_INVALID_ARGUMENT
+
+
+def test_scan_method_validation(rb):
+    """Ablation entry: checks run before any launch."""
+    f = rb.recblr_scan_forward_method
+    assert f(7, addr(0), addr(1), addr(2), addr(3), addr(4), 2, 3, 4, rb.F32, None, 0,
+             None) == rb.ERR_INVALID_ARGUMENT                           # unknown method
+    assert f(rb.SCAN_TREE, addr(0), addr(1), addr(2), addr(3), addr(4), 2, 5000, 4, rb.F32,
+             None, 0, None) == rb.ERR_UNSUPPORTED                       # tree longer than 4096
+    assert f(rb.SCAN_SERIAL, None, addr(1), addr(2), addr(3), addr(4), 2, 3, 4, rb.F32, None, 0,
+             None) == rb.ERR_INVALID_ARGUMENT                           # null x
+    assert f(rb.SCAN_TREE, addr(0), addr(1), addr(2), addr(3), addr(0), 2, 3, 4, rb.F32, None, 0,
+             None) == rb.ERR_INVALID_ARGUMENT                           # h over x
+    assert f(rb.SCAN_SERIAL, addr(0), addr(1), addr(2), addr(3), addr(4), 2, 3, 4, 5, None, 0,
+             None) == rb.ERR_UNSUPPORTED                                # unknown dtype
+    assert f(rb.SCAN_TREE, None, None, None, None, None, 0, 3, 4, rb.F32, None, 0,
+             None) == rb.OK                                             # empty batch

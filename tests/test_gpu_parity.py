@@ -286,6 +286,39 @@ def test_full_forward_without_bias(rb):
     assert_close(host(h), oh, "f32", "h")
 
 
+# ------------------------------------------------------------------ efficiency-ablation scans
+
+ABLATION_SHAPES = [(3, 200, 64), (2, 257, 128), (4, 100, 72), (1, 1, 8), (2, 64, 32),
+                   (1, 1000, 16)]
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", ABLATION_SHAPES)
+@pytest.mark.parametrize("method", ["serial", "tree"])
+def test_scan_methods(rb, method, shape, io):
+    B, L, D = shape
+    inp = dg.scan_inputs(B, L, D, 6000 + B + L + D, io=io)
+    m = rb.SCAN_SERIAL if method == "serial" else rb.SCAN_TREE
+    h = rb.scan_forward_method(m, dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io),
+                               dev32(inp.lam))
+    oh, _ = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam)
+    assert_close(host(h), oh, io, f"{method} h")
+
+
+def test_tree_scan_sequence_padding(rb):
+    """Sequence padding: inputs left-padded to a power of two with zero x
+    (any z) give the unpadded result on the real positions (zero state)."""
+    B, L, D, P = 3, 200, 64, 256
+    inp = dg.scan_inputs(B, L, D, 6100)
+    pad = dg.scan_inputs(B, P - L, D, 6101)
+    x = np.concatenate([np.zeros_like(pad.x), inp.x], axis=1)
+    zr = np.concatenate([pad.zr, inp.zr], axis=1)
+    zi = np.concatenate([pad.zi, inp.zi], axis=1)
+    h = rb.scan_forward_method(rb.SCAN_TREE, dev(x), dev(zr), dev(zi), dev32(inp.lam))
+    oh, _ = oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam)
+    assert_close(host(h)[:, P - L:], oh, "f32", "tree h, sequence padding")
+
+
 # ------------------------------------------------------------------ named workloads at full size
 
 def _sample_rows(B, k=3):
