@@ -50,6 +50,7 @@ def _load():
             "oracle_forward": [i64, i64, i64] + [p] * 9,
             "oracle_backward": [i64, i64, i64] + [p] * 16,
             "oracle_step": [i64, i64] + [p] * 8,
+            "oracle_gated_forward": [i64, i64, i64, i64] + [p] * 13,
         }
         for name, args in sigs.items():
             fn = getattr(_lib, name)
@@ -154,3 +155,20 @@ def step(x, Wr, br, Wi, bi, lam, h_prev):
     _load().oracle_step(B, D, _ptr(x), _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam),
                         _ptr(h_prev), _ptr(out))
     return out
+
+
+def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None):
+    """Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+    x' = SiLU(causal depthwise Conv1d(hx)), h = BD-LRU(x'), y = h * SiLU(hz).
+    conv_w is [D][K]. Returns (y, h, hT)."""
+    hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0 = map(
+        _in, (hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0))
+    B, L, D = hx.shape
+    K = conv_w.shape[1]
+    y = np.empty_like(hx)
+    h = np.empty_like(hx)
+    hT = np.empty((B, D))
+    _load().oracle_gated_forward(B, L, D, K, _ptr(hx), _ptr(hz), _ptr(conv_w), _ptr(conv_b),
+                                 _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam), _ptr(h0),
+                                 _ptr(y), _ptr(h), _ptr(hT))
+    return y, h, hT

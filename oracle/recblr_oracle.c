@@ -25,6 +25,11 @@
  *     it is the same number, without the cancellation of 1 - alpha*alpha.
  *   - The backward pass is the exact adjoint of the forward recurrence
  *     (derived here; the paper gives no backward formulas).
+ *   - Gated recurrent layer (Algorithm alg:gated_recurrent, lines 3 to 5):
+ *     the causal Conv1d is depthwise with K taps and a bias per channel,
+ *     c_t[d] = b[d] + sum_{j<K} w[d][j] hx_{t-j}[d] with hx_{t<0} = 0 (the
+ *     kernel size is not stated); x' = SiLU(c) feeds both the gate
+ *     projections and the recurrence; the output is y = h (x) SiLU(hz).
  */
 #include <math.h>
 #include <stdint.h>
@@ -252,6 +257,41 @@ void oracle_backward(int64_t B, int64_t L, int64_t D, const double* x, const dou
     free(zi);
     free(dzr);
     free(dzi);
+}
+
+/*
+ * Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+ *   x'_t = SiLU(conv_b + sum_{j<K} conv_w[.][j] * hx_{t-j})   (causal, depthwise)
+ *   h    = BD-LRU(x') with z = x' W^T + b                    (section 3.2)
+ *   y_t  = h_t * SiLU(hz_t)
+ * hx, hz, y, h: [B][L][D]; conv_w: [D][K]; conv_b: [D] or NULL.  h may be NULL.
+ */
+static double silu(double v) { return v / (1.0 + exp(-v)); }
+
+void oracle_gated_forward(int64_t B, int64_t L, int64_t D, int64_t K, const double* hx,
+                          const double* hz, const double* conv_w, const double* conv_b,
+                          const double* Wr, const double* br, const double* Wi,
+                          const double* bi, const double* lambda, const double* h0, double* y,
+                          double* h, double* hT) {
+    size_t n = (size_t)(B * L * D);
+    double* xp = (double*)malloc((n ? n : 1) * sizeof(double));
+    double* hh = (double*)malloc((n ? n : 1) * sizeof(double));
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t d = 0; d < D; ++d)
+            for (int64_t t = 0; t < L; ++t) {
+                double c = conv_b ? conv_b[d] : 0.0;
+                for (int64_t j = 0; j < K && j <= t; ++j)
+                    c += conv_w[d * K + j] * hx[(b * L + t - j) * D + d];
+                xp[(b * L + t) * D + d] = silu(c);
+            }
+    oracle_forward(B, L, D, xp, Wr, br, Wi, bi, lambda, h0, hh, hT);
+    for (size_t e = 0; e < n; ++e) {
+        y[e] = hh[e] * silu(hz[e]);
+        if (h) h[e] = hh[e];
+    }
+    free(xp);
+    free(hh);
 }
 
 /* Full single step: projections of x_t, then one recurrence step. */

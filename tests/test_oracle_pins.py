@@ -13,6 +13,7 @@ the paper's two-tree parallel scan, exact rational arithmetic, library routines
 (scipy's expit, numpy's logaddexp and matmul) and central finite differences.
 """
 import json
+import math
 import os
 from fractions import Fraction
 
@@ -477,3 +478,75 @@ def test_golden_small_case_regression():
     np.testing.assert_allclose(hT.ravel(), g["hT"], rtol=1e-12, atol=1e-14)
     for k in ("dx", "dzr", "dzi", "dlambda", "dh0"):
         np.testing.assert_allclose(bw[k].ravel(), g[k], rtol=1e-12, atol=1e-14, err_msg=k)
+
+
+# ------------------------------------------------------------------ gated recurrent layer core
+# Algorithm alg:gated_recurrent, lines 3 to 5: x' = SiLU(Conv1d(hx)), BD-LRU, y = h * SiLU(hz).
+
+def _gated_case(B, L, D, K, seed):
+    rng = np.random.default_rng(seed)
+    f = dg.full_inputs(B, L, D, seed, bias=True, h0=True)
+    hz = rng.standard_normal((B, L, D))
+    w = rng.standard_normal((D, K))
+    cb = rng.standard_normal(D)
+    return f, hz, w, cb
+
+
+def test_gated_conv_brute_force():
+    """The causal depthwise conv written out with explicit loops (tap j reads
+    step t - j, no history before t = 0), fed to the pinned forward."""
+    B, L, D, K = 2, 7, 3, 3
+    f, hz, w, cb = _gated_case(B, L, D, K, 91)
+    xp = np.zeros((B, L, D))
+    for b in range(B):
+        for t in range(L):
+            for d in range(D):
+                c = cb[d]
+                for j in range(K):
+                    if t - j >= 0:
+                        c += w[d, j] * f.x[b, t - j, d]
+                xp[b, t, d] = c / (1.0 + math.exp(-c))
+    h_ref, hT_ref = oracle.forward(xp, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    y, h, hT = oracle.gated_forward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    np.testing.assert_allclose(h, h_ref, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(hT, hT_ref, rtol=1e-13, atol=1e-14)
+    silu_hz = hz / (1.0 + np.exp(-hz))
+    np.testing.assert_allclose(y, h_ref * silu_hz, rtol=1e-13, atol=1e-14)
+
+
+def test_gated_single_tap_identity():
+    """K = 1, w = 1, no bias: x' = SiLU(hx)."""
+    B, L, D = 2, 9, 4
+    f, hz, _, _ = _gated_case(B, L, D, 1, 92)
+    y, h, _ = oracle.gated_forward(f.x, hz, np.ones((D, 1)), None, f.Wr, f.br, f.Wi, f.bi,
+                                   f.lam, f.h0)
+    xs = f.x / (1.0 + np.exp(-f.x.astype(np.float64)))
+    h_ref, _ = oracle.forward(xs, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    np.testing.assert_allclose(h, h_ref, rtol=1e-13, atol=1e-14)
+
+
+def test_gated_silu_values_and_zero_gate():
+    """SiLU(v) = v / (1 + e^-v) at given points, and SiLU(0) = 0 closes the gate."""
+    B, L, D, K = 1, 3, 3, 2
+    f, _, w, cb = _gated_case(B, L, D, K, 93)
+    vals = np.array([-2.0, 0.5, 1.0])
+    hz = np.broadcast_to(vals, (B, L, D)).copy()
+    y, h, _ = oracle.gated_forward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam)
+    expect = [v / (1.0 + math.exp(-v)) for v in vals]  # SiLU(1) = 0.7310585786300049
+    assert abs(expect[2] - 0.7310585786300049) < 1e-15
+    np.testing.assert_allclose(y, h * np.array(expect), rtol=1e-14)
+    y0, _, _ = oracle.gated_forward(f.x, np.zeros((B, L, D)), w, cb, f.Wr, f.br, f.Wi, f.bi,
+                                    f.lam)
+    assert not y0.any()
+
+
+def test_gated_causality():
+    """Changing hx at step 5 leaves every earlier output unchanged, changes step 5."""
+    B, L, D, K = 2, 12, 4, 4
+    f, hz, w, cb = _gated_case(B, L, D, K, 94)
+    y1, _, _ = oracle.gated_forward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    x2 = f.x.copy()
+    x2[:, 5] += 1.0
+    y2, _, _ = oracle.gated_forward(x2, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    np.testing.assert_array_equal(y1[:, :5], y2[:, :5])
+    assert np.abs(y1[:, 5] - y2[:, 5]).max() > 1e-6
