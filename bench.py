@@ -1,7 +1,7 @@
 """Benchmark of the BD-LRU scan on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
-                    [--api scan|full|step|scan_step|ablation]
+                    [--api scan|full|step|scan_step|ablation|gated]
 
 A step is one pass of the hot path over one batch: the gated scan forward
 (recblr_bdlru_scan_forward) followed by its backward
@@ -17,7 +17,9 @@ pre-activations (recblr_bdlru_scan_step).  --api ablation times the layer
 forward (gate projections + scan) with the scan algorithms of the paper's
 efficiency ablation (serial scan; two-tree scan with sequence padding or with
 embedding padding; the production chunked scan) at the paper's three
-sequence lengths.
+sequence lengths.  --api gated times the gated recurrent layer core forward
+(causal conv + SiLU, BD-LRU with projections, SiLU output gate;
+recblr_gated_forward) on the workload.
 Prints ONE JSON line (metric, value, roofline of the dominant call, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).
 """
@@ -126,6 +128,77 @@ ABLATION_WORKLOADS = [("ml1m-like", 2048, 200, 128), ("gowalla-like", 2048, 100,
                       # few channels, long histories: where parallelism along the
                       # sequence matters (4096 channels, one wave each for the serial scan)
                       ("long-history", 16, 4096, 256)]
+
+
+def gated_main(args, torch, dg, rb):
+    """Gated recurrent layer core forward (conv taps K = 4) on a workload."""
+    cfg = dg.CONFIGS[args.workload or "c5"]
+    B, L, D = cfg.B, cfg.L, cfg.D
+    dev = torch.device("cuda:0")
+    dtype = torch.float32 if cfg.io == "f32" else torch.bfloat16
+    log(f"generating {cfg.name}: B={B} L={L} D={D} {cfg.io} (gated layer core)")
+    f = dg.full_inputs(B, L, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True)
+    rng = np.random.default_rng(cfg.seed + 1)
+    hz = rng.standard_normal((B, L, D), dtype=np.float32)
+    w = (rng.standard_normal((D, 4)) * 0.5).astype(np.float32)
+    cb = (rng.standard_normal(D) * 0.1).astype(np.float32)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dtype)
+    HX, HZ, Wr, br, Wi, bi = T(f.x), T(hz), T(f.Wr), T(f.br), T(f.Wi), T(f.bi)
+    W4, CB, lam = (torch.from_numpy(a).to(dev) for a in (w, cb, f.lam))
+    y = torch.empty_like(HX)
+    io = rb.io_code(dtype)
+    nws = rb.recblr_workspace_size(rb.OP_GATED_FORWARD, B, L, D, io)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    s = torch.cuda.current_stream()
+    p = lambda t: t.data_ptr()
+
+    def step():
+        st = rb.recblr_gated_forward(p(HX), p(HZ), p(W4), p(CB), 4, p(Wr), p(br), p(Wi), p(bi),
+                                     p(lam), None, p(y), None, None, B, L, D, io, p(ws), nws,
+                                     s.cuda_stream)
+        assert st == 0, st
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(s)
+    for k in range(K):
+        step()
+        ev[k + 1].record(s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    N = B * L * D
+    esz = 4 if cfg.io == "f32" else 2
+    ach = 3 * esz * N / float(np.mean(dts)) / 1e9  # hx, hz read; y written
+    log(f"gated forward {np.mean(dts)*1e6:.1f} us ({ach:.0f} GB/s)")
+    out = {"metric": "gated recurrent layer core forward elements/sec (B*L*D)",
+           "value": N * K / wall, "unit": "elements/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": wall / K * 1e3, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": cfg.io,
+           "data": "synthetic (seeded normal hx, hz, conv taps; decay bases per the paper's "
+                   "initialisation)",
+           "config": {"workload": f"{cfg.name}: gated layer core forward (conv K=4), {cfg.note}",
+                      "B": B, "L": L, "D": D, "io": cfg.io, "elements": N},
+           "us_forward": float(np.mean(dts)) * 1e6,
+           "roofline": {"bound": "hbm", "kernel": "gated_forward", "achieved": ach,
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                        "traffic": None}}
+    if not args.no_cpu_baseline:
+        import oracle
+        rows, t0, passes = 1, time.perf_counter(), 0
+        while time.perf_counter() - t0 < 10.0:
+            oracle.gated_forward(f.x[:rows], hz[:rows], w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam)
+            passes += 1
+        total = time.perf_counter() - t0
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        out["cpu_baseline"] = {"value": passes * rows * L * D / total, "unit": "elements/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"fp64 oracle gated forward over {rows} of {B} batch "
+                                         f"rows (L={L}, D={D}), {passes} passes, {total:.1f} s"}
+    print(json.dumps(out), flush=True)
 
 
 def ablation_main(args, torch, dg, rb):
@@ -296,7 +369,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation"],
+    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation", "gated"],
                     default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
@@ -325,6 +398,8 @@ def main():
         return decode_main(args, torch, dg, rb)
     if args.api == "ablation":
         return ablation_main(args, torch, dg, rb)
+    if args.api == "gated":
+        return gated_main(args, torch, dg, rb)
     cfg = dg.CONFIGS[args.workload or "c4"]
     if "bwd" not in cfg.ops:
         sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")

@@ -75,7 +75,8 @@ enum {
     RECBLR_OP_SCAN_BACKWARD = 1,
     RECBLR_OP_FORWARD = 2,
     RECBLR_OP_BACKWARD = 3,
-    RECBLR_OP_STEP = 4
+    RECBLR_OP_STEP = 4,
+    RECBLR_OP_GATED_FORWARD = 5
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -160,6 +161,30 @@ int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const
 int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const void* W_i,
                       const void* b_i, const float* lambda, const float* h_prev, float* h_next,
                       int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+ *   x'_t = SiLU(conv_b + sum_{j<K} conv_w[d][j] hx_{t-j})   causal, depthwise
+ *   h    = BD-LRU(x') with z = x' W^T + b                  (as recblr_bdlru_forward)
+ *   y_t  = h_t * SiLU(hz_t)
+ * The kernel size is not stated in the paper; 1 <= K <= 4, and hx before step
+ * 0 counts as zero.  The linear layers around this core (Algorithm lines 1,
+ * 2 and 6) are plain GEMMs outside the library.
+ *   hx, hz, y : [B][L][D] io;  h : [B][L][D] io or NULL (the BD-LRU output,
+ *   kept for a backward);  conv_w : [D][K] float;  conv_b : [D] float or NULL;
+ *   W_r, b_r, W_i, b_i, lambda, h0, hT : as recblr_bdlru_forward.
+ * Workspace: recblr_workspace_size(RECBLR_OP_GATED_FORWARD, ...).  x' is
+ * formed by one streaming kernel; where the scan forward with the
+ * projections fused in applies (few channel groups, D % 64 == 0) it reads x'
+ * and stores y directly (neither z nor h needs to reach memory).
+ * Errors: UNSUPPORTED for K outside 1..4 or D > 1024; otherwise as
+ * recblr_bdlru_forward.
+ */
+int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
+                         const float* conv_b, int K, const void* W_r, const void* b_r,
+                         const void* W_i, const void* b_i, const float* lambda, const float* h0,
+                         void* y, void* h, float* hT, int64_t B, int64_t L, int64_t D, int io,
+                         void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Scan algorithms of the efficiency ablation (section 4, Table tab:efficiency;

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "librecblr.so")
-SOURCES = ["capi.cpp", "scan_fwd.hip", "scan_bwd.hip", "step.hip", "gemm.hip", "ablation.hip"]
+SOURCES = ["capi.cpp", "scan_fwd.hip", "scan_bwd.hip", "step.hip", "gemm.hip", "ablation.hip", "gated.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",

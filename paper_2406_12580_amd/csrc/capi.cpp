@@ -102,6 +102,23 @@ FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     return l;
 }
 
+// Gated layer: conv taps and bias, then x' and h scratch for the unfused
+// path, then the layout of the entry points with weights.
+struct GatedLayout {
+    size_t w4, b4, xp, hbuf, full, total;
+};
+GatedLayout gated_layout(int64_t B, int64_t L, int64_t D, int io) {
+    GatedLayout l;
+    const size_t n = align_up((size_t)(B * L * D) * esz(io));
+    l.w4 = 0;
+    l.b4 = align_up((size_t)(kConvTaps * D) * sizeof(float));
+    l.xp = l.b4 + align_up((size_t)D * sizeof(float));
+    l.hbuf = l.xp + n;
+    l.full = l.hbuf + n;
+    l.total = l.full + full_fwd_layout(B, L, D, io).total;
+    return l;
+}
+
 // Step: z_r, z_i scratch, then the packed weights.
 size_t step_z_bytes(int64_t B, int64_t D) { return align_up((size_t)(B * D) * sizeof(float)); }
 size_t step_pack_bytes(int64_t D, int io) {
@@ -138,6 +155,7 @@ size_t recblr_workspace_size(int op, int64_t B, int64_t L, int64_t D, int io) {
         case RECBLR_OP_FORWARD: return full_fwd_layout(B, L, D, io).total;
         case RECBLR_OP_BACKWARD: return full_bwd_layout(B, L, D, io).total;
         case RECBLR_OP_STEP: return step_ws(B, D, io);
+        case RECBLR_OP_GATED_FORWARD: return gated_layout(B, L, D, io).total;
         default: return 0;
     }
 }
@@ -281,6 +299,66 @@ int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const 
     ScanFwdArgs a{x, zr, zi, lambda, h0, h, hT, B, L, D, io_of(io), IoType::kF32,
                   at(ws, lay.scan), lay.total - lay.scan};
     return status_of(launch_scan_forward(a, strm));
+}
+
+int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
+                         const float* conv_b, int K, const void* W_r, const void* b_r,
+                         const void* W_i, const void* b_i, const float* lambda, const float* h0,
+                         void* y, void* h, float* hT, int64_t B, int64_t L, int64_t D, int io,
+                         void* ws, size_t ws_bytes, void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D > kMaxProjD || K < 1 || K > kConvTaps) return RECBLR_ERR_UNSUPPORTED;
+    if (B == 0 || D == 0) return RECBLR_OK;
+    if (!lambda || !W_r || !W_i || !conv_w || (L > 0 && (!hx || !hz || !y)))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {hx, hz, W_r, W_i, b_r, b_i, (const void*)y, (const void*)h})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)hT,
+                          (const void*)conv_w, (const void*)conv_b})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 w = (size_t)(D * D) * esz(io), bb = (size_t)D * esz(io), df = (size_t)D * 4;
+    if (h && overlaps({h, n}, {y, n})) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{y, n}, {h, n}, {hT, s}},
+                  {{hx, n}, {hz, n}, {W_r, w}, {W_i, w}, {b_r, bb}, {b_i, bb}, {lambda, df},
+                   {h0, s}, {conv_w, (size_t)(D * K) * 4}, {conv_b, df}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    const GatedLayout lay = gated_layout(B, L, D, io);
+    st = check_ws(ws, ws_bytes, lay.total);
+    if (st) return st;
+    if (!disjoint({{ws, lay.total}}, {{hx, n}, {hz, n}, {y, n}, {h, n}, {hT, s}, {h0, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    float* w4 = (float*)at(ws, lay.w4);
+    float* b4 = (float*)at(ws, lay.b4);
+    if (launch_pack_conv(conv_w, conv_b, K, D, w4, b4, strm) != hipSuccess) return RECBLR_ERR_HIP;
+    const FullFwdLayout fl = full_fwd_layout(B, L, D, io);
+    char* fws = at(ws, lay.full);
+    void* pack = fws + fl.pack;
+    void* xp = at(ws, lay.xp);
+    // x' = SiLU(conv(hx)) is formed once, in a streaming kernel: doing it on
+    // the fly inside the fused scan kernel (its tap loads held in registers)
+    // cost that kernel three quarters of its occupancy.
+    if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), strm) != hipSuccess)
+        return RECBLR_ERR_HIP;
+    if (L > 0 && fused_forward_applies(B, L, D, io_of(io), xp, pack)) {
+        if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
+            return RECBLR_ERR_HIP;
+        return status_of(launch_fused_gated_forward(xp, hz, pack, b_r, b_i, lambda, h0, y, h, hT,
+                                                    B, L, D, io_of(io), fws + fl.scan, strm));
+    }
+    // Otherwise the layer forward on x', then the gate.
+    void* hout = h ? h : at(ws, lay.hbuf);
+    if (L > 0) {
+        hipError_t e = launch_project_forward(xp, W_r, b_r, W_i, b_i, fws + fl.zr, fws + fl.zi,
+                                              B * L, D, io_of(io), pack, strm);
+        if (e != hipSuccess) return RECBLR_ERR_HIP;
+    }
+    ScanFwdArgs a{xp, fws + fl.zr, fws + fl.zi, lambda, h0, hout, hT, B, L, D, io_of(io),
+                  IoType::kF32, fws + fl.scan, fl.total - fl.scan};
+    if (launch_scan_forward(a, strm) != hipSuccess) return RECBLR_ERR_HIP;
+    return status_of(launch_gate_out(hout, hz, y, B * L * D, io_of(io), strm));
 }
 
 int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const void* W_i,

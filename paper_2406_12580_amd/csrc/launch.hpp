@@ -83,4 +83,23 @@ hipError_t launch_scan_forward_serial(const ScanFwdArgs& a, hipStream_t stream);
 hipError_t launch_scan_forward_tree(const ScanFwdArgs& a, hipStream_t stream);
 bool tree_scan_supported(int64_t L);
 
+// Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5).
+// Conv taps are packed as [kConvTaps][D] (zero past K) plus a [D] bias.
+constexpr int kConvTaps = 4;
+hipError_t launch_pack_conv(const float* w, const float* b, int K, int64_t D, float* w4,
+                            float* b4, hipStream_t stream);
+// x' = SiLU(causal depthwise conv(hx)) into xp ([B][L][D], I/O type).
+hipError_t launch_conv_silu(const void* hx, const float* w4, const float* b4, void* xp, int64_t B,
+                            int64_t L, int64_t D, IoType io, hipStream_t stream);
+// y = h * SiLU(hz) over n elements.
+hipError_t launch_gate_out(const void* h, const void* hz, void* y, int64_t n, IoType io,
+                           hipStream_t stream);
+// The scan forward with the projections fused in (fused_forward_applies) on
+// x = x', storing y = h * SiLU(hz) (and h if not null).
+hipError_t launch_fused_gated_forward(const void* x, const void* hz, const void* pack,
+                                      const void* br, const void* bi, const float* lambda,
+                                      const float* h0, void* y, void* h, float* hT, int64_t B,
+                                      int64_t L, int64_t D, IoType io, void* ws,
+                                      hipStream_t stream);
+
 }  // namespace recblr

@@ -366,15 +366,25 @@ __device__ __forceinline__ void strip_mma(__bf16 (*la)[fastmm::BM][fastmm::KP],
         }
     }
 }
+// Gated-layer output (Algorithm alg:gated_recurrent, line 5): with GATED the
+// kernel stores y = h * SiLU(hz) (and h only where asked for).
+struct GatedArgs {
+    const void* hz;  // [B][L][D], I/O type
+    void* y;         // [B][L][D], I/O type
+};
+
+__device__ __forceinline__ float silu(float c) { return c * sigmoid(c); }
 }  // namespace fusedfwd
 
-// P.p0 is x; P.p1, P.p2 are unused.  pack: [W_r; W_i] ordered by channel
+// P.p0 is x; P.p1, P.p2 are unused; P.h may be null for GATED (then only y
+// is stored).  pack: [W_r; W_i] ordered by channel
 // group of 64 (launch_pack_groups); D % 64 == 0.
 // Occupancy: 3 workgroups per CU for bf16 I/O (LDS 48 KB each, 6 waves per
 // SIMD), 2 for fp32 (its split operands double the staging LDS).
-template <typename T, int K, typename Off>
-__global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void scan_fwd_fused_kernel(
-    FwdParams P, const __bf16* pack, const T* br, const T* bi) {
+template <typename T, int K, typename Off, bool GATED>
+__global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void
+scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
+                      fusedfwd::GatedArgs G) {
     using namespace fastmm;
     constexpr int W = fusedfwd::W, C = fusedfwd::C, NT = fusedfwd::NT, ZP = fusedfwd::ZP;
     constexpr bool F32 = sizeof(T) == 4;
@@ -414,19 +424,22 @@ __global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void scan_fwd
                     (uint32_t)(P.D * sizeof(T)), 0, 0, 0};
         const OpB wb{resource(pack + cg * 128 * P.D, (PB - 1) * plane + (uint32_t)(128 * P.D * 2)),
                      (uint32_t)(P.D * 2), 0, 0, plane};
-        const Stager<OpA, NT> sa(a, t0, tid);
         const Stager<OpB, NT> sb(wb, 0, tid);
-        typename OpA::raw_t ra[quads<NT>()];
         typename OpB::raw_t rb[quads<NT>()];
         const int64_t nsl = (P.D + BK - 1) / BK;
-        sa.fetch(a, 0, P.D, tid, ra);
         sb.fetch(wb, 0, P.D, tid, rb);
+        constexpr int Q = quads<NT>();
+        const Stager<OpA, NT> sa(a, t0, tid);
+        typename OpA::raw_t ra[Q];
+        auto fetch_a = [&](int64_t k0) { sa.fetch(a, k0, P.D, tid, ra); };
+        auto stage_a = [&]() { store_slice<OpA, NT>(la, tid, ra); };
+        fetch_a(0);
         for (int64_t sl = 0; sl < nsl; ++sl) {
-            store_slice<OpA, NT>(la, tid, ra);
+            stage_a();
             store_slice<OpB, NT>(lb, tid, rb);
             __syncthreads();
             if (sl + 1 < nsl) {
-                sa.fetch(a, (sl + 1) * BK, P.D, tid, ra);
+                fetch_a((sl + 1) * BK);
                 sb.fetch(wb, (sl + 1) * BK, P.D, tid, rb);
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -470,14 +483,19 @@ __global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void scan_fwd
     const int64_t tw = t0 + (int64_t)w * C;
     const bool full = (s + 1) * W * C <= P.L;  // workgroup-uniform
     float a[C][1], u[C][1];
+    float xs[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        const int64_t t = (full || tw + j < P.L) ? tw + j : P.L - 1;
+        float v[1];
+        load_vec<T, 1>((const T*)P.p0, ln.at(t), v);
+        xs[j] = v[0];
+    }
 #pragma unroll
     for (int j = 0; j < C; ++j) {
         const bool ok = full || tw + j < P.L;
-        const int64_t t = ok ? tw + j : P.L - 1;
-        float xv[1];
-        load_vec<T, 1>((const T*)P.p0, ln.at(t), xv);
         float aj, uj;
-        gate_forward(xv[0], zr[j], zi[j], cc[0], aj, uj);
+        gate_forward(xs[j], zr[j], zi[j], cc[0], aj, uj);
         a[j][0] = ok ? aj : 1.0f;
         u[j][0] = ok ? uj : 0.0f;
     }
@@ -510,8 +528,25 @@ __global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void scan_fwd
     }
     __syncthreads();
     float hv[1] = {fmaf(pre.A, carry_sh[lane][0], pre.H)};
-    if (full) emit_steps<true, T, C, 1, Off>(P, ln, tw, a, u, hv);
-    else emit_steps<false, T, C, 1, Off>(P, ln, tw, a, u, hv);
+    if constexpr (GATED) {
+        // y_t = h_t * SiLU(hz_t); h itself only if asked for.
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            hv[0] = fmaf(a[j][0], hv[0], u[j][0]);
+            const bool ok = ln.valid && (full || tw + j < P.L);
+            const int64_t t = (full || tw + j < P.L) ? tw + j : P.L - 1;
+            float gz[1];
+            load_vec<T, 1>((const T*)G.hz, ln.at(t), gz);
+            float yv[1] = {hv[0] * fusedfwd::silu(gz[0])};
+            if (ok) {
+                store_vec<T, 1>((T*)G.y, ln.at(t), yv);
+                if (P.h) store_vec<T, 1>((T*)P.h, ln.at(t), hv);
+            }
+        }
+    } else {
+        if (full) emit_steps<true, T, C, 1, Off>(P, ln, tw, a, u, hv);
+        else emit_steps<false, T, C, 1, Off>(P, ln, tw, a, u, hv);
+    }
     if (s == P.nseg - 1 && w == W - 1 && ln.valid && P.hT) P.hT[ln.c0] = hv[0];
 }
 
@@ -668,10 +703,11 @@ bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const voi
            (L + fastmm::BM) * D * (int64_t)esz < ((int64_t)1 << 31);
 }
 
-hipError_t launch_fused_forward(const void* x, const void* pack, const void* br, const void* bi,
-                                const float* lambda, const float* h0, void* h, float* hT,
-                                int64_t B, int64_t L, int64_t D, IoType io, void* ws,
-                                hipStream_t stream) {
+template <bool GATED>
+static hipError_t launch_fused_t(const void* x, const void* pack, const void* br, const void* bi,
+                                 const float* lambda, const float* h0, void* h, float* hT,
+                                 int64_t B, int64_t L, int64_t D, IoType io, void* ws,
+                                 const fusedfwd::GatedArgs& G, hipStream_t stream) {
     const size_t esz = io_bytes(io);
     const FwdPlan plan = plan_forward(B, L, D, esz, 1);
     FwdParams P{x, nullptr, nullptr, lambda, h0, h, hT, L, D, B * D, plan.ngroups, plan.nseg,
@@ -680,26 +716,44 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedfwd::NT);
     const bool small = (uint64_t)(B * L * D) * esz < (1ull << 32);
+    constexpr int K = lb_window<1>();
     if (io == IoType::kF32) {
         if (small)
-            hipLaunchKernelGGL((scan_fwd_fused_kernel<float, lb_window<1>(), uint32_t>), grid,
-                               block, 0, stream, P, (const __bf16*)pack, (const float*)br,
-                               (const float*)bi);
+            hipLaunchKernelGGL((scan_fwd_fused_kernel<float, K, uint32_t, GATED>), grid, block, 0,
+                               stream, P, (const __bf16*)pack, (const float*)br, (const float*)bi,
+                               G);
         else
-            hipLaunchKernelGGL((scan_fwd_fused_kernel<float, lb_window<1>(), uint64_t>), grid,
-                               block, 0, stream, P, (const __bf16*)pack, (const float*)br,
-                               (const float*)bi);
+            hipLaunchKernelGGL((scan_fwd_fused_kernel<float, K, uint64_t, GATED>), grid, block, 0,
+                               stream, P, (const __bf16*)pack, (const float*)br, (const float*)bi,
+                               G);
     } else {
         if (small)
-            hipLaunchKernelGGL((scan_fwd_fused_kernel<bf16, lb_window<1>(), uint32_t>), grid,
-                               block, 0, stream, P, (const __bf16*)pack, (const bf16*)br,
-                               (const bf16*)bi);
+            hipLaunchKernelGGL((scan_fwd_fused_kernel<bf16, K, uint32_t, GATED>), grid, block, 0,
+                               stream, P, (const __bf16*)pack, (const bf16*)br, (const bf16*)bi,
+                               G);
         else
-            hipLaunchKernelGGL((scan_fwd_fused_kernel<bf16, lb_window<1>(), uint64_t>), grid,
-                               block, 0, stream, P, (const __bf16*)pack, (const bf16*)br,
-                               (const bf16*)bi);
+            hipLaunchKernelGGL((scan_fwd_fused_kernel<bf16, K, uint64_t, GATED>), grid, block, 0,
+                               stream, P, (const __bf16*)pack, (const bf16*)br, (const bf16*)bi,
+                               G);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_fused_forward(const void* x, const void* pack, const void* br, const void* bi,
+                                const float* lambda, const float* h0, void* h, float* hT,
+                                int64_t B, int64_t L, int64_t D, IoType io, void* ws,
+                                hipStream_t stream) {
+    return launch_fused_t<false>(x, pack, br, bi, lambda, h0, h, hT, B, L, D, io, ws,
+                                 fusedfwd::GatedArgs{}, stream);
+}
+
+hipError_t launch_fused_gated_forward(const void* x, const void* hz, const void* pack,
+                                      const void* br, const void* bi, const float* lambda,
+                                      const float* h0, void* y, void* h, float* hT, int64_t B,
+                                      int64_t L, int64_t D, IoType io, void* ws,
+                                      hipStream_t stream) {
+    return launch_fused_t<true>(x, pack, br, bi, lambda, h0, h, hT, B, L, D, io, ws,
+                                fusedfwd::GatedArgs{hz, y}, stream);
 }
 
 // Serial scan of the efficiency ablation: one wave per 64 channels walks the

@@ -29,14 +29,14 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
-OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP = range(5)
+OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP, OP_GATED_FORWARD = range(6)
 SCAN_CHUNKED, SCAN_SERIAL, SCAN_TREE = range(3)
 
 EXPORTS = (
     "recblr_status_string", "recblr_workspace_size", "recblr_bdlru_scan_forward",
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
-    "recblr_scan_forward_method",
+    "recblr_scan_forward_method", "recblr_gated_forward",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
@@ -51,6 +51,8 @@ _SIGS = {
     "recblr_bdlru_step": ([_p] * 8 + [_i64] * 2 + [_int, _p, _sz, _p], _int),
     "recblr_linear_scan_forward": ([_p] * 5 + [_i64] * 3 + [_p], _int),
     "recblr_scan_forward_method": ([_int] + [_p] * 5 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_gated_forward": ([_p] * 4 + [_int] + [_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p],
+                             _int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -238,3 +240,21 @@ def scan_forward_method(method, x, zr, zi, lam, stream=None):
                                       B, L, D, io, _ptr(ws), nws, _stream(stream)),
            "recblr_scan_forward_method")
     return h
+
+
+def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None, keep_h=True,
+                  stream=None):
+    """Gated recurrent layer core: y = BD-LRU(SiLU(conv(hx))) * SiLU(hz).
+    conv_w is [D][K] float32. Returns (y, h, hT) (h is None unless keep_h)."""
+    B, L, D = hx.shape
+    K = conv_w.shape[1]
+    io = io_code(hx.dtype)
+    y = torch.empty_like(hx)
+    h = torch.empty_like(hx) if keep_h else None
+    hT = torch.empty((B, D), dtype=torch.float32, device=hx.device)
+    ws, nws = _workspace(OP_GATED_FORWARD, B, L, D, io, hx.device)
+    _check(recblr_gated_forward(_ptr(hx), _ptr(hz), _ptr(conv_w), _ptr(conv_b), K, _ptr(Wr),
+                                _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam), _ptr(h0), _ptr(y),
+                                _ptr(h), _ptr(hT), B, L, D, io, _ptr(ws), nws, _stream(stream)),
+           "recblr_gated_forward")
+    return y, h, hT

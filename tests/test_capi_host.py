@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 10
+    assert len(syms) == 11
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -155,3 +155,16 @@ def test_scan_method_validation(rb):
              None) == rb.ERR_UNSUPPORTED                                # unknown dtype
     assert f(rb.SCAN_TREE, None, None, None, None, None, 0, 3, 4, rb.F32, None, 0,
              None) == rb.OK                                             # empty batch
+
+
+def test_gated_forward_validation(rb):
+    def call(K=2, conv_w=addr(7), nws=1 << 20, hx=addr(0)):
+        return rb.recblr_gated_forward(hx, addr(1), conv_w, None, K, addr(2), None, addr(3), None,
+                                       addr(4), None, addr(5), None, None, 2, 3, 64, rb.F32,
+                                       addr(6), nws, None)
+    assert call(K=0) == rb.ERR_UNSUPPORTED
+    assert call(K=5) == rb.ERR_UNSUPPORTED
+    assert call(conv_w=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(hx=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(nws=16) == rb.ERR_WORKSPACE
+    assert rb.recblr_workspace_size(rb.OP_GATED_FORWARD, 2, 3, 64, rb.F32) > 0

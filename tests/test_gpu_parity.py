@@ -319,6 +319,43 @@ def test_tree_scan_sequence_padding(rb):
     assert_close(host(h)[:, P - L:], oh, "f32", "tree h, sequence padding")
 
 
+# ------------------------------------------------------------------ gated recurrent layer core
+# Few channel groups, L > 128 and D % 64 == 0 take the fused kernel (conv on
+# load, gate on store); the others the unfused path.
+GATED_CASES = [((2, 300, 64), 4), ((1, 700, 128), 2), ((1, 513, 256), 1), ((8, 50, 64), 4),
+               ((2, 300, 72), 3), ((3, 1, 64), 4)]
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("case", GATED_CASES)
+def test_gated_forward(rb, case, io):
+    import torch
+    (B, L, D), K = case
+    f = dg.full_inputs(B, L, D, 8000 + B + L + D + K, io=io, a_range=(0.99, 0.9999), bias=True,
+                       h0=True)
+    rng = np.random.default_rng(8000 + L)
+    hz = rng.standard_normal((B, L, D)).astype(np.float32)
+    if io == "bf16":
+        hz = dg.round_bf16(hz)
+    w = (rng.standard_normal((D, K)) * 0.5).astype(np.float32)
+    cb = (rng.standard_normal(D) * 0.1).astype(np.float32)
+    y, h, hT = rb.gated_forward(dev(f.x, io), dev(hz, io), dev32(w), dev32(cb),
+                                *(dev(a, io) for a in (f.Wr, f.br, f.Wi, f.bi)), dev32(f.lam),
+                                dev32(f.h0))
+    y2, h2, _ = rb.gated_forward(dev(f.x, io), dev(hz, io), dev32(w), None,
+                                 *(dev(a, io) for a in (f.Wr, f.br, f.Wi, f.bi)), dev32(f.lam),
+                                 keep_h=False)
+    torch.cuda.synchronize()
+    print(f"gated {case} {io}: GPU done", flush=True)
+    oy, oh, ohT = oracle.gated_forward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    assert_close(host(y), oy, io, "y")
+    assert_close(host(h), oh, io, "h")
+    assert_close(host(hT), ohT, "f32" if io == "f32" else "bf16", "hT")
+    oy2, _, _ = oracle.gated_forward(f.x, hz, w, None, f.Wr, f.br, f.Wi, f.bi, f.lam)
+    assert h2 is None
+    assert_close(host(y2), oy2, io, "y (no bias, no h0, h not kept)")
+
+
 # ------------------------------------------------------------------ named workloads at full size
 
 def _sample_rows(B, k=3):
