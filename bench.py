@@ -20,8 +20,11 @@ embedding padding; the production chunked scan) at the paper's three
 sequence lengths.  --api gated times the gated recurrent layer core forward
 (causal conv + SiLU, BD-LRU with projections, SiLU output gate;
 recblr_gated_forward) on the workload.
-Prints ONE JSON line (metric, value, roofline of the dominant call, and the
-fp64 CPU oracle timed on a bounded sample of the same workload).
+Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
+fp64 CPU oracle timed on a bounded sample of the same workload).  With the
+scan API the roofline takes the scan kernel's own duration, from a HIP event
+pair the library records on the launch stream right around that kernel
+(recblr_bdlru_scan_*_timed); the other APIs report it for the whole call.
 """
 from __future__ import annotations
 
@@ -50,9 +53,9 @@ ARRAYS = {"scan": (4, 8), "full": (2, 4)}
 # valid only for the kernel sources they were taken on: the sha256 prefix of
 # the listed files must match, else the traffic is reported as null.
 TRAFFIC = {
-    ("c4", "scan_bwd"): {"bytes": 2_169_322_496, "sha": "501c4d3e26cefe5d",
+    ("c4", "scan_bwd"): {"bytes": 2_185_769_952, "sha": "fa110b538ec55819",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c4", "scan_fwd"): {"bytes": 1_074_294_784, "sha": "5851d76487e378dd",
+    ("c4", "scan_fwd"): {"bytes": 1_074_309_088, "sha": "0783e2ddc3a272c0",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
 }
 
@@ -429,15 +432,22 @@ def main():
         wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
         wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
 
+        # The measurement entry points also record a HIP event pair on the launch
+        # stream right around the scan kernel itself (kev[0] forward, kev[1]
+        # backward); the pairs of the timed steps give the kernel durations.
+        kev = [None, None]
+
         def fwd():
-            st = rb.recblr_bdlru_scan_forward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(hT), B, L,
-                                              D, io, p(wsf), nf, s)
+            e = kev[0] or (None, None)
+            st = rb.recblr_bdlru_scan_forward_timed(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(hT),
+                                                    B, L, D, io, p(wsf), nf, s, e[0], e[1])
             assert st == 0, st
 
         def bwd():
-            st = rb.recblr_bdlru_scan_backward(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(DH), None,
-                                               p(dx), p(dzr), p(dzi), p(dlam), p(dh0), B, L, D,
-                                               io, p(wsb), nb, s)
+            e = kev[1] or (None, None)
+            st = rb.recblr_bdlru_scan_backward_timed(p(X), p(ZR), p(ZI), p(lam), None, p(h), p(DH),
+                                                     None, p(dx), p(dzr), p(dzi), p(dlam), p(dh0),
+                                                     B, L, D, io, p(wsb), nb, s, e[0], e[1])
             assert st == 0, st
     else:
         f = dg.full_inputs(B, L, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True,
@@ -471,18 +481,37 @@ def main():
     torch.cuda.synchronize()
     K = args.steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    kernel_ev = None
+    if args.api == "scan":
+        # torch creates an event on its first record; record each once so that
+        # the raw handles exist before the library records them.
+        kernel_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        for row in kernel_ev:
+            for e in row:
+                e.record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(K):
         ev[k][0].record(stream)
-        fwd()
-        ev[k][1].record(stream)
-        bwd()
+        if kernel_ev is not None:
+            # Every event record costs stream time, so the split between the
+            # calls is the forward kernel's end event (only that kernel runs
+            # after it in the forward call).
+            r = kernel_ev[k]
+            kev[0] = (r[0].cuda_event, r[1].cuda_event)
+            kev[1] = (r[2].cuda_event, r[3].cuda_event)
+            fwd()
+            bwd()
+        else:
+            fwd()
+            ev[k][1].record(stream)
+            bwd()
         ev[k][2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    t_fwd = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e-3
-    t_bwd = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
+    mid = [kernel_ev[k][1] if kernel_ev is not None else ev[k][1] for k in range(K)]
+    t_fwd = np.array([ev[k][0].elapsed_time(mid[k]) for k in range(K)]) * 1e-3
+    t_bwd = np.array([mid[k].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
     step_s = wall / K
     fb_s = float(np.mean(t_fwd + t_bwd))
     fwd_arrays, bwd_arrays = ARRAYS[args.api]
@@ -492,6 +521,15 @@ def main():
     bwd_gbs = bwd_bytes / float(np.mean(t_bwd)) / 1e9
     dom = "bwd" if np.mean(t_bwd) >= np.mean(t_fwd) else "fwd"
     ach = bwd_gbs if dom == "bwd" else fwd_gbs
+    kernel_us = None
+    if kernel_ev is not None:
+        # Roofline of the dominant kernel on its own duration (the events bracket
+        # only the scan kernel; the call times above include the look-back reset
+        # and the dLambda reduction).
+        k_fwd = np.array([r[0].elapsed_time(r[1]) for r in kernel_ev]) * 1e-3
+        k_bwd = np.array([r[2].elapsed_time(r[3]) for r in kernel_ev]) * 1e-3
+        kernel_us = {"fwd": float(np.mean(k_fwd)) * 1e6, "bwd": float(np.mean(k_bwd)) * 1e6}
+        ach = (bwd_bytes if dom == "bwd" else fwd_bytes) / (kernel_us[dom] * 1e-6) / 1e9
     log(f"fwd {np.mean(t_fwd)*1e6:.1f} us ({fwd_gbs:.0f} GB/s)  bwd {np.mean(t_bwd)*1e6:.1f} us "
         f"({bwd_gbs:.0f} GB/s)  wall/step {step_s*1e6:.1f} us")
 
@@ -520,6 +558,7 @@ def main():
         "us_bwd": float(np.mean(t_bwd)) * 1e6,
         "fwd_hbm_gbs": fwd_gbs,
         "bwd_hbm_gbs": bwd_gbs,
+        "kernel_us": kernel_us,
         "roofline": {"bound": "hbm", "kernel": kname,
                      "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": ach / PEAK_HBM_GBS,

@@ -123,6 +123,28 @@ int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
                                int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Measurement variants of the two scans above: the same work, arguments and
+ * errors, plus two caller-created HIP events (hipEvent_t; either may be NULL)
+ * recorded on `stream` immediately before and after the launch of the scan
+ * kernel itself.  The look-back state reset before it and, in the backward,
+ * the two dLambda reduction kernels after it fall outside the pair, so the
+ * time between the events is that one kernel's duration.  The events are
+ * recorded only when the scan kernel is launched (not for B, D or L = 0); a
+ * validation error records neither.
+ */
+int recblr_bdlru_scan_forward_timed(const void* x, const void* z_r, const void* z_i,
+                                    const float* lambda, const float* h0, void* h, float* hT,
+                                    int64_t B, int64_t L, int64_t D, int io, void* ws,
+                                    size_t ws_bytes, void* stream, void* ev_begin,
+                                    void* ev_end);
+int recblr_bdlru_scan_backward_timed(const void* x, const void* z_r, const void* z_i,
+                                     const float* lambda, const float* h0, const void* h,
+                                     const void* dh, const float* dhT, void* dx, void* dz_r,
+                                     void* dz_i, float* dlambda, float* dh0, int64_t B,
+                                     int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
+                                     void* stream, void* ev_begin, void* ev_end);
+
+/*
  * One recurrent step for inference (eq:linrnn applied once; the paper's
  * low-cost recurrent inference):  h_next = alpha(z_r) h_prev + beta(z_r, z_i) x.
  *   x, z_r, z_i : [B][D] io;  h_prev, h_next : [B][D] float (h_next may == h_prev)

@@ -164,6 +164,15 @@ int recblr_bdlru_scan_forward(const void* x, const void* z_r, const void* z_i,
                               const float* lambda, const float* h0, void* h, float* hT,
                               int64_t B, int64_t L, int64_t D, int io, void* ws,
                               size_t ws_bytes, void* stream) {
+    return recblr_bdlru_scan_forward_timed(x, z_r, z_i, lambda, h0, h, hT, B, L, D, io, ws,
+                                           ws_bytes, stream, nullptr, nullptr);
+}
+
+int recblr_bdlru_scan_forward_timed(const void* x, const void* z_r, const void* z_i,
+                                    const float* lambda, const float* h0, void* h, float* hT,
+                                    int64_t B, int64_t L, int64_t D, int io, void* ws,
+                                    size_t ws_bytes, void* stream, void* ev_begin,
+                                    void* ev_end) {
     int st = check_dims(B, L, D, io);
     if (st) return st;
     if (B == 0 || D == 0) return RECBLR_OK;
@@ -179,7 +188,8 @@ int recblr_bdlru_scan_forward(const void* x, const void* z_r, const void* z_i,
         return RECBLR_ERR_INVALID_ARGUMENT;
     st = check_ws(ws, ws_bytes, scan_forward_workspace(B, L, D, io_of(io)));
     if (st) return st;
-    ScanFwdArgs a{x, z_r, z_i, lambda, h0, h, hT, B, L, D, io_of(io), io_of(io), ws, ws_bytes};
+    ScanFwdArgs a{x, z_r, z_i, lambda, h0, h, hT, B, L, D, io_of(io), io_of(io), ws, ws_bytes,
+                  (hipEvent_t)ev_begin, (hipEvent_t)ev_end};
     return status_of(launch_scan_forward(a, (hipStream_t)stream));
 }
 
@@ -213,6 +223,17 @@ int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
                                const void* dh, const float* dhT, void* dx, void* dz_r,
                                void* dz_i, float* dlambda, float* dh0, int64_t B, int64_t L,
                                int64_t D, int io, void* ws, size_t ws_bytes, void* stream) {
+    return recblr_bdlru_scan_backward_timed(x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i,
+                                            dlambda, dh0, B, L, D, io, ws, ws_bytes, stream,
+                                            nullptr, nullptr);
+}
+
+int recblr_bdlru_scan_backward_timed(const void* x, const void* z_r, const void* z_i,
+                                     const float* lambda, const float* h0, const void* h,
+                                     const void* dh, const float* dhT, void* dx, void* dz_r,
+                                     void* dz_i, float* dlambda, float* dh0, int64_t B,
+                                     int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
+                                     void* stream, void* ev_begin, void* ev_end) {
     int st = check_dims(B, L, D, io);
     if (st) return st;
     if (D == 0) return RECBLR_OK;
@@ -236,7 +257,8 @@ int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
     st = check_ws(ws, ws_bytes, scan_backward_workspace(B, L, D, io_of(io)));
     if (st) return st;
     ScanBwdArgs a{x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
-                  B, L, D, io_of(io), io_of(io), ws, ws_bytes};
+                  B, L, D, io_of(io), io_of(io), ws, ws_bytes,
+                  (hipEvent_t)ev_begin, (hipEvent_t)ev_end};
     return status_of(launch_scan_backward(a, strm));
 }
 

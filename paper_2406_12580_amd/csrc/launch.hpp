@@ -26,6 +26,8 @@ struct ScanFwdArgs {
     IoType zio;       // element type of z_r, z_i (fp32 scratch in the entry points with weights)
     void* ws;         // look-back state, when the launcher uses it
     size_t ws_bytes;
+    hipEvent_t ev_begin = nullptr;  // recorded right before / after the main scan
+    hipEvent_t ev_end = nullptr;    // kernel's launch when not null
 };
 
 struct ScanBwdArgs {
@@ -47,7 +49,14 @@ struct ScanBwdArgs {
     IoType zio;       // element type of z_r, z_i, dz_r, dz_i
     void* ws;
     size_t ws_bytes;
+    hipEvent_t ev_begin = nullptr;  // as in ScanFwdArgs
+    hipEvent_t ev_end = nullptr;
 };
+
+// Records e on stream unless e is null (the measurement events of the scans).
+inline hipError_t mark_event(hipEvent_t e, hipStream_t stream) {
+    return e ? hipEventRecord(e, stream) : hipSuccess;
+}
 
 // Workspace (bytes) the scan launchers need for a given problem.
 size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io);

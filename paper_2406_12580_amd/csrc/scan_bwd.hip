@@ -513,7 +513,7 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
 #define RECBLR_BWD_LB_W 8
 #endif
 #ifndef RECBLR_BWD_LB_E
-#define RECBLR_BWD_LB_E 8
+#define RECBLR_BWD_LB_E 16
 #endif
 // Channels per lane at most, per kernel (measured best on MI355X).
 #ifndef RECBLR_BWD_CHAIN_MAX_VEC
@@ -534,10 +534,15 @@ template <int E, int VEC>
 constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
 // Steps of one look-back tile for a given VEC.
 constexpr int64_t lb_tile_steps(int vec) { return (int64_t)kLbW * (kLbE / vec > 0 ? kLbE / vec : 1); }
-// The chain kernel is used when its workgroups alone fill the GPU (one
-// workgroup per compute unit at least); lanes then take as many channels as
-// keep that many workgroups.
+// Lanes of the chain kernel take as many channels as keep this many
+// workgroups (one per compute unit).
 constexpr int64_t kChainMinGroups = 256;
+// The chain kernel runs when it has at least four workgroups per compute
+// unit; below that the look-back kernel is faster (its 16 steps per wave
+// amortise the carry fold over four times as many steps as the chain
+// kernel's 4; 256 x 2048 x 128 fp32: 378 us against 404 us on MI355X),
+// above it the chain kernel is (2048 x 200 x 64: 177 us against 183 us).
+constexpr int64_t kLookbackBelowGroups = 1024;
 // Largest channels-per-lane of a kernel for an element size (8-byte accesses
 // per lane at most).
 constexpr int max_vec(size_t esz, bool lookback, int64_t nch = INT64_MAX) {
@@ -557,7 +562,7 @@ struct BwdPlan {
 // forward launcher).
 static bool backward_uses_lookback(int64_t B, int64_t L, int64_t D, size_t esz) {
     const int64_t groups_one = (B * D + kWave - 1) / kWave;
-    return groups_one < kChainMinGroups && L > lb_tile_steps(max_vec(esz, true));
+    return groups_one < kLookbackBelowGroups && L > lb_tile_steps(max_vec(esz, true));
 }
 
 static BwdPlan plan_backward(int64_t B, int64_t L, int64_t D, size_t esz, int vec) {
@@ -603,38 +608,45 @@ size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
     return bwd_layout(B, D, plan_backward(B, L, D, esz, max_vec(esz, lb))).total;
 }
 
+// ev0 / ev1 (may be null) are recorded right before and after the scan kernel.
 template <typename TX, typename TZ, typename Off, int VEC>
-static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStream_t stream) {
+static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStream_t stream,
+                                 hipEvent_t ev0, hipEvent_t ev1) {
+    hipError_t e;
     if (!plan.lookback) {
+        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
         hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, steps_per_wave<kChainE, VEC>(),
                                                   VEC, Off>),
                            dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
-        return hipGetLastError();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return mark_event(ev1, stream);
     }
-    hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
-    if (e != hipSuccess) return e;
+    if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
+    if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
     hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(), VEC,
                                                  lb_window<VEC>(), Off>),
                        dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0, stream,
                        P);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return mark_event(ev1, stream);
 }
 
 template <typename TX, typename TZ>
-static hipError_t launch_bwd_typed(const BwdParams& P, const BwdPlan& plan, hipStream_t stream) {
+static hipError_t launch_bwd_typed(const BwdParams& P, const BwdPlan& plan, hipStream_t stream,
+                                   hipEvent_t ev0, hipEvent_t ev1) {
     // 32-bit byte offsets whenever a whole [B, L, D] tensor spans less than 4 GiB.
     const bool small = (uint64_t)(P.nch * P.L) * sizeof(TZ) < (1ull << 32);
     // VEC = 4 only exists for 2-byte x (8-byte accesses per lane).
     if (small) {
         if constexpr (sizeof(TX) == 2)
-            if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint32_t, 4>(P, plan, stream);
-        if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint32_t, 2>(P, plan, stream);
-        return launch_bwd_vec<TX, TZ, uint32_t, 1>(P, plan, stream);
+            if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint32_t, 4>(P, plan, stream, ev0, ev1);
+        if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint32_t, 2>(P, plan, stream, ev0, ev1);
+        return launch_bwd_vec<TX, TZ, uint32_t, 1>(P, plan, stream, ev0, ev1);
     }
     if constexpr (sizeof(TX) == 2)
-        if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint64_t, 4>(P, plan, stream);
-    if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint64_t, 2>(P, plan, stream);
-    return launch_bwd_vec<TX, TZ, uint64_t, 1>(P, plan, stream);
+        if (plan.vec == 4) return launch_bwd_vec<TX, TZ, uint64_t, 4>(P, plan, stream, ev0, ev1);
+    if (plan.vec == 2) return launch_bwd_vec<TX, TZ, uint64_t, 2>(P, plan, stream, ev0, ev1);
+    return launch_bwd_vec<TX, TZ, uint64_t, 1>(P, plan, stream, ev0, ev1);
 }
 
 hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
@@ -648,9 +660,11 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
                       plan.ngroups, plan.nseg,
                       plan.lookback ? lookback_ws(ws + lay.lb) : LookbackWs{}};
     hipError_t e;
-    if (a.io == IoType::kF32) e = launch_bwd_typed<float, float>(P, plan, stream);
-    else if (a.zio == IoType::kF32) e = launch_bwd_typed<bf16, float>(P, plan, stream);
-    else e = launch_bwd_typed<bf16, bf16>(P, plan, stream);
+    if (a.io == IoType::kF32)
+        e = launch_bwd_typed<float, float>(P, plan, stream, a.ev_begin, a.ev_end);
+    else if (a.zio == IoType::kF32)
+        e = launch_bwd_typed<bf16, float>(P, plan, stream, a.ev_begin, a.ev_end);
+    else e = launch_bwd_typed<bf16, bf16>(P, plan, stream, a.ev_begin, a.ev_end);
     if (e != hipSuccess) return e;
     const int64_t rows = plan.nseg * a.B;
     const int64_t nblk = (rows + kReduceRows - 1) / kReduceRows;

@@ -642,42 +642,49 @@ size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
     return lookback_ws_bytes(plan_forward(B, L, D, esz, max_vec(esz, true)).nseg, B * D);
 }
 
+// ev0 / ev1 (may be null) are recorded right before and after the scan kernel.
 template <typename TX, typename TZ, bool RAW, typename Off, int VEC>
-static hipError_t launch_vec(const FwdParams& P, const FwdPlan& plan, hipStream_t stream) {
+static hipError_t launch_vec(const FwdParams& P, const FwdPlan& plan, hipStream_t stream,
+                             hipEvent_t ev0, hipEvent_t ev1) {
+    hipError_t e;
     if (!plan.lookback) {
+        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
         hipLaunchKernelGGL((scan_fwd_chain_kernel<TX, TZ, kChainW,
                                                   steps_per_wave<kChainE, VEC>(), VEC, RAW, Off>),
                            dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
-        return hipGetLastError();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return mark_event(ev1, stream);
     }
     if constexpr (RAW) {
         return hipErrorInvalidValue;  // the raw scan always runs the chain kernel
     } else {
-        hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
-        if (e != hipSuccess) return e;
+        if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
+        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
         hipLaunchKernelGGL((scan_fwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(),
                                                      VEC, lb_window<VEC>(), Off>),
                            dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0,
                            stream, P);
-        return hipGetLastError();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return mark_event(ev1, stream);
     }
 }
 
 template <typename TX, typename TZ, bool RAW>
-static hipError_t launch_typed(const FwdParams& P, const FwdPlan& plan, hipStream_t stream) {
+static hipError_t launch_typed(const FwdParams& P, const FwdPlan& plan, hipStream_t stream,
+                               hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
     // 32-bit byte offsets whenever a whole [B, L, D] tensor spans less than 4 GiB.
     const bool small = (uint64_t)(P.nch * P.L) * sizeof(TZ) < (1ull << 32);
     // VEC = 4 only exists for 2-byte x (8-byte accesses per lane).
     if (small) {
         if constexpr (sizeof(TX) == 2)
-            if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint32_t, 4>(P, plan, stream);
-        if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint32_t, 2>(P, plan, stream);
-        return launch_vec<TX, TZ, RAW, uint32_t, 1>(P, plan, stream);
+            if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint32_t, 4>(P, plan, stream, ev0, ev1);
+        if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint32_t, 2>(P, plan, stream, ev0, ev1);
+        return launch_vec<TX, TZ, RAW, uint32_t, 1>(P, plan, stream, ev0, ev1);
     }
     if constexpr (sizeof(TX) == 2)
-        if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint64_t, 4>(P, plan, stream);
-    if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint64_t, 2>(P, plan, stream);
-    return launch_vec<TX, TZ, RAW, uint64_t, 1>(P, plan, stream);
+        if (plan.vec == 4) return launch_vec<TX, TZ, RAW, uint64_t, 4>(P, plan, stream, ev0, ev1);
+    if (plan.vec == 2) return launch_vec<TX, TZ, RAW, uint64_t, 2>(P, plan, stream, ev0, ev1);
+    return launch_vec<TX, TZ, RAW, uint64_t, 1>(P, plan, stream, ev0, ev1);
 }
 
 hipError_t launch_scan_forward(const ScanFwdArgs& a, hipStream_t stream) {
@@ -689,9 +696,11 @@ hipError_t launch_scan_forward(const ScanFwdArgs& a, hipStream_t stream) {
     const FwdPlan plan = plan_forward(a.B, a.L, a.D, esz, vec);
     FwdParams P{a.x, a.zr, a.zi, a.lambda, a.h0, a.h, a.hT, a.L, a.D, a.B * a.D,
                 plan.ngroups, plan.nseg, plan.lookback ? lookback_ws(a.ws) : LookbackWs{}};
-    if (a.io == IoType::kF32) return launch_typed<float, float, false>(P, plan, stream);
-    if (a.zio == IoType::kF32) return launch_typed<bf16, float, false>(P, plan, stream);
-    return launch_typed<bf16, bf16, false>(P, plan, stream);
+    if (a.io == IoType::kF32)
+        return launch_typed<float, float, false>(P, plan, stream, a.ev_begin, a.ev_end);
+    if (a.zio == IoType::kF32)
+        return launch_typed<bf16, float, false>(P, plan, stream, a.ev_begin, a.ev_end);
+    return launch_typed<bf16, bf16, false>(P, plan, stream, a.ev_begin, a.ev_end);
 }
 
 bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,

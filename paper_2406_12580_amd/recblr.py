@@ -36,7 +36,8 @@ EXPORTS = (
     "recblr_status_string", "recblr_workspace_size", "recblr_bdlru_scan_forward",
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
-    "recblr_scan_forward_method", "recblr_gated_forward",
+    "recblr_scan_forward_method", "recblr_gated_forward", "recblr_bdlru_scan_forward_timed",
+    "recblr_bdlru_scan_backward_timed",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
@@ -45,6 +46,9 @@ _SIGS = {
     "recblr_workspace_size": ([_int, _i64, _i64, _i64, _int], _sz),
     "recblr_bdlru_scan_forward": ([_p] * 7 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
     "recblr_bdlru_scan_backward": ([_p] * 13 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_bdlru_scan_forward_timed": ([_p] * 7 + [_i64] * 3 + [_int, _p, _sz, _p, _p, _p], _int),
+    "recblr_bdlru_scan_backward_timed": ([_p] * 13 + [_i64] * 3 + [_int, _p, _sz, _p, _p, _p],
+                                         _int),
     "recblr_bdlru_scan_step": ([_p] * 6 + [_i64] * 2 + [_int, _p], _int),
     "recblr_bdlru_forward": ([_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
     "recblr_bdlru_backward": ([_p] * 17 + [_i64] * 3 + [_int, _p, _sz, _p], _int),

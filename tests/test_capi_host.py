@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 11
+    assert len(syms) == 13
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -100,6 +100,25 @@ def test_scan_backward_validation(rb):
     assert call(nws=16) == rb.ERR_WORKSPACE
     assert call(ws=addr(10) + 64) == rb.ERR_WORKSPACE                       # not 256-aligned
     assert call(io=5) == rb.ERR_UNSUPPORTED
+
+
+def test_timed_scan_validation(rb):
+    """The measurement variants validate exactly as the plain scans (events untouched)."""
+    ev = (addr(20), addr(21))  # never recorded: every call below fails validation
+    f = lambda **kw: rb.recblr_bdlru_scan_forward_timed(
+        kw.get("x", addr(0)), addr(1), addr(2), kw.get("lam", addr(3)), None, addr(4), None,
+        2, kw.get("L", 3), 4, kw.get("io", 0), None, 0, None, *ev)
+    assert f(x=None) == rb.ERR_INVALID_ARGUMENT
+    assert f(lam=None) == rb.ERR_INVALID_ARGUMENT
+    assert f(L=-1) == rb.ERR_INVALID_ARGUMENT
+    assert f(io=7) == rb.ERR_UNSUPPORTED
+    g = lambda **kw: rb.recblr_bdlru_scan_backward_timed(
+        addr(0), addr(1), addr(2), addr(3), None, addr(4), addr(5), None, addr(6),
+        kw.get("dzr", addr(7)), addr(8), kw.get("dlam", addr(9)), None, 2, 3, 4, 0,
+        kw.get("ws", addr(10)), 1 << 20, None, *ev)
+    assert g(dlam=None) == rb.ERR_INVALID_ARGUMENT
+    assert g(dzr=addr(6)) == rb.ERR_INVALID_ARGUMENT
+    assert g(ws=None) == rb.ERR_WORKSPACE
 
 
 def test_step_validation(rb):

@@ -445,16 +445,17 @@ def test_config_full_api(rb, name):
 
 
 # ------------------------------------------------------------------ kernel modes
-# Few channel groups and long sequences run the look-back kernels; many
-# channel groups run the chain kernels.  Forward chain lanes carry 1, 2 or 4
-# channels depending on D, the I/O type and pointer alignment.
+# Few channel groups and long sequences run the look-back kernels (forward:
+# under 256 groups of 64 channels, backward: under 1024); many channel groups
+# run the chain kernels.  Forward chain lanes carry 1, 2 or 4 channels
+# depending on D, the I/O type and pointer alignment.
 MODE_CASES = [
     ((1, 5000, 64), "f32"),    # look-back, one channel group
     ((2, 3000, 256), "bf16"),  # look-back, 8 groups
     ((1, 2000, 3), "f32"),     # look-back, mostly idle lanes
     ((3, 1000, 40), "f32"),    # look-back, partially idle group
-    ((64, 300, 512), "f32"),   # chain, 2 channels per lane forward
-    ((64, 130, 1024), "bf16"), # chain, 4 channels per lane forward
+    ((64, 300, 512), "f32"),   # chain forward, 2 channels per lane; look-back backward
+    ((64, 130, 1024), "bf16"), # chain, 4 channels per lane forward; chain backward
     ((11000, 70, 3), "f32"),   # chain, 1 channel per lane, ragged last group
 ]
 
@@ -475,6 +476,48 @@ def test_kernel_modes(rb, shape, io):
     for k in ("dx", "dzr", "dzi", "dlambda"):
         assert_close(host(got[k]), want[k], io, k)
     assert_close(host(got["dh0"]), want["dh0"], "f32", "dh0")
+
+
+@pytest.mark.parametrize("shape,io", [((2, 700, 64), "f32"), ((64, 300, 512), "f32"),
+                                      ((2, 1000, 256), "bf16"), ((300, 90, 64), "bf16")])
+def test_timed_scans(rb, shape, io):
+    """The measurement entry points compute bit for bit what the plain ones do,
+    and the event pair they record brackets a positive duration."""
+    import torch
+    B, L, D = shape
+    inp = dg.scan_inputs(B, L, D, 5200 + L, io=io, h0=True, grad=True)
+    X, ZR, ZI, DH = (dev(a, io) for a in (inp.x, inp.zr, inp.zi, inp.dh))
+    lam, h0 = dev32(inp.lam), dev32(inp.h0)
+    code = rb.io_code(X.dtype)
+    p = lambda t: t.data_ptr()
+    s = torch.cuda.current_stream().cuda_stream
+    nf = rb.recblr_workspace_size(rb.OP_SCAN_FORWARD, B, L, D, code)
+    nb = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, B, L, D, code)
+    wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=X.device)
+    wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=X.device)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record()
+    outs = []
+    for timed in (False, True):
+        h, dx, dzr, dzi = (torch.empty_like(X) for _ in range(4))
+        hT, dh0 = (torch.empty((B, D), dtype=torch.float32, device=X.device) for _ in range(2))
+        dl = torch.empty(D, dtype=torch.float32, device=X.device)
+        fa = (p(X), p(ZR), p(ZI), p(lam), p(h0), p(h), p(hT), B, L, D, code, p(wsf), nf, s)
+        ba = (p(X), p(ZR), p(ZI), p(lam), p(h0), p(h), p(DH), None, p(dx), p(dzr), p(dzi),
+              p(dl), p(dh0), B, L, D, code, p(wsb), nb, s)
+        if timed:
+            assert rb.recblr_bdlru_scan_forward_timed(*fa, ev[0].cuda_event, ev[1].cuda_event) == 0
+            assert rb.recblr_bdlru_scan_backward_timed(*ba, ev[2].cuda_event, ev[3].cuda_event) == 0
+        else:
+            assert rb.recblr_bdlru_scan_forward(*fa) == 0
+            assert rb.recblr_bdlru_scan_backward(*ba) == 0
+        torch.cuda.synchronize()
+        outs.append([host(t) for t in (h, hT, dx, dzr, dzi, dl, dh0)])
+    print(f"timed scans {shape} {io}: GPU done", flush=True)
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+    assert ev[0].elapsed_time(ev[1]) > 0 and ev[2].elapsed_time(ev[3]) > 0
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
