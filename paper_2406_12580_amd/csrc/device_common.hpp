@@ -4,8 +4,8 @@
 // (RecBLR, arXiv 2406.12580, section 3.2):
 //   r = sigmoid(z_r), i = sigmoid(z_i), q = softplus(Lambda) * r
 //   alpha = exp(-q), beta = sqrt(1 - alpha^2) * i
-// evaluated in fp32 with the hardware transcendental units (v_exp, v_rcp,
-// v_sqrt, v_rsq), and 1 - alpha^2 = 1 - exp(-2q) evaluated without
+// evaluated in fp32 with the hardware transcendental units (v_exp, v_log,
+// v_rcp, v_sqrt, v_rsq), and 1 - alpha^2 = 1 - exp(-2q) evaluated without
 // cancellation when q is small (see one_minus_exp_neg).
 #pragma once
 
@@ -141,9 +141,29 @@ __device__ __forceinline__ float sigmoid(float z) {
     return fast_rcp(1.0f + fast_exp2(-z * kLog2e));
 }
 
-// softplus(v) = log(1 + e^v) = max(v, 0) + log1p(e^-|v|); once per channel.
+__device__ __forceinline__ float fast_log2(float v) { return __builtin_amdgcn_logf(v); }
+constexpr float kLn2 = 0.6931471805599453f;
+
+// softplus(v) = log(1 + e^v) = max(v, 0) + log1p(e), e = e^-|v| in [0, 1].
+// For e < 1/16, log1p(e) is its Maclaurin series e - e^2/2 + ... - e^6/6; the
+// first omitted term bounds the relative error by (1/16)^6 / 7 < 1e-8, and the
+// series keeps full relative accuracy however small e is.  From 1/16 on,
+// log1p(e) = ln(1 + e) with 1 + e in [17/16, 2]: its rounding (2^-24) moves
+// the logarithm by at most 2^-24 / (17/16 ln(17/16)) < 1e-6 relative, on top
+// of the hardware log2's own error (checked against fp64 over the range).  Once
+// per lane (channel) per launch, so hardware exp2 / log2 are used: this is
+// ~20 instructions against ~140 for the libm log1pf(expf()).
 __device__ __forceinline__ float softplus(float v) {
-    return fmaxf(v, 0.0f) + log1pf(expf(-fabsf(v)));
+    const float e = fast_exp2(-fabsf(v) * kLog2e);
+    float p = -1.0f / 6.0f;
+    p = fmaf(p, e, 1.0f / 5.0f);
+    p = fmaf(p, e, -1.0f / 4.0f);
+    p = fmaf(p, e, 1.0f / 3.0f);
+    p = fmaf(p, e, -1.0f / 2.0f);
+    p = fmaf(p, e, 1.0f);
+    const float series = e * p;
+    const float direct = fast_log2(1.0f + e) * kLn2;
+    return fmaxf(v, 0.0f) + (e < 0.0625f ? series : direct);
 }
 
 // 1 - e^-y for y >= 0.  For y < 1/8 the Maclaurin series of 1 - e^-y,
