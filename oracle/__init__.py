@@ -51,6 +51,7 @@ def _load():
             "oracle_backward": [i64, i64, i64] + [p] * 16,
             "oracle_step": [i64, i64] + [p] * 8,
             "oracle_gated_forward": [i64, i64, i64, i64] + [p] * 13,
+            "oracle_gated_backward": [i64, i64, i64, i64] + [p] * 22,
         }
         for name, args in sigs.items():
             fn = getattr(_lib, name)
@@ -172,3 +173,23 @@ def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None):
                                  _ptr(Wr), _ptr(br), _ptr(Wi), _ptr(bi), _ptr(lam), _ptr(h0),
                                  _ptr(y), _ptr(h), _ptr(hT))
     return y, h, hT
+
+
+def gated_backward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, dy, h0=None, dhT=None):
+    """Backward of gated_forward (exact adjoint).  Returns a dict with dhx, dhz,
+    dconv_w [D][K], dconv_b [D], dWr, dbr, dWi, dbi, dlambda, dh0."""
+    hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, dy, h0, dhT = map(
+        _in, (hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, dy, h0, dhT))
+    B, L, D = hx.shape
+    K = conv_w.shape[1]
+    out = {"dhx": np.empty_like(hx), "dhz": np.empty_like(hx), "dconv_w": np.empty((D, K)),
+           "dconv_b": np.empty(D), "dWr": np.empty((D, D)), "dbr": np.empty(D),
+           "dWi": np.empty((D, D)), "dbi": np.empty(D), "dlambda": np.empty(D),
+           "dh0": np.empty((B, D))}
+    _load().oracle_gated_backward(
+        B, L, D, K, _ptr(hx), _ptr(hz), _ptr(conv_w), _ptr(conv_b), _ptr(Wr), _ptr(br),
+        _ptr(Wi), _ptr(bi), _ptr(lam), _ptr(h0), _ptr(dy), _ptr(dhT), _ptr(out["dhx"]),
+        _ptr(out["dhz"]), _ptr(out["dconv_w"]), _ptr(out["dconv_b"]), _ptr(out["dWr"]),
+        _ptr(out["dbr"]), _ptr(out["dWi"]), _ptr(out["dbi"]), _ptr(out["dlambda"]),
+        _ptr(out["dh0"]))
+    return out

@@ -30,6 +30,7 @@
  *     c_t[d] = b[d] + sum_{j<K} w[d][j] hx_{t-j}[d] with hx_{t<0} = 0 (the
  *     kernel size is not stated); x' = SiLU(c) feeds both the gate
  *     projections and the recurrence; the output is y = h (x) SiLU(hz).
+ *     Its backward is the chain rule through those three lines.
  */
 #include <math.h>
 #include <stdint.h>
@@ -292,6 +293,83 @@ void oracle_gated_forward(int64_t B, int64_t L, int64_t D, int64_t K, const doub
     }
     free(xp);
     free(hh);
+}
+
+/*
+ * Backward of oracle_gated_forward (the paper states no backward; this is the
+ * exact adjoint of the three lines, by the chain rule):
+ *   dh    = dy * SiLU(hz)                      (plus dhT on the final state)
+ *   dhz   = dy * h * SiLU'(hz),  SiLU'(v) = s (1 + v (1 - s)), s = sigma(v)
+ *   dx', dW_r, db_r, dW_i, db_i, dLambda, dh0 = oracle_backward at x' with dh
+ *   dc    = dx' * SiLU'(c)                     (c: the conv output, x' = SiLU(c))
+ *   dhx_t = sum_{j<K, t+j<L} conv_w[.][j] dc_{t+j}     (the causal conv's transpose)
+ *   dconv_w[d][j] = sum_{b, t>=j} dc_t[d] hx_{t-j}[d],  dconv_b[d] = sum_{b,t} dc_t[d]
+ * dy, dhx, dhz: [B][L][D]; dhT, h0, dh0: [B][D] or NULL; dconv_w: [D][K];
+ * dconv_b: [D] (always written).
+ */
+static double dsilu(double v) {
+    double s = sigmoid(v);
+    return s * (1.0 + v * (1.0 - s));
+}
+
+void oracle_gated_backward(int64_t B, int64_t L, int64_t D, int64_t K, const double* hx,
+                           const double* hz, const double* conv_w, const double* conv_b,
+                           const double* Wr, const double* br, const double* Wi,
+                           const double* bi, const double* lambda, const double* h0,
+                           const double* dy, const double* dhT, double* dhx, double* dhz,
+                           double* dconv_w, double* dconv_b, double* dWr, double* dbr,
+                           double* dWi, double* dbi, double* dlambda, double* dh0) {
+    size_t n = (size_t)(B * L * D);
+    size_t nb = (n ? n : 1) * sizeof(double);
+    double* c = (double*)malloc(nb);
+    double* xp = (double*)malloc(nb);
+    double* hh = (double*)malloc(nb);
+    double* dh = (double*)malloc(nb);
+    double* dxp = (double*)malloc(nb);
+    double* hT = (double*)malloc((size_t)(B * D ? B * D : 1) * sizeof(double));
+    /* forward recomputation: the conv, x' and h */
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < L; ++t)
+            for (int64_t d = 0; d < D; ++d) {
+                double acc = conv_b ? conv_b[d] : 0.0;
+                for (int64_t j = 0; j < K && j <= t; ++j)
+                    acc += conv_w[d * K + j] * hx[(b * L + t - j) * D + d];
+                c[(b * L + t) * D + d] = acc;
+                xp[(b * L + t) * D + d] = silu(acc);
+            }
+    oracle_forward(B, L, D, xp, Wr, br, Wi, bi, lambda, h0, hh, hT);
+    /* output gate */
+    for (size_t e = 0; e < n; ++e) {
+        dh[e] = dy[e] * silu(hz[e]);
+        dhz[e] = dy[e] * hh[e] * dsilu(hz[e]);
+    }
+    /* BD-LRU with its projections */
+    oracle_backward(B, L, D, xp, Wr, br, Wi, bi, lambda, h0, dh, dhT, dxp, dWr, dbr, dWi, dbi,
+                    dlambda, dh0);
+    /* SiLU and the causal depthwise conv */
+    for (size_t e = 0; e < n; ++e) dxp[e] *= dsilu(c[e]);  /* now dc */
+    for (int64_t d = 0; d < D; ++d) {
+        for (int64_t j = 0; j < K; ++j) dconv_w[d * K + j] = 0.0;
+        dconv_b[d] = 0.0;
+    }
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < L; ++t)
+            for (int64_t d = 0; d < D; ++d) {
+                double acc = 0.0;
+                for (int64_t j = 0; j < K && t + j < L; ++j)
+                    acc += conv_w[d * K + j] * dxp[(b * L + t + j) * D + d];
+                dhx[(b * L + t) * D + d] = acc;
+                double g = dxp[(b * L + t) * D + d];
+                dconv_b[d] += g;
+                for (int64_t j = 0; j < K && j <= t; ++j)
+                    dconv_w[d * K + j] += g * hx[(b * L + t - j) * D + d];
+            }
+    free(c);
+    free(xp);
+    free(hh);
+    free(dh);
+    free(dxp);
+    free(hT);
 }
 
 /* Full single step: projections of x_t, then one recurrence step. */

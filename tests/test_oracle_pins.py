@@ -550,3 +550,75 @@ def test_gated_causality():
     y2, _, _ = oracle.gated_forward(x2, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
     np.testing.assert_array_equal(y1[:, :5], y2[:, :5])
     assert np.abs(y1[:, 5] - y2[:, 5]).max() > 1e-6
+
+
+# Backward of the gated layer core: the paper gives no backward, so the pins
+# are the forward itself (pinned above) differentiated numerically.
+
+@pytest.mark.parametrize("K,seed", [(3, 95), (1, 96), (4, 97)])
+def test_gated_backward_central_differences(K, seed):
+    """Every gradient of the gated core against central differences of
+    loss = <dy, y> + <dhT, hT> through oracle.gated_forward."""
+    B, L, D = 2, 6, 3
+    f, hz, w, cb = _gated_case(B, L, D, K, seed)
+    rng = np.random.default_rng(seed + 100)
+    dy = rng.standard_normal((B, L, D))
+    dhT = rng.standard_normal((B, D))
+    hx = f.x.astype(np.float64)
+    par = {"hx": hx, "hz": hz, "conv_w": w, "conv_b": cb, "Wr": f.Wr.astype(np.float64),
+           "br": f.br.astype(np.float64), "Wi": f.Wi.astype(np.float64),
+           "bi": f.bi.astype(np.float64), "lam": f.lam.astype(np.float64),
+           "h0": f.h0.astype(np.float64)}
+    got = oracle.gated_backward(par["hx"], par["hz"], par["conv_w"], par["conv_b"], par["Wr"],
+                                par["br"], par["Wi"], par["bi"], par["lam"], dy, par["h0"], dhT)
+
+    def loss():
+        y, _, hT = oracle.gated_forward(par["hx"], par["hz"], par["conv_w"], par["conv_b"],
+                                        par["Wr"], par["br"], par["Wi"], par["bi"], par["lam"],
+                                        par["h0"])
+        return float(np.sum(dy * y) + np.sum(dhT * hT))
+
+    for gname, pname in (("dhx", "hx"), ("dhz", "hz"), ("dconv_w", "conv_w"),
+                         ("dconv_b", "conv_b"), ("dWr", "Wr"), ("dbr", "br"), ("dWi", "Wi"),
+                         ("dbi", "bi"), ("dlambda", "lam"), ("dh0", "h0")):
+        np.testing.assert_allclose(got[gname], _fd(loss, par[pname]), rtol=1e-6, atol=1e-8,
+                                   err_msg=gname)
+
+
+def test_gated_backward_output_gate_closed_form():
+    """dhz = dy * h * SiLU'(hz) with SiLU'(v) = d/dv v sigma(v), and a zero dy gives
+    zero gradients everywhere (the layer is linear in dy)."""
+    B, L, D, K = 2, 5, 3, 2
+    f, hz, w, cb = _gated_case(B, L, D, K, 98)
+    dy = np.random.default_rng(99).standard_normal((B, L, D))
+    y, h, _ = oracle.gated_forward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
+    got = oracle.gated_backward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, dy, f.h0)
+    s = expit(hz)
+    np.testing.assert_allclose(got["dhz"], dy * h * (s + hz * s * (1.0 - s)), rtol=1e-13)
+    zero = oracle.gated_backward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam,
+                                 np.zeros((B, L, D)), f.h0)
+    for k, v in zero.items():
+        assert not np.asarray(v).any(), k
+
+
+def test_gated_backward_adjoint_dot_product():
+    """<dy, J v> = <J^T dy, v> along one random direction in all inputs at once."""
+    B, L, D, K = 2, 9, 4, 3
+    f, hz, w, cb = _gated_case(B, L, D, K, 101)
+    rng = np.random.default_rng(102)
+    dy = rng.standard_normal((B, L, D))
+    base = [np.asarray(a, dtype=np.float64) for a in
+            (f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)]
+    v = [rng.standard_normal(a.shape) for a in base]
+    eps = 1e-6
+
+    def loss(args):
+        y, _, _ = oracle.gated_forward(*args)
+        return float(np.sum(dy * y))
+
+    jv = (loss([a + eps * u for a, u in zip(base, v)]) -
+          loss([a - eps * u for a, u in zip(base, v)])) / (2 * eps)
+    got = oracle.gated_backward(*base[:9], dy, base[9])
+    names = ("dhx", "dhz", "dconv_w", "dconv_b", "dWr", "dbr", "dWi", "dbi", "dlambda", "dh0")
+    jtg = sum(float(np.sum(got[k] * u)) for k, u in zip(names, v))
+    assert abs(jv - jtg) <= 1e-7 * max(1.0, abs(jv))
