@@ -18,8 +18,8 @@ forward (gate projections + scan) with the scan algorithms of the paper's
 efficiency ablation (serial scan; two-tree scan with sequence padding or with
 embedding padding; the production chunked scan) at the paper's three
 sequence lengths.  --api gated times the gated recurrent layer core forward
-(causal conv + SiLU, BD-LRU with projections, SiLU output gate;
-recblr_gated_forward) on the workload.
+and backward (causal conv + SiLU, BD-LRU with projections, SiLU output gate;
+recblr_gated_forward / recblr_gated_backward) on the workload.
 Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).  With the
 scan API the roofline takes the scan kernel's own duration, from a HIP event
@@ -134,72 +134,98 @@ ABLATION_WORKLOADS = [("ml1m-like", 2048, 200, 128), ("gowalla-like", 2048, 100,
 
 
 def gated_main(args, torch, dg, rb):
-    """Gated recurrent layer core forward (conv taps K = 4) on a workload."""
+    """Gated recurrent layer core (conv taps K = 4) forward + backward on a workload."""
     cfg = dg.CONFIGS[args.workload or "c5"]
     B, L, D = cfg.B, cfg.L, cfg.D
     dev = torch.device("cuda:0")
     dtype = torch.float32 if cfg.io == "f32" else torch.bfloat16
     log(f"generating {cfg.name}: B={B} L={L} D={D} {cfg.io} (gated layer core)")
-    f = dg.full_inputs(B, L, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True)
+    f = dg.full_inputs(B, L, D, cfg.seed, io=cfg.io, a_range=cfg.a_range, bias=True, grad=True)
     rng = np.random.default_rng(cfg.seed + 1)
     hz = rng.standard_normal((B, L, D), dtype=np.float32)
     w = (rng.standard_normal((D, 4)) * 0.5).astype(np.float32)
     cb = (rng.standard_normal(D) * 0.1).astype(np.float32)
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dtype)
-    HX, HZ, Wr, br, Wi, bi = T(f.x), T(hz), T(f.Wr), T(f.br), T(f.Wi), T(f.bi)
+    HX, HZ, Wr, br, Wi, bi, DY = T(f.x), T(hz), T(f.Wr), T(f.br), T(f.Wi), T(f.bi), T(f.dh)
     W4, CB, lam = (torch.from_numpy(a).to(dev) for a in (w, cb, f.lam))
-    y = torch.empty_like(HX)
+    y, h = torch.empty_like(HX), torch.empty_like(HX)
+    dhx, dhz = torch.empty_like(HX), torch.empty_like(HX)
+    f32 = dict(dtype=torch.float32, device=dev)
+    dW4, dCB, dWr, dWi = (torch.empty(sh, **f32) for sh in ((D, 4), D, (D, D), (D, D)))
+    dbr, dbi, dlam = (torch.empty(D, **f32) for _ in range(3))
     io = rb.io_code(dtype)
-    nws = rb.recblr_workspace_size(rb.OP_GATED_FORWARD, B, L, D, io)
-    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    nf = rb.recblr_workspace_size(rb.OP_GATED_FORWARD, B, L, D, io)
+    nb = rb.recblr_workspace_size(rb.OP_GATED_BACKWARD, B, L, D, io)
+    wsf = torch.empty(max(nf, 1), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
     s = torch.cuda.current_stream()
     p = lambda t: t.data_ptr()
 
-    def step():
+    def fwd():
         st = rb.recblr_gated_forward(p(HX), p(HZ), p(W4), p(CB), 4, p(Wr), p(br), p(Wi), p(bi),
-                                     p(lam), None, p(y), None, None, B, L, D, io, p(ws), nws,
+                                     p(lam), None, p(y), p(h), None, B, L, D, io, p(wsf), nf,
                                      s.cuda_stream)
         assert st == 0, st
+
+    def bwd():
+        st = rb.recblr_gated_backward(p(HX), p(HZ), p(W4), p(CB), 4, p(Wr), p(br), p(Wi), p(bi),
+                                      p(lam), None, p(h), p(DY), None, p(dhx), p(dhz), p(dW4),
+                                      p(dCB), p(dWr), p(dbr), p(dWi), p(dbi), p(dlam), None,
+                                      B, L, D, io, p(wsb), nb, s.cuda_stream)
+        assert st == 0, st
     for _ in range(args.warmup):
-        step()
+        fwd()
+        bwd()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     t0 = time.perf_counter()
-    ev[0].record(s)
     for k in range(K):
-        step()
-        ev[k + 1].record(s)
+        ev[k][0].record(s)
+        fwd()
+        ev[k][1].record(s)
+        bwd()
+        ev[k][2].record(s)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    t_f = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e-3
+    t_b = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
     N = B * L * D
     esz = 4 if cfg.io == "f32" else 2
-    ach = 3 * esz * N / float(np.mean(dts)) / 1e9  # hx, hz read; y written
-    log(f"gated forward {np.mean(dts)*1e6:.1f} us ({ach:.0f} GB/s)")
-    out = {"metric": "gated recurrent layer core forward elements/sec (B*L*D)",
+    # Boundary bytes: forward reads hx, hz and writes y, h; backward reads hx,
+    # hz, h, dy and writes dhx, dhz.
+    f_gbs = 4 * esz * N / float(np.mean(t_f)) / 1e9
+    b_gbs = 6 * esz * N / float(np.mean(t_b)) / 1e9
+    dom = "backward" if np.mean(t_b) >= np.mean(t_f) else "forward"
+    ach = b_gbs if dom == "backward" else f_gbs
+    log(f"gated forward {np.mean(t_f)*1e6:.1f} us ({f_gbs:.0f} GB/s), backward "
+        f"{np.mean(t_b)*1e6:.1f} us ({b_gbs:.0f} GB/s)")
+    out = {"metric": "gated recurrent layer core elements/sec (B*L*D), forward+backward",
            "value": N * K / wall, "unit": "elements/s", "n_gpus": 1, "steps": K,
            "warmup": args.warmup, "ms_per_step": wall / K * 1e3, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": cfg.io,
-           "data": "synthetic (seeded normal hx, hz, conv taps; decay bases per the paper's "
-                   "initialisation)",
-           "config": {"workload": f"{cfg.name}: gated layer core forward (conv K=4), {cfg.note}",
+           "data": "synthetic (seeded normal hx, hz, dL/dy, conv taps; decay bases per the "
+                   "paper's initialisation)",
+           "config": {"workload": f"{cfg.name}: gated layer core forward+backward (conv K=4), "
+                                  f"{cfg.note}",
                       "B": B, "L": L, "D": D, "io": cfg.io, "elements": N},
-           "us_forward": float(np.mean(dts)) * 1e6,
-           "roofline": {"bound": "hbm", "kernel": "gated_forward", "achieved": ach,
+           "us_forward": float(np.mean(t_f)) * 1e6, "us_backward": float(np.mean(t_b)) * 1e6,
+           "roofline": {"bound": "hbm", "kernel": f"gated_{dom}", "achieved": ach,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
                         "traffic": None}}
     if not args.no_cpu_baseline:
         import oracle
         rows, t0, passes = 1, time.perf_counter(), 0
         while time.perf_counter() - t0 < 10.0:
-            oracle.gated_forward(f.x[:rows], hz[:rows], w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam)
+            oracle.gated_backward(f.x[:rows], hz[:rows], w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam,
+                                  f.dh[:rows])
             passes += 1
         total = time.perf_counter() - t0
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
         out["cpu_baseline"] = {"value": passes * rows * L * D / total, "unit": "elements/s",
                                "cores": threads, "kind": "oracle",
-                               "sample": f"fp64 oracle gated forward over {rows} of {B} batch "
+                               "sample": f"fp64 oracle gated forward+backward (the backward "
+                                         f"recomputes the forward) over {rows} of {B} batch "
                                          f"rows (L={L}, D={D}), {passes} passes, {total:.1f} s"}
     print(json.dumps(out), flush=True)
 

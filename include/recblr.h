@@ -76,7 +76,8 @@ enum {
     RECBLR_OP_FORWARD = 2,
     RECBLR_OP_BACKWARD = 3,
     RECBLR_OP_STEP = 4,
-    RECBLR_OP_GATED_FORWARD = 5
+    RECBLR_OP_GATED_FORWARD = 5,
+    RECBLR_OP_GATED_BACKWARD = 6
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -207,6 +208,35 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
                          const void* W_i, const void* b_i, const float* lambda, const float* h0,
                          void* y, void* h, float* hT, int64_t B, int64_t L, int64_t D, int io,
                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of recblr_gated_forward.  The paper gives no backward pass; this is
+ * the exact chain rule through Algorithm alg:gated_recurrent, lines 3 to 5:
+ *   dh    = dy (x) SiLU(hz)                     (dhT adds on the final state)
+ *   dhz   = dy (x) h (x) SiLU'(hz)
+ *   dx', dW_r, db_r, dW_i, db_i, dlambda, dh0   as recblr_bdlru_backward at x'
+ *   dc    = dx' (x) SiLU'(c),  c the conv output (x' = SiLU(c))
+ *   dhx_t = sum_{j<K, t+j<L} conv_w[d][j] dc_{t+j}
+ *   dconv_w[d][j] = sum_{b, t>=j} dc_t hx_{t-j},  dconv_b[d] = sum_{b,t} dc_t
+ *   hx, hz, conv_w, conv_b, K, W_*, b_*, lambda, h0 : the forward's inputs
+ *   h    : [B][L][D] io   the forward's BD-LRU output (its `h` argument)
+ *   dy   : [B][L][D] io   dLoss/dy;  dhT : [B][D] float|NULL  dLoss/dh_L
+ * Outputs: dhx, dhz : [B][L][D] io;  dconv_w : [D][K] float;  dconv_b : [D]
+ *   float|NULL;  dW_*, db_*, dlambda, dh0 : as recblr_bdlru_backward.  Every
+ *   sum over b and t is taken in a fixed order, so results are bitwise
+ *   repeatable.
+ * Workspace: recblr_workspace_size(RECBLR_OP_GATED_BACKWARD, ...).  x' is
+ * formed again from hx (one streaming kernel) rather than kept by the forward.
+ * Errors: as recblr_gated_forward; outputs overlapping inputs or each other
+ * give INVALID_ARGUMENT.
+ */
+int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
+                          const float* conv_b, int K, const void* W_r, const void* b_r,
+                          const void* W_i, const void* b_i, const float* lambda, const float* h0,
+                          const void* h, const void* dy, const float* dhT, void* dhx, void* dhz,
+                          float* dconv_w, float* dconv_b, float* dW_r, float* db_r, float* dW_i,
+                          float* db_i, float* dlambda, float* dh0, int64_t B, int64_t L,
+                          int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Scan algorithms of the efficiency ablation (section 4, Table tab:efficiency;

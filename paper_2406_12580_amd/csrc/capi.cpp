@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <initializer_list>
+#include <utility>
 
 #include "gemm.hpp"
 #include "launch.hpp"
@@ -119,6 +120,31 @@ GatedLayout gated_layout(int64_t B, int64_t L, int64_t D, int io) {
     return l;
 }
 
+// Gated layer backward.  The BD-LRU part runs in fp32 whatever the I/O type
+// (its input gradient dh sums over long horizons in the adjoint, so rounding
+// it to bf16 costs more than the bf16 tolerance): conv taps, fp32 x', dh and
+// dx', for bf16 I/O fp32 copies of h and of the weights, the conv backward
+// partials, then the layout of recblr_bdlru_backward at fp32.
+struct GatedBwdLayout {
+    size_t w4, b4, xp, dh, dxp, h32, wts, conv, full, total;
+};
+GatedBwdLayout gated_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
+    GatedBwdLayout l;
+    const size_t n32 = align_up((size_t)(B * L * D) * sizeof(float));
+    const bool widen = io == RECBLR_BF16;
+    l.w4 = 0;
+    l.b4 = align_up((size_t)(kConvTaps * D) * sizeof(float));
+    l.xp = l.b4 + align_up((size_t)D * sizeof(float));
+    l.dh = l.xp + n32;
+    l.dxp = l.dh + n32;
+    l.h32 = l.dxp + n32;
+    l.wts = l.h32 + (widen ? n32 : 0);
+    l.conv = l.wts + (widen ? align_up((size_t)(2 * D * D + 2 * D) * sizeof(float)) : 0);
+    l.full = l.conv + align_up(conv_backward_workspace(B, L, D));
+    l.total = l.full + full_bwd_layout(B, L, D, RECBLR_F32).total;
+    return l;
+}
+
 // Step: z_r, z_i scratch, then the packed weights.
 size_t step_z_bytes(int64_t B, int64_t D) { return align_up((size_t)(B * D) * sizeof(float)); }
 size_t step_pack_bytes(int64_t D, int io) {
@@ -156,6 +182,7 @@ size_t recblr_workspace_size(int op, int64_t B, int64_t L, int64_t D, int io) {
         case RECBLR_OP_BACKWARD: return full_bwd_layout(B, L, D, io).total;
         case RECBLR_OP_STEP: return step_ws(B, D, io);
         case RECBLR_OP_GATED_FORWARD: return gated_layout(B, L, D, io).total;
+        case RECBLR_OP_GATED_BACKWARD: return gated_bwd_layout(B, L, D, io).total;
         default: return 0;
     }
 }
@@ -362,7 +389,7 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
     // x' = SiLU(conv(hx)) is formed once, in a streaming kernel: doing it on
     // the fly inside the fused scan kernel (its tap loads held in registers)
     // cost that kernel three quarters of its occupancy.
-    if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), strm) != hipSuccess)
+    if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), io_of(io), strm) != hipSuccess)
         return RECBLR_ERR_HIP;
     if (L > 0 && fused_forward_applies(B, L, D, io_of(io), xp, pack)) {
         if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
@@ -381,6 +408,97 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
                   IoType::kF32, fws + fl.scan, fl.total - fl.scan};
     if (launch_scan_forward(a, strm) != hipSuccess) return RECBLR_ERR_HIP;
     return status_of(launch_gate_out(hout, hz, y, B * L * D, io_of(io), strm));
+}
+
+int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
+                          const float* conv_b, int K, const void* W_r, const void* b_r,
+                          const void* W_i, const void* b_i, const float* lambda, const float* h0,
+                          const void* h, const void* dy, const float* dhT, void* dhx, void* dhz,
+                          float* dconv_w, float* dconv_b, float* dW_r, float* db_r, float* dW_i,
+                          float* db_i, float* dlambda, float* dh0, int64_t B, int64_t L,
+                          int64_t D, int io, void* ws, size_t ws_bytes, void* stream) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D > kMaxProjD || K < 1 || K > kConvTaps) return RECBLR_ERR_UNSUPPORTED;
+    if (D == 0) return RECBLR_OK;
+    if (!lambda || !W_r || !W_i || !conv_w || !dconv_w || !dW_r || !dW_i || !db_r || !db_i ||
+        !dlambda)
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    if (B > 0 && L > 0 && (!hx || !hz || !h || !dy || !dhx || !dhz))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {hx, hz, W_r, W_i, b_r, b_i, h, dy, (const void*)dhx, (const void*)dhz})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)dhT,
+                          (const void*)conv_w, (const void*)conv_b, (const void*)dconv_w,
+                          (const void*)dconv_b, (const void*)dW_r, (const void*)db_r,
+                          (const void*)dW_i, (const void*)db_i, (const void*)dlambda,
+                          (const void*)dh0})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 w = (size_t)(D * D) * esz(io), bb = (size_t)D * esz(io), wf = (size_t)(D * D) * 4,
+                 df = (size_t)D * 4, cw = (size_t)(D * K) * 4;
+    if (!disjoint({{dhx, n}, {dhz, n}, {dconv_w, cw}, {dconv_b, df}, {dW_r, wf}, {db_r, df},
+                   {dW_i, wf}, {db_i, df}, {dlambda, df}, {dh0, s}},
+                  {{hx, n}, {hz, n}, {conv_w, cw}, {conv_b, df}, {W_r, w}, {W_i, w}, {b_r, bb},
+                   {b_i, bb}, {lambda, df}, {h0, s}, {h, n}, {dy, n}, {dhT, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    const GatedBwdLayout lay = gated_bwd_layout(B, L, D, io);
+    st = check_ws(ws, ws_bytes, lay.total);
+    if (st) return st;
+    if (!disjoint({{ws, lay.total}},
+                  {{hx, n}, {hz, n}, {h, n}, {dy, n}, {dhx, n}, {dhz, n}, {dh0, s}, {dhT, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    if (B == 0 || L == 0) {
+        // No steps: every sum is empty, and dh0 = dhT (h_L = h0).
+        for (auto pr : {std::make_pair(dconv_w, (int64_t)(D * K)), std::make_pair(dconv_b, D),
+                        std::make_pair(dW_r, D * D), std::make_pair(dW_i, D * D),
+                        std::make_pair(db_r, D), std::make_pair(db_i, D),
+                        std::make_pair(dlambda, D)})
+            if (pr.first && launch_fill(pr.first, 0.0f, pr.second, strm) != hipSuccess)
+                return RECBLR_ERR_HIP;
+        if (dh0 && B > 0) {
+            hipError_t e = dhT ? hipMemcpyAsync(dh0, dhT, s, hipMemcpyDeviceToDevice, strm)
+                               : launch_fill(dh0, 0.0f, B * D, strm);
+            if (e != hipSuccess) return RECBLR_ERR_HIP;
+        }
+        return RECBLR_OK;
+    }
+    float* w4 = (float*)at(ws, lay.w4);
+    float* b4 = (float*)at(ws, lay.b4);
+    void* xp = at(ws, lay.xp);
+    void* dh = at(ws, lay.dh);
+    void* dxp = at(ws, lay.dxp);
+    const int64_t n_el = B * L * D;
+    if (launch_pack_conv(conv_w, conv_b, K, D, w4, b4, strm) != hipSuccess) return RECBLR_ERR_HIP;
+    if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), IoType::kF32, strm) != hipSuccess)
+        return RECBLR_ERR_HIP;
+    if (launch_gate_backward(dy, hz, h, dh, dhz, n_el, io_of(io), IoType::kF32, strm) !=
+        hipSuccess)
+        return RECBLR_ERR_HIP;
+    // fp32 views of h and of the weights for the BD-LRU backward.
+    const void *h32 = h, *wr32 = W_r, *br32 = b_r, *wi32 = W_i, *bi32 = b_i;
+    if (io == RECBLR_BF16) {
+        float* hw = (float*)at(ws, lay.h32);
+        float* wt = (float*)at(ws, lay.wts);
+        if (launch_widen(h, hw, n_el, strm) != hipSuccess ||
+            launch_widen(W_r, wt, D * D, strm) != hipSuccess ||
+            launch_widen(W_i, wt + D * D, D * D, strm) != hipSuccess ||
+            (b_r && launch_widen(b_r, wt + 2 * D * D, D, strm) != hipSuccess) ||
+            (b_i && launch_widen(b_i, wt + 2 * D * D + D, D, strm) != hipSuccess))
+            return RECBLR_ERR_HIP;
+        h32 = hw;
+        wr32 = wt;
+        wi32 = wt + D * D;
+        br32 = b_r ? wt + 2 * D * D : nullptr;
+        bi32 = b_i ? wt + 2 * D * D + D : nullptr;
+    }
+    st = recblr_bdlru_backward(xp, wr32, br32, wi32, bi32, lambda, h0, h32, dh, dhT, dxp, dW_r,
+                               db_r, dW_i, db_i, dlambda, dh0, B, L, D, RECBLR_F32,
+                               at(ws, lay.full), lay.total - lay.full, stream);
+    if (st) return st;
+    return status_of(launch_conv_backward(hx, dxp, w4, b4, dhx, dconv_w, dconv_b, K, B, L, D,
+                                          io_of(io), IoType::kF32, at(ws, lay.conv), strm));
 }
 
 int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const void* W_i,

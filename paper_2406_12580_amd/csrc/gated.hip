@@ -2,7 +2,13 @@
 // alg:gated_recurrent, lines 3 to 5) outside the fused scan: the causal
 // depthwise Conv1d + SiLU that forms the BD-LRU input, and the output gate
 // y = h * SiLU(hz).  The scan kernel with the projections fused in applies
-// both on the fly; these kernels serve the shapes it does not cover.
+// the gate on the fly; these kernels serve the shapes it does not cover.
+//
+// Backward (the paper gives none; exact chain rule through the three lines):
+//   dh = dy SiLU(hz),  dhz = dy h SiLU'(hz),  SiLU'(v) = s (1 + v (1 - s)), s = sigma(v)
+//   (BD-LRU backward with projections at x' gives dx')
+//   dc_t = dx'_t SiLU'(c_t),  dhx_t = sum_{j<K, t+j<L} w_j dc_{t+j}
+//   dw_j = sum_{b, t>=j} dc_t hx_{t-j},  db = sum_{b,t} dc_t
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -22,12 +28,13 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, const float* __res
     b4[d] = b ? b[d] : 0.0f;
 }
 
-// x'_t = SiLU(b + sum_j w_j hx_{t-j}) with hx_{t<0} = 0, one element per thread.
-template <typename T>
+// x'_t = SiLU(b + sum_j w_j hx_{t-j}) with hx_{t<0} = 0, one element per
+// thread; x' is stored as TO (the I/O type, or fp32 for a backward).
+template <typename T, typename TO>
 __global__ __launch_bounds__(kGateThreads) void conv_silu_kernel(const T* __restrict__ hx,
                                                                  const float* __restrict__ w4,
                                                                  const float* __restrict__ b4,
-                                                                 T* __restrict__ xp, int64_t L,
+                                                                 TO* __restrict__ xp, int64_t L,
                                                                  int64_t D, int64_t n) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n) return;
@@ -39,12 +46,12 @@ __global__ __launch_bounds__(kGateThreads) void conv_silu_kernel(const T* __rest
     store(xp + e, c * sigmoid(c));
 }
 
-// The same with 16-byte accesses: V = 16 / sizeof(T) consecutive channels per
+// The same with 16-byte loads: V = 16 / sizeof(T) consecutive channels per
 // thread (D % V == 0, 16-byte aligned tensors).
-template <typename T>
+template <typename T, typename TO>
 __global__ __launch_bounds__(kGateThreads) void conv_silu_vec_kernel(
     const T* __restrict__ hx, const float* __restrict__ w4, const float* __restrict__ b4,
-    T* __restrict__ xp, int64_t L, int64_t D, int64_t nvec) {
+    TO* __restrict__ xp, int64_t L, int64_t D, int64_t nvec) {
     constexpr int V = 16 / sizeof(T);
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= nvec) return;
@@ -61,11 +68,15 @@ __global__ __launch_bounds__(kGateThreads) void conv_silu_vec_kernel(
 #pragma unroll
         for (int i = 0; i < V; ++i) c[i] = fmaf(w4[j * D + d + i], to_f32(v[i]), c[i]);
     }
-    uint4 out;
-    T* o = (T*)&out;
+    constexpr int VO = 16 / sizeof(TO);  // outputs per 16-byte store
 #pragma unroll
-    for (int i = 0; i < V; ++i) o[i] = from_f32<T>(c[i] * sigmoid(c[i]));
-    *(uint4*)(xp + e) = out;
+    for (int s0 = 0; s0 < V; s0 += VO) {
+        uint4 out;
+        TO* o = (TO*)&out;
+#pragma unroll
+        for (int i = 0; i < VO; ++i) o[i] = from_f32<TO>(c[s0 + i] * sigmoid(c[s0 + i]));
+        *(uint4*)(xp + e + s0) = out;
+    }
 }
 
 template <typename T>
@@ -99,6 +110,330 @@ __global__ __launch_bounds__(kGateThreads) void gate_out_vec_kernel(const T* __r
     *(uint4*)(y + q * V) = out;
 }
 
+// ------------------------------------------------------------------ backward
+__device__ __forceinline__ float dsilu(float v, float s) { return s * fmaf(v, 1.0f - s, 1.0f); }
+
+// dh = dy SiLU(hz) and dhz = dy h SiLU'(hz), one element per thread; dh is
+// stored as TG (fp32 when it feeds an fp32 backward).
+template <typename T, typename TG>
+__global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(
+    const T* __restrict__ dy, const T* __restrict__ hz, const T* __restrict__ h,
+    TG* __restrict__ dh, T* __restrict__ dhz, int64_t n) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n) return;
+    const float g = load(hz + e), s = sigmoid(g), gy = load(dy + e);
+    store(dh + e, gy * (g * s));
+    store(dhz + e, gy * load(h + e) * dsilu(g, s));
+}
+
+// The same with 16-byte loads (n % V == 0, 16-byte aligned tensors).
+template <typename T, typename TG>
+__global__ __launch_bounds__(kGateThreads) void gate_bwd_vec_kernel(
+    const T* __restrict__ dy, const T* __restrict__ hz, const T* __restrict__ h,
+    TG* __restrict__ dh, T* __restrict__ dhz, int64_t nvec) {
+    constexpr int V = 16 / sizeof(T);
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= nvec) return;
+    const uint4 ry = *(const uint4*)(dy + q * V), rz = *(const uint4*)(hz + q * V),
+                rh = *(const uint4*)(h + q * V);
+    const T* vy = (const T*)&ry;
+    const T* vz = (const T*)&rz;
+    const T* vh = (const T*)&rh;
+    float g1[V];
+    uint4 o2;
+    T* b = (T*)&o2;
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+        const float g = to_f32(vz[i]), s = sigmoid(g), gy = to_f32(vy[i]);
+        g1[i] = gy * (g * s);
+        b[i] = from_f32<T>(gy * to_f32(vh[i]) * dsilu(g, s));
+    }
+    constexpr int VG = 16 / sizeof(TG);
+#pragma unroll
+    for (int s0 = 0; s0 < V; s0 += VG) {
+        uint4 o1;
+        TG* a = (TG*)&o1;
+#pragma unroll
+        for (int i = 0; i < VG; ++i) a[i] = from_f32<TG>(g1[s0 + i]);
+        *(uint4*)(dh + q * V + s0) = o1;
+    }
+    *(uint4*)(dhz + q * V) = o2;
+}
+
+// bf16 to fp32, 8 elements per thread (n % 8 == 0, 16-byte aligned) or one.
+__global__ __launch_bounds__(kGateThreads) void widen_kernel(const bf16* __restrict__ src,
+                                                             float* __restrict__ dst, int64_t n,
+                                                             bool vec) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (vec) {
+        if (q * 8 >= n) return;
+        const uint4 raw = *(const uint4*)(src + q * 8);
+        const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+        float4 lo, hi;
+        lo.x = bf16_lo(w[0]); lo.y = bf16_hi(w[0]); lo.z = bf16_lo(w[1]); lo.w = bf16_hi(w[1]);
+        hi.x = bf16_lo(w[2]); hi.y = bf16_hi(w[2]); hi.z = bf16_lo(w[3]); hi.w = bf16_hi(w[3]);
+        *(float4*)(dst + q * 8) = lo;
+        *(float4*)(dst + q * 8 + 4) = hi;
+    } else if (q < n) {
+        dst[q] = to_f32(src[q]);
+    }
+}
+
+// Conv backward (dx' of type TG: the I/O type or fp32).  A workgroup is 4 waves; lane l of wave w owns VEC channels
+// d0 = (blockIdx.y * 64 + l) * VEC of batch row b and the chunk of kConvChunk
+// steps number 4 * cg + w, with blockIdx.x = b * groups + cg.  The lane walks
+// its chunk and the 3 steps after it (whose dc its last outputs need):
+// it rebuilds c_t from hx with a 3-step window, forms dc_t, emits
+// dhx_{t-3} = sum_j w_j dc_{t-3+j} from a 4-step window of dc (dc = 0 past
+// L), and sums dc_t hx_{t-j} and dc_t over its own steps.  The 4 waves' sums
+// are added in wave order and written as one row of partial[row][5][D]
+// (taps 0..3, then the bias), row = blockIdx.x.
+constexpr int kConvChunk = 64;
+constexpr int kConvRowCols = kConvTaps + 1;
+
+template <typename T, typename TG, int VEC>
+__global__ __launch_bounds__(256) void conv_bwd_kernel(
+    const T* __restrict__ hx, const TG* __restrict__ dxp, const float* __restrict__ w4,
+    const float* __restrict__ b4, T* __restrict__ dhx, float* __restrict__ partial, int64_t L,
+    int64_t D, int64_t groups) {
+    __shared__ float red[4][kConvRowCols][kWave][VEC];
+    const int lane = threadIdx.x & (kWave - 1), w = wave_id();
+    const int64_t b = blockIdx.x / groups, cg = blockIdx.x - b * groups;
+    const int64_t d0 = ((int64_t)blockIdx.y * kWave + lane) * VEC;
+    const bool valid = d0 < D;
+    const int64_t dc0 = valid ? d0 : 0;  // idle lanes shadow channel 0 and store nothing
+    const int64_t t0 = (4 * cg + w) * kConvChunk;
+    const int64_t end = t0 + kConvChunk < L ? t0 + kConvChunk : L;  // may be <= t0
+    const int64_t tend = end + 3 < L ? end + 3 : L;
+    float wt[kConvTaps][VEC], bias[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        bias[k] = b4[dc0 + k];
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) wt[j][k] = w4[j * D + dc0 + k];
+    }
+    const int64_t rowb = b * L * D + dc0;  // element offset of (b, 0, d0)
+    float h1[VEC], h2[VEC], h3[VEC];         // hx at t-1, t-2, t-3
+    float e0[VEC], e1[VEC], e2[VEC], e3[VEC];  // dc at t, t-1, t-2, t-3
+    float sw[kConvTaps][VEC], sb[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        h1[k] = h2[k] = h3[k] = 0.0f;
+        e0[k] = e1[k] = e2[k] = e3[k] = 0.0f;
+        sb[k] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) sw[j][k] = 0.0f;
+    }
+    if (t0 < end) {
+        if (t0 >= 3) load_vec<T, VEC>(hx, (rowb + (t0 - 3) * D) * (int64_t)sizeof(T), h3);
+        if (t0 >= 2) load_vec<T, VEC>(hx, (rowb + (t0 - 2) * D) * (int64_t)sizeof(T), h2);
+        if (t0 >= 1) load_vec<T, VEC>(hx, (rowb + (t0 - 1) * D) * (int64_t)sizeof(T), h1);
+        for (int64_t t = t0; t < end + 3; ++t) {
+            float dcv[VEC], x0[VEC];
+            if (t < tend) {
+                float g[VEC];
+                load_vec<T, VEC>(hx, (rowb + t * D) * (int64_t)sizeof(T), x0);
+                load_vec<TG, VEC>(dxp, (rowb + t * D) * (int64_t)sizeof(TG), g);
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    float c = bias[k];
+                    c = fmaf(wt[0][k], x0[k], c);
+                    c = fmaf(wt[1][k], h1[k], c);
+                    c = fmaf(wt[2][k], h2[k], c);
+                    c = fmaf(wt[3][k], h3[k], c);
+                    dcv[k] = g[k] * dsilu(c, sigmoid(c));
+                }
+                if (t < end) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) {
+                        sb[k] += dcv[k];
+                        sw[0][k] = fmaf(dcv[k], x0[k], sw[0][k]);
+                        sw[1][k] = fmaf(dcv[k], h1[k], sw[1][k]);
+                        sw[2][k] = fmaf(dcv[k], h2[k], sw[2][k]);
+                        sw[3][k] = fmaf(dcv[k], h3[k], sw[3][k]);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) dcv[k] = x0[k] = 0.0f;
+            }
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                e3[k] = e2[k];
+                e2[k] = e1[k];
+                e1[k] = e0[k];
+                e0[k] = dcv[k];
+                h3[k] = h2[k];
+                h2[k] = h1[k];
+                h1[k] = x0[k];
+            }
+            if (t - 3 >= t0 && valid) {
+                float o[VEC];
+#pragma unroll
+                for (int k = 0; k < VEC; ++k)
+                    o[k] = fmaf(wt[0][k], e3[k],
+                                fmaf(wt[1][k], e2[k], fmaf(wt[2][k], e1[k], wt[3][k] * e0[k])));
+                store_vec<T, VEC>(dhx, (rowb + (t - 3) * D) * (int64_t)sizeof(T), o);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) red[w][j][lane][k] = sw[j][k];
+        red[w][kConvTaps][lane][k] = sb[k];
+    }
+    __syncthreads();
+    if (w == 0 && valid) {
+        float* row = partial + (int64_t)blockIdx.x * kConvRowCols * D + dc0;
+#pragma unroll
+        for (int j = 0; j < kConvRowCols; ++j)
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+                row[j * D + k] = red[0][j][lane][k] + red[1][j][lane][k] + red[2][j][lane][k] +
+                                 red[3][j][lane][k];
+    }
+}
+
+// Column sums of partial[rows][cols] in a fixed order, in double: block
+// (nb, cb) adds rows [nb * 64, nb * 64 + 64) of columns [cb * 256, + 256).
+constexpr int kColRows = 64;
+__global__ __launch_bounds__(256) void colsum_rows_kernel(const float* __restrict__ partial,
+                                                          double* __restrict__ part2,
+                                                          int64_t rows, int64_t cols) {
+    const int64_t col = (int64_t)blockIdx.y * 256 + threadIdx.x;
+    if (col >= cols) return;
+    const int64_t r0 = (int64_t)blockIdx.x * kColRows;
+    const int64_t r1 = r0 + kColRows < rows ? r0 + kColRows : rows;
+    double acc = 0.0;
+    for (int64_t r = r0; r < r1; ++r) acc += (double)partial[r * cols + col];
+    part2[(int64_t)blockIdx.x * cols + col] = acc;
+}
+
+// The row blocks added in order, then written as dconv_w[d][j] (j < K) and
+// dconv_b[d] (if not null) from the columns [j][d] and [kConvTaps][d].
+__global__ __launch_bounds__(256) void conv_grad_final_kernel(const double* __restrict__ part2,
+                                                              int64_t nblk, int64_t D, int K,
+                                                              float* __restrict__ dw,
+                                                              float* __restrict__ db) {
+    const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t cols = kConvRowCols * D;
+    if (col >= cols) return;
+    double acc = 0.0;
+    for (int64_t r = 0; r < nblk; ++r) acc += part2[r * cols + col];
+    const int64_t j = col / D, d = col - j * D;
+    if (j < K) dw[d * K + j] = (float)acc;
+    else if (j == kConvTaps && db) db[d] = (float)acc;
+}
+
+namespace {
+template <typename T, typename TG>
+hipError_t gate_backward_t(const void* dy, const void* hz, const void* h, void* dh, void* dhz,
+                           int64_t n, hipStream_t stream) {
+    constexpr int V = 16 / sizeof(T);
+    if (n % V == 0 &&
+        ((uintptr_t)dy | (uintptr_t)hz | (uintptr_t)h | (uintptr_t)dh | (uintptr_t)dhz) % 16 == 0) {
+        const int64_t nvec = n / V;
+        hipLaunchKernelGGL((gate_bwd_vec_kernel<T, TG>),
+                           dim3((unsigned)((nvec + kGateThreads - 1) / kGateThreads)),
+                           dim3(kGateThreads), 0, stream, (const T*)dy, (const T*)hz, (const T*)h,
+                           (TG*)dh, (T*)dhz, nvec);
+    } else {
+        hipLaunchKernelGGL((gate_bwd_kernel<T, TG>),
+                           dim3((unsigned)((n + kGateThreads - 1) / kGateThreads)),
+                           dim3(kGateThreads), 0, stream, (const T*)dy, (const T*)hz, (const T*)h,
+                           (TG*)dh, (T*)dhz, n);
+    }
+    return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_gate_backward(const void* dy, const void* hz, const void* h, void* dh,
+                                void* dhz, int64_t n, IoType io, IoType dh_io,
+                                hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    if (io == IoType::kF32) return gate_backward_t<float, float>(dy, hz, h, dh, dhz, n, stream);
+    if (dh_io == IoType::kF32) return gate_backward_t<bf16, float>(dy, hz, h, dh, dhz, n, stream);
+    return gate_backward_t<bf16, bf16>(dy, hz, h, dh, dhz, n, stream);
+}
+
+hipError_t launch_widen(const void* src, float* dst, int64_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const bool vec = n % 8 == 0 && ((uintptr_t)src | (uintptr_t)dst) % 16 == 0;
+    const int64_t threads = vec ? n / 8 : n;
+    hipLaunchKernelGGL(widen_kernel, dim3((unsigned)((threads + kGateThreads - 1) / kGateThreads)),
+                       dim3(kGateThreads), 0, stream, (const bf16*)src, dst, n, vec);
+    return hipGetLastError();
+}
+
+namespace {
+struct ConvBwdPlan {
+    int64_t groups;  // workgroups along the sequence per batch row (4 chunks each)
+    int64_t rows;    // partial rows = B * groups
+    int64_t nblk;    // row blocks of the column sums
+    size_t partial_bytes, part2_bytes;
+};
+ConvBwdPlan conv_bwd_plan(int64_t B, int64_t L, int64_t D) {
+    ConvBwdPlan p;
+    const int64_t chunks = (L + kConvChunk - 1) / kConvChunk;
+    p.groups = chunks > 0 ? (chunks + 3) / 4 : 1;
+    p.rows = B * p.groups;
+    p.nblk = (p.rows + kColRows - 1) / kColRows;
+    p.partial_bytes = (size_t)(p.rows * kConvRowCols * D) * sizeof(float);
+    p.part2_bytes = (size_t)(p.nblk * kConvRowCols * D) * sizeof(double);
+    return p;
+}
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+}  // namespace
+
+size_t conv_backward_workspace(int64_t B, int64_t L, int64_t D) {
+    const ConvBwdPlan p = conv_bwd_plan(B, L, D);
+    return align256(p.partial_bytes) + align256(p.part2_bytes);
+}
+
+namespace {
+template <typename T, typename TG, int VEC>
+void conv_backward_t(dim3 grid, const void* hx, const void* dxp, const float* w4, const float* b4,
+                     void* dhx, float* partial, int64_t L, int64_t D, int64_t groups,
+                     hipStream_t stream) {
+    hipLaunchKernelGGL((conv_bwd_kernel<T, TG, VEC>), grid, dim3(256), 0, stream, (const T*)hx,
+                       (const TG*)dxp, w4, b4, (T*)dhx, partial, L, D, groups);
+}
+}  // namespace
+
+hipError_t launch_conv_backward(const void* hx, const void* dxp, const float* w4, const float* b4,
+                                void* dhx, float* dw, float* db, int K, int64_t B, int64_t L,
+                                int64_t D, IoType io, IoType dxp_io, void* ws,
+                                hipStream_t stream) {
+    const ConvBwdPlan p = conv_bwd_plan(B, L, D);
+    float* partial = (float*)ws;
+    double* part2 = (double*)((char*)ws + align256(p.partial_bytes));
+    const uintptr_t amask = (uintptr_t)hx | (uintptr_t)dhx;
+    const bool v4 = D % 4 == 0 && amask % (4 * io_bytes(io)) == 0 &&
+                    (uintptr_t)dxp % (4 * io_bytes(dxp_io)) == 0;
+    const dim3 grid((unsigned)(B * p.groups), (unsigned)((D / (v4 ? 4 : 1) + kWave - 1) / kWave));
+    const bool g32 = dxp_io == IoType::kF32;
+    if (io == IoType::kF32) {
+        if (v4) conv_backward_t<float, float, 4>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+        else conv_backward_t<float, float, 1>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+    } else if (g32) {
+        if (v4) conv_backward_t<bf16, float, 4>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+        else conv_backward_t<bf16, float, 1>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+    } else {
+        if (v4) conv_backward_t<bf16, bf16, 4>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+        else conv_backward_t<bf16, bf16, 1>(grid, hx, dxp, w4, b4, dhx, partial, L, D, p.groups, stream);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t cols = kConvRowCols * D;
+    hipLaunchKernelGGL(colsum_rows_kernel, dim3((unsigned)p.nblk, (unsigned)((cols + 255) / 256)),
+                       dim3(256), 0, stream, partial, part2, p.rows, cols);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(conv_grad_final_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0,
+                       stream, part2, p.nblk, D, K, dw, db);
+    return hipGetLastError();
+}
+
 hipError_t launch_pack_conv(const float* w, const float* b, int K, int64_t D, float* w4,
                             float* b4, hipStream_t stream) {
     hipLaunchKernelGGL(pack_conv_kernel, dim3((unsigned)((D + 255) / 256)), dim3(256), 0, stream,
@@ -106,30 +441,33 @@ hipError_t launch_pack_conv(const float* w, const float* b, int K, int64_t D, fl
     return hipGetLastError();
 }
 
-hipError_t launch_conv_silu(const void* hx, const float* w4, const float* b4, void* xp, int64_t B,
-                            int64_t L, int64_t D, IoType io, hipStream_t stream) {
-    const int64_t n = B * L * D;
-    if (n == 0) return hipSuccess;
-    const int V = io == IoType::kF32 ? 4 : 8;
+namespace {
+template <typename T, typename TO>
+hipError_t conv_silu_t(const void* hx, const float* w4, const float* b4, void* xp, int64_t L,
+                       int64_t D, int64_t n, hipStream_t stream) {
+    constexpr int V = 16 / sizeof(T);
     if (D % V == 0 && ((uintptr_t)hx | (uintptr_t)xp) % 16 == 0) {
         const int64_t nvec = n / V;
-        const dim3 grid((unsigned)((nvec + kGateThreads - 1) / kGateThreads));
-        if (io == IoType::kF32)
-            hipLaunchKernelGGL(conv_silu_vec_kernel<float>, grid, dim3(kGateThreads), 0, stream,
-                               (const float*)hx, w4, b4, (float*)xp, L, D, nvec);
-        else
-            hipLaunchKernelGGL(conv_silu_vec_kernel<bf16>, grid, dim3(kGateThreads), 0, stream,
-                               (const bf16*)hx, w4, b4, (bf16*)xp, L, D, nvec);
-        return hipGetLastError();
+        hipLaunchKernelGGL((conv_silu_vec_kernel<T, TO>),
+                           dim3((unsigned)((nvec + kGateThreads - 1) / kGateThreads)),
+                           dim3(kGateThreads), 0, stream, (const T*)hx, w4, b4, (TO*)xp, L, D,
+                           nvec);
+    } else {
+        hipLaunchKernelGGL((conv_silu_kernel<T, TO>),
+                           dim3((unsigned)((n + kGateThreads - 1) / kGateThreads)),
+                           dim3(kGateThreads), 0, stream, (const T*)hx, w4, b4, (TO*)xp, L, D, n);
     }
-    const dim3 grid((unsigned)((n + kGateThreads - 1) / kGateThreads));
-    if (io == IoType::kF32)
-        hipLaunchKernelGGL(conv_silu_kernel<float>, grid, dim3(kGateThreads), 0, stream,
-                           (const float*)hx, w4, b4, (float*)xp, L, D, n);
-    else
-        hipLaunchKernelGGL(conv_silu_kernel<bf16>, grid, dim3(kGateThreads), 0, stream,
-                           (const bf16*)hx, w4, b4, (bf16*)xp, L, D, n);
     return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_conv_silu(const void* hx, const float* w4, const float* b4, void* xp, int64_t B,
+                            int64_t L, int64_t D, IoType io, IoType out_io, hipStream_t stream) {
+    const int64_t n = B * L * D;
+    if (n == 0) return hipSuccess;
+    if (io == IoType::kF32) return conv_silu_t<float, float>(hx, w4, b4, xp, L, D, n, stream);
+    if (out_io == IoType::kF32) return conv_silu_t<bf16, float>(hx, w4, b4, xp, L, D, n, stream);
+    return conv_silu_t<bf16, bf16>(hx, w4, b4, xp, L, D, n, stream);
 }
 
 hipError_t launch_gate_out(const void* h, const void* hz, void* y, int64_t n, IoType io,

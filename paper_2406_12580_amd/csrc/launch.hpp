@@ -69,7 +69,6 @@ hipError_t launch_linear_scan(const float* a, const float* u, const float* h0, f
 hipError_t launch_scan_step(const void* x, const void* zr, const void* zi, const float* lambda,
                             const float* h_prev, float* h_next, int64_t B, int64_t D, IoType io,
                             IoType zio, hipStream_t stream);
-hipError_t launch_copy_state(const float* src, float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream);
 
 // Scan forward with the gate projections computed per tile on the matrix
@@ -97,12 +96,29 @@ bool tree_scan_supported(int64_t L);
 constexpr int kConvTaps = 4;
 hipError_t launch_pack_conv(const float* w, const float* b, int K, int64_t D, float* w4,
                             float* b4, hipStream_t stream);
-// x' = SiLU(causal depthwise conv(hx)) into xp ([B][L][D], I/O type).
+// x' = SiLU(causal depthwise conv(hx)) into xp ([B][L][D]; hx of type io, x'
+// of type out_io: the I/O type, or fp32 for a backward).
 hipError_t launch_conv_silu(const void* hx, const float* w4, const float* b4, void* xp, int64_t B,
-                            int64_t L, int64_t D, IoType io, hipStream_t stream);
+                            int64_t L, int64_t D, IoType io, IoType out_io, hipStream_t stream);
 // y = h * SiLU(hz) over n elements.
 hipError_t launch_gate_out(const void* h, const void* hz, void* y, int64_t n, IoType io,
                            hipStream_t stream);
+// Output gate backward: dh = dy * SiLU(hz) (stored as dh_io), dhz = dy * h *
+// SiLU'(hz) (I/O type).
+hipError_t launch_gate_backward(const void* dy, const void* hz, const void* h, void* dh,
+                                void* dhz, int64_t n, IoType io, IoType dh_io,
+                                hipStream_t stream);
+// bf16 to fp32 copy of n elements.
+hipError_t launch_widen(const void* src, float* dst, int64_t n, hipStream_t stream);
+// Conv + SiLU backward from dx' (the BD-LRU input gradient, of type dxp_io):
+// dhx, and the tap and bias gradients dw ([D][K]) and db ([D], may be null),
+// summed over b and t in a fixed order (double).  ws: conv_backward_workspace
+// bytes.
+size_t conv_backward_workspace(int64_t B, int64_t L, int64_t D);
+hipError_t launch_conv_backward(const void* hx, const void* dxp, const float* w4, const float* b4,
+                                void* dhx, float* dw, float* db, int K, int64_t B, int64_t L,
+                                int64_t D, IoType io, IoType dxp_io, void* ws,
+                                hipStream_t stream);
 // The scan forward with the projections fused in (fused_forward_applies) on
 // x = x', storing y = h * SiLU(hz) (and h if not null).
 hipError_t launch_fused_gated_forward(const void* x, const void* hz, const void* pack,

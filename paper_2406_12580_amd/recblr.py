@@ -29,7 +29,8 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
-OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP, OP_GATED_FORWARD = range(6)
+(OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP, OP_GATED_FORWARD,
+ OP_GATED_BACKWARD) = range(7)
 SCAN_CHUNKED, SCAN_SERIAL, SCAN_TREE = range(3)
 
 EXPORTS = (
@@ -37,7 +38,7 @@ EXPORTS = (
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
     "recblr_scan_forward_method", "recblr_gated_forward", "recblr_bdlru_scan_forward_timed",
-    "recblr_bdlru_scan_backward_timed",
+    "recblr_bdlru_scan_backward_timed", "recblr_gated_backward",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
@@ -57,6 +58,8 @@ _SIGS = {
     "recblr_scan_forward_method": ([_int] + [_p] * 5 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
     "recblr_gated_forward": ([_p] * 4 + [_int] + [_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p],
                              _int),
+    "recblr_gated_backward": ([_p] * 4 + [_int] + [_p] * 19 + [_i64] * 3 + [_int, _p, _sz, _p],
+                              _int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -262,3 +265,29 @@ def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None, keep_h=T
                                 _ptr(h), _ptr(hT), B, L, D, io, _ptr(ws), nws, _stream(stream)),
            "recblr_gated_forward")
     return y, h, hT
+
+
+def gated_backward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h, dy, h0=None, dhT=None,
+                   stream=None):
+    """Backward of gated_forward (h: its BD-LRU output).  Returns a dict with dhx,
+    dhz, dconv_w [D][K], dconv_b (None without a conv bias), dWr, dbr, dWi, dbi,
+    dlambda, dh0 (None without h0)."""
+    B, L, D = hx.shape
+    K = conv_w.shape[1]
+    io = io_code(hx.dtype)
+    f32 = dict(dtype=torch.float32, device=hx.device)
+    out = {"dhx": torch.empty_like(hx), "dhz": torch.empty_like(hx),
+           "dconv_w": torch.empty((D, K), **f32),
+           "dconv_b": torch.empty(D, **f32) if conv_b is not None else None,
+           "dWr": torch.empty((D, D), **f32), "dbr": torch.empty(D, **f32),
+           "dWi": torch.empty((D, D), **f32), "dbi": torch.empty(D, **f32),
+           "dlambda": torch.empty(D, **f32),
+           "dh0": torch.empty((B, D), **f32) if h0 is not None else None}
+    ws, nws = _workspace(OP_GATED_BACKWARD, B, L, D, io, hx.device)
+    _check(recblr_gated_backward(
+        _ptr(hx), _ptr(hz), _ptr(conv_w), _ptr(conv_b), K, _ptr(Wr), _ptr(br), _ptr(Wi),
+        _ptr(bi), _ptr(lam), _ptr(h0), _ptr(h), _ptr(dy), _ptr(dhT), _ptr(out["dhx"]),
+        _ptr(out["dhz"]), _ptr(out["dconv_w"]), _ptr(out["dconv_b"]), _ptr(out["dWr"]),
+        _ptr(out["dbr"]), _ptr(out["dWi"]), _ptr(out["dbi"]), _ptr(out["dlambda"]),
+        _ptr(out["dh0"]), B, L, D, io, _ptr(ws), nws, _stream(stream)), "recblr_gated_backward")
+    return out

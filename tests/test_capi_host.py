@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 13
+    assert len(syms) == 14
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -187,3 +187,25 @@ def test_gated_forward_validation(rb):
     assert call(hx=None) == rb.ERR_INVALID_ARGUMENT
     assert call(nws=16) == rb.ERR_WORKSPACE
     assert rb.recblr_workspace_size(rb.OP_GATED_FORWARD, 2, 3, 64, rb.F32) > 0
+
+
+def test_gated_backward_validation(rb):
+    def call(K=2, conv_w=addr(7), dconv_w=addr(11), nws=1 << 26, hx=addr(0), dhx=addr(12),
+             dlam=addr(17), ws=addr(20)):
+        return rb.recblr_gated_backward(
+            hx, addr(1), conv_w, None, K, addr(2), None, addr(3), None, addr(4), None, addr(5),
+            addr(6), None, dhx, addr(13), dconv_w, None, addr(14), addr(15), addr(16),
+            addr(18), dlam, None, 2, 3, 64, rb.F32, ws, nws, None)
+    assert call(K=0) == rb.ERR_UNSUPPORTED
+    assert call(K=5) == rb.ERR_UNSUPPORTED
+    assert call(conv_w=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(dconv_w=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(hx=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(dlam=None) == rb.ERR_INVALID_ARGUMENT
+    assert call(dhx=addr(0)) == rb.ERR_INVALID_ARGUMENT                    # dhx over hx
+    assert call(dconv_w=addr(7)) == rb.ERR_INVALID_ARGUMENT                # over conv_w
+    assert call(nws=16) == rb.ERR_WORKSPACE
+    assert call(ws=addr(1)) == rb.ERR_INVALID_ARGUMENT                     # ws over hz
+    need = rb.recblr_workspace_size(rb.OP_GATED_BACKWARD, 2, 3, 64, rb.F32)
+    assert need >= rb.recblr_workspace_size(rb.OP_BACKWARD, 2, 3, 64, rb.F32) + 3 * 2 * 3 * 64 * 4
+

@@ -356,6 +356,45 @@ def test_gated_forward(rb, case, io):
     assert_close(host(y2), oy2, io, "y (no bias, no h0, h not kept)")
 
 
+GATED_BWD_CASES = [((2, 300, 64), 4), ((1, 700, 128), 2), ((3, 130, 72), 3), ((8, 50, 64), 1),
+                   ((2, 5, 8), 4), ((3, 1, 64), 4), ((2, 0, 64), 3)]
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("case", GATED_BWD_CASES)
+def test_gated_backward(rb, case, io):
+    """Every gradient of the gated layer core against the oracle's chain rule,
+    with and without a conv bias / h0 / dhT."""
+    import torch
+    (B, L, D), K = case
+    seed = 8100 + B + L + D + K
+    f = dg.full_inputs(B, L, D, seed, io=io, a_range=(0.99, 0.9999), bias=True, h0=True,
+                       grad=True, dhT=True)
+    rng = np.random.default_rng(seed)
+    hz = rng.standard_normal((B, L, D)).astype(np.float32)
+    if io == "bf16":
+        hz = dg.round_bf16(hz)
+    w = (rng.standard_normal((D, K)) * 0.5).astype(np.float32)
+    cb = (rng.standard_normal(D) * 0.1).astype(np.float32)
+    args = [dev(f.Wr, io), dev(f.br, io), dev(f.Wi, io), dev(f.bi, io), dev32(f.lam)]
+    HX, HZ, DY = dev(f.x, io), dev(hz, io), dev(f.dh, io)
+    _, h, _ = rb.gated_forward(HX, HZ, dev32(w), dev32(cb), *args, dev32(f.h0))
+    got = rb.gated_backward(HX, HZ, dev32(w), dev32(cb), *args, h, DY, dev32(f.h0),
+                            dev32(f.dhT))
+    _, h2, _ = rb.gated_forward(HX, HZ, dev32(w), None, *args)
+    got2 = rb.gated_backward(HX, HZ, dev32(w), None, *args, h2, DY)
+    torch.cuda.synchronize()
+    print(f"gated backward {case} {io}: GPU done", flush=True)
+    want = oracle.gated_backward(f.x, hz, w, cb, f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh, f.h0,
+                                 f.dhT)
+    for k in ("dhx", "dhz", "dconv_w", "dconv_b", "dWr", "dbr", "dWi", "dbi", "dlambda", "dh0"):
+        assert_close(host(got[k]), want[k], io, k)
+    want2 = oracle.gated_backward(f.x, hz, w, None, f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh)
+    assert got2["dconv_b"] is None and got2["dh0"] is None
+    for k in ("dhx", "dhz", "dconv_w", "dWr", "dlambda"):
+        assert_close(host(got2[k]), want2[k], io, k + " (no bias, no h0)")
+
+
 # ------------------------------------------------------------------ named workloads at full size
 
 def _sample_rows(B, k=3):
