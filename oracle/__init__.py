@@ -8,7 +8,8 @@ The arithmetic lives in ``recblr_oracle.c`` (a plain sequential loop over t
 per channel, in double precision); this module compiles it with gcc when the
 shared object is missing or older than its source and wraps it with ctypes.
 Every function takes numpy arrays of any real dtype, widens them exactly to
-float64 and returns float64 arrays.
+float64 and returns float64 arrays.  ``oracle.model`` holds the oracle of a
+whole model training step (plain PyTorch CPU ops in float64).
 """
 from __future__ import annotations
 

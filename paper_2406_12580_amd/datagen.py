@@ -190,3 +190,61 @@ def step_inputs(B, D, seed, io="bf16", a_range=(0.99, 0.9999)):
     lam = lambda_from_base(rng.uniform(a_range[0], a_range[1], size=D))
     h_prev = rng.standard_normal((B, D), dtype=np.float32)
     return ScanInputs(x, zr, zi, lam, h0=h_prev, io=io)
+
+
+# ------------------------------------------------------------------ full model (f4)
+@dataclass
+class ModelDims:
+    B: int
+    T: int
+    D: int
+    E: int = 2          # expansion factor of the gated recurrent layer
+    V: int = 3416       # items (MovieLens-1M after the paper's preprocessing)
+    layers: int = 2     # behaviour-modelling layers (section 4 implementation details)
+    K: int = 4          # conv taps
+    eps: float = 1e-12  # LayerNorm epsilon
+
+
+# MovieLens-1M training shape of the paper's implementation details: batch
+# 2048, maximum length 200, embedding dimension 64, expansion factor 2, two
+# behaviour-modelling layers, 3,416 items.
+MODEL_CONFIGS = {
+    "ml1m": ModelDims(B=2048, T=200, D=64),
+    "ml1m-small": ModelDims(B=4, T=37, D=64, V=211),
+}
+
+
+def model_params(dims: ModelDims, seed: int) -> dict:
+    """Named float32 parameters: weights ~ N(0, 1/fan_in), biases ~ U[-0.1, 0.1],
+    embeddings ~ N(0, 1), LayerNorm gains 1 + U[-0.1, 0.1] and shifts U[-0.1, 0.1],
+    conv taps ~ N(0, 1/K), and Lambda from decay bases a ~ U[0.9, 0.999]
+    (the paper's initialisation)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    D, E, V, K = dims.D, dims.E, dims.V, dims.K
+    ED = E * D
+    f32 = lambda a: np.asarray(a, dtype=np.float32)
+    w = lambda o, i: f32(rng.standard_normal((o, i)) / np.sqrt(i))
+    u = lambda n, s=0.1: f32(rng.uniform(-s, s, n))
+    p = {"emb": f32(rng.standard_normal((V, D))), "emb_ln_g": f32(1.0 + u(D)),
+         "emb_ln_b": u(D)}
+    for l in range(dims.layers):
+        q = {"Wx": w(ED, D), "bx": u(ED), "Wz": w(ED, D), "bz": u(ED),
+             "conv_w": f32(rng.standard_normal((ED, K)) / np.sqrt(K)), "conv_b": u(ED),
+             "Wr": w(ED, ED), "br": u(ED), "Wi": w(ED, ED), "bi": u(ED),
+             "lambda": f32(lambda_from_base(rng.uniform(0.9, 0.999, ED))),
+             "Wo": w(D, ED), "bo": u(D), "ln1_g": f32(1.0 + u(D)), "ln1_b": u(D),
+             "W1": w(4 * D, D), "b1": u(4 * D), "W2": w(D, 4 * D), "b2": u(D),
+             "ln2_g": f32(1.0 + u(D)), "ln2_b": u(D)}
+        p.update({f"l{l}.{k}": v for k, v in q.items()})
+    return p
+
+
+def model_batch(dims: ModelDims, seed: int):
+    """Item ids [B][T] and next-item targets [B] (int32), drawn with Zipf(1)
+    popularity over the V items (item v has weight 1 / (v + 1))."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pr = 1.0 / np.arange(1, dims.V + 1, dtype=np.float64)
+    pr /= pr.sum()
+    ids = rng.choice(dims.V, size=(dims.B, dims.T), p=pr).astype(np.int32)
+    targets = rng.choice(dims.V, size=dims.B, p=pr).astype(np.int32)
+    return ids, targets
