@@ -1,7 +1,7 @@
 """Benchmark of the BD-LRU scan on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
-                    [--api scan|full|step|scan_step|ablation|gated]
+                    [--api scan|full|step|scan_step|ablation|gated|model]
 
 A step is one pass of the hot path over one batch: the gated scan forward
 (recblr_bdlru_scan_forward) followed by its backward
@@ -19,7 +19,11 @@ efficiency ablation (serial scan; two-tree scan with sequence padding or with
 embedding padding; the production chunked scan) at the paper's three
 sequence lengths.  --api gated times the gated recurrent layer core forward
 and backward (causal conv + SiLU, BD-LRU with projections, SiLU output gate;
-recblr_gated_forward / recblr_gated_backward) on the workload.
+recblr_gated_forward / recblr_gated_backward) on the workload.  --api model
+times a full 2-layer RecBLR training step (embedding, behaviour-modelling
+layers, softmax cross entropy, backward, Adam) at the MovieLens-1M training
+shape of the paper (B=2048, T=200, D=64, E=2, 3,416 items); its roofline is
+matrix-multiply flops against the fp32 matrix-core peak.
 Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).  With the
 scan API the roofline takes the scan kernel's own duration, from a HIP event
@@ -230,6 +234,92 @@ def gated_main(args, torch, dg, rb):
     print(json.dumps(out), flush=True)
 
 
+def model_flops(d):
+    """Matrix-multiply flops of one training step (forward + backward = 3x forward):
+    per token and layer the linear layers Wx, Wz (D -> ED), the BD-LRU gate
+    projections (ED -> ED, two), Wo (ED -> D) and the PFFN (D -> 4D -> D); per row
+    the prediction h_T E^T."""
+    ED = d.E * d.D
+    per_token = d.layers * 2 * (2 * d.D * ED + 2 * ED * ED + ED * d.D + 8 * d.D * d.D)
+    return 3 * (per_token * d.B * d.T + 2 * d.D * d.V * d.B)
+
+
+def model_main(args, torch, dg, rb):
+    """Full RecBLR model training step (forward, backward, Adam) on the MovieLens-1M
+    training shape."""
+    d = dg.MODEL_CONFIGS[args.workload or "ml1m"]
+    dev = torch.device("cuda:0")
+    log(f"model {d}")
+    named = dg.model_params(d, 1)
+    ids, targets = dg.model_batch(d, 2)
+    rd = rb.model_dims(d.B, d.T, d.D, d.E, d.V, d.layers, d.K, d.eps)
+    offs = rb.model_param_offsets(rd)
+    # model_params lists the tensors in the documented parameter order
+    assert len(offs) == len(named)
+    flat = np.zeros(rb.recblr_model_param_count(rd), dtype=np.float32)
+    for (name, arr), o in zip(named.items(), offs):
+        flat[o:o + arr.size] = arr.ravel()
+    P = torch.from_numpy(flat).to(dev)
+    G, M1, M2 = torch.empty_like(P), torch.zeros_like(P), torch.zeros_like(P)
+    I, Tg = torch.from_numpy(ids).to(dev), torch.from_numpy(targets).to(dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    step = rb.ModelStep(rd)
+    n = [0]
+
+    def one():
+        step.train_step(P, I, Tg, G, loss)
+        n[0] += 1
+        rb.adam_update(P, G, M1, M2, n[0])
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    first = loss.item()
+    K = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for k in range(K):
+        one()
+        ev[k + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    tokens = d.B * d.T
+    fl = model_flops(d)
+    ach = fl / float(np.mean(dts)) / 1e12
+    log(f"model step {np.mean(dts)*1e3:.2f} ms, loss {first:.4f} -> {loss.item():.4f}")
+    out = {"metric": "RecBLR model training tokens/sec (B*T per step: forward, backward, Adam)",
+           "value": tokens * K / wall, "unit": "tokens/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": wall / K * 1e3, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (Zipf item ids, seeded random-init weights)",
+           "config": {"workload": f"{args.workload or 'ml1m'}: 2-layer RecBLR, MovieLens-1M "
+                                  "training shape", "B": d.B, "T": d.T, "D": d.D, "E": d.E,
+                      "V": d.V, "layers": d.layers, "K": d.K},
+           "loss_first_last": [first, loss.item()],
+           "roofline": {"bound": "mfma", "kernel": "model_step (matrix-multiply flops)",
+                        "achieved": ach, "peak": 157.3, "unit": "TFLOP/s", "frac": ach / 157.3,
+                        "traffic": None}}
+    step.close()
+    if not args.no_cpu_baseline:
+        from oracle import model as om
+        lay, total = om.layout(d.D, d.E, d.V, d.layers, d.K)
+        rows, t0, passes = 2, time.perf_counter(), 0
+        f64 = np.zeros(total)
+        for name, shape, o in lay:
+            f64[o:o + int(np.prod(shape))] = named[name].ravel()
+        while time.perf_counter() - t0 < 10.0:
+            om.train_step(f64, ids[:rows], targets[:rows], d.D, d.E, d.V, d.layers, d.K, d.eps)
+            passes += 1
+        total = time.perf_counter() - t0
+        threads = torch.get_num_threads()
+        out["cpu_baseline"] = {"value": passes * rows * d.T / total, "unit": "tokens/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"fp64 oracle model step over {rows} of {d.B} rows "
+                                         f"(T={d.T}), {passes} passes, {total:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def ablation_main(args, torch, dg, rb):
     """Layer forward (projections + scan) per scan algorithm.
 
@@ -398,8 +488,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation", "gated"],
-                    default="scan")
+    ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation", "gated",
+                                      "model"], default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
                     help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
@@ -429,6 +519,8 @@ def main():
         return ablation_main(args, torch, dg, rb)
     if args.api == "gated":
         return gated_main(args, torch, dg, rb)
+    if args.api == "model":
+        return model_main(args, torch, dg, rb)
     cfg = dg.CONFIGS[args.workload or "c4"]
     if "bwd" not in cfg.ops:
         sys.exit(f"workload {cfg.name} has no backward; pick one of c3, c4, c5")

@@ -239,6 +239,81 @@ int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
                           int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Full RecBLR model: one training step of the paper's model (sections 2 and
+ * 3.1), as a model-level harness around the BD-LRU path:
+ *   H = LayerNorm(E[ids])                               (eq:layernorm; no positions)
+ *   `layers` times (behaviour-modelling layer):
+ *     H1 = LayerNorm(H + GRL(H))     GRL: Algorithm alg:gated_recurrent with
+ *          Hx, Hz = H Wx^T + bx, H Wz^T + bz (D -> E*D), the gated layer core of
+ *          recblr_gated_forward (h0 = 0), output projection Wo (E*D -> D)
+ *     H  = LayerNorm(H1 + PFFN(H1))  PFFN = SiLU(H1 W1^T + b1) W2^T + b2 (eq. PFFN)
+ *   logits = h_T E^T over the V items (h_T: each row's last step);
+ *   loss = mean over rows of the cross entropy of softmax(logits) with targets.
+ * Readings (the paper leaves them open): residual + LayerNorm after each
+ * sub-layer, dropout as the identity, the cross entropy of the next item at
+ * the last step.  The plain linear layers are rocBLAS fp32 GEMMs; all other
+ * steps run in this library's kernels.
+ *
+ * Parameters are one flat float buffer, each tensor starting at a multiple of
+ * 64 floats (recblr_model_param_offsets), weights [out][in], in this order:
+ *   E [V][D], emb_ln_g [D], emb_ln_b [D], then per layer
+ *   Wx [ED][D], bx [ED], Wz [ED][D], bz [ED], conv_w [ED][K], conv_b [ED],
+ *   Wr [ED][ED], br [ED], Wi [ED][ED], bi [ED], lambda [ED], Wo [D][ED], bo [D],
+ *   ln1_g [D], ln1_b [D], W1 [4D][D], b1 [4D], W2 [D][4D], b2 [D], ln2_g [D],
+ *   ln2_b [D]                                               (ED = E * D)
+ */
+typedef struct {
+    int64_t B;      /* rows (sequences) per batch */
+    int64_t T;      /* steps per sequence */
+    int64_t D;      /* embedding dimension: 64, 128 or 256 */
+    int64_t E;      /* expansion factor of the gated recurrent layer, E * D <= 1024 */
+    int64_t V;      /* items */
+    int64_t layers; /* behaviour-modelling layers, 1..64 */
+    int K;          /* conv taps, 1..4 */
+    float ln_eps;   /* LayerNorm epsilon, >= 0 */
+} recblr_model_dims;
+
+/* Number of floats of the flat parameter (and gradient) buffer; 0 for
+ * unsupported dimensions. */
+size_t recblr_model_param_count(const recblr_model_dims* m);
+/* Writes the offset (in floats) of each tensor, in the order above, to
+ * offsets[0 .. n) and returns the number of tensors (3 + 21 * layers); -1 for
+ * unsupported dimensions. */
+int64_t recblr_model_param_offsets(const recblr_model_dims* m, int64_t* offsets, int64_t n);
+/* Workspace bytes of recblr_model_train_step (saved activations of every
+ * layer, backward scratch, the sort of the item ids); 0 if unsupported. */
+size_t recblr_model_workspace_size(const recblr_model_dims* m);
+
+/* rocBLAS handle for the model step's GEMMs: created and destroyed by the
+ * caller (creation allocates rocBLAS' own state; the step itself allocates
+ * nothing).  A handle serves one stream at a time. */
+int recblr_blas_create(void** handle);
+int recblr_blas_destroy(void* handle);
+
+/*
+ * Forward and backward of one batch:
+ *   params : flat float parameters (256-byte aligned);  ids : [B][T] int32 item
+ *   ids;  targets : [B] int32 next items;  grads : flat float, the layout of
+ *   params (padding zero);  loss : one float.
+ * Every sum over rows is taken in a fixed order (double), so loss and
+ * gradients repeat bitwise for a given rocBLAS handle and GPU.  An id or
+ * target outside [0, V) makes the loss NaN (nothing is read out of bounds).
+ * Errors: INVALID_ARGUMENT for a NULL pointer or misaligned buffer or
+ * overlapping outputs; UNSUPPORTED for dimensions outside the ranges above;
+ * WORKSPACE; HIP for a failed launch or GEMM.
+ */
+int recblr_model_train_step(const recblr_model_dims* m, const float* params, const int32_t* ids,
+                            const int32_t* targets, float* grads, float* loss, void* ws,
+                            size_t ws_bytes, void* blas, void* stream);
+
+/*
+ * Adam (Kingma and Ba, Algorithm 1) over n floats, in place: step is the
+ * 1-based update count; m1, m2 the moment buffers (zero before step 1).
+ */
+int recblr_adam_update(float* params, const float* grads, float* m1, float* m2, int64_t n,
+                       int64_t step, float lr, float beta1, float beta2, float eps, void* stream);
+
+/*
  * Scan algorithms of the efficiency ablation (section 4, Table tab:efficiency;
  * the two-tree scan of section 3.3, figure fig:scan): the gated scan forward
  * from a zero initial state by one of

@@ -10,6 +10,7 @@
 
 #include "gemm.hpp"
 #include "launch.hpp"
+#include "model.hpp"
 
 using namespace recblr;
 
@@ -594,6 +595,101 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     return status_of(
         launch_scan_step(x, zr, zi, lambda, h_prev, h_next, B, D, io_of(io), IoType::kF32, strm));
+}
+
+}  // extern "C"
+
+namespace {
+bool model_dims_ok(const recblr_model_dims* m) {
+    if (!m) return false;
+    const int64_t ED = m->E * m->D;
+    return m->B >= 1 && m->T >= 1 && (m->D == 64 || m->D == 128 || m->D == 256) && m->E >= 1 &&
+           ED <= kMaxProjD && m->V >= 1 && m->V < (1ll << 31) && m->layers >= 1 &&
+           m->layers <= model::kMaxLayers && m->K >= 1 && m->K <= kConvTaps &&
+           m->ln_eps >= 0.0f && m->B * m->T < (1ll << 31) && m->B * m->V < (1ll << 31);
+}
+model::Dims model_dims(const recblr_model_dims* m) {
+    return model::Dims{m->B, m->T, m->D, m->E, m->V, m->layers, m->K, m->ln_eps};
+}
+}  // namespace
+
+extern "C" {
+
+size_t recblr_model_param_count(const recblr_model_dims* m) {
+    return model_dims_ok(m) ? (size_t)model::param_offsets(model_dims(m), nullptr) : 0;
+}
+
+int64_t recblr_model_param_offsets(const recblr_model_dims* m, int64_t* offsets, int64_t n) {
+    if (!model_dims_ok(m)) return -1;
+    const model::Dims d = model_dims(m);
+    const int64_t count = model::tensor_count(d);
+    int64_t all[3 + model::kLayerTensors * model::kMaxLayers];
+    model::param_offsets(d, all);
+    for (int64_t i = 0; offsets && i < n && i < count; ++i) offsets[i] = all[i];
+    return count;
+}
+
+size_t recblr_model_workspace_size(const recblr_model_dims* m) {
+    return model_dims_ok(m) ? model::workspace_size(model_dims(m)) : 0;
+}
+
+int recblr_blas_create(void** handle) {
+    if (!handle) return RECBLR_ERR_INVALID_ARGUMENT;
+    rocblas_handle h = nullptr;
+    if (rocblas_create_handle(&h) != rocblas_status_success) return RECBLR_ERR_HIP;
+    *handle = (void*)h;
+    return RECBLR_OK;
+}
+
+int recblr_blas_destroy(void* handle) {
+    if (!handle) return RECBLR_OK;
+    return rocblas_destroy_handle((rocblas_handle)handle) == rocblas_status_success
+               ? RECBLR_OK
+               : RECBLR_ERR_HIP;
+}
+
+int recblr_model_train_step(const recblr_model_dims* m, const float* params, const int32_t* ids,
+                            const int32_t* targets, float* grads, float* loss, void* ws,
+                            size_t ws_bytes, void* blas, void* stream) {
+    if (!m) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!model_dims_ok(m)) return RECBLR_ERR_UNSUPPORTED;
+    if (!params || !ids || !targets || !grads || !loss || !blas)
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!aligned(params, kWsAlign) || !aligned(grads, kWsAlign) || !aligned(ids, 4) ||
+        !aligned(targets, 4) || !aligned(loss, 4))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    const model::Dims d = model_dims(m);
+    const size_t np = (size_t)model::param_offsets(d, nullptr) * 4,
+                 ni = (size_t)(m->B * m->T) * 4, nt = (size_t)m->B * 4;
+    if (!disjoint({{grads, np}, {loss, 4}}, {{params, np}, {ids, ni}, {targets, nt}}) ||
+        overlaps({grads, np}, {loss, 4}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t need = model::workspace_size(d);
+    if (need == 0) return RECBLR_ERR_UNSUPPORTED;
+    int st = check_ws(ws, ws_bytes, need);
+    if (st) return st;
+    if (!disjoint({{ws, need}}, {{params, np}, {ids, ni}, {targets, nt}, {grads, np}, {loss, 4}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    return model::train_step(d, params, ids, targets, grads, loss, ws, (rocblas_handle)blas,
+                             (hipStream_t)stream);
+}
+
+int recblr_adam_update(float* params, const float* grads, float* m1, float* m2, int64_t n,
+                       int64_t step, float lr, float beta1, float beta2, float eps,
+                       void* stream) {
+    if (n < 0 || step < 1) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (n == 0) return RECBLR_OK;
+    if (!params || !grads || !m1 || !m2) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)params, (const void*)grads, (const void*)m1,
+                          (const void*)m2})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t b = (size_t)n * 4;
+    if (overlaps({params, b}, {grads, b}) || overlaps({params, b}, {m1, b}) ||
+        overlaps({params, b}, {m2, b}) || overlaps({m1, b}, {m2, b}) ||
+        overlaps({grads, b}, {m1, b}) || overlaps({grads, b}, {m2, b}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    return status_of(model::adam(params, grads, m1, m2, n, step, lr, beta1, beta2, eps,
+                                 (hipStream_t)stream));
 }
 
 int recblr_linear_scan_forward(const float* a, const float* u, const float* h0, float* h,

@@ -348,6 +348,85 @@ hipError_t gate_backward_t(const void* dy, const void* hz, const void* h, void* 
 }
 }  // namespace
 
+// Column sums of a tall [rows][cols] matrix, in a fixed order.  Stage 1:
+// workgroup (b, tile) adds rows [b * R, b * R + R) of up to 256 columns; its
+// 256 threads are J = 256 / tc row lanes of tc columns, lane j adding rows
+// j, j + J, ... in double, and the J lanes are then added in lane order.
+// Stage 2 adds the G workgroup sums of each column in order.
+constexpr int kColsumGroups = 512;
+__global__ __launch_bounds__(256) void colsum_part_kernel(const float* __restrict__ src,
+                                                          double* __restrict__ part,
+                                                          int64_t rows, int64_t cols,
+                                                          int64_t rows_per_group) {
+    __shared__ double sh[256];
+    const int64_t tc = cols < 256 ? cols : 256;
+    const int J = (int)(256 / tc);
+    const int t = threadIdx.x;
+    const int j = (int)(t / tc);
+    const int64_t c = (int64_t)blockIdx.y * 256 + (t % tc);
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_group;
+    const int64_t r1 = r0 + rows_per_group < rows ? r0 + rows_per_group : rows;
+    double acc = 0.0;
+    if (j < J && c < cols) {
+        // 8 loads in flight, added in row order
+        int64_t r = r0 + j;
+        for (; r + 7 * J < r1; r += 8 * J) {
+            float v[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = src[(r + q * J) * cols + c];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc += (double)v[q];
+        }
+        for (; r < r1; r += J) acc += (double)src[r * cols + c];
+    }
+    sh[t] = acc;
+    __syncthreads();
+    if (j == 0 && c < cols) {
+        double s = sh[t];
+        for (int q = 1; q < J; ++q) s += sh[q * tc + t];
+        part[(int64_t)blockIdx.x * cols + c] = s;
+    }
+}
+
+__global__ __launch_bounds__(256) void colsum_final_kernel(const double* __restrict__ part,
+                                                           int64_t groups, int64_t cols,
+                                                           float* __restrict__ out) {
+    const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (col >= cols) return;
+    double acc = 0.0;
+    int64_t r = 0;
+    for (; r + 8 <= groups; r += 8) {  // 8 loads in flight, added in order
+        double v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = part[(r + q) * cols + col];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc += v[q];
+    }
+    for (; r < groups; ++r) acc += part[r * cols + col];
+    out[col] = (float)acc;
+}
+
+size_t colsum_workspace(int64_t rows, int64_t cols) {
+    const int64_t g = rows < kColsumGroups ? (rows > 0 ? rows : 1) : kColsumGroups;
+    return (size_t)(g * cols) * sizeof(double);
+}
+
+hipError_t launch_colsum(const float* src, int64_t rows, int64_t cols, float* out, void* ws,
+                         hipStream_t stream) {
+    if (cols == 0) return hipSuccess;
+    if (rows == 0) return launch_fill(out, 0.0f, cols, stream);
+    const int64_t groups = rows < kColsumGroups ? rows : kColsumGroups;
+    const int64_t per = (rows + groups - 1) / groups;
+    double* part = (double*)ws;
+    hipLaunchKernelGGL(colsum_part_kernel, dim3((unsigned)groups, (unsigned)((cols + 255) / 256)),
+                       dim3(256), 0, stream, src, part, rows, cols, per);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0,
+                       stream, part, groups, cols, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_gate_backward(const void* dy, const void* hz, const void* h, void* dh,
                                 void* dhz, int64_t n, IoType io, IoType dh_io,
                                 hipStream_t stream) {

@@ -108,6 +108,11 @@ hipError_t launch_gate_out(const void* h, const void* hz, void* y, int64_t n, Io
 hipError_t launch_gate_backward(const void* dy, const void* hz, const void* h, void* dh,
                                 void* dhz, int64_t n, IoType io, IoType dh_io,
                                 hipStream_t stream);
+// out[c] = sum over r of src[r][c] ([rows][cols] fp32), in a fixed order in
+// double; ws: colsum_workspace bytes.
+size_t colsum_workspace(int64_t rows, int64_t cols);
+hipError_t launch_colsum(const float* src, int64_t rows, int64_t cols, float* out, void* ws,
+                         hipStream_t stream);
 // bf16 to fp32 copy of n elements.
 hipError_t launch_widen(const void* src, float* dst, int64_t n, hipStream_t stream);
 // Conv + SiLU backward from dx' (the BD-LRU input gradient, of type dxp_io):

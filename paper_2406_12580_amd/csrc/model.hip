@@ -1,0 +1,773 @@
+// One training step of the full RecBLR model (arXiv 2406.12580): embedding
+// with LayerNorm (section 2, eq:layernorm), `layers` behaviour-modelling
+// layers (section 3.1: the gated recurrent layer of Algorithm
+// alg:gated_recurrent, then the PFFN of eq. PFFN, each sub-layer followed by a
+// residual connection and LayerNorm), and the prediction layer (section 2:
+// softmax over h_T E^T) with the cross entropy of the next item; then Adam.
+//
+// The plain linear layers are rocBLAS fp32 GEMMs; everything else runs in
+// the kernels of this library: the gated recurrent layer core through
+// recblr_gated_forward / recblr_gated_backward (conv, BD-LRU scan with its
+// gate projections, output gate), and here the embedding gather, the
+// LayerNorms, bias broadcasts, SiLU, the cross entropy, the sums over rows
+// for bias and LayerNorm gradients (fixed order, double), the embedding
+// gradient (positions sorted by item, then summed per item in position
+// order) and Adam.  Dropout is the identity.
+#include <hip/hip_runtime.h>
+#include <rocblas/rocblas.h>
+
+#include <hipcub/hipcub.hpp>
+
+#include "device_common.hpp"
+#include "launch.hpp"
+#include "model.hpp"
+#include "recblr.h"
+
+namespace recblr {
+namespace model {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRowsPerWave = 4;  // rows of a LayerNorm kernel's workgroup per pass (one per wave)
+constexpr int64_t kLnBwdRows = 256;  // rows per workgroup of the LayerNorm backward
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// ------------------------------------------------------------------ LayerNorm
+// y = (v - mean) / sqrt(var + eps) * g + b over rows of D = 64 * NV features,
+// one wave per row (lane holds features lane + 64 j).  v = a + r (r may be
+// null: no residual) and, if s is not null, v is stored for the backward.
+// EMB: v is row ids[row] of the embedding a (an id outside [0, V) gives NaN).
+template <int NV, bool EMB>
+__global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
+    const float* __restrict__ a, const float* __restrict__ r, const int* __restrict__ ids,
+    const float* __restrict__ g, const float* __restrict__ b, float* __restrict__ s,
+    float* __restrict__ y, float* __restrict__ mu, float* __restrict__ rs, int64_t M, int64_t V,
+    float eps) {
+    constexpr int D = 64 * NV;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = (int64_t)blockIdx.x * kRowsPerWave + wave_id();
+    if (row >= M) return;
+    float v[NV];
+    float bad = 0.0f;
+    const float* src = a + row * D;
+    if constexpr (EMB) {
+        const int64_t id = ids[row];
+        const bool ok = id >= 0 && id < V;
+        src = a + (ok ? id : 0) * D;
+        bad = ok ? 0.0f : __builtin_nanf("");
+    }
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        v[j] = src[lane + 64 * j] + bad;
+        if (!EMB && r) v[j] += r[row * D + lane + 64 * j];
+        sum += v[j];
+    }
+    const float m = wave_sum(sum) * (1.0f / D);
+    float var = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) var += (v[j] - m) * (v[j] - m);
+    const float rstd = 1.0f / sqrtf(wave_sum(var) * (1.0f / D) + eps);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        if (s) s[row * D + c] = v[j];
+        y[row * D + c] = (v[j] - m) * rstd * g[c] + b[c];
+    }
+    if (lane == 0) {
+        mu[row] = m;
+        rs[row] = rstd;
+    }
+}
+
+// LayerNorm backward: dx = rstd (gd - mean(gd) - xh mean(gd xh)), gd = dy g,
+// xh = (v - mean) rstd with v from s (or the embedding rows by id).  The
+// workgroup handles rows [blk * kLnBwdRows, + kLnBwdRows), wave w the rows
+// w, w + 4, ...; the sums of dy xh and dy over its rows are added in wave
+// order and written to pg[blk], pb[blk] (summed over workgroups later).
+template <int NV, bool EMB>
+__global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
+    const float* __restrict__ dy, const float* __restrict__ s, const int* __restrict__ ids,
+    const float* __restrict__ mu, const float* __restrict__ rs, const float* __restrict__ g,
+    float* __restrict__ dx, float* __restrict__ pg, float* __restrict__ pb, int64_t M,
+    int64_t V) {
+    constexpr int D = 64 * NV;
+    __shared__ float red[4][2][D];
+    const int lane = threadIdx.x & (kWave - 1), w = wave_id();
+    const int64_t r0 = (int64_t)blockIdx.x * kLnBwdRows;
+    const int64_t r1 = r0 + kLnBwdRows < M ? r0 + kLnBwdRows : M;
+    float ag[NV], ab[NV], gc[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        ag[j] = ab[j] = 0.0f;
+        gc[j] = g[lane + 64 * j];
+    }
+    for (int64_t row = r0 + w; row < r1; row += 4) {
+        const float* src = s + row * D;
+        if constexpr (EMB) {
+            const int64_t id = ids[row];
+            src = s + (id >= 0 && id < V ? id : 0) * D;
+        }
+        const float m = mu[row], rstd = rs[row];
+        float xh[NV], d[NV], gd[NV];
+        float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int c = lane + 64 * j;
+            xh[j] = (src[c] - m) * rstd;
+            d[j] = dy[row * D + c];
+            gd[j] = d[j] * gc[j];
+            s1 += gd[j];
+            s2 += gd[j] * xh[j];
+        }
+        const float m1 = wave_sum(s1) * (1.0f / D), m2 = wave_sum(s2) * (1.0f / D);
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            dx[row * D + lane + 64 * j] = rstd * (gd[j] - m1 - xh[j] * m2);
+            ag[j] = fmaf(d[j], xh[j], ag[j]);
+            ab[j] += d[j];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        red[w][0][lane + 64 * j] = ag[j];
+        red[w][1][lane + 64 * j] = ab[j];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int c = lane + 64 * j;
+            pg[blockIdx.x * D + c] = ((red[0][0][c] + red[1][0][c]) + red[2][0][c]) + red[3][0][c];
+            pb[blockIdx.x * D + c] = ((red[0][1][c] + red[1][1][c]) + red[2][1][c]) + red[3][1][c];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ elementwise
+// C[m][n] = bias[n] (the GEMM then accumulates onto it).
+__global__ __launch_bounds__(kThreads) void bias_rows_kernel(const float* __restrict__ bias,
+                                                             float* __restrict__ C, int64_t M,
+                                                             int64_t N) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e * 4 >= M * N) return;
+    const int64_t n = (e * 4) % N;  // N % 4 == 0
+    *(float4*)(C + e * 4) = *(const float4*)(bias + n);
+}
+
+__global__ __launch_bounds__(kThreads) void silu_fwd_kernel(const float* __restrict__ A,
+                                                            float* __restrict__ P, int64_t n) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e * 4 >= n) return;
+    float4 a = *(const float4*)(A + e * 4);
+    a.x *= sigmoid(a.x);
+    a.y *= sigmoid(a.y);
+    a.z *= sigmoid(a.z);
+    a.w *= sigmoid(a.w);
+    *(float4*)(P + e * 4) = a;
+}
+
+// dA = dP SiLU'(A), SiLU'(v) = s (1 + v (1 - s)), in place over dP.
+__global__ __launch_bounds__(kThreads) void silu_bwd_kernel(float* __restrict__ dP,
+                                                            const float* __restrict__ A,
+                                                            int64_t n) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e * 4 >= n) return;
+    const float4 a = *(const float4*)(A + e * 4);
+    float4 d = *(const float4*)(dP + e * 4);
+    const float av[4] = {a.x, a.y, a.z, a.w};
+    float dv[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float sg = sigmoid(av[i]);
+        dv[i] *= sg * fmaf(av[i], 1.0f - sg, 1.0f);
+    }
+    *(float4*)(dP + e * 4) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+}
+
+// ------------------------------------------------------------------ prediction and loss
+// Block sum / max over 256 threads in a fixed tree order.
+template <bool MAX>
+__device__ __forceinline__ float block_reduce(float v, float* sh) {
+    sh[threadIdx.x] = v;
+    __syncthreads();
+    for (int o = kThreads / 2; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o)
+            sh[threadIdx.x] = MAX ? fmaxf(sh[threadIdx.x], sh[threadIdx.x + o])
+                                  : sh[threadIdx.x] + sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    const float r = sh[0];
+    __syncthreads();
+    return r;
+}
+
+// Row b of the logits: loss_b = logsumexp - logit[target], and
+// dlogits = (softmax - onehot(target)) / B.  A target outside [0, V) gives NaN.
+__global__ __launch_bounds__(kThreads) void ce_kernel(const float* __restrict__ logits,
+                                                      const int* __restrict__ targets, int64_t B,
+                                                      int64_t V, float* __restrict__ dlogits,
+                                                      float* __restrict__ lossb) {
+    __shared__ float sh[kThreads];
+    const int64_t b = blockIdx.x;
+    const float* l = logits + b * V;
+    float mx = -__builtin_huge_valf();
+    for (int64_t v = threadIdx.x; v < V; v += kThreads) mx = fmaxf(mx, l[v]);
+    mx = block_reduce<true>(mx, sh);
+    float se = 0.0f;
+    for (int64_t v = threadIdx.x; v < V; v += kThreads) se += expf(l[v] - mx);
+    se = block_reduce<false>(se, sh);
+    const int64_t t = targets[b];
+    const bool ok = t >= 0 && t < V;
+    const float inv = 1.0f / se, scale = 1.0f / (float)B;
+    for (int64_t v = threadIdx.x; v < V; v += kThreads)
+        dlogits[b * V + v] = (expf(l[v] - mx) * inv - (v == t ? 1.0f : 0.0f)) * scale;
+    if (threadIdx.x == 0) lossb[b] = ok ? logf(se) + mx - l[t] : __builtin_nanf("");
+}
+
+// loss = sum_b loss_b / B, in order, in double.
+__global__ void loss_final_kernel(const float* __restrict__ lossb, int64_t B,
+                                  float* __restrict__ loss) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    double acc = 0.0;
+    for (int64_t b = 0; b < B; ++b) acc += (double)lossb[b];
+    *loss = (float)(acc / (double)B);
+}
+
+// ------------------------------------------------------------------ embedding gradient
+__global__ void iota_kernel(int* __restrict__ p, int64_t n) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e < n) p[e] = (int)e;
+}
+
+__device__ __forceinline__ int64_t lower_bound_u32(const unsigned* a, int64_t n, unsigned key) {
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (a[mid] < key) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// The input side of dE: for each item v, the rows of dx at the positions
+// holding v, summed in position order (ids sorted stably with their
+// positions).  Popular items hold many positions, so the work is cut into
+// pieces of kPiece sorted positions: item v has ceil(n_v / kPiece) pieces
+// starting at poff[v] (an exclusive scan); one wave sums each piece, then one
+// wave per item adds its pieces in order.
+constexpr int64_t kPiece = 256;
+
+__global__ __launch_bounds__(kThreads) void emb_count_kernel(const unsigned* __restrict__ ids_sorted,
+                                                             int64_t M, int64_t V,
+                                                             int64_t* __restrict__ lo,
+                                                             int64_t* __restrict__ hi,
+                                                             int64_t* __restrict__ npiece) {
+    const int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (v >= V) return;
+    const int64_t a = lower_bound_u32(ids_sorted, M, (unsigned)v);
+    const int64_t b = lower_bound_u32(ids_sorted, M, (unsigned)v + 1u);
+    lo[v] = a;
+    hi[v] = b;
+    npiece[v] = (b - a + kPiece - 1) / kPiece;
+}
+
+// out[i] = sum of in[0 .. i) for i <= n (one workgroup of 1024 threads).
+__global__ __launch_bounds__(1024) void exclusive_scan_kernel(const int64_t* __restrict__ in,
+                                                              int64_t* __restrict__ out,
+                                                              int64_t n) {
+    __shared__ int64_t buf[2][1024];
+    const int t = threadIdx.x;
+    int64_t carry = 0;
+    for (int64_t base = 0; base < n; base += 1024) {
+        const int64_t x = base + t < n ? in[base + t] : 0;
+        int cur = 0;
+        buf[cur][t] = x;
+        __syncthreads();
+        for (int o = 1; o < 1024; o <<= 1) {
+            const int64_t v = buf[cur][t] + (t >= o ? buf[cur][t - o] : 0);
+            buf[cur ^ 1][t] = v;
+            cur ^= 1;
+            __syncthreads();
+        }
+        if (base + t < n) out[base + t] = carry + buf[cur][t] - x;
+        carry += buf[cur][1023];
+        __syncthreads();
+    }
+    if (t == 0) out[n] = carry;
+}
+
+template <int NV>
+__global__ __launch_bounds__(kThreads) void emb_piece_kernel(
+    const int* __restrict__ pos_sorted, const float* __restrict__ dx,
+    const int64_t* __restrict__ lo, const int64_t* __restrict__ hi,
+    const int64_t* __restrict__ poff, float* __restrict__ part, int64_t V, int64_t max_pieces) {
+    constexpr int D = 64 * NV;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t p = (int64_t)blockIdx.x * 4 + wave_id();
+    if (p >= max_pieces || p >= poff[V]) return;
+    // the item whose pieces contain p: the last v with poff[v] <= p
+    int64_t a = 0, b = V;
+    while (b - a > 1) {
+        const int64_t mid = (a + b) >> 1;
+        if (poff[mid] <= p) a = mid;
+        else b = mid;
+    }
+    const int64_t start = lo[a] + (p - poff[a]) * kPiece;
+    const int64_t end = start + kPiece < hi[a] ? start + kPiece : hi[a];
+    float acc[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) acc[j] = 0.0f;
+    for (int64_t i = start; i < end; ++i) {
+        const int64_t r = pos_sorted[i];
+#pragma unroll
+        for (int j = 0; j < NV; ++j) acc[j] += dx[r * D + lane + 64 * j];
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) part[p * D + lane + 64 * j] = acc[j];
+}
+
+template <int NV>
+__global__ __launch_bounds__(kThreads) void emb_item_kernel(const int64_t* __restrict__ poff,
+                                                            const float* __restrict__ part,
+                                                            float* __restrict__ dE, int64_t V) {
+    constexpr int D = 64 * NV;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t v = (int64_t)blockIdx.x * 4 + wave_id();
+    if (v >= V || poff[v] == poff[v + 1]) return;
+    float acc[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) acc[j] = 0.0f;
+    for (int64_t p = poff[v]; p < poff[v + 1]; ++p)
+#pragma unroll
+        for (int j = 0; j < NV; ++j) acc[j] += part[p * D + lane + 64 * j];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) dE[v * D + lane + 64 * j] += acc[j];
+}
+
+// ------------------------------------------------------------------ Adam
+// Kingma and Ba, Algorithm 1: m = b1 m + (1 - b1) g, v = b2 v + (1 - b2) g^2,
+// p -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps).
+__global__ __launch_bounds__(kThreads) void adam_kernel(float* __restrict__ p,
+                                                        const float* __restrict__ g,
+                                                        float* __restrict__ m1,
+                                                        float* __restrict__ m2, int64_t n,
+                                                        float lr, float b1, float b2, float eps,
+                                                        float c1, float c2) {
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= n) return;
+    const float gv = g[e];
+    const float a = b1 * m1[e] + (1.0f - b1) * gv;
+    const float b = b2 * m2[e] + (1.0f - b2) * gv * gv;
+    m1[e] = a;
+    m2[e] = b;
+    p[e] -= lr * (a / c1) / (sqrtf(b / c2) + eps);
+}
+
+unsigned blocks_for(int64_t n, int64_t per = kThreads) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+// ------------------------------------------------------------------ parameter layout
+int64_t layer_tensor_size(const Dims& d, int k) {
+    const int64_t D = d.D, ED = d.E * d.D, F = 4 * d.D;
+    switch (k) {
+        case kWx: case kWz: return ED * D;
+        case kConvW: return ED * d.K;
+        case kWr: case kWi: return ED * ED;
+        case kWo: return D * ED;
+        case kW1: return F * D;
+        case kb1: return F;
+        case kW2: return D * F;
+        case kbo: case kLn1g: case kLn1b: case kb2: case kLn2g: case kLn2b: return D;
+        default: return ED;  // bx, bz, conv_b, br, bi, lambda
+    }
+}
+
+int64_t tensor_count(const Dims& d) { return 3 + kLayerTensors * d.layers; }
+
+// Offsets (floats) of every tensor in order; returns the total (a multiple of 64).
+int64_t param_offsets(const Dims& d, int64_t* off) {
+    int64_t at = 0, i = 0;
+    auto put = [&](int64_t size) {
+        if (off) off[i] = at;
+        ++i;
+        at += (size + 63) / 64 * 64;
+    };
+    put(d.V * d.D);
+    put(d.D);
+    put(d.D);
+    for (int64_t l = 0; l < d.layers; ++l)
+        for (int k = 0; k < kLayerTensors; ++k) put(layer_tensor_size(d, k));
+    return at;
+}
+
+// ------------------------------------------------------------------ workspace
+struct Layout {
+    size_t H, Hx, Hz, hb, y, s1, H1, A, P, s2, stats, emb_stats, logits, dlogits, lossb;
+    size_t X, Y, dP, dY, dHx, dHz, lnp, dwp, colsum, emb_lo, emb_hi, emb_np, emb_poff, emb_part;
+    size_t ids_s, pos, pos_s, sort_tmp, gated, total;
+    size_t sort_bytes, gated_bytes;
+};
+
+constexpr int64_t kDwChunk = 4096;  // rows per partial of a weight gradient
+
+Layout layout(const Dims& d) {
+    const int64_t M = d.B * d.T, D = d.D, ED = d.E * d.D, F = 4 * d.D, L = d.layers;
+    const size_t f = sizeof(float);
+    Layout w{};
+    size_t at = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = at;
+        at += align_up(bytes);
+        return o;
+    };
+    w.H = take((size_t)((L + 1) * M * D) * f);  // layer inputs / outputs
+    w.Hx = take((size_t)(L * M * ED) * f);
+    w.Hz = take((size_t)(L * M * ED) * f);
+    w.hb = take((size_t)(L * M * ED) * f);      // BD-LRU outputs
+    w.y = take((size_t)(L * M * ED) * f);
+    w.s1 = take((size_t)(L * M * D) * f);
+    w.H1 = take((size_t)(L * M * D) * f);
+    w.A = take((size_t)(L * M * F) * f);
+    w.P = take((size_t)(L * M * F) * f);
+    w.s2 = take((size_t)(L * M * D) * f);
+    w.stats = take((size_t)(L * 4 * M) * f);    // mean and 1/std of both LayerNorms
+    w.emb_stats = take((size_t)(2 * M) * f);
+    w.logits = take((size_t)(d.B * d.V) * f);
+    w.dlogits = take((size_t)(d.B * d.V) * f);
+    w.lossb = take((size_t)d.B * f);
+    w.X = take((size_t)(M * D) * f);
+    w.Y = take((size_t)(M * D) * f);
+    w.dP = take((size_t)(M * F) * f);
+    w.dY = take((size_t)(M * ED) * f);
+    w.dHx = take((size_t)(M * ED) * f);
+    w.dHz = take((size_t)(M * ED) * f);
+    const int64_t lnblk = (M + kLnBwdRows - 1) / kLnBwdRows;
+    w.lnp = take((size_t)(2 * lnblk * D) * f);
+    // weight gradients: one partial per chunk of kDwChunk rows, summed after
+    const int64_t NK = 4 * D * D > ED * D ? 4 * D * D : ED * D;
+    const int64_t slices = M / kDwChunk + 1;
+    w.dwp = take((size_t)(slices * NK) * f);
+    // column sums: bias gradients (widths D, 4D, E*D), LayerNorm partials, the
+    // weight-gradient slices
+    size_t cs = colsum_workspace(M, F > ED ? F : ED);
+    if (colsum_workspace(lnblk, D) > cs) cs = colsum_workspace(lnblk, D);
+    if (colsum_workspace(slices, NK) > cs) cs = colsum_workspace(slices, NK);
+    w.colsum = take(cs);
+    const int64_t max_pieces = (M + kPiece - 1) / kPiece + d.V;
+    w.emb_lo = take((size_t)d.V * sizeof(int64_t));
+    w.emb_hi = take((size_t)d.V * sizeof(int64_t));
+    w.emb_np = take((size_t)(d.V + 1) * sizeof(int64_t));
+    w.emb_poff = take((size_t)(d.V + 1) * sizeof(int64_t));
+    w.emb_part = take((size_t)(max_pieces * D) * f);
+    w.ids_s = take((size_t)M * sizeof(unsigned));
+    w.pos = take((size_t)M * sizeof(int));
+    w.pos_s = take((size_t)M * sizeof(int));
+    size_t sb = 0;
+    hipcub::DeviceRadixSort::SortPairs(nullptr, sb, (const unsigned*)nullptr, (unsigned*)nullptr,
+                                       (const int*)nullptr, (int*)nullptr, (int)M, 0, 32);
+    w.sort_bytes = sb;
+    w.sort_tmp = take(sb);
+    const size_t gf = recblr_workspace_size(RECBLR_OP_GATED_FORWARD, d.B, d.T, ED, RECBLR_F32);
+    const size_t gb = recblr_workspace_size(RECBLR_OP_GATED_BACKWARD, d.B, d.T, ED, RECBLR_F32);
+    w.gated_bytes = gf > gb ? gf : gb;
+    w.gated = take(w.gated_bytes);
+    w.total = at;
+    return w;
+}
+
+size_t workspace_size(const Dims& d) { return layout(d).total; }
+
+// ------------------------------------------------------------------ runner
+namespace {
+
+struct Ctx {
+    rocblas_handle blas;
+    hipStream_t stream;
+    char* ws;
+    const Layout& w;
+    bool ok = true;
+};
+
+// Row-major Y[M][N] (+)= X[M][K] W[N][K]^T: column-major Y^T = W X^T.
+bool gemm_xwT(Ctx& c, const float* X, int64_t ldx, const float* W, float* Y, int64_t ldy,
+              int64_t M, int64_t N, int64_t K, float beta) {
+    const float one = 1.0f;
+    return rocblas_sgemm(c.blas, rocblas_operation_transpose, rocblas_operation_none, (int)N,
+                         (int)M, (int)K, &one, W, (int)K, X, (int)ldx, &beta, Y,
+                         (int)ldy) == rocblas_status_success;
+}
+// Row-major dX[M][K] (+)= dY[M][N] W[N][K]: column-major dX^T = W^T dY^T.
+bool gemm_dyW(Ctx& c, const float* dY, int64_t lddy, const float* W, float* dX, int64_t lddx,
+              int64_t M, int64_t N, int64_t K, float beta) {
+    const float one = 1.0f;
+    return rocblas_sgemm(c.blas, rocblas_operation_none, rocblas_operation_none, (int)K, (int)M,
+                         (int)N, &one, W, (int)K, dY, (int)lddy, &beta, dX,
+                         (int)lddx) == rocblas_status_success;
+}
+// Row-major dW[N][K] = dY[M][N]^T X[M][K]: column-major dW^T = X^T dY.
+bool gemm_dyTx(Ctx& c, const float* X, int64_t ldx, const float* dY, int64_t lddy, float* dW,
+               int64_t M, int64_t N, int64_t K) {
+    const float one = 1.0f, zero = 0.0f;
+    return rocblas_sgemm(c.blas, rocblas_operation_none, rocblas_operation_transpose, (int)K,
+                         (int)N, (int)M, &one, X, (int)ldx, dY, (int)lddy, &zero, dW,
+                         (int)K) == rocblas_status_success;
+}
+
+// dW[N][K] = dY^T X over M rows: a GEMM per chunk of kDwChunk rows (one
+// strided-batched call), then the chunk partials summed in order (double).
+// A single GEMM over all rows would reduce along 409,600 rows inside the
+// library, which its kernels do slowly.
+bool weight_grad(Ctx& c, const float* X, int64_t ldx, const float* dY, int64_t lddy, float* dW,
+                 int64_t M, int64_t N, int64_t K) {
+    const int64_t nb = M / kDwChunk, rem = M - nb * kDwChunk;
+    if (nb < 2) return gemm_dyTx(c, X, ldx, dY, lddy, dW, M, N, K);
+    float* part = (float*)(c.ws + c.w.dwp);
+    const float one = 1.0f, zero = 0.0f;
+    if (rocblas_sgemm_strided_batched(c.blas, rocblas_operation_none, rocblas_operation_transpose,
+                                      (int)K, (int)N, (int)kDwChunk, &one, X, (int)ldx,
+                                      kDwChunk * ldx, dY, (int)lddy, kDwChunk * lddy, &zero, part,
+                                      (int)K, K * N, (int)nb) != rocblas_status_success)
+        return false;
+    int64_t slices = nb;
+    if (rem > 0) {
+        if (!gemm_dyTx(c, X + nb * kDwChunk * ldx, ldx, dY + nb * kDwChunk * lddy, lddy,
+                       part + nb * K * N, rem, N, K))
+            return false;
+        ++slices;
+    }
+    return launch_colsum(part, slices, N * K, dW, c.ws + c.w.colsum, c.stream) == hipSuccess;
+}
+
+bool linear_fwd(Ctx& c, const float* X, const float* W, const float* b, float* Y, int64_t M,
+                int64_t N, int64_t K) {
+    hipLaunchKernelGGL(bias_rows_kernel, dim3(blocks_for(M * N / 4)), dim3(kThreads), 0, c.stream,
+                       b, Y, M, N);
+    if (hipGetLastError() != hipSuccess) return false;
+    return gemm_xwT(c, X, K, W, Y, N, M, N, K, 1.0f);
+}
+
+// db[n] = sum_m dY[m][n] in a fixed order (double).
+bool bias_grad(Ctx& c, const float* dY, int64_t M, int64_t N, float* db) {
+    return launch_colsum(dY, M, N, db, c.ws + c.w.colsum, c.stream) == hipSuccess;
+}
+
+template <int NV>
+bool ln_fwd(Ctx& c, const float* a, const float* r, const int* ids, const float* g,
+            const float* b, float* s, float* y, float* mu, float* rs, int64_t M, int64_t V,
+            float eps) {
+    const dim3 grid(blocks_for(M, kRowsPerWave));
+    if (ids)
+        hipLaunchKernelGGL((ln_fwd_kernel<NV, true>), grid, dim3(kThreads), 0, c.stream, a, r,
+                           ids, g, b, s, y, mu, rs, M, V, eps);
+    else
+        hipLaunchKernelGGL((ln_fwd_kernel<NV, false>), grid, dim3(kThreads), 0, c.stream, a, r,
+                           ids, g, b, s, y, mu, rs, M, V, eps);
+    return hipGetLastError() == hipSuccess;
+}
+
+// LayerNorm backward; gamma / beta gradients into dg, db.
+template <int NV>
+bool ln_bwd(Ctx& c, const float* dy, const float* s, const int* ids, const float* mu,
+            const float* rs, const float* g, float* dx, float* dg, float* db, int64_t M,
+            int64_t V) {
+    constexpr int D = 64 * NV;
+    const int64_t nblk = (M + kLnBwdRows - 1) / kLnBwdRows;
+    float* pg = (float*)(c.ws + c.w.lnp);
+    float* pb = pg + nblk * D;
+    if (ids)
+        hipLaunchKernelGGL((ln_bwd_kernel<NV, true>), dim3((unsigned)nblk), dim3(kThreads), 0,
+                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V);
+    else
+        hipLaunchKernelGGL((ln_bwd_kernel<NV, false>), dim3((unsigned)nblk), dim3(kThreads), 0,
+                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V);
+    if (hipGetLastError() != hipSuccess) return false;
+    return launch_colsum(pg, nblk, D, dg, c.ws + c.w.colsum, c.stream) == hipSuccess &&
+           launch_colsum(pb, nblk, D, db, c.ws + c.w.colsum, c.stream) == hipSuccess;
+}
+
+template <int NV>
+int train_step_t(const Dims& d, const float* params, const int* ids, const int* targets,
+                 float* grads, float* loss, char* ws, const Layout& w, rocblas_handle blas,
+                 hipStream_t stream) {
+    Ctx c{blas, stream, ws, w};
+    const int64_t B = d.B, T = d.T, M = B * T, D = d.D, ED = d.E * d.D, F = 4 * d.D, V = d.V;
+    const int64_t nt = tensor_count(d);
+    int64_t off[3 + kLayerTensors * 64];
+    if (nt > (int64_t)(sizeof(off) / sizeof(off[0]))) return RECBLR_ERR_UNSUPPORTED;
+    param_offsets(d, off);
+    auto P = [&](int64_t l, int k) { return params + off[3 + l * kLayerTensors + k]; };
+    auto G = [&](int64_t l, int k) { return grads + off[3 + l * kLayerTensors + k]; };
+    auto buf = [&](size_t o) { return (float*)(ws + o); };
+    float* H = buf(w.H);
+    auto Hl = [&](int64_t l) { return H + l * M * D; };
+    auto per = [&](size_t o, int64_t l, int64_t width) { return buf(o) + l * M * width; };
+    float* st = buf(w.stats);
+    auto stat = [&](int64_t l, int k) { return st + (l * 4 + k) * M; };
+    float* mu0 = buf(w.emb_stats);
+    float* rs0 = mu0 + M;
+    const float* E = params + off[0];
+    if (rocblas_set_stream(blas, stream) != rocblas_status_success) return RECBLR_ERR_HIP;
+    int st_ = RECBLR_OK;
+#define CHECK(x) \
+    do {         \
+        if (!(x)) return RECBLR_ERR_HIP; \
+    } while (0)
+#define CHECK_ST(x)                  \
+    do {                             \
+        if ((st_ = (x)) != RECBLR_OK) return st_; \
+    } while (0)
+
+    // ---- forward
+    CHECK(ln_fwd<NV>(c, E, nullptr, ids, params + off[1], params + off[2], nullptr, Hl(0), mu0,
+                     rs0, M, V, d.eps));
+    for (int64_t l = 0; l < d.layers; ++l) {
+        float *Hx = per(w.Hx, l, ED), *Hz = per(w.Hz, l, ED), *hb = per(w.hb, l, ED),
+              *y = per(w.y, l, ED), *s1 = per(w.s1, l, D), *H1 = per(w.H1, l, D),
+              *A = per(w.A, l, F), *Pp = per(w.P, l, F), *s2 = per(w.s2, l, D);
+        CHECK(linear_fwd(c, Hl(l), P(l, kWx), P(l, kbx), Hx, M, ED, D));
+        CHECK(linear_fwd(c, Hl(l), P(l, kWz), P(l, kbz), Hz, M, ED, D));
+        CHECK_ST(recblr_gated_forward(Hx, Hz, P(l, kConvW), P(l, kConvB), d.K, P(l, kWr),
+                                      P(l, kbr), P(l, kWi), P(l, kbi), P(l, kLam), nullptr, y, hb,
+                                      nullptr, B, T, ED, RECBLR_F32, ws + w.gated, w.gated_bytes,
+                                      stream));
+        // O = y Wo^T + bo goes to s1, then s1 += H and H1 = LN(s1).
+        CHECK(linear_fwd(c, y, P(l, kWo), P(l, kbo), s1, M, D, ED));
+        CHECK(ln_fwd<NV>(c, s1, Hl(l), nullptr, P(l, kLn1g), P(l, kLn1b), s1, H1, stat(l, 0),
+                         stat(l, 1), M, V, d.eps));
+        CHECK(linear_fwd(c, H1, P(l, kW1), P(l, kb1), A, M, F, D));
+        hipLaunchKernelGGL(silu_fwd_kernel, dim3(blocks_for(M * F / 4)), dim3(kThreads), 0,
+                           stream, A, Pp, M * F);
+        CHECK(hipGetLastError() == hipSuccess);
+        CHECK(linear_fwd(c, Pp, P(l, kW2), P(l, kb2), s2, M, D, F));
+        CHECK(ln_fwd<NV>(c, s2, H1, nullptr, P(l, kLn2g), P(l, kLn2b), s2, Hl(l + 1),
+                         stat(l, 2), stat(l, 3), M, V, d.eps));
+    }
+    // prediction: logits = h_T E^T with h_T the last step of every row
+    const float* hT = Hl(d.layers) + (T - 1) * D;
+    float* logits = buf(w.logits);
+    float* dlogits = buf(w.dlogits);
+    CHECK(gemm_xwT(c, hT, T * D, E, logits, V, B, V, D, 0.0f));
+    hipLaunchKernelGGL(ce_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, logits, targets, B,
+                       V, dlogits, buf(w.lossb));
+    CHECK(hipGetLastError() == hipSuccess);
+    hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(64), 0, stream, buf(w.lossb), B, loss);
+    CHECK(hipGetLastError() == hipSuccess);
+
+    // ---- backward
+    float *X = buf(w.X), *Y = buf(w.Y), *dP = buf(w.dP), *dY = buf(w.dY), *dHx = buf(w.dHx),
+          *dHz = buf(w.dHz);
+    float* dE = grads + off[0];
+    // dE = dlogits^T h_T (the prediction's use of E); the input side adds on later.
+    CHECK(gemm_dyTx(c, hT, T * D, dlogits, V, dE, B, V, D));
+    // dH of the last layer's output: zero except the last step, dlogits E.
+    CHECK(launch_fill(Y, 0.0f, M * D, stream) == hipSuccess);
+    CHECK(gemm_dyW(c, dlogits, V, E, Y + (T - 1) * D, T * D, B, V, D, 0.0f));
+    for (int64_t l = d.layers - 1; l >= 0; --l) {
+        float *Hx = per(w.Hx, l, ED), *Hz = per(w.Hz, l, ED), *hb = per(w.hb, l, ED),
+              *y = per(w.y, l, ED), *s1 = per(w.s1, l, D), *H1 = per(w.H1, l, D),
+              *A = per(w.A, l, F), *Pp = per(w.P, l, F), *s2 = per(w.s2, l, D);
+        // LN2: Y (dH2) -> X (ds2 = dQ, and the residual part of dH1)
+        CHECK(ln_bwd<NV>(c, Y, s2, nullptr, stat(l, 2), stat(l, 3), P(l, kLn2g), X, G(l, kLn2g),
+                         G(l, kLn2b), M, V));
+        // PFFN: Q = P W2^T + b2, P = SiLU(A), A = H1 W1^T + b1
+        CHECK(bias_grad(c, X, M, D, G(l, kb2)));
+        CHECK(weight_grad(c, Pp, F, X, D, G(l, kW2), M, D, F));
+        CHECK(gemm_dyW(c, X, D, P(l, kW2), dP, F, M, D, F, 0.0f));
+        hipLaunchKernelGGL(silu_bwd_kernel, dim3(blocks_for(M * F / 4)), dim3(kThreads), 0,
+                           stream, dP, A, M * F);
+        CHECK(hipGetLastError() == hipSuccess);
+        CHECK(bias_grad(c, dP, M, F, G(l, kb1)));
+        CHECK(weight_grad(c, H1, D, dP, F, G(l, kW1), M, F, D));
+        CHECK(gemm_dyW(c, dP, F, P(l, kW1), X, D, M, F, D, 1.0f));  // X = dH1
+        // LN1: X (dH1) -> Y (ds1 = dO, and the residual part of dH)
+        CHECK(ln_bwd<NV>(c, X, s1, nullptr, stat(l, 0), stat(l, 1), P(l, kLn1g), Y, G(l, kLn1g),
+                         G(l, kLn1b), M, V));
+        // O = y Wo^T + bo
+        CHECK(bias_grad(c, Y, M, D, G(l, kbo)));
+        CHECK(weight_grad(c, y, ED, Y, D, G(l, kWo), M, D, ED));
+        CHECK(gemm_dyW(c, Y, D, P(l, kWo), dY, ED, M, D, ED, 0.0f));
+        CHECK_ST(recblr_gated_backward(Hx, Hz, P(l, kConvW), P(l, kConvB), d.K, P(l, kWr),
+                                       P(l, kbr), P(l, kWi), P(l, kbi), P(l, kLam), nullptr, hb,
+                                       dY, nullptr, dHx, dHz, G(l, kConvW), G(l, kConvB),
+                                       G(l, kWr), G(l, kbr), G(l, kWi), G(l, kbi), G(l, kLam),
+                                       nullptr, B, T, ED, RECBLR_F32, ws + w.gated, w.gated_bytes,
+                                       stream));
+        // Hx = H Wx^T + bx, Hz = H Wz^T + bz; Y becomes dH of this layer's input.
+        CHECK(bias_grad(c, dHx, M, ED, G(l, kbx)));
+        CHECK(bias_grad(c, dHz, M, ED, G(l, kbz)));
+        CHECK(weight_grad(c, Hl(l), D, dHx, ED, G(l, kWx), M, ED, D));
+        CHECK(weight_grad(c, Hl(l), D, dHz, ED, G(l, kWz), M, ED, D));
+        CHECK(gemm_dyW(c, dHx, ED, P(l, kWx), Y, D, M, ED, D, 1.0f));
+        CHECK(gemm_dyW(c, dHz, ED, P(l, kWz), Y, D, M, ED, D, 1.0f));
+    }
+    // embedding LayerNorm, then the input side of dE: rows summed per item
+    CHECK(ln_bwd<NV>(c, Y, E, ids, mu0, rs0, params + off[1], X, grads + off[1], grads + off[2], M,
+                     V));
+    unsigned* ids_s = (unsigned*)(ws + w.ids_s);
+    int* pos = (int*)(ws + w.pos);
+    int* pos_s = (int*)(ws + w.pos_s);
+    hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(M)), dim3(kThreads), 0, stream, pos, M);
+    CHECK(hipGetLastError() == hipSuccess);
+    size_t sb = w.sort_bytes;
+    CHECK(hipcub::DeviceRadixSort::SortPairs(ws + w.sort_tmp, sb, (const unsigned*)ids, ids_s,
+                                             (const int*)pos, pos_s, (int)M, 0, 32,
+                                             stream) == hipSuccess);
+    int64_t* lo = (int64_t*)(ws + w.emb_lo);
+    int64_t* hi = (int64_t*)(ws + w.emb_hi);
+    int64_t* np_ = (int64_t*)(ws + w.emb_np);
+    int64_t* poff = (int64_t*)(ws + w.emb_poff);
+    float* epart = buf(w.emb_part);
+    const int64_t max_pieces = (M + kPiece - 1) / kPiece + V;
+    hipLaunchKernelGGL(emb_count_kernel, dim3(blocks_for(V)), dim3(kThreads), 0, stream, ids_s, M,
+                       V, lo, hi, np_);
+    CHECK(hipGetLastError() == hipSuccess);
+    hipLaunchKernelGGL(exclusive_scan_kernel, dim3(1), dim3(1024), 0, stream, np_, poff, V);
+    CHECK(hipGetLastError() == hipSuccess);
+    hipLaunchKernelGGL((emb_piece_kernel<NV>), dim3(blocks_for(max_pieces, 4)), dim3(kThreads), 0,
+                       stream, pos_s, X, lo, hi, poff, epart, V, max_pieces);
+    CHECK(hipGetLastError() == hipSuccess);
+    hipLaunchKernelGGL((emb_item_kernel<NV>), dim3(blocks_for(V, 4)), dim3(kThreads), 0, stream,
+                       poff, epart, dE, V);
+    CHECK(hipGetLastError() == hipSuccess);
+#undef CHECK
+#undef CHECK_ST
+    return RECBLR_OK;
+}
+
+}  // namespace
+
+int train_step(const Dims& d, const float* params, const int* ids, const int* targets,
+               float* grads, float* loss, void* ws, rocblas_handle blas, hipStream_t stream) {
+    const Layout w = layout(d);
+    // Padding between tensors is zero in the gradient.
+    if (launch_fill(grads, 0.0f, param_offsets(d, nullptr), stream) != hipSuccess)
+        return RECBLR_ERR_HIP;
+    switch (d.D / 64) {
+        case 1: return train_step_t<1>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
+        case 2: return train_step_t<2>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
+        case 4: return train_step_t<4>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
+        default: return RECBLR_ERR_UNSUPPORTED;
+    }
+}
+
+hipError_t adam(float* p, const float* g, float* m1, float* m2, int64_t n, int64_t step, float lr,
+                float b1, float b2, float eps, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const float c1 = 1.0f - powf(b1, (float)step), c2 = 1.0f - powf(b2, (float)step);
+    hipLaunchKernelGGL(adam_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, stream, p, g, m1, m2,
+                       n, lr, b1, b2, eps, c1, c2);
+    return hipGetLastError();
+}
+
+}  // namespace model
+}  // namespace recblr

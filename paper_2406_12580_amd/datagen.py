@@ -215,7 +215,9 @@ MODEL_CONFIGS = {
 
 
 def model_params(dims: ModelDims, seed: int) -> dict:
-    """Named float32 parameters: weights ~ N(0, 1/fan_in), biases ~ U[-0.1, 0.1],
+    """Named float32 parameters, in the flat parameter order of the model step
+    (embedding, its LayerNorm, then each layer's tensors): weights ~ N(0, 1/fan_in),
+    biases ~ U[-0.1, 0.1],
     embeddings ~ N(0, 1), LayerNorm gains 1 + U[-0.1, 0.1] and shifts U[-0.1, 0.1],
     conv taps ~ N(0, 1/K), and Lambda from decay bases a ~ U[0.9, 0.999]
     (the paper's initialisation)."""

@@ -38,10 +38,22 @@ EXPORTS = (
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
     "recblr_scan_forward_method", "recblr_gated_forward", "recblr_bdlru_scan_forward_timed",
-    "recblr_bdlru_scan_backward_timed", "recblr_gated_backward",
+    "recblr_bdlru_scan_backward_timed", "recblr_gated_backward", "recblr_model_param_count",
+    "recblr_model_param_offsets", "recblr_model_workspace_size", "recblr_blas_create",
+    "recblr_blas_destroy", "recblr_model_train_step", "recblr_adam_update",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+_f = ctypes.c_float
+
+
+class ModelDims(ctypes.Structure):
+    """recblr_model_dims."""
+    _fields_ = [("B", _i64), ("T", _i64), ("D", _i64), ("E", _i64), ("V", _i64),
+                ("layers", _i64), ("K", _int), ("ln_eps", _f)]
+
+
+_pd = ctypes.POINTER(ModelDims)
 _SIGS = {
     "recblr_status_string": ([_int], ctypes.c_char_p),
     "recblr_workspace_size": ([_int, _i64, _i64, _i64, _int], _sz),
@@ -60,6 +72,13 @@ _SIGS = {
                              _int),
     "recblr_gated_backward": ([_p] * 4 + [_int] + [_p] * 19 + [_i64] * 3 + [_int, _p, _sz, _p],
                               _int),
+    "recblr_model_param_count": ([_pd], _sz),
+    "recblr_model_param_offsets": ([_pd, _p, _i64], _i64),
+    "recblr_model_workspace_size": ([_pd], _sz),
+    "recblr_blas_create": ([ctypes.POINTER(_p)], _int),
+    "recblr_blas_destroy": ([_p], _int),
+    "recblr_model_train_step": ([_pd] + [_p] * 6 + [_sz, _p, _p], _int),
+    "recblr_adam_update": ([_p] * 4 + [_i64, _i64, _f, _f, _f, _f, _p], _int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -291,3 +310,67 @@ def gated_backward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h, dy, h0=None, 
         _ptr(out["dbr"]), _ptr(out["dWi"]), _ptr(out["dbi"]), _ptr(out["dlambda"]),
         _ptr(out["dh0"]), B, L, D, io, _ptr(ws), nws, _stream(stream)), "recblr_gated_backward")
     return out
+
+
+# ------------------------------------------------------------------ full model step
+
+def model_dims(B, T, D, E=2, V=3416, layers=2, K=4, eps=1e-12) -> ModelDims:
+    return ModelDims(B, T, D, E, V, layers, K, eps)
+
+
+def model_param_offsets(dims: ModelDims):
+    """Offsets (floats) of the flat parameter tensors, in the documented order."""
+    n = recblr_model_param_offsets(ctypes.byref(dims), None, 0)
+    if n < 0:
+        raise RecblrError(ERR_UNSUPPORTED, "recblr_model_param_offsets")
+    arr = (ctypes.c_int64 * n)()
+    recblr_model_param_offsets(ctypes.byref(dims), arr, n)
+    return list(arr)
+
+
+class ModelStep:
+    """One training step of the full model on the GPU: holds the rocBLAS handle
+    and the workspace for fixed dimensions."""
+
+    def __init__(self, dims: ModelDims, device="cuda"):
+        self.dims = dims
+        self.count = recblr_model_param_count(ctypes.byref(dims))
+        if self.count == 0:
+            raise RecblrError(ERR_UNSUPPORTED, "recblr_model_param_count")
+        n = recblr_model_workspace_size(ctypes.byref(dims))
+        if n == 0:
+            raise RecblrError(ERR_UNSUPPORTED, "recblr_model_workspace_size")
+        self.ws = torch.empty(n, dtype=torch.uint8, device=device)
+        h = _p()
+        _check(recblr_blas_create(ctypes.byref(h)), "recblr_blas_create")
+        self.blas = h
+
+    def close(self):
+        if self.blas is not None:
+            recblr_blas_destroy(self.blas)
+            self.blas = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def train_step(self, params, ids, targets, grads=None, loss=None, stream=None):
+        """Loss and gradients (flat, the parameter layout) of one batch."""
+        if grads is None:
+            grads = torch.empty_like(params)
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float32, device=params.device)
+        _check(recblr_model_train_step(ctypes.byref(self.dims), _ptr(params), _ptr(ids),
+                                       _ptr(targets), _ptr(grads), _ptr(loss), _ptr(self.ws),
+                                       self.ws.numel(), self.blas, _stream(stream)),
+               "recblr_model_train_step")
+        return loss, grads
+
+
+def adam_update(params, grads, m1, m2, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                stream=None):
+    _check(recblr_adam_update(_ptr(params), _ptr(grads), _ptr(m1), _ptr(m2), params.numel(),
+                              step, lr, beta1, beta2, eps, _stream(stream)), "recblr_adam_update")
+

@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 14
+    assert len(syms) == 21
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -208,4 +208,35 @@ def test_gated_backward_validation(rb):
     assert call(ws=addr(1)) == rb.ERR_INVALID_ARGUMENT                     # ws over hz
     need = rb.recblr_workspace_size(rb.OP_GATED_BACKWARD, 2, 3, 64, rb.F32)
     assert need >= rb.recblr_workspace_size(rb.OP_BACKWARD, 2, 3, 64, rb.F32) + 3 * 2 * 3 * 64 * 4
+
+
+def test_model_layout_matches_the_oracle(rb):
+    """The library's parameter offsets against the oracle's own reading of the
+    documented order (two implementations of one layout)."""
+    from oracle import model as om
+    for D, E, V, layers, K in ((64, 2, 3416, 2, 4), (128, 1, 5, 1, 2), (64, 3, 211, 3, 3)):
+        dims = rb.model_dims(2, 3, D, E, V, layers, K)
+        lay, total = om.layout(D, E, V, layers, K)
+        assert rb.model_param_offsets(dims) == [o for _, _, o in lay]
+        assert rb.recblr_model_param_count(dims) == total
+
+
+def test_model_validation(rb):
+    import ctypes
+    ok = rb.model_dims(2, 3, 64)
+    assert rb.recblr_model_param_count(rb.model_dims(2, 3, 48)) == 0        # D not 64/128/256
+    assert rb.recblr_model_param_count(rb.model_dims(2, 3, 64, K=5)) == 0
+    assert rb.recblr_model_param_count(rb.model_dims(2, 3, 64, E=17)) == 0   # E*D > 1024
+    assert rb.recblr_model_param_offsets(rb.model_dims(0, 3, 64), None, 0) == -1
+    step = lambda m, params=addr(0), ids=addr(1), grads=addr(3), ws=addr(5), nws=1 << 40: \
+        rb.recblr_model_train_step(ctypes.byref(m), params, ids, addr(2), grads, addr(4), ws, nws,
+                                   addr(6), None)
+    assert step(rb.model_dims(2, 3, 48)) == rb.ERR_UNSUPPORTED
+    assert step(ok, params=None) == rb.ERR_INVALID_ARGUMENT
+    assert step(ok, params=addr(0) + 4) == rb.ERR_INVALID_ARGUMENT          # not 256-aligned
+    assert step(ok, grads=addr(0)) == rb.ERR_INVALID_ARGUMENT               # grads over params
+    assert rb.recblr_adam_update(addr(0), addr(1), addr(2), addr(3), 10, 0, 1e-3, 0.9, 0.999,
+                                 1e-8, None) == rb.ERR_INVALID_ARGUMENT    # step < 1
+    assert rb.recblr_adam_update(addr(0), addr(0), addr(2), addr(3), 10, 1, 1e-3, 0.9, 0.999,
+                                 1e-8, None) == rb.ERR_INVALID_ARGUMENT    # grads == params
 

@@ -1,0 +1,124 @@
+"""GPU parity of the full RecBLR model training step (recblr_model_train_step,
+recblr_adam_update) against the fp64 oracle of oracle/model.py.
+
+Every gradient tensor is compared with the floored relative error of the
+other parity tests at the fp32 bar (1e-4).
+"""
+import numpy as np
+import pytest
+
+from helpers import assert_close
+from oracle import model as om
+from paper_2406_12580_amd import datagen as dg
+
+pytestmark = pytest.mark.gpu
+
+CASES = [dg.MODEL_CONFIGS["ml1m-small"],
+         dg.ModelDims(B=2, T=5, D=128, E=1, V=37, layers=1, K=2, eps=1e-5),
+         dg.ModelDims(B=3, T=70, D=64, E=3, V=300, layers=3, K=4, eps=1e-6),
+         # 8,320 rows: weight gradients in chunks of 4,096 rows plus a remainder;
+         # popular items span several 256-position pieces of the embedding gradient
+         dg.ModelDims(B=64, T=130, D=64, E=2, V=500, layers=1, K=4)]
+
+
+@pytest.fixture(scope="module")
+def rb():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2406_12580_amd import recblr
+    return recblr
+
+
+def _device_params(rb, dims, named):
+    import torch
+    rd = rb.model_dims(dims.B, dims.T, dims.D, dims.E, dims.V, dims.layers, dims.K, dims.eps)
+    offs = rb.model_param_offsets(rd)
+    lay, total = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
+    flat = np.zeros(rb.recblr_model_param_count(rd), dtype=np.float32)
+    for (name, shape, _), o in zip(lay, offs):
+        flat[o:o + int(np.prod(shape))] = named[name].ravel()
+    return rd, torch.from_numpy(flat).cuda(), flat
+
+
+def _oracle_flat(dims, named):
+    lay, total = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
+    flat = np.zeros(total)
+    for n, s, o in lay:
+        flat[o:o + int(np.prod(s))] = named[n].astype(np.float64).ravel()
+    return flat, lay
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_model_train_step(rb, case):
+    import torch
+    dims = CASES[case]
+    named = dg.model_params(dims, 700 + case)
+    ids, targets = dg.model_batch(dims, 800 + case)
+    rd, P, _ = _device_params(rb, dims, named)
+    step = rb.ModelStep(rd)
+    I, Tg = torch.from_numpy(ids).cuda(), torch.from_numpy(targets).cuda()
+    loss, grads = step.train_step(P, I, Tg)
+    loss2, grads2 = step.train_step(P, I, Tg)
+    torch.cuda.synchronize()
+    print(f"model step {dims}: GPU done", flush=True)
+    g = grads.cpu().numpy()
+    assert np.array_equal(g.view(np.uint32), grads2.cpu().numpy().view(np.uint32)), \
+        "gradients must repeat bitwise"
+    assert loss.item() == loss2.item()
+    flat, lay = _oracle_flat(dims, named)
+    want_loss, want = om.train_step(flat, ids, targets, dims.D, dims.E, dims.V, dims.layers,
+                                    dims.K, dims.eps)
+    assert abs(loss.item() - want_loss) <= 1e-4 * abs(want_loss), (loss.item(), want_loss)
+    offs = rb.model_param_offsets(rd)
+    for (name, shape, o_ref), o in zip(lay, offs):
+        n = int(np.prod(shape))
+        assert_close(g[o:o + n], want[o_ref:o_ref + n], "f32", name)
+    # padding between tensors stays zero
+    mask = np.ones(g.size, dtype=bool)
+    for (name, shape, _), o in zip(lay, offs):
+        mask[o:o + int(np.prod(shape))] = False
+    assert not g[mask].any()
+    step.close()
+
+
+def test_adam_update(rb):
+    import torch
+    rng = np.random.default_rng(5)
+    n = 1000
+    p, g = rng.standard_normal(n).astype(np.float32), rng.standard_normal(n).astype(np.float32)
+    m1, m2 = (rng.standard_normal(n) * 0.1).astype(np.float32), \
+        np.abs(rng.standard_normal(n) * 0.01).astype(np.float32)
+    P, G, M1, M2 = (torch.from_numpy(a.copy()).cuda() for a in (p, g, m1, m2))
+    rb.adam_update(P, G, M1, M2, 7, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8)
+    torch.cuda.synchronize()
+    pr, m1r, m2r = (a.astype(np.float64) for a in (p, m1, m2))
+    # the hyper-parameters the library received: their float32 values, widened exactly
+    f = lambda v: float(np.float32(v))
+    om.adam(pr, g.astype(np.float64), m1r, m2r, 7, lr=f(1e-3), beta1=f(0.9), beta2=f(0.999),
+            eps=f(1e-8))
+    # fp32 against fp64: each result within a few ulp of its largest operand
+    # (|p| below 4, |0.9 m1| and |0.1 g| below 0.4, m2 below 0.05).
+    ulp = 2.0 ** -23
+    np.testing.assert_allclose(P.cpu().numpy(), pr, rtol=8 * ulp, atol=4 * 4 * ulp)
+    np.testing.assert_allclose(M1.cpu().numpy(), m1r, rtol=8 * ulp, atol=4 * 0.4 * ulp)
+    np.testing.assert_allclose(M2.cpu().numpy(), m2r, rtol=8 * ulp, atol=4 * 0.05 * ulp)
+
+
+def test_out_of_range_ids_give_nan_loss(rb):
+    """An item id or target outside [0, V) is read as row 0 and makes the loss NaN."""
+    import torch
+    dims = dg.ModelDims(B=2, T=6, D=64, E=2, V=50, layers=1, K=4, eps=1e-5)
+    named = dg.model_params(dims, 9)
+    ids, targets = dg.model_batch(dims, 10)
+    rd, P, _ = _device_params(rb, dims, named)
+    step = rb.ModelStep(rd)
+    bad_ids = ids.copy()
+    bad_ids[1, 3] = dims.V
+    loss, _ = step.train_step(P, torch.from_numpy(bad_ids).cuda(), torch.from_numpy(targets).cuda())
+    bad_t = targets.copy()
+    bad_t[0] = -1
+    loss2, _ = step.train_step(P, torch.from_numpy(ids).cuda(), torch.from_numpy(bad_t).cuda())
+    torch.cuda.synchronize()
+    assert np.isnan(loss.item()) and np.isnan(loss2.item())
+    step.close()
