@@ -75,10 +75,9 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
 }
 
-template <typename T, int VEC, typename Off>
-__device__ __forceinline__ void load_vec(const T* p, Off off_bytes, float (&out)[VEC]) {
-    using V = typename VecT<T, VEC>::type;
-    V v = __builtin_nontemporal_load((const V*)((const char*)p + off_bytes));
+// Widen a raw VEC-element access to fp32.
+template <typename T, int VEC>
+__device__ __forceinline__ void unpack_vec(typename VecT<T, VEC>::type v, float (&out)[VEC]) {
     if constexpr (sizeof(T) == 4) {
         if constexpr (VEC == 1) out[0] = v;
         else {
@@ -96,6 +95,19 @@ __device__ __forceinline__ void load_vec(const T* p, Off off_bytes, float (&out)
         out[2] = bf16_lo(v[1]);
         out[3] = bf16_hi(v[1]);
     }
+}
+
+// One lane's VEC elements as they are in memory (bf16 pairs stay packed, so
+// a register holds two of them until they are used).
+template <typename T, int VEC, typename Off>
+__device__ __forceinline__ typename VecT<T, VEC>::type load_raw(const T* p, Off off_bytes) {
+    using V = typename VecT<T, VEC>::type;
+    return __builtin_nontemporal_load((const V*)((const char*)p + off_bytes));
+}
+
+template <typename T, int VEC, typename Off>
+__device__ __forceinline__ void load_vec(const T* p, Off off_bytes, float (&out)[VEC]) {
+    unpack_vec<T, VEC>(load_raw<T, VEC>(p, off_bytes), out);
 }
 
 template <typename T, int VEC, typename Off>

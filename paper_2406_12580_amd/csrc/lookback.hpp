@@ -72,6 +72,44 @@ __device__ __forceinline__ uint64_t wait_ready(const uint64_t* p, uint64_t w) {
     return w;
 }
 
+// Carry from the state words of tiles r-1 .. r-N of one channel (wd[i] is
+// tile r-1-i, all ready): starting from the nearest inclusive state, the
+// aggregates after it are applied oldest first.  If none of the N is
+// inclusive, waits (bounded) for tile r-N's inclusive state at `oldest`.
+// Unrolled with selects: no dynamic indexing, no branches but the wait.
+template <int N>
+__device__ __forceinline__ float fold_window(uint64_t (&wd)[N], const uint64_t* oldest) {
+    int nearest = N;
+#pragma unroll
+    for (int i = N - 1; i >= 0; --i)
+        if (word_inclusive(wd[i])) nearest = i;
+    if (nearest == N) {
+        // None of the N is inclusive yet: wait for the oldest to be.  (Waiting
+        // for tile r-1 instead would chain the tiles one after another
+        // whenever more than N tile rows are in flight.)
+        uint64_t w = wd[N - 1];
+        int spins = 0;
+        while (!word_inclusive(w)) {
+            if (++spins > kSpinLimit) {
+                w = pack_inclusive(__uint_as_float(0x7FC00000u));
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+            w = peek(oldest);
+        }
+        wd[N - 1] = w;
+        nearest = N - 1;
+    }
+    float v = 0.0f;
+#pragma unroll
+    for (int i = N - 1; i >= 0; --i) {
+        const Seg e = word_aggregate(wd[i]);
+        const float f = fmaf(e.A, v, e.H);
+        v = i == nearest ? word_value(wd[i]) : (i < nearest ? f : v);
+    }
+    return v;
+}
+
 // Carry into tile r (tile index in processing order) from the state words of
 // tiles < r, bitwise reproducibly.
 //
@@ -85,8 +123,10 @@ __device__ __forceinline__ uint64_t wait_ready(const uint64_t* p, uint64_t w) {
 // All W waves call this.  Wave q reads the window of tiles
 // r-1-q*K .. r-q*K-K (waiting until each word is ready) into LDS; wave 0
 // then finds the nearest inclusive state and applies the aggregates after it.
-// If the W*K tiles read hold no inclusive state, wave 0 waits for tile r-1's
-// own inclusive state instead.  Tiles before tile 0 stand for `init`.
+// If the W*K tiles read hold no inclusive state, wave 0 waits for the oldest
+// of them, tile r-W*K, to publish its inclusive state, and folds the others
+// onto it; so a tile never waits on the tile right before it, and the chain
+// of waits advances W*K tiles at a time.  Tiles before tile 0 stand for `init`.
 // Leaves the carry of every lane in carry_sh.
 template <int W, int VEC, int K>
 __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ states, int64_t nch,
@@ -115,36 +155,10 @@ __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ stat
     if (w == 0) {
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
-            int nearest = -1;
-            for (int i = 0; i < W * K; ++i) {
-                if (word_inclusive(win_sh[i][lane][k])) {
-                    nearest = i;
-                    break;
-                }
-            }
-            float v;
-            if (nearest >= 0) {
-                v = word_value(win_sh[nearest][lane][k]);
-                for (int i = nearest - 1; i >= 0; --i) {
-                    const Seg e = word_aggregate(win_sh[i][lane][k]);
-                    v = fmaf(e.A, v, e.H);
-                }
-            } else {
-                // No inclusive state among the W*K nearest tiles: wait for tile r-1's.
-                const uint64_t* src = states + (r - 1) * nch + c0 + k;
-                uint64_t wd = peek(src);
-                int spins = 0;
-                while (!word_ready(wd) || !word_inclusive(wd)) {
-                    if (++spins > kSpinLimit) {
-                        wd = pack_inclusive(__uint_as_float(0x7FC00000u));
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                    wd = peek(src);
-                }
-                v = word_value(wd);
-            }
-            carry_sh[lane][k] = v;
+            uint64_t wd[W * K];
+#pragma unroll
+            for (int i = 0; i < W * K; ++i) wd[i] = win_sh[i][lane][k];
+            carry_sh[lane][k] = fold_window<W * K>(wd, states + (r - W * K) * nch + c0 + k);
         }
     }
 }

@@ -105,17 +105,44 @@ struct BwdIn {
     }
 };
 
-// Per-step pieces of the reverse recurrence: r_t, alpha_t, and the pair
-// (alpha_{t+1}, G_t) (identity (1, 0) past the end; alpha_{L+1} = 0).
-template <int C, int VEC>
+// Step pairs are stored for fp32 I/O and formed on use for bf16 I/O (the
+// faster choice for each on MI355X).
+template <typename TX>
+constexpr bool kKeepPairs = sizeof(TX) == 4;
+
+// Per-step pieces of the reverse recurrence kept in registers: r_t and
+// alpha_t of every step of the chunk, alpha of the step right after it, and
+// the pair (alpha_{t+1}, G_t) of every step (identity (1, 0) past the end,
+// alpha_{L+1} = 0, dhT added at t = L-1).  With KEEP the pairs are stored
+// once; without, each is formed where it is used, which saves two registers
+// per step (bf16 I/O: 126 instead of 160 VGPRs at 12 steps per wave, so two
+// 8-wave workgroups fit on a compute unit).
+template <int C, int VEC, bool KEEP>
 struct BwdSteps {
-    float r[C][VEC], al[C][VEC], ap[C][VEC], gg[C][VEC];
+    float r[C][VEC], al[C][VEC], al_after[VEC], dhT[VEC];
+    float ap[KEEP ? C : 1][VEC], gg[KEEP ? C : 1][VEC];
+    int64_t t_first, L;
+
+    template <bool FULL>
+    __device__ __forceinline__ Seg form_pair(const float (&g)[VEC], int j, int k) const {
+        const float nxt = j + 1 < C ? al[j + 1 < C ? j + 1 : j][k] : al_after[k];
+        if (FULL) return Seg{nxt, g[k]};
+        const int64_t t = t_first + j;
+        const float gj = g[k] + (t == L - 1 ? dhT[k] : 0.0f);
+        return Seg{t < L ? (t + 1 < L ? nxt : 0.0f) : 1.0f, t < L ? gj : 0.0f};
+    }
+    template <bool FULL>
+    __device__ __forceinline__ Seg pair(const float (&g)[VEC], int j, int k) const {
+        if constexpr (KEEP) return Seg{ap[KEEP ? j : 0][k], gg[KEEP ? j : 0][k]};
+        else return form_pair<FULL>(g, j, k);
+    }
 };
 
-template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off>
+template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off, bool KEEP>
 __device__ __forceinline__ void form_bwd(const BwdIn<TX, TZ, C, VEC, Off>& in,
                                          const ChannelConst (&cc)[VEC], const float (&dhTv)[VEC],
-                                         int64_t t_first, int64_t L, BwdSteps<C, VEC>& st) {
+                                         int64_t t_first, int64_t L,
+                                         BwdSteps<C, VEC, KEEP>& st) {
 #pragma unroll
     for (int j = 0; j < C; ++j)
 #pragma unroll
@@ -124,41 +151,41 @@ __device__ __forceinline__ void form_bwd(const BwdIn<TX, TZ, C, VEC, Off>& in,
             st.al[j][k] = fast_exp2(st.r[j][k] * cc[k].neg_s_l2);
         }
 #pragma unroll
-    for (int j = 0; j < C; ++j) {
-        const int64_t t = t_first + j;
+    for (int k = 0; k < VEC; ++k) {
+        st.al_after[k] = fast_exp2(sigmoid(in.zr_after[k]) * cc[k].neg_s_l2);
+        st.dhT[k] = dhTv[k];
+    }
+    st.t_first = t_first;
+    st.L = L;
+    if constexpr (KEEP) {
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            float nxt = j + 1 < C ? st.al[j + 1 < C ? j + 1 : j][k]
-                                  : fast_exp2(sigmoid(in.zr_after[k]) * cc[k].neg_s_l2);
-            if (FULL) {
-                st.ap[j][k] = nxt;
-                st.gg[j][k] = in.g[j][k];
-            } else {
-                if (t + 1 >= L) nxt = 0.0f;
-                const float gj = in.g[j][k] + (t == L - 1 ? dhTv[k] : 0.0f);
-                st.ap[j][k] = t < L ? nxt : 1.0f;
-                st.gg[j][k] = t < L ? gj : 0.0f;
+        for (int j = 0; j < C; ++j)
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const Seg p = st.template form_pair<FULL>(in.g[j], j, k);
+                st.ap[KEEP ? j : 0][k] = p.A;
+                st.gg[KEEP ? j : 0][k] = p.H;
             }
-        }
     }
 }
 
-template <int C, int VEC>
-__device__ __forceinline__ void local_reverse(const BwdSteps<C, VEC>& st, Seg (&s)[VEC]) {
+template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off, bool KEEP>
+__device__ __forceinline__ void local_reverse(const BwdIn<TX, TZ, C, VEC, Off>& in,
+                                              const BwdSteps<C, VEC, KEEP>& st, Seg (&s)[VEC]) {
 #pragma unroll
     for (int k = 0; k < VEC; ++k) {
         s[k] = Seg{1.0f, 0.0f};
 #pragma unroll
-        for (int j = C - 1; j >= 0; --j) s[k] = compose(Seg{st.ap[j][k], st.gg[j][k]}, s[k]);
+        for (int j = C - 1; j >= 0; --j) s[k] = compose(st.template pair<FULL>(in.g[j], j, k), s[k]);
     }
 }
 
 // Run the chunk backwards from delta (the adjoint right after the chunk) and
 // apply the gate-gradient epilogue to every step before L.
-template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off>
+template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off, bool KEEP>
 __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
                                          const BwdIn<TX, TZ, C, VEC, Off>& in,
-                                         const BwdSteps<C, VEC>& st,
+                                         const BwdSteps<C, VEC, KEEP>& st,
                                          const ChannelConst (&cc)[VEC], int64_t t_first,
                                          float (&delta)[VEC], float (&dsum)[VEC]) {
 #pragma unroll
@@ -167,7 +194,8 @@ __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, V
         float dxv[VEC], dzrv[VEC], dziv[VEC];
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
-            delta[k] = fmaf(st.ap[j][k], delta[k], st.gg[j][k]);
+            const Seg pj = st.template pair<FULL>(in.g[j], j, k);
+            delta[k] = fmaf(pj.A, delta[k], pj.H);
             const float r = st.r[j][k], al = st.al[j][k];
             const float i = sigmoid(in.zi[j][k]);
             const float q = r * cc[k].s;
@@ -238,10 +266,10 @@ __device__ __forceinline__ void chain_bwd_step(const BwdParams& P, const BwdLane
                                                Seg (&agg)[W][kWave][VEC], int64_t tw, int w,
                                                int lane, float (&carry)[VEC],
                                                float (&dsum)[VEC]) {
-    BwdSteps<C, VEC> st;
+    BwdSteps<C, VEC, kKeepPairs<TX>> st;
     form_bwd<FULL>(cur, cc, dhTv, tw, P.L, st);
     Seg s[VEC];
-    local_reverse(st, s);
+    local_reverse<FULL>(cur, st, s);
 #pragma unroll
     for (int k = 0; k < VEC; ++k) agg[w][lane][k] = s[k];
     __syncthreads();
@@ -368,7 +396,7 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     const int64_t tw = s * W * C + (int64_t)w * C;
     const bool full = s > 0 && (s + 1) * W * C < P.L;  // workgroup-uniform
     BwdIn<TX, TZ, C, VEC, Off> in;
-    BwdSteps<C, VEC> st;
+    BwdSteps<C, VEC, kKeepPairs<TX>> st;
     if (full) {
         in.template fetch<true>(P, ln, h0v, tw);
         form_bwd<true>(in, cc, dhTv, tw, P.L, st);
@@ -378,7 +406,8 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     }
     {
         Seg sg[VEC];
-        local_reverse(st, sg);
+        if (full) local_reverse<true>(in, st, sg);
+        else local_reverse<false>(in, st, sg);
 #pragma unroll
         for (int k = 0; k < VEC; ++k) agg[w][lane][k] = sg[k];
     }
@@ -523,7 +552,15 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
 #define RECBLR_BWD_LB_MAX_VEC 1
 #endif
 constexpr int kChainW = RECBLR_BWD_CHAIN_W, kChainE = RECBLR_BWD_CHAIN_E;
-constexpr int kLbW = RECBLR_BWD_LB_W, kLbE = RECBLR_BWD_LB_E;
+// bf16 I/O takes 12 steps per wave: with the step pairs formed on use that is
+// 126 VGPRs, two workgroups per compute unit (16 x 16384 x 256 backward:
+// 222 us against 255 us at 16 steps); fp32 I/O keeps 16 (256 x 2048 x 128:
+// 370 us against 410 us at 12).
+#ifndef RECBLR_BWD_LB_E_BF16
+#define RECBLR_BWD_LB_E_BF16 12
+#endif
+constexpr int kLbW = RECBLR_BWD_LB_W;
+constexpr int lb_elems(size_t esz) { return esz == 2 ? RECBLR_BWD_LB_E_BF16 : RECBLR_BWD_LB_E; }
 // Look-back window per wave: K tiles, K * VEC state words per lane.
 #ifndef RECBLR_BWD_LB_WORDS
 #define RECBLR_BWD_LB_WORDS 1
@@ -533,7 +570,9 @@ constexpr int lb_window() { return RECBLR_BWD_LB_WORDS / VEC > 0 ? RECBLR_BWD_LB
 template <int E, int VEC>
 constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
 // Steps of one look-back tile for a given VEC.
-constexpr int64_t lb_tile_steps(int vec) { return (int64_t)kLbW * (kLbE / vec > 0 ? kLbE / vec : 1); }
+constexpr int64_t lb_tile_steps(size_t esz, int vec) {
+    return (int64_t)kLbW * (lb_elems(esz) / vec > 0 ? lb_elems(esz) / vec : 1);
+}
 // Lanes of the chain kernel take as many channels as keep this many
 // workgroups (one per compute unit).
 constexpr int64_t kChainMinGroups = 256;
@@ -562,7 +601,7 @@ struct BwdPlan {
 // forward launcher).
 static bool backward_uses_lookback(int64_t B, int64_t L, int64_t D, size_t esz) {
     const int64_t groups_one = (B * D + kWave - 1) / kWave;
-    return groups_one < kLookbackBelowGroups && L > lb_tile_steps(max_vec(esz, true));
+    return groups_one < kLookbackBelowGroups && L > lb_tile_steps(esz, max_vec(esz, true));
 }
 
 static BwdPlan plan_backward(int64_t B, int64_t L, int64_t D, size_t esz, int vec) {
@@ -570,7 +609,7 @@ static BwdPlan plan_backward(int64_t B, int64_t L, int64_t D, size_t esz, int ve
     p.vec = vec;
     p.lookback = backward_uses_lookback(B, L, D, esz);
     p.ngroups = (B * D / vec + kWave - 1) / kWave;
-    p.nseg = p.lookback ? (L + lb_tile_steps(vec) - 1) / lb_tile_steps(vec) : 1;
+    p.nseg = p.lookback ? (L + lb_tile_steps(esz, vec) - 1) / lb_tile_steps(esz, vec) : 1;
     return p;
 }
 
@@ -623,7 +662,7 @@ static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStr
     }
     if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
     if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
-    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(), VEC,
+    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<lb_elems(sizeof(TX)), VEC>(), VEC,
                                                  lb_window<VEC>(), Off>),
                        dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0, stream,
                        P);
