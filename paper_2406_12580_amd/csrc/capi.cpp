@@ -83,7 +83,11 @@ FullFwdLayout full_fwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     l.zi = zbytes;
     l.pack = 2 * zbytes;
     l.scan = l.pack + align_up(project_pack_workspace(D, io_of(io)));
-    l.total = l.scan + align_up(scan_forward_workspace(B, L, D, io_of(io)));
+    // The scan part serves either the scan after the projections or the
+    // fused kernel (D % 64 == 0), whichever the call takes.
+    const size_t scan = scan_forward_workspace(B, L, D, io_of(io));
+    const size_t fused = D % 64 == 0 ? fused_forward_workspace(B, L, D) : 0;
+    l.total = l.scan + align_up(scan > fused ? scan : fused);
     return l;
 }
 

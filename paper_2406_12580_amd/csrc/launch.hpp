@@ -78,6 +78,8 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream);
 // workspace.
 bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
                            const void* pack);
+// Look-back workspace of the fused forward (0 for empty shapes).
+size_t fused_forward_workspace(int64_t B, int64_t L, int64_t D);
 hipError_t launch_fused_forward(const void* x, const void* pack, const void* br, const void* bi,
                                 const float* lambda, const float* h0, void* h, float* hT,
                                 int64_t B, int64_t L, int64_t D, IoType io, void* ws,

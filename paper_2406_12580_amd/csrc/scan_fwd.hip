@@ -706,10 +706,25 @@ hipError_t launch_scan_forward(const ScanFwdArgs& a, hipStream_t stream) {
 bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
                            const void* pack) {
     const size_t esz = io_bytes(io);
-    return B > 0 && D > 0 && D % kWave == 0 && forward_uses_lookback(B, L, D, esz) &&
-           lb_tile_steps(1) == (int64_t)fusedfwd::W * fusedfwd::C &&
+    return B > 0 && L > 0 && D > 0 && D % kWave == 0 &&
            ((uintptr_t)x | (uintptr_t)pack) % 16 == 0 &&
            (L + fastmm::BM) * D * (int64_t)esz < ((int64_t)1 << 31);
+}
+
+// Tiles of the fused forward: 64 channels x 128 steps, in tile rows along L.
+static FwdPlan plan_fused(int64_t B, int64_t L, int64_t D) {
+    constexpr int64_t kSteps = (int64_t)fusedfwd::W * fusedfwd::C;
+    FwdPlan p;
+    p.lookback = true;
+    p.vec = 1;
+    p.ngroups = (B * D + kWave - 1) / kWave;
+    p.nseg = (L + kSteps - 1) / kSteps;
+    return p;
+}
+
+size_t fused_forward_workspace(int64_t B, int64_t L, int64_t D) {
+    if (B <= 0 || L <= 0 || D <= 0) return 0;
+    return lookback_ws_bytes(plan_fused(B, L, D).nseg, B * D);
 }
 
 template <bool GATED>
@@ -718,7 +733,7 @@ static hipError_t launch_fused_t(const void* x, const void* pack, const void* br
                                  int64_t B, int64_t L, int64_t D, IoType io, void* ws,
                                  const fusedfwd::GatedArgs& G, hipStream_t stream) {
     const size_t esz = io_bytes(io);
-    const FwdPlan plan = plan_forward(B, L, D, esz, 1);
+    const FwdPlan plan = plan_fused(B, L, D);
     FwdParams P{x, nullptr, nullptr, lambda, h0, h, hT, L, D, B * D, plan.ngroups, plan.nseg,
                 lookback_ws(ws)};
     hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
