@@ -103,7 +103,11 @@ FullBwdLayout full_bwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     l.dzi = 3 * zbytes;
     l.pack = 4 * zbytes;
     l.scan = l.pack + align_up(project_pack_workspace(D, io_of(io)));
-    l.dw = l.scan + align_up(scan_backward_workspace(B, L, D, io_of(io)));
+    // The scan part serves either the scan after the projection or the fused
+    // kernel (D % 64 == 0), whichever the call takes.
+    const size_t scan = scan_backward_workspace(B, L, D, io_of(io));
+    const size_t fused = D % 64 == 0 ? fused_backward_workspace(B, L, D) : 0;
+    l.dw = l.scan + align_up(scan > fused ? scan : fused);
     l.total = l.dw + align_up(project_dw_workspace(B * L, D));
     return l;
 }
@@ -551,12 +555,21 @@ int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const
         return RECBLR_OK;
     }
     const int64_t M = B * L;
-    e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, M, D, io_of(io), at(ws, lay.pack),
-                               strm);
-    if (e != hipSuccess) return RECBLR_ERR_HIP;
-    ScanBwdArgs a{x, zr, zi, lambda, h0, h, dh, dhT, dx, dzr, dzi, dlambda, dh0,
-                  B, L, D, io_of(io), IoType::kF32, at(ws, lay.scan), lay.dw - lay.scan};
-    e = launch_scan_backward(a, strm);
+    void* pack = at(ws, lay.pack);
+    if (L > 0 && fused_backward_applies(B, L, D, io_of(io), x, pack)) {
+        // The scan backward recomputes z on the matrix cores (z never reaches HBM).
+        if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
+            return RECBLR_ERR_HIP;
+        const FusedBwdArgs fa{x,  pack, b_r, b_i, lambda, h0, h, dh, dhT, dx, (float*)dzr,
+                              (float*)dzi, dlambda, dh0, B, L, D, io_of(io), at(ws, lay.scan)};
+        e = launch_fused_backward(fa, strm);
+    } else {
+        e = launch_project_forward(x, W_r, b_r, W_i, b_i, zr, zi, M, D, io_of(io), pack, strm);
+        if (e != hipSuccess) return RECBLR_ERR_HIP;
+        ScanBwdArgs a{x, zr, zi, lambda, h0, h, dh, dhT, dx, dzr, dzi, dlambda, dh0,
+                      B, L, D, io_of(io), IoType::kF32, at(ws, lay.scan), lay.dw - lay.scan};
+        e = launch_scan_backward(a, strm);
+    }
     if (e != hipSuccess) return RECBLR_ERR_HIP;
     e = launch_project_backward_data(dzr, dzi, W_r, W_i, dx, M, D, io_of(io), at(ws, lay.pack),
                                      strm);

@@ -89,6 +89,34 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
 // x, z, h share the I/O type): a serial scan (one wave per 64 channels walks
 // the sequence) and the two-tree scan over the power of two >= L with the
 // leading positions as identity (embedding padding), L <= 4096.
+// Layer backward's scan with the gate projections recomputed inside
+// (scan_bwd_fused_kernel): x, weights packed by channel group
+// (launch_pack_groups), biases (may be null); dx in the I/O type, dz_r and
+// dz_i in fp32, [B][L][D].
+struct FusedBwdArgs {
+    const void* x;
+    const void* pack;
+    const void* br;
+    const void* bi;
+    const float* lambda;
+    const float* h0;
+    const void* h;
+    const void* dh;
+    const float* dhT;
+    void* dx;
+    float* dzr;
+    float* dzi;
+    float* dlambda;
+    float* dh0;
+    int64_t B, L, D;
+    IoType io;
+    void* ws;
+};
+bool fused_backward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
+                            const void* pack);
+size_t fused_backward_workspace(int64_t B, int64_t L, int64_t D);
+hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream);
+
 hipError_t launch_scan_forward_serial(const ScanFwdArgs& a, hipStream_t stream);
 hipError_t launch_scan_forward_tree(const ScanFwdArgs& a, hipStream_t stream);
 bool tree_scan_supported(int64_t L);

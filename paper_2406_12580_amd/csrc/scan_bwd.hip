@@ -23,6 +23,7 @@
 // the end too, so that tile index r in processing order is macro-chunk
 // nseg-1-r and the forward look-back code applies unchanged.
 #include "device_common.hpp"
+#include "fused_z.hpp"
 #include "launch.hpp"
 #include "lookback.hpp"
 
@@ -457,6 +458,171 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     write_partial<W, VEC>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
 }
 
+// ------------------------------------------------------------------ projections fused in
+// The layer backward's scan: a look-back kernel that recomputes its own gate
+// pre-activations on the matrix cores (fused_z.hpp) instead of reading z, so
+// the layer backward does not project x once more through HBM.  The adjoint
+// runs in the form
+//   eps_t = alpha_t (G_t + eps_{t+1}),   eps_L = dhT,   delta_t = G_t + eps_{t+1},
+// (eps_t = alpha_t delta_t is what flows from step t into h_{t-1}), whose
+// per-step pair (alpha_t, alpha_t G_t) belongs to step t alone: a tile needs
+// no z of the step after it.  dh0 = eps_0.  The epilogue is that of emit_bwd.
+// x: [B][L][D] I/O type; dx is written in the I/O type, dz_r, dz_i in fp32.
+// A wave's C rows (steps) of its 64 channels of one tensor, staged into LDS
+// with 16-byte direct-to-LDS loads (the channels of a wave are contiguous
+// because D % 64 == 0): step j of lane l lands at ((T*)dst)[j * 64 + l].
+// Rows are t_first + shift + j, clamped to [0, L-1].
+template <typename T, int C>
+__device__ __forceinline__ void stage_rows(const T* tensor, int64_t b, int64_t L, int64_t D,
+                                           int64_t dg, int64_t t_first, int shift, char* dst,
+                                           int lane) {
+    constexpr int kRow = kWave * (int)sizeof(T);  // bytes of one step's 64 channels
+    constexpr int kLanesPerRow = kRow / 16;
+    constexpr int kRowsPerLoad = kWave / kLanesPerRow;
+    static_assert(C % kRowsPerLoad == 0, "whole loads per wave");
+    const int64_t col = (int64_t)(lane % kLanesPerRow) * (16 / (int)sizeof(T));
+#pragma unroll
+    for (int i = 0; i < C / kRowsPerLoad; ++i) {
+        int64_t t = t_first + shift + i * kRowsPerLoad + lane / kLanesPerRow;
+        t = t < 0 ? 0 : (t < L ? t : L - 1);
+        const T* gp = tensor + (b * L + t) * D + dg + col;
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)gp,
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                         16, 0, 0);
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ float lds_elem(const char* base, int idx) {
+    if constexpr (sizeof(T) == 4) return ((const float*)base)[idx];
+    else return __uint_as_float((uint32_t)((const uint16_t*)base)[idx] << 16);
+}
+
+template <typename T, int K, typename Off>
+__global__ __launch_bounds__(fusedz::NT, 4) void
+scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi) {
+    constexpr int W = fusedz::W, C = fusedz::C;
+    __shared__ __attribute__((aligned(16))) char smem[fusedz::Tile<T>::kSmem];
+    __shared__ Seg agg[W][kWave][1];
+    __shared__ uint64_t win_sh[W * K][kWave][1];
+    __shared__ float carry_sh[kWave][1];
+    __shared__ float red[W][kWave][1];
+    __shared__ int64_t tile_sh;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int w = wave_id();
+    if (tid == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
+    __syncthreads();
+    const int64_t tile = tile_sh;
+    if (tile >= P.ngroups * P.nseg) return;  // only if the workspace was shared by two calls
+    const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
+    const int64_t g = tile - r * P.ngroups;
+    const int64_t s = P.nseg - 1 - r;    // tile row along L
+    const int64_t gpr = P.D / kWave;      // channel groups per batch row
+    const int64_t b = g / gpr, cg = g - b * gpr;
+    const int64_t t0 = s * W * C;
+    float zr[C], zi[C];
+    fusedz::tile_z<T>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, t0, smem, tid, w, lane, zr,
+                      zi);
+
+    BwdLane<T, 1, Off> ln;
+    ln.init(g, lane, P.L, P.D, P.nch);
+    ChannelConst cc[1];
+    float h0v[1], dhTv[1];
+    bwd_lane_consts<1>(P, ln.c0, ln.d0, cc, h0v, dhTv);
+    const int64_t tw = t0 + (int64_t)w * C;
+    const bool full = s > 0 && (s + 1) * W * C <= P.L;  // workgroup-uniform
+    // x and h_{t-1} are only needed in the epilogue: they wait in LDS (the
+    // staging area of the product is free once every wave holds its z), not
+    // in registers.
+    __syncthreads();
+    constexpr int kStaged = C * kWave * (int)sizeof(T);  // one tensor's rows of a wave
+    static_assert(2 * W * kStaged <= (int)fusedz::Tile<T>::kSmem, "staging fits");
+    char* const xs = smem + w * 2 * kStaged;
+    char* const hs = xs + kStaged;
+    stage_rows<T, C>((const T*)P.x, b, P.L, P.D, cg * kWave, tw, 0, xs, lane);
+    stage_rows<T, C>((const T*)P.h, b, P.L, P.D, cg * kWave, tw, -1, hs, lane);
+    float gv[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        const int64_t t = tw + j < P.L ? tw + j : P.L - 1;
+        float v[1];
+        load_vec<T, 1>((const T*)P.dh, ln.at(t), v);
+        gv[j] = v[0];
+    }
+    float rr[C], al[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        rr[j] = sigmoid(zr[j]);
+        al[j] = fast_exp2(rr[j] * cc[0].neg_s_l2);
+    }
+    {
+        Seg sg{1.0f, 0.0f};
+#pragma unroll
+        for (int j = C - 1; j >= 0; --j) {
+            const bool ok = full || tw + j < P.L;
+            sg = compose(ok ? Seg{al[j], al[j] * gv[j]} : Seg{1.0f, 0.0f}, sg);
+        }
+        agg[w][lane][0] = sg;
+    }
+    __syncthreads();
+    // pre: the waves after this one (applied first); tot: the whole tile.
+    Seg pre{1.0f, 0.0f}, tot{1.0f, 0.0f};
+#pragma unroll
+    for (int q = W - 1; q >= 0; --q) {
+        const Seg e = agg[q][lane][0];
+        if (q > w) pre = compose(e, pre);
+        tot = compose(e, tot);
+    }
+    __syncthreads();  // agg is reused below
+    uint64_t* const own = P.lb.states + r * P.nch + ln.c0;
+    if (r == 0) {
+        if (w == 0) {
+            carry_sh[lane][0] = dhTv[0];
+            if (ln.valid) publish(own, pack_inclusive(fmaf(tot.A, dhTv[0], tot.H)));
+        }
+    } else {
+        if (w == 0 && ln.valid) publish(own, pack_aggregate(tot));
+        lookback_carry<W, 1, K>(P.lb.states, P.nch, ln.c0, r, dhTv, win_sh, carry_sh, w, lane);
+        if (w == 0 && ln.valid)
+            publish(own, pack_inclusive(fmaf(tot.A, carry_sh[lane][0], tot.H)));
+    }
+    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the staged x and h rows are in LDS
+    float eps = fmaf(pre.A, carry_sh[lane][0], pre.H);
+    float dsum[1] = {0.0f};
+#pragma unroll
+    for (int j = C - 1; j >= 0; --j) {
+        const int64_t t = tw + j;
+        if (!(full || t < P.L)) continue;  // past the end: the identity
+        const float delta = gv[j] + eps;
+        const float rj = rr[j], a = al[j];
+        const float i = sigmoid(zi[j]);
+        const float q = rj * cc[0].s;
+        const float mm = one_minus_exp_neg(rj * cc[0].two_s, a);
+        const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
+        const float sq = mm * rs;  // sqrt(1 - alpha^2)
+        const float hprev = !full && t == 0 ? h0v[0] : lds_elem<T>(hs, j * kWave + lane);
+        const float g_alpha = delta * hprev;
+        const float g_beta = delta * lds_elem<T>(xs, j * kWave + lane);
+        const float g1 = -a * g_alpha;
+        const float g2 = g_beta * i * a * a;
+        dsum[0] = fmaf(g1, rj, fmaf(g2, rj * rs, dsum[0]));
+        const float dxv[1] = {delta * sq * i};
+        const float dzrv[1] = {fmaf(g1, q, g2 * (q * rs)) * (1.0f - rj)};
+        const float dziv[1] = {g_beta * sq * i * (1.0f - i)};
+        eps = a * delta;
+        if (ln.valid) {
+            const Off off = ln.at(t);
+            store_vec<T, 1>((T*)P.dx, off, dxv);
+            store_vec<float, 1>((float*)P.dzr, z_offset<T, float>(off), dzrv);
+            store_vec<float, 1>((float*)P.dzi, z_offset<T, float>(off), dziv);
+            if (!full && t == 0 && P.dh0) P.dh0[ln.c0] = eps;
+        }
+    }
+    write_partial<W, 1>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
+}
+
 // ------------------------------------------------------------------ dLambda reduction
 // dLambda[d] = sigmoid(Lambda_d) * sum_rows partial[row][d], in double and in a
 // fixed order, in two fence-free launches: block (nb, dg) of the first sums
@@ -688,6 +854,20 @@ static hipError_t launch_bwd_typed(const BwdParams& P, const BwdPlan& plan, hipS
     return launch_bwd_vec<TX, TZ, uint64_t, 1>(P, plan, stream, ev0, ev1);
 }
 
+// dLambda from the per-tile partials [rows][D]: two fixed-order launches.
+static hipError_t launch_dlambda(const float* partial, double* partial2, int64_t rows, int64_t D,
+                                 const float* lambda, float* dlambda, hipStream_t stream) {
+    const int64_t nblk = (rows + kReduceRows - 1) / kReduceRows;
+    dim3 rgrid((unsigned)nblk, (unsigned)((D + kWave - 1) / kWave));
+    hipLaunchKernelGGL(dlambda_rows_kernel, rgrid, dim3(256), 0, stream, partial, partial2, rows,
+                       D);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((D + kWave - 1) / kWave)),
+                       dim3(kWave * kFinalGroups), 0, stream, partial2, nblk, lambda, dlambda, D);
+    return hipGetLastError();
+}
+
 hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
     const BwdPlan plan = plan_backward(a.B, a.L, a.D, io_bytes(a.io), pick_vec_bwd(a));
     const BwdLayout lay = bwd_layout(a.B, a.D, plan);
@@ -705,17 +885,67 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
         e = launch_bwd_typed<bf16, float>(P, plan, stream, a.ev_begin, a.ev_end);
     else e = launch_bwd_typed<bf16, bf16>(P, plan, stream, a.ev_begin, a.ev_end);
     if (e != hipSuccess) return e;
-    const int64_t rows = plan.nseg * a.B;
-    const int64_t nblk = (rows + kReduceRows - 1) / kReduceRows;
-    dim3 rgrid((unsigned)nblk, (unsigned)((a.D + kWave - 1) / kWave));
-    hipLaunchKernelGGL(dlambda_rows_kernel, rgrid, dim3(256), 0, stream, partial, partial2, rows,
-                       a.D);
-    e = hipGetLastError();
+    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, stream);
+}
+
+// ------------------------------------------------------------------ fused backward
+static BwdPlan plan_fused_backward(int64_t B, int64_t L, int64_t D) {
+    constexpr int64_t kSteps = (int64_t)fusedz::W * fusedz::C;
+    BwdPlan p;
+    p.lookback = true;
+    p.vec = 1;
+    p.ngroups = (B * D + kWave - 1) / kWave;
+    p.nseg = (L + kSteps - 1) / kSteps;
+    return p;
+}
+
+bool fused_backward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
+                            const void* pack) {
+    const size_t esz = io_bytes(io);
+    return B > 0 && L > 0 && D > 0 && D % kWave == 0 &&
+           ((uintptr_t)x | (uintptr_t)pack) % 16 == 0 &&
+           (L + fastmm::BM) * D * (int64_t)esz < ((int64_t)1 << 31);
+}
+
+size_t fused_backward_workspace(int64_t B, int64_t L, int64_t D) {
+    if (B <= 0 || L <= 0 || D <= 0) return 0;
+    return bwd_layout(B, D, plan_fused_backward(B, L, D)).total;
+}
+
+hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
+    const BwdPlan plan = plan_fused_backward(a.B, a.L, a.D);
+    const BwdLayout lay = bwd_layout(a.B, a.D, plan);
+    char* ws = (char*)a.ws;
+    float* partial = (float*)(ws + lay.partial);
+    double* partial2 = (double*)(ws + lay.partial2);
+    const BwdParams P{a.x,  nullptr, nullptr, a.lambda, a.h0, a.h,   a.dh,  a.dhT,
+                      a.dx, a.dzr,   a.dzi,   a.dh0,    partial, a.L, a.D,  a.B * a.D,
+                      plan.ngroups, plan.nseg, lookback_ws(ws + lay.lb)};
+    hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((a.D + kWave - 1) / kWave)),
-                       dim3(kWave * kFinalGroups), 0, stream, partial2, nblk, a.lambda, a.dlambda,
-                       a.D);
-    return hipGetLastError();
+    const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedz::NT);
+    const size_t esz = io_bytes(a.io);
+    const bool small = (uint64_t)(a.B * a.L * a.D) * 4 < (1ull << 32);
+    constexpr int K = lb_window<1>();
+    if (esz == 4) {
+        if (small)
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, K, uint32_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
+                               (const float*)a.bi);
+        else
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, K, uint64_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
+                               (const float*)a.bi);
+    } else {
+        if (small)
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, K, uint32_t>), grid, block, 0, stream,
+                               P, (const __bf16*)a.pack, (const bf16*)a.br, (const bf16*)a.bi);
+        else
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, K, uint64_t>), grid, block, 0, stream,
+                               P, (const __bf16*)a.pack, (const bf16*)a.br, (const bf16*)a.bi);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, stream);
 }
 
 }  // namespace recblr

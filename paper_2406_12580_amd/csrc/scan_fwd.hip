@@ -26,6 +26,7 @@
 #include "device_common.hpp"
 #include "launch.hpp"
 #include "lookback.hpp"
+#include "fused_z.hpp"
 #include "mfma_tile.hpp"
 
 namespace recblr {
@@ -325,47 +326,12 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
 }
 
 // ------------------------------------------------------------------ projections fused in
-// Look-back kernel that computes its own gate pre-activations: the tile's
-// z = x [W_r; W_i]^T + b for 128 steps x 64 channels (both gates) is one
-// 128 x 128 matrix-core product of x[128 steps x D] and the channel group's
-// 128 packed weight rows (K = D).  Wave w computes the 16 x 128 strip of the
-// 16 steps it then scans, turns it into the lane-per-channel layout through
-// a wave-private LDS strip, and the scan proceeds as in the look-back kernel.
-// z never reaches HBM: the kernel reads x and writes h.
+// Look-back kernel that computes its own gate pre-activations (fused_z.hpp):
+// the tile's z for 128 steps x 64 channels (both gates) is one 128 x 128
+// matrix-core product, each wave receives its 16 steps in the lane-per-channel
+// layout, and the scan proceeds as in the look-back kernel.  z never reaches
+// HBM: the kernel reads x and writes h.
 namespace fusedfwd {
-constexpr int W = 8, C = 16;       // waves; steps per wave (tile = 128 steps)
-constexpr int NT = W * kWave;      // threads
-constexpr int ZP = 20;             // z strip pitch (floats) per column: 16 steps + 4
-
-// Wave w's 16 x 128 strip of the staged slices: rows 16 w .. 16 w + 15 of A,
-// all 128 rows of B, k-steps of 32 (lane l supplies row l % 16 and
-// k = 8 (l / 16) .. +7 of each fragment).
-template <int PA, int PB>
-__device__ __forceinline__ void strip_mma(__bf16 (*la)[fastmm::BM][fastmm::KP],
-                                          __bf16 (*lb)[fastmm::BN][fastmm::KP], fastmm::f4 (&acc)[8],
-                                          int w, int lane) {
-    using namespace fastmm;
-    const int fr = lane & 15, fk = 8 * (lane >> 4);
-#pragma unroll
-    for (int ks = 0; ks < BK; ks += 32) {
-        const int ra = 16 * w + fr;
-        b8 fa[PA];
-#pragma unroll
-        for (int p = 0; p < PA; ++p) fa[p] = *(const b8*)&la[p][ra][lds_col(ra, ks + fk)];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int rb = 16 * j + fr;
-            b8 fb[PB];
-#pragma unroll
-            for (int p = 0; p < PB; ++p) fb[p] = *(const b8*)&lb[p][rb][lds_col(rb, ks + fk)];
-            if constexpr (PB == 2)
-                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0], fb[1], acc[j], 0, 0, 0);
-            if constexpr (PA == 2)
-                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1], fb[0], acc[j], 0, 0, 0);
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0], fb[0], acc[j], 0, 0, 0);
-        }
-    }
-}
 // Gated-layer output (Algorithm alg:gated_recurrent, line 5): with GATED the
 // kernel stores y = h * SiLU(hz) (and h only where asked for).
 struct GatedArgs {
@@ -382,18 +348,11 @@ __device__ __forceinline__ float silu(float c) { return c * sigmoid(c); }
 // Occupancy: 3 workgroups per CU for bf16 I/O (LDS 48 KB each, 6 waves per
 // SIMD), 2 for fp32 (its split operands double the staging LDS).
 template <typename T, int K, typename Off, bool GATED>
-__global__ __launch_bounds__(fusedfwd::NT, sizeof(T) == 2 ? 6 : 4) void
+__global__ __launch_bounds__(fusedz::NT, sizeof(T) == 2 ? 6 : 4) void
 scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
                       fusedfwd::GatedArgs G) {
-    using namespace fastmm;
-    constexpr int W = fusedfwd::W, C = fusedfwd::C, NT = fusedfwd::NT, ZP = fusedfwd::ZP;
-    constexpr bool F32 = sizeof(T) == 4;
-    using OpA = Operand<F32 ? kF32 : kBf16, true>;
-    using OpB = Operand<F32 ? kPack2 : kPack1, true>;
-    constexpr int PA = OpA::kPlanes, PB = OpB::kPlanes;
-    constexpr size_t kStage = (size_t)(PA * BM + PB * BN) * KP * 2;
-    constexpr size_t kZ = (size_t)W * 64 * ZP * sizeof(float);
-    __shared__ __attribute__((aligned(16))) char smem[kStage > kZ ? kStage : kZ];
+    constexpr int W = fusedz::W, C = fusedz::C;
+    __shared__ __attribute__((aligned(16))) char smem[fusedz::Tile<T>::kSmem];
     __shared__ Seg agg[W][kWave][1];
     __shared__ uint64_t win_sh[W * K][kWave][1];
     __shared__ float carry_sh[kWave][1];
@@ -410,69 +369,9 @@ scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
     const int64_t gpr = P.D / kWave;  // channel groups per batch row
     const int64_t b = g / gpr, cg = g - b * gpr;
     const int64_t t0 = s * W * C;
-
-    // ---- z for the tile on the matrix cores (rows: steps t0.., columns: the
-    // group's 64 z_r then its 64 z_i; steps past L read as zero)
-    f4 acc[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    {
-        __bf16 (*la)[BM][KP] = (__bf16 (*)[BM][KP])smem;
-        __bf16 (*lb)[BN][KP] = (__bf16 (*)[BN][KP])(smem + (size_t)PA * BM * KP * 2);
-        const uint32_t plane = (uint32_t)(2 * P.D * P.D * 2);
-        const OpA a{resource((const T*)P.p0 + b * P.L * P.D, (uint32_t)(P.L * P.D * sizeof(T))),
-                    (uint32_t)(P.D * sizeof(T)), 0, 0, 0};
-        const OpB wb{resource(pack + cg * 128 * P.D, (PB - 1) * plane + (uint32_t)(128 * P.D * 2)),
-                     (uint32_t)(P.D * 2), 0, 0, plane};
-        const Stager<OpB, NT> sb(wb, 0, tid);
-        typename OpB::raw_t rb[quads<NT>()];
-        const int64_t nsl = (P.D + BK - 1) / BK;
-        sb.fetch(wb, 0, P.D, tid, rb);
-        constexpr int Q = quads<NT>();
-        const Stager<OpA, NT> sa(a, t0, tid);
-        typename OpA::raw_t ra[Q];
-        auto fetch_a = [&](int64_t k0) { sa.fetch(a, k0, P.D, tid, ra); };
-        auto stage_a = [&]() { store_slice<OpA, NT>(la, tid, ra); };
-        fetch_a(0);
-        for (int64_t sl = 0; sl < nsl; ++sl) {
-            stage_a();
-            store_slice<OpB, NT>(lb, tid, rb);
-            __syncthreads();
-            if (sl + 1 < nsl) {
-                fetch_a((sl + 1) * BK);
-                sb.fetch(wb, (sl + 1) * BK, P.D, tid, rb);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            fusedfwd::strip_mma<PA, PB>(la, lb, acc, w, lane);
-            __syncthreads();
-        }
-    }
-    // ---- bias, then the strip to the lane-per-channel layout, one gate at a
-    // time through a wave-private LDS strip of 64 columns: column c (16
-    // consecutive steps) becomes lane c's z_r, then its z_i.  A wave's LDS
-    // operations execute in order, so the second gate may reuse the strip.
-    float* zs = (float*)smem + w * 64 * ZP;
     float zr[C], zi[C];
-    {
-        const ElemReader<T> rbr(br, P.D), rbi(bi, P.D);
-        const int64_t d = cg * kWave + (lane & 15);
-#pragma unroll
-        for (int gate = 0; gate < 2; ++gate) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int col = 16 * j + (lane & 15);
-                const float bias = gate == 0 ? rbr(d + 16 * j) : rbi(d + 16 * j);
-                *(f4*)&zs[col * ZP + 4 * (lane >> 4)] = acc[4 * gate + j] + f4{bias, bias, bias, bias};
-            }
-            float* dst = gate == 0 ? zr : zi;
-#pragma unroll
-            for (int q = 0; q < C / 4; ++q) {
-                const f4 v = *(const f4*)&zs[lane * ZP + 4 * q];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) dst[4 * q + e] = v[e];
-            }
-        }
-    }
+    fusedz::tile_z<T>((const T*)P.p0, pack, br, bi, P.L, P.D, b, cg, t0, smem, tid, w, lane, zr,
+                      zi);
 
     // ---- the look-back scan of the tile (as scan_fwd_lookback_kernel, VEC = 1)
     LaneChannels<T, 1, Off> ln;
@@ -713,7 +612,7 @@ bool fused_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const voi
 
 // Tiles of the fused forward: 64 channels x 128 steps, in tile rows along L.
 static FwdPlan plan_fused(int64_t B, int64_t L, int64_t D) {
-    constexpr int64_t kSteps = (int64_t)fusedfwd::W * fusedfwd::C;
+    constexpr int64_t kSteps = (int64_t)fusedz::W * fusedz::C;
     FwdPlan p;
     p.lookback = true;
     p.vec = 1;
@@ -738,7 +637,7 @@ static hipError_t launch_fused_t(const void* x, const void* pack, const void* br
                 lookback_ws(ws)};
     hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
-    const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedfwd::NT);
+    const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedz::NT);
     const bool small = (uint64_t)(B * L * D) * esz < (1ull << 32);
     constexpr int K = lb_window<1>();
     if (io == IoType::kF32) {
