@@ -220,9 +220,10 @@ def test_full_forward_backward(rb, shape, io):
         assert_close(host(got[k]), want[k], io, k)
 
 
-# Few channel groups and sequences longer than one look-back tile (128 steps)
-# with D % 64 == 0 run the forward with the projections fused into the
-# look-back scan; D = 72 takes the two-kernel path.
+# With D % 64 == 0 the forward and the backward recompute the gate
+# projections inside the look-back scan (tiles of 64 channels x 128 steps);
+# these shapes span several tiles with a ragged last one.  D = 72 takes the
+# path through the separate projection kernels.
 FUSED_FWD = [(1, 1000, 64), (3, 700, 128), (2, 257, 192), (1, 129, 256), (2, 1000, 72)]
 
 
@@ -238,6 +239,23 @@ def test_full_forward_fused(rb, shape, io):
     oh, ohT = oracle.forward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.h0)
     assert_close(host(h), oh, io, "h")
     assert_close(host(hT), ohT, "f32" if io == "f32" else "bf16", "hT")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", FUSED_FWD)
+def test_full_backward_fused(rb, shape, io):
+    """Layer backward over several tiles, with h0 and dL/dh_T given."""
+    B, L, D = shape
+    f = dg.full_inputs(B, L, D, 4400 + B + L + D, io=io, a_range=(0.99, 0.9999), bias=True,
+                       h0=True, grad=True, dhT=True)
+    X, Wr, br, Wi, bi = (dev(a, io) for a in (f.x, f.Wr, f.br, f.Wi, f.bi))
+    lam, h0 = dev32(f.lam), dev32(f.h0)
+    h, _ = rb.bdlru_forward(X, Wr, br, Wi, bi, lam, h0)
+    got = rb.bdlru_backward(X, Wr, br, Wi, bi, lam, h, dev(f.dh, io), h0, dev32(f.dhT))
+    print(f"fused backward {shape} {io}: GPU done", flush=True)
+    want = oracle.backward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh, f.h0, f.dhT)
+    for k in ("dx", "dWr", "dbr", "dWi", "dbi", "dlambda", "dh0"):
+        assert_close(host(got[k]), want[k], io, k)
 
 
 # (B, D): D % 8 == 0 runs the step fused with the projection (z in registers),
