@@ -498,33 +498,25 @@ __device__ __forceinline__ float lds_elem(const char* base, int idx) {
     else return __uint_as_float((uint32_t)((const uint16_t*)base)[idx] << 16);
 }
 
-template <typename T, int K, typename Off>
-__global__ __launch_bounds__(fusedz::NT, 4) void
-scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi) {
-    constexpr int W = fusedz::W, C = fusedz::C;
-    __shared__ __attribute__((aligned(16))) char smem[fusedz::Tile<T>::kSmem];
-    __shared__ Seg agg[W][kWave][1];
-    __shared__ uint64_t win_sh[W * K][kWave][1];
-    __shared__ float carry_sh[kWave][1];
-    __shared__ float red[W][kWave][1];
-    __shared__ int64_t tile_sh;
-    const int tid = threadIdx.x;
-    const int lane = tid & (kWave - 1);
-    const int w = wave_id();
-    if (tid == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
-    __syncthreads();
-    const int64_t tile = tile_sh;
-    if (tile >= P.ngroups * P.nseg) return;  // only if the workspace was shared by two calls
-    const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
-    const int64_t g = tile - r * P.ngroups;
-    const int64_t s = P.nseg - 1 - r;    // tile row along L
-    const int64_t gpr = P.D / kWave;      // channel groups per batch row
-    const int64_t b = g / gpr, cg = g - b * gpr;
+// One backward tile in the eps form, from its gate pre-activations: zr, zi
+// hold the lane's channel at this wave's C steps (tile row s = nseg-1-r of
+// channel group g, batch row b, group cg within the row).  x and h_{t-1} are
+// staged into `stage` (2 * W * C * 64 elements of T, free on entry) by direct
+// loads and read back in the epilogue.  dz_r, dz_i are stored as TZ.  (Used
+// by the fused kernel; with z read from memory instead, for the scan entry
+// point, the same tile measured 376 against 366 µs for 256 x 2048 x 128 fp32
+// and 215-222 against 220-223 µs for 16 x 16384 x 256 bf16, so the scan
+// keeps its own kernels.)
+template <typename T, typename TZ, int W, int C, int K, typename Off>
+__device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int64_t g, int64_t b,
+                                             int64_t cg, const float (&zr)[C],
+                                             const float (&zi)[C], char* stage,
+                                             Seg (&agg)[W][kWave][1],
+                                             uint64_t (&win_sh)[W * K][kWave][1],
+                                             float (&carry_sh)[kWave][1],
+                                             float (&red)[W][kWave][1], int w, int lane) {
+    const int64_t s = P.nseg - 1 - r;  // tile row along L
     const int64_t t0 = s * W * C;
-    float zr[C], zi[C];
-    fusedz::tile_z<T>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, t0, smem, tid, w, lane, zr,
-                      zi);
-
     BwdLane<T, 1, Off> ln;
     ln.init(g, lane, P.L, P.D, P.nch);
     ChannelConst cc[1];
@@ -532,13 +524,10 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
     bwd_lane_consts<1>(P, ln.c0, ln.d0, cc, h0v, dhTv);
     const int64_t tw = t0 + (int64_t)w * C;
     const bool full = s > 0 && (s + 1) * W * C <= P.L;  // workgroup-uniform
-    // x and h_{t-1} are only needed in the epilogue: they wait in LDS (the
-    // staging area of the product is free once every wave holds its z), not
-    // in registers.
-    __syncthreads();
+    // x and h_{t-1} are only needed in the epilogue: they wait in LDS, not in
+    // registers.
     constexpr int kStaged = C * kWave * (int)sizeof(T);  // one tensor's rows of a wave
-    static_assert(2 * W * kStaged <= (int)fusedz::Tile<T>::kSmem, "staging fits");
-    char* const xs = smem + w * 2 * kStaged;
+    char* const xs = stage + w * 2 * kStaged;
     char* const hs = xs + kStaged;
     stage_rows<T, C>((const T*)P.x, b, P.L, P.D, cg * kWave, tw, 0, xs, lane);
     stage_rows<T, C>((const T*)P.h, b, P.L, P.D, cg * kWave, tw, -1, hs, lane);
@@ -615,12 +604,44 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
         if (ln.valid) {
             const Off off = ln.at(t);
             store_vec<T, 1>((T*)P.dx, off, dxv);
-            store_vec<float, 1>((float*)P.dzr, z_offset<T, float>(off), dzrv);
-            store_vec<float, 1>((float*)P.dzi, z_offset<T, float>(off), dziv);
+            store_vec<TZ, 1>((TZ*)P.dzr, z_offset<T, TZ>(off), dzrv);
+            store_vec<TZ, 1>((TZ*)P.dzi, z_offset<T, TZ>(off), dziv);
             if (!full && t == 0 && P.dh0) P.dh0[ln.c0] = eps;
         }
     }
     write_partial<W, 1>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
+}
+
+template <typename T, int K, typename Off>
+__global__ __launch_bounds__(fusedz::NT, 4) void
+scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi) {
+    constexpr int W = fusedz::W, C = fusedz::C;
+    static_assert(2 * W * C * kWave * (int)sizeof(T) <= (int)fusedz::Tile<T>::kSmem,
+                  "x and h staging fits in the product's LDS");
+    __shared__ __attribute__((aligned(16))) char smem[fusedz::Tile<T>::kSmem];
+    __shared__ Seg agg[W][kWave][1];
+    __shared__ uint64_t win_sh[W * K][kWave][1];
+    __shared__ float carry_sh[kWave][1];
+    __shared__ float red[W][kWave][1];
+    __shared__ int64_t tile_sh;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int w = wave_id();
+    if (tid == 0) tile_sh = (int64_t)atomicAdd(P.lb.ticket, 1u);
+    __syncthreads();
+    const int64_t tile = tile_sh;
+    if (tile >= P.ngroups * P.nseg) return;  // only if the workspace was shared by two calls
+    const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
+    const int64_t g = tile - r * P.ngroups;
+    const int64_t s = P.nseg - 1 - r;    // tile row along L
+    const int64_t gpr = P.D / kWave;      // channel groups per batch row
+    const int64_t b = g / gpr, cg = g - b * gpr;
+    float zr[C], zi[C];
+    fusedz::tile_z<T>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, s * W * C, smem, tid, w,
+                      lane, zr, zi);
+    __syncthreads();  // every wave holds its z: the product's LDS is free
+    bwd_eps_tile<T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh, carry_sh, red,
+                                         w, lane);
 }
 
 // ------------------------------------------------------------------ dLambda reduction
@@ -828,10 +849,11 @@ static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStr
     }
     if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
     if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
-    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<lb_elems(sizeof(TX)), VEC>(), VEC,
+    const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(kLbW * kWave);
+    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW,
+                                                 steps_per_wave<lb_elems(sizeof(TX)), VEC>(), VEC,
                                                  lb_window<VEC>(), Off>),
-                       dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0, stream,
-                       P);
+                       grid, block, 0, stream, P);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return mark_event(ev1, stream);
 }
