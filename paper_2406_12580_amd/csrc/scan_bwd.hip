@@ -719,11 +719,12 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
 // Tile shapes: W waves per workgroup and E elements per lane per macro-chunk
 // (C = E / VEC steps per wave), so a wave moves the same bytes per
 // macro-chunk whatever VEC is.
+// The chain kernel runs 8 waves of 4 or 5 steps (macro-chunks of 32 or 40
+// steps), whichever pads L less: 2048 x 200 x 64 fp32 backward 151 us with 40
+// (200 = 5 x 40), against 158 us with 32 and 168-173 us with 16 waves of 4
+// (64 steps: 200 = 3 x 64 + 8, the last macro-chunk one eighth used).
 #ifndef RECBLR_BWD_CHAIN_W
-#define RECBLR_BWD_CHAIN_W 16
-#endif
-#ifndef RECBLR_BWD_CHAIN_E
-#define RECBLR_BWD_CHAIN_E 4
+#define RECBLR_BWD_CHAIN_W 8
 #endif
 #ifndef RECBLR_BWD_LB_W
 #define RECBLR_BWD_LB_W 8
@@ -738,7 +739,13 @@ hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream) {
 #ifndef RECBLR_BWD_LB_MAX_VEC
 #define RECBLR_BWD_LB_MAX_VEC 1
 #endif
-constexpr int kChainW = RECBLR_BWD_CHAIN_W, kChainE = RECBLR_BWD_CHAIN_E;
+constexpr int kChainW = RECBLR_BWD_CHAIN_W;
+// Steps per wave of the chain kernel for a sequence of L steps.
+inline int chain_steps(int64_t L) {
+    const int64_t p4 = (L + 4 * kChainW - 1) / (4 * kChainW) * (4 * kChainW);
+    const int64_t p5 = (L + 5 * kChainW - 1) / (5 * kChainW) * (5 * kChainW);
+    return p5 < p4 ? 5 : 4;
+}
 // bf16 I/O takes 12 steps per wave: with the step pairs formed on use that is
 // 126 VGPRs, two workgroups per compute unit (16 x 16384 x 256 backward:
 // 222 us against 255 us at 16 steps); fp32 I/O keeps 16 (256 x 2048 x 128:
@@ -768,7 +775,10 @@ constexpr int64_t kChainMinGroups = 256;
 // amortise the carry fold over four times as many steps as the chain
 // kernel's 4; 256 x 2048 x 128 fp32: 378 us against 404 us on MI355X),
 // above it the chain kernel is (2048 x 200 x 64: 177 us against 183 us).
-constexpr int64_t kLookbackBelowGroups = 1024;
+#ifndef RECBLR_BWD_LB_BELOW
+#define RECBLR_BWD_LB_BELOW 1024
+#endif
+constexpr int64_t kLookbackBelowGroups = RECBLR_BWD_LB_BELOW;
 // Largest channels-per-lane of a kernel for an element size (8-byte accesses
 // per lane at most).
 constexpr int max_vec(size_t esz, bool lookback, int64_t nch = INT64_MAX) {
@@ -841,9 +851,18 @@ static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStr
     hipError_t e;
     if (!plan.lookback) {
         if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
-        hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, steps_per_wave<kChainE, VEC>(),
-                                                  VEC, Off>),
-                           dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
+        // The chain kernel takes one channel per lane (RECBLR_BWD_CHAIN_MAX_VEC).
+        if constexpr (VEC != 1) {
+            return hipErrorInvalidValue;
+        } else {
+            const dim3 grid((unsigned)plan.ngroups), block(kChainW * kWave);
+            if (chain_steps(P.L) == 5)
+                hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, 5, 1, Off>), grid,
+                                   block, 0, stream, P);
+            else
+                hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, 4, 1, Off>), grid,
+                                   block, 0, stream, P);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         return mark_event(ev1, stream);
     }
