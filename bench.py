@@ -57,13 +57,13 @@ ARRAYS = {"scan": (4, 8), "full": (2, 4)}
 # valid only for the kernel sources they were taken on: the sha256 prefix of
 # the listed files must match, else the traffic is reported as null.
 TRAFFIC = {
-    ("c4", "scan_bwd"): {"bytes": 2_186_467_328, "sha": "480e09ac4d6f1b85",
+    ("c4", "scan_bwd"): {"bytes": 2_187_259_936, "sha": "21048842a52346e0",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c4", "scan_fwd"): {"bytes": 1_074_319_360, "sha": "86a377c3d850f0fa",
+    ("c4", "scan_fwd"): {"bytes": 1_074_261_280, "sha": "a20986a2ecc07bf0",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c5", "scan_bwd"): {"bytes": 1_120_595_968, "sha": "480e09ac4d6f1b85",
+    ("c5", "scan_bwd"): {"bytes": 1_120_474_784, "sha": "21048842a52346e0",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c5", "scan_fwd"): {"bytes": 570_664_960, "sha": "86a377c3d850f0fa",
+    ("c5", "scan_fwd"): {"bytes": 570_724_352, "sha": "a20986a2ecc07bf0",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
 }
 
