@@ -605,6 +605,9 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
     void* zi = at(ws, step_z_bytes(B, D));
     void* pack = at(ws, 2 * step_z_bytes(B, D));
     hipError_t e = hipSuccess;
+    if (launch_step_resident(x, W_r, b_r, W_i, b_i, lambda, h_prev, h_next, B, D, io_of(io),
+                             strm, &e))
+        return status_of(e);
     if (launch_fused_step(x, W_r, b_r, W_i, b_i, lambda, h_prev, h_next, B, D, io_of(io), pack,
                           strm, &e))
         return status_of(e);

@@ -70,6 +70,15 @@ hipError_t launch_scan_step(const void* x, const void* zr, const void* zi, const
                             const float* h_prev, float* h_next, int64_t B, int64_t D, IoType io,
                             IoType zio, hipStream_t stream);
 hipError_t launch_fill(float* dst, float value, int64_t n, hipStream_t stream);
+// Recurrent step with the gate projections fused in, for bf16 I/O and
+// D in {64, 128, 192, 256}: persistent workgroups keep W_r and W_i resident
+// in registers (no workspace).  Returns false, having launched nothing, where
+// it does not apply (other dtype or D, x / W_r / W_i not 16-byte aligned,
+// B * D * 4 >= 2^31); else launches and stores the launch status in *err.
+bool launch_step_resident(const void* x, const void* wr, const void* br, const void* wi,
+                          const void* bi, const float* lambda, const float* h_prev,
+                          float* h_next, int64_t B, int64_t D, IoType io, hipStream_t stream,
+                          hipError_t* err);
 
 // Scan forward with the gate projections computed per tile on the matrix
 // cores (z never reaches HBM).  Applies when the look-back kernel runs,

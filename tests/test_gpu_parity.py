@@ -272,6 +272,27 @@ def test_full_step(rb, io, shape):
     assert_close(host(got), want, io, "h_next")
 
 
+# bf16 with D in {64, 128, 192, 256} runs the step with the weights resident
+# in registers: blocks of 16 rows handed out round-robin to persistent
+# workgroups.  B = 12293 gives 769 blocks at D = 256 (an odd count for some
+# workgroups, which ends on a half round) and a ragged last block; B = 5 is
+# one partial block.
+@pytest.mark.parametrize("shape,bias", [((5, 64), True), ((4111, 128), True),
+                                        ((1000, 192), False), ((33, 256), True),
+                                        ((12293, 256), True), ((40000, 64), False)])
+def test_full_step_resident(rb, shape, bias):
+    B, D = shape
+    f = dg.full_inputs(B, 1, D, 4170 + B + D, io="bf16", bias=bias, h0=True)
+    x = f.x[:, 0]
+    br = dev(f.br, "bf16") if bias else None
+    bi = dev(f.bi, "bf16") if bias else None
+    got = rb.bdlru_step(dev(x, "bf16"), dev(f.Wr, "bf16"), br, dev(f.Wi, "bf16"), bi,
+                        dev32(f.lam), dev32(f.h0))
+    want = oracle.step(x, f.Wr, f.br if bias else None, f.Wi, f.bi if bias else None, f.lam,
+                       f.h0)
+    assert_close(host(got), want, "bf16", "h_next")
+
+
 @pytest.mark.parametrize("io", ["f32", "bf16"])
 def test_full_step_in_place(rb, io):
     """h_next may be h_prev; two steps in a row match two oracle steps."""
