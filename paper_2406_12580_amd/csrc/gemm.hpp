@@ -1,6 +1,8 @@
 // Host launchers of the gate-projection products (internal to librecblr.so).
 #pragma once
 
+#include <initializer_list>
+
 #include "launch.hpp"
 
 namespace recblr {
@@ -45,6 +47,19 @@ bool launch_fused_step(const void* x, const void* wr, const void* br, const void
                        const void* bi, const float* lambda, const float* h_prev, float* h_next,
                        int64_t B, int64_t D, IoType io, void* pack, hipStream_t stream,
                        hipError_t* err);
+
+// Weight gradient of a plain fp32 linear layer Y = X W^T + b (W[N][K]) on
+// the matrix-core tiles (3-term bf16 split of both operands):
+// dW[N][K] = dY[M][N]^T X[M][K] and db[N] = column sums of dY (db may be
+// null), as split-M partials (wgrad_workspace bytes at ws) summed in a fixed
+// order (launch_colsum, colsum_workspace(wgrad_splits, N * K) bytes at
+// colsum_ws).  Applies when wgrad_fast_ok holds (row-major contiguous
+// operands, N and K multiples of 4, 16-byte alignment, under 2 GiB each).
+bool wgrad_fast_ok(std::initializer_list<const void*> ptrs, int64_t M, int64_t N, int64_t K);
+int64_t wgrad_splits(int64_t M, int64_t N, int64_t K);
+size_t wgrad_workspace(int64_t M, int64_t N, int64_t K);
+hipError_t launch_wgrad(const float* dy, const float* x, float* dw, float* db, int64_t M,
+                        int64_t N, int64_t K, void* ws, void* colsum_ws, hipStream_t stream);
 
 int64_t project_dw_splits(int64_t M, int64_t D);
 size_t project_dw_workspace(int64_t M, int64_t D);

@@ -19,6 +19,7 @@
 #include <hipcub/hipcub.hpp>
 
 #include "device_common.hpp"
+#include "gemm.hpp"
 #include "launch.hpp"
 #include "model.hpp"
 #include "recblr.h"
@@ -456,12 +457,22 @@ Layout layout(const Dims& d) {
     // weight gradients: one partial per chunk of kDwChunk rows, summed after
     const int64_t NK = 4 * D * D > ED * D ? 4 * D * D : ED * D;
     const int64_t slices = M / kDwChunk + 1;
-    w.dwp = take((size_t)(slices * NK) * f);
+    // (or, on the matrix-core path, one partial per split of the rows, and
+    // the bias gradient's partials after them)
+    const int64_t wshape[4][2] = {{D, F}, {F, D}, {D, ED}, {ED, D}};
+    size_t dwp = (size_t)(slices * NK) * f;
+    for (const auto& nk : wshape)
+        if (wgrad_workspace(M, nk[0], nk[1]) > dwp) dwp = wgrad_workspace(M, nk[0], nk[1]);
+    w.dwp = take(dwp);
     // column sums: bias gradients (widths D, 4D, E*D), LayerNorm partials, the
-    // weight-gradient slices
+    // weight-gradient slices or splits
     size_t cs = colsum_workspace(M, F > ED ? F : ED);
     if (colsum_workspace(lnblk, D) > cs) cs = colsum_workspace(lnblk, D);
     if (colsum_workspace(slices, NK) > cs) cs = colsum_workspace(slices, NK);
+    for (const auto& nk : wshape) {
+        const int64_t sp = wgrad_splits(M, nk[0], nk[1]);
+        if (colsum_workspace(sp, nk[0] * nk[1]) > cs) cs = colsum_workspace(sp, nk[0] * nk[1]);
+    }
     w.colsum = take(cs);
     const int64_t max_pieces = (M + kPiece - 1) / kPiece + d.V;
     w.emb_lo = take((size_t)d.V * sizeof(int64_t));
@@ -559,6 +570,18 @@ bool linear_fwd(Ctx& c, const float* X, const float* W, const float* b, float* Y
 // db[n] = sum_m dY[m][n] in a fixed order (double).
 bool bias_grad(Ctx& c, const float* dY, int64_t M, int64_t N, float* db) {
     return launch_colsum(dY, M, N, db, c.ws + c.w.colsum, c.stream) == hipSuccess;
+}
+
+// Weight and bias gradients of Y = X W^T + b: dW[N][K] = dY^T X and db =
+// column sums of dY, both in a fixed order; on the matrix-core tiles when the
+// operands allow (always, for the model's shapes and workspace), else a
+// library GEMM per chunk of rows and column sums.
+bool linear_wgrad(Ctx& c, const float* X, const float* dY, float* dW, float* db, int64_t M,
+                  int64_t N, int64_t K) {
+    if (wgrad_fast_ok({X, dY, dW, db}, M, N, K))
+        return launch_wgrad(dY, X, dW, db, M, N, K, c.ws + c.w.dwp, c.ws + c.w.colsum,
+                            c.stream) == hipSuccess;
+    return bias_grad(c, dY, M, N, db) && weight_grad(c, X, K, dY, N, dW, M, N, K);
 }
 
 template <int NV>
@@ -680,21 +703,18 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         CHECK(ln_bwd<NV>(c, Y, s2, nullptr, stat(l, 2), stat(l, 3), P(l, kLn2g), X, G(l, kLn2g),
                          G(l, kLn2b), M, V));
         // PFFN: Q = P W2^T + b2, P = SiLU(A), A = H1 W1^T + b1
-        CHECK(bias_grad(c, X, M, D, G(l, kb2)));
-        CHECK(weight_grad(c, Pp, F, X, D, G(l, kW2), M, D, F));
+        CHECK(linear_wgrad(c, Pp, X, G(l, kW2), G(l, kb2), M, D, F));
         CHECK(gemm_dyW(c, X, D, P(l, kW2), dP, F, M, D, F, 0.0f));
         hipLaunchKernelGGL(silu_bwd_kernel, dim3(blocks_for(M * F / 4)), dim3(kThreads), 0,
                            stream, dP, A, M * F);
         CHECK(hipGetLastError() == hipSuccess);
-        CHECK(bias_grad(c, dP, M, F, G(l, kb1)));
-        CHECK(weight_grad(c, H1, D, dP, F, G(l, kW1), M, F, D));
+        CHECK(linear_wgrad(c, H1, dP, G(l, kW1), G(l, kb1), M, F, D));
         CHECK(gemm_dyW(c, dP, F, P(l, kW1), X, D, M, F, D, 1.0f));  // X = dH1
         // LN1: X (dH1) -> Y (ds1 = dO, and the residual part of dH)
         CHECK(ln_bwd<NV>(c, X, s1, nullptr, stat(l, 0), stat(l, 1), P(l, kLn1g), Y, G(l, kLn1g),
                          G(l, kLn1b), M, V));
         // O = y Wo^T + bo
-        CHECK(bias_grad(c, Y, M, D, G(l, kbo)));
-        CHECK(weight_grad(c, y, ED, Y, D, G(l, kWo), M, D, ED));
+        CHECK(linear_wgrad(c, y, Y, G(l, kWo), G(l, kbo), M, D, ED));
         CHECK(gemm_dyW(c, Y, D, P(l, kWo), dY, ED, M, D, ED, 0.0f));
         CHECK_ST(recblr_gated_backward(Hx, Hz, P(l, kConvW), P(l, kConvB), d.K, P(l, kWr),
                                        P(l, kbr), P(l, kWi), P(l, kbi), P(l, kLam), nullptr, hb,
@@ -703,10 +723,8 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
                                        nullptr, B, T, ED, RECBLR_F32, ws + w.gated, w.gated_bytes,
                                        stream));
         // Hx = H Wx^T + bx, Hz = H Wz^T + bz; Y becomes dH of this layer's input.
-        CHECK(bias_grad(c, dHx, M, ED, G(l, kbx)));
-        CHECK(bias_grad(c, dHz, M, ED, G(l, kbz)));
-        CHECK(weight_grad(c, Hl(l), D, dHx, ED, G(l, kWx), M, ED, D));
-        CHECK(weight_grad(c, Hl(l), D, dHz, ED, G(l, kWz), M, ED, D));
+        CHECK(linear_wgrad(c, Hl(l), dHx, G(l, kWx), G(l, kbx), M, ED, D));
+        CHECK(linear_wgrad(c, Hl(l), dHz, G(l, kWz), G(l, kbz), M, ED, D));
         CHECK(gemm_dyW(c, dHx, ED, P(l, kWx), Y, D, M, ED, D, 1.0f));
         CHECK(gemm_dyW(c, dHz, ED, P(l, kWz), Y, D, M, ED, D, 1.0f));
     }
