@@ -673,6 +673,178 @@ __global__ __launch_bounds__(256, 2) void dw_kernel(const float* dzr, uint32_t h
     }
 }
 
+// ---- fp32 tiles (v_mfma_f32_16x16x4_f32), for products whose rounding must
+// stay that of fp32: the forward products and data gradients of the model's
+// linear layers (the 3-term bf16 split above moved the model's gradients by
+// up to 3e-4 there).  Same 128 x 128 output tiles, 4-wave layout, epilogues
+// and slice prefetch as above; both operands have the contracted index
+// contiguous in memory (KFAST) and sit in LDS as fp32 rows of BK floats
+// padded to KP32 (16-byte aligned rows; a fragment read of 8 consecutive
+// rows touches 8 distinct bank groups).  Within a slice, lane group
+// g = lane / 16 contracts k = 16 g .. 16 g + 15: MFMA step s takes
+// k = 16 g + s for the four "k" inputs of the instruction, so that each lane
+// reads its fragments as 16-byte vectors.
+constexpr int KP32 = BK + 4;
+constexpr size_t kLds32 = (size_t)(BM + BN) * KP32 * sizeof(float);
+
+__device__ __forceinline__ void store_slice32(float (*lds)[KP32], int tid, const f4 (&r)[NQ]) {
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) *(f4*)&lds[(tid >> 4) + 16 * j][4 * (tid & 15)] = r[j];
+}
+
+__device__ __forceinline__ void mma_slice32(float (*la)[KP32], float (*lb)[KP32],
+                                            f4 (&acc)[4][4], int wm, int wn, int fr, int g) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        f4 fa[4], fb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[i] = *(const f4*)&la[wm * 64 + 16 * i + fr][16 * g + 4 * c];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fb[j] = *(const f4*)&lb[wn * 64 + 16 * j + fr][16 * g + 4 * c];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] =
+                        __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
+    }
+}
+
+// One output tile at (m0, n0): the sum over k in [0, K) of A(m, k) B(n, k),
+// handed to epi.
+template <class Epi>
+__device__ __forceinline__ void tile32(const Operand<kF32, true>& a, const Operand<kF32, true>& b,
+                                       int64_t m0, int64_t n0, int64_t K, const Epi& epi,
+                                       char* smem) {
+    using Op = Operand<kF32, true>;
+    float (*la)[KP32] = (float (*)[KP32])smem;
+    float (*lb)[KP32] = (float (*)[KP32])(smem + (size_t)BM * KP32 * sizeof(float));
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1, fr = lane & 15, g = lane >> 4;
+    const int64_t m0w = m0 + wm * 64, n0w = n0 + wn * 64;
+    const int64_t nsl = (K + BK - 1) / BK;
+    const Stager<Op> sa(a, m0, tid);
+    const Stager<Op> sb(b, n0, tid);
+    f4 ra[NQ], rb[NQ];
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    typename Epi::pre_t pre{};
+    int64_t mr[4];
+    strip_rows(m0w, 0, lane, mr);
+    const int64_t ne = n0w + 4 * (lane & 15);
+    sa.fetch(a, 0, K, tid, ra);
+    sb.fetch(b, 0, K, tid, rb);
+    for (int64_t sl = 0; sl < nsl; ++sl) {
+        store_slice32(la, tid, ra);
+        store_slice32(lb, tid, rb);
+        __syncthreads();
+        if (sl + 1 < nsl) {
+            sa.fetch(a, (sl + 1) * BK, K, tid, ra);
+            sb.fetch(b, (sl + 1) * BK, K, tid, rb);
+        } else {
+            epi.load(mr, ne, pre);
+        }
+        // Keep the loads ahead of the MFMAs (see tile()).
+        __builtin_amdgcn_sched_barrier(0);
+        mma_slice32(la, lb, acc, wm, wn, fr, g);
+        __syncthreads();
+    }
+    tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+}
+
+// Epilogues of the linear layers' products C (M x N, row-major outputs).
+enum LinMode {
+    kLinStore,     // y = C + bias (bias may be null); act, if given, = SiLU(y)
+    kLinAcc,       // y += C
+    kLinSiluGrad,  // y = C * SiLU'(aux), aux laid out as y
+};
+
+template <int MODE>
+struct LinEpi {
+    static constexpr bool kOwnStore = false;
+    static constexpr bool kStripLoads = MODE != kLinStore;
+    struct pre_t {
+        f4 v[4];
+    };
+    float* y;
+    const float* bias;
+    float* act;
+    const float* aux;
+    int64_t M, N;
+    __device__ void load(const int64_t (&m)[4], int64_t n, pre_t& pre) const {
+        if constexpr (MODE == kLinStore) {
+            const ElemReader<float> rb(bias, N);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) pre.v[0][c] = rb(n + c < N ? n + c : -1);
+        } else {
+            const __amdgpu_buffer_rsrc_t r =
+                resource(MODE == kLinAcc ? y : aux, (uint32_t)(M * N * 4));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t off = (n < N && m[q] < M) ? (uint32_t)((m[q] * N + n) * 4) : kOOB;
+                const u4v w = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+                pre.v[q] = f4{__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z),
+                              __uint_as_float(w.w)};
+            }
+        }
+    }
+    __device__ void run(const int64_t (&m)[4], int64_t n, const f4 (&v)[4],
+                        const pre_t& pre) const {
+        if (n >= N) return;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (m[q] >= M) continue;
+            f4 r;
+            if constexpr (MODE == kLinStore) {
+                r = v[q] + pre.v[0];
+                if (act) {
+                    f4 sv;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) sv[c] = r[c] * sigmoid(r[c]);
+                    *(f4*)(act + m[q] * N + n) = sv;
+                }
+            } else if constexpr (MODE == kLinAcc) {
+                r = pre.v[q] + v[q];
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float x = pre.v[q][c], sg = sigmoid(x);
+                    r[c] = v[q][c] * (sg * fmaf(x, 1.0f - sg, 1.0f));
+                }
+            }
+            *(f4*)(y + m[q] * N + n) = r;
+        }
+    }
+};
+
+// Y[M][N] (epilogue MODE) of C = A B^T: A[M][K], B[N][K], both row-major.
+template <int MODE>
+__global__ __launch_bounds__(256, 2) void linear32_kernel(const float* a, const float* b,
+                                                          LinEpi<MODE> epi, int64_t K) {
+    __shared__ __attribute__((aligned(16))) char smem[kLds32 > kEpiBytes ? kLds32 : kEpiBytes];
+    const int64_t M = epi.M, N = epi.N;
+    const int64_t ntn = (N + BN - 1) / BN;
+    const int64_t t = xcd_tile(((M + BM - 1) / BM) * ntn);
+    if (t < 0) return;
+    const Operand<kF32, true> oa{resource(a, (uint32_t)(M * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
+    const Operand<kF32, true> ob{resource(b, (uint32_t)(N * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
+    tile32(oa, ob, (t / ntn) * BM, (t % ntn) * BN, K, epi, smem);
+}
+
+// out[K][N] = in[N][K] (the data gradient's weight operand, once per call).
+__global__ __launch_bounds__(256) void transpose_kernel(const float* in, float* out, int64_t N,
+                                                        int64_t K) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= N * K) return;
+    const int64_t k = e / N, n = e % N;
+    out[e] = in[n * K + k];
+}
+
 // ---- weight gradients of plain fp32 linear layers (the model around the
 // BD-LRU): dW = dY^T X and db = column sums of dY, on the same tiles (3-term
 // bf16 split of both operands).  Each weight gradient's error stays local to
@@ -1105,10 +1277,52 @@ hipError_t launch_project_backward_weights(const void* dzr, const void* dzi, con
     return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ linear-layer weight gradients
+// ------------------------------------------------------------------ linear layers
 bool wgrad_fast_ok(std::initializer_list<const void*> ptrs, int64_t M, int64_t N, int64_t K) {
     return M > 0 && N > 0 && K > 0 && N % 4 == 0 && K % 4 == 0 && aligned16(ptrs) &&
            (M + fastmm::BM) * (N > K ? N : K) * 4 < kFastLimit;
+}
+
+hipError_t launch_linear_fwd32(const float* x, const float* w, const float* bias, float* y,
+                               float* act, int64_t M, int64_t N, int64_t K, hipStream_t stream) {
+    const int64_t t = ((M + fastmm::BM - 1) / fastmm::BM) * ((N + fastmm::BN - 1) / fastmm::BN);
+    const fastmm::LinEpi<fastmm::kLinStore> e{y, bias, act, nullptr, M, N};
+    hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinStore>, dim3(fastmm::grid_of(t)),
+                       dim3(256), 0, stream, x, w, e, K);
+    return hipGetLastError();
+}
+
+hipError_t launch_linear_dgrad32(const float* dy, const float* w, float* dx, LinearMode mode,
+                                 const float* aux, int64_t M, int64_t N, int64_t K, float* wt,
+                                 hipStream_t stream) {
+    hipLaunchKernelGGL(fastmm::transpose_kernel, dim3((unsigned)((N * K + 255) / 256)), dim3(256),
+                       0, stream, w, wt, N, K);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    // dX[M][K] = dY[M][N] W^T[K][N]^T: output width K, contraction N.
+    const int64_t t = ((M + fastmm::BM - 1) / fastmm::BM) * ((K + fastmm::BN - 1) / fastmm::BN);
+    const dim3 grid(fastmm::grid_of(t)), block(256);
+    switch (mode) {
+        case LinearMode::kStore: {
+            const fastmm::LinEpi<fastmm::kLinStore> e{dx, nullptr, nullptr, nullptr, M, K};
+            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinStore>, grid, block, 0, stream,
+                               dy, wt, e, N);
+            break;
+        }
+        case LinearMode::kAccumulate: {
+            const fastmm::LinEpi<fastmm::kLinAcc> e{dx, nullptr, nullptr, nullptr, M, K};
+            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinAcc>, grid, block, 0, stream,
+                               dy, wt, e, N);
+            break;
+        }
+        case LinearMode::kSiluGrad: {
+            const fastmm::LinEpi<fastmm::kLinSiluGrad> e{dx, nullptr, nullptr, aux, M, K};
+            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinSiluGrad>, grid, block, 0,
+                               stream, dy, wt, e, N);
+            break;
+        }
+    }
+    return hipGetLastError();
 }
 
 // About one workgroup per CU in all (each split's partial is summed again

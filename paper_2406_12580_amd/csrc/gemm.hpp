@@ -48,6 +48,21 @@ bool launch_fused_step(const void* x, const void* wr, const void* br, const void
                        int64_t B, int64_t D, IoType io, void* pack, hipStream_t stream,
                        hipError_t* err);
 
+// Plain fp32 linear layer Y = X W^T + b, W[N][K] (nn.Linear layout), all
+// operands row-major and contiguous, on fp32 matrix-core tiles (fp32
+// products): the forward Y[M][N] = X[M][K] W^T + bias (bias may be null;
+// act, if given, receives SiLU(Y)), and the data gradient
+// dX[M][K] = dY[M][N] W in one of three epilogues: store, accumulate, or
+// multiply by SiLU'(aux) with aux[M][K] the SiLU's input.  The data gradient
+// first writes W^T into wt (N * K floats).  Preconditions: wgrad_fast_ok for
+// the operands and the shape (N and K multiples of 4).
+enum class LinearMode { kStore, kAccumulate, kSiluGrad };
+hipError_t launch_linear_fwd32(const float* x, const float* w, const float* bias, float* y,
+                               float* act, int64_t M, int64_t N, int64_t K, hipStream_t stream);
+hipError_t launch_linear_dgrad32(const float* dy, const float* w, float* dx, LinearMode mode,
+                                 const float* aux, int64_t M, int64_t N, int64_t K, float* wt,
+                                 hipStream_t stream);
+
 // Weight gradient of a plain fp32 linear layer Y = X W^T + b (W[N][K]) on
 // the matrix-core tiles (3-term bf16 split of both operands):
 // dW[N][K] = dY[M][N]^T X[M][K] and db[N] = column sums of dY (db may be

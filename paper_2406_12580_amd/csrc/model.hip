@@ -414,7 +414,7 @@ int64_t param_offsets(const Dims& d, int64_t* off) {
 // ------------------------------------------------------------------ workspace
 struct Layout {
     size_t H, Hx, Hz, hb, y, s1, H1, A, P, s2, stats, emb_stats, logits, dlogits, lossb;
-    size_t X, Y, dP, dY, dHx, dHz, lnp, dwp, colsum, emb_lo, emb_hi, emb_np, emb_poff, emb_part;
+    size_t X, Y, dP, dY, dHx, dHz, lnp, dwp, wt, colsum, emb_lo, emb_hi, emb_np, emb_poff, emb_part;
     size_t ids_s, pos, pos_s, sort_tmp, gated, total;
     size_t sort_bytes, gated_bytes;
 };
@@ -464,6 +464,7 @@ Layout layout(const Dims& d) {
     for (const auto& nk : wshape)
         if (wgrad_workspace(M, nk[0], nk[1]) > dwp) dwp = wgrad_workspace(M, nk[0], nk[1]);
     w.dwp = take(dwp);
+    w.wt = take((size_t)NK * f);  // a transposed weight (data gradients)
     // column sums: bias gradients (widths D, 4D, E*D), LayerNorm partials, the
     // weight-gradient slices or splits
     size_t cs = colsum_workspace(M, F > ED ? F : ED);
@@ -559,12 +560,38 @@ bool weight_grad(Ctx& c, const float* X, int64_t ldx, const float* dY, int64_t l
     return launch_colsum(part, slices, N * K, dW, c.ws + c.w.colsum, c.stream) == hipSuccess;
 }
 
+// Y[M][N] = X[M][K] W[N][K]^T + b; act, if given, gets SiLU(Y).  On the
+// library's fp32 matrix-core tiles with the bias and the SiLU in the
+// epilogue when the operands allow (always, for the model's shapes and
+// workspace), else bias rows, a library GEMM and a SiLU pass.
 bool linear_fwd(Ctx& c, const float* X, const float* W, const float* b, float* Y, int64_t M,
-                int64_t N, int64_t K) {
+                int64_t N, int64_t K, float* act = nullptr) {
+    if (wgrad_fast_ok({X, W, b, Y, act}, M, N, K))
+        return launch_linear_fwd32(X, W, b, Y, act, M, N, K, c.stream) == hipSuccess;
     hipLaunchKernelGGL(bias_rows_kernel, dim3(blocks_for(M * N / 4)), dim3(kThreads), 0, c.stream,
                        b, Y, M, N);
     if (hipGetLastError() != hipSuccess) return false;
-    return gemm_xwT(c, X, K, W, Y, N, M, N, K, 1.0f);
+    if (!gemm_xwT(c, X, K, W, Y, N, M, N, K, 1.0f)) return false;
+    if (!act) return true;
+    hipLaunchKernelGGL(silu_fwd_kernel, dim3(blocks_for(M * N / 4)), dim3(kThreads), 0, c.stream,
+                       Y, act, M * N);
+    return hipGetLastError() == hipSuccess;
+}
+
+// Data gradient of Y = X W^T: dX[M][K] = dY[M][N] W[N][K] (kStore), dX += it
+// (kAccumulate), or dX = it * SiLU'(A) with A[M][K] the SiLU's input
+// (kSiluGrad); same choice of path as linear_fwd.
+bool linear_dgrad(Ctx& c, const float* dY, const float* W, float* dX, int64_t M, int64_t N,
+                  int64_t K, LinearMode mode, const float* A = nullptr) {
+    float* wt = (float*)(c.ws + c.w.wt);
+    if (wgrad_fast_ok({dY, W, dX, A, wt}, M, N, K))
+        return launch_linear_dgrad32(dY, W, dX, mode, A, M, N, K, wt, c.stream) == hipSuccess;
+    if (!gemm_dyW(c, dY, N, W, dX, K, M, N, K, mode == LinearMode::kAccumulate ? 1.0f : 0.0f))
+        return false;
+    if (mode != LinearMode::kSiluGrad) return true;
+    hipLaunchKernelGGL(silu_bwd_kernel, dim3(blocks_for(M * K / 4)), dim3(kThreads), 0, c.stream,
+                       dX, A, M * K);
+    return hipGetLastError() == hipSuccess;
 }
 
 // db[n] = sum_m dY[m][n] in a fixed order (double).
@@ -667,10 +694,7 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         CHECK(linear_fwd(c, y, P(l, kWo), P(l, kbo), s1, M, D, ED));
         CHECK(ln_fwd<NV>(c, s1, Hl(l), nullptr, P(l, kLn1g), P(l, kLn1b), s1, H1, stat(l, 0),
                          stat(l, 1), M, V, d.eps));
-        CHECK(linear_fwd(c, H1, P(l, kW1), P(l, kb1), A, M, F, D));
-        hipLaunchKernelGGL(silu_fwd_kernel, dim3(blocks_for(M * F / 4)), dim3(kThreads), 0,
-                           stream, A, Pp, M * F);
-        CHECK(hipGetLastError() == hipSuccess);
+        CHECK(linear_fwd(c, H1, P(l, kW1), P(l, kb1), A, M, F, D, Pp));  // Pp = SiLU(A)
         CHECK(linear_fwd(c, Pp, P(l, kW2), P(l, kb2), s2, M, D, F));
         CHECK(ln_fwd<NV>(c, s2, H1, nullptr, P(l, kLn2g), P(l, kLn2b), s2, Hl(l + 1),
                          stat(l, 2), stat(l, 3), M, V, d.eps));
@@ -704,18 +728,16 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
                          G(l, kLn2b), M, V));
         // PFFN: Q = P W2^T + b2, P = SiLU(A), A = H1 W1^T + b1
         CHECK(linear_wgrad(c, Pp, X, G(l, kW2), G(l, kb2), M, D, F));
-        CHECK(gemm_dyW(c, X, D, P(l, kW2), dP, F, M, D, F, 0.0f));
-        hipLaunchKernelGGL(silu_bwd_kernel, dim3(blocks_for(M * F / 4)), dim3(kThreads), 0,
-                           stream, dP, A, M * F);
-        CHECK(hipGetLastError() == hipSuccess);
+        // dP = (dQ W2) * SiLU'(A)
+        CHECK(linear_dgrad(c, X, P(l, kW2), dP, M, D, F, LinearMode::kSiluGrad, A));
         CHECK(linear_wgrad(c, H1, dP, G(l, kW1), G(l, kb1), M, F, D));
-        CHECK(gemm_dyW(c, dP, F, P(l, kW1), X, D, M, F, D, 1.0f));  // X = dH1
+        CHECK(linear_dgrad(c, dP, P(l, kW1), X, M, F, D, LinearMode::kAccumulate));  // X = dH1
         // LN1: X (dH1) -> Y (ds1 = dO, and the residual part of dH)
         CHECK(ln_bwd<NV>(c, X, s1, nullptr, stat(l, 0), stat(l, 1), P(l, kLn1g), Y, G(l, kLn1g),
                          G(l, kLn1b), M, V));
         // O = y Wo^T + bo
         CHECK(linear_wgrad(c, y, Y, G(l, kWo), G(l, kbo), M, D, ED));
-        CHECK(gemm_dyW(c, Y, D, P(l, kWo), dY, ED, M, D, ED, 0.0f));
+        CHECK(linear_dgrad(c, Y, P(l, kWo), dY, M, D, ED, LinearMode::kStore));
         CHECK_ST(recblr_gated_backward(Hx, Hz, P(l, kConvW), P(l, kConvB), d.K, P(l, kWr),
                                        P(l, kbr), P(l, kWi), P(l, kbi), P(l, kLam), nullptr, hb,
                                        dY, nullptr, dHx, dHz, G(l, kConvW), G(l, kConvB),
@@ -725,8 +747,8 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         // Hx = H Wx^T + bx, Hz = H Wz^T + bz; Y becomes dH of this layer's input.
         CHECK(linear_wgrad(c, Hl(l), dHx, G(l, kWx), G(l, kbx), M, ED, D));
         CHECK(linear_wgrad(c, Hl(l), dHz, G(l, kWz), G(l, kbz), M, ED, D));
-        CHECK(gemm_dyW(c, dHx, ED, P(l, kWx), Y, D, M, ED, D, 1.0f));
-        CHECK(gemm_dyW(c, dHz, ED, P(l, kWz), Y, D, M, ED, D, 1.0f));
+        CHECK(linear_dgrad(c, dHx, P(l, kWx), Y, M, ED, D, LinearMode::kAccumulate));
+        CHECK(linear_dgrad(c, dHz, P(l, kWz), Y, M, ED, D, LinearMode::kAccumulate));
     }
     // embedding LayerNorm, then the input side of dE: rows summed per item
     CHECK(ln_bwd<NV>(c, Y, E, ids, mu0, rs0, params + off[1], X, grads + off[1], grads + off[2], M,
