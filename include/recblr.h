@@ -251,8 +251,11 @@ int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
  *   loss = mean over rows of the cross entropy of softmax(logits) with targets.
  * Readings (the paper leaves them open): residual + LayerNorm after each
  * sub-layer, dropout as the identity, the cross entropy of the next item at
- * the last step.  The plain linear layers are rocBLAS fp32 GEMMs; all other
- * steps run in this library's kernels.
+ * the last step.  The linear layers of the behaviour-modelling layers run on
+ * this library's matrix-core kernels (fp32 products for the forward and the
+ * data gradients; bias, SiLU and its derivative fused in); the prediction
+ * layer's products are rocBLAS fp32 GEMMs; all other steps run in this
+ * library's kernels.
  *
  * Parameters are one flat float buffer, each tensor starting at a multiple of
  * 64 floats (recblr_model_param_offsets), weights [out][in], in this order:
@@ -284,9 +287,9 @@ int64_t recblr_model_param_offsets(const recblr_model_dims* m, int64_t* offsets,
  * layer, backward scratch, the sort of the item ids); 0 if unsupported. */
 size_t recblr_model_workspace_size(const recblr_model_dims* m);
 
-/* rocBLAS handle for the model step's GEMMs: created and destroyed by the
- * caller (creation allocates rocBLAS' own state; the step itself allocates
- * nothing).  A handle serves one stream at a time. */
+/* rocBLAS handle for the model step's prediction-layer GEMMs: created and
+ * destroyed by the caller (creation allocates rocBLAS' own state; the step
+ * itself allocates nothing).  A handle serves one stream at a time. */
 int recblr_blas_create(void** handle);
 int recblr_blas_destroy(void* handle);
 

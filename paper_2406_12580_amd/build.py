@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "librecblr.so")
 SOURCES = ["capi.cpp", "scan_fwd.hip", "scan_bwd.hip", "step.hip", "gemm.hip", "ablation.hip",
            "gated.hip", "model.hip"]
-# The plain linear layers of the full-model step are rocBLAS GEMMs.
+# The prediction layer of the full-model step uses rocBLAS GEMMs.
 LIBS = ["-L/opt/rocm/lib", "-lrocblas"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -5,8 +5,11 @@
 // residual connection and LayerNorm), and the prediction layer (section 2:
 // softmax over h_T E^T) with the cross entropy of the next item; then Adam.
 //
-// The plain linear layers are rocBLAS fp32 GEMMs; everything else runs in
-// the kernels of this library: the gated recurrent layer core through
+// The linear layers of the behaviour-modelling layers run on the matrix-core
+// kernels of gemm.hip (fp32 MFMAs for forward products and data gradients,
+// with the bias, SiLU and SiLU' in their epilogues; bf16-split tiles for the
+// weight gradients); the prediction layer's products are rocBLAS fp32 GEMMs;
+// everything else runs in the kernels of this library: the gated recurrent layer core through
 // recblr_gated_forward / recblr_gated_backward (conv, BD-LRU scan with its
 // gate projections, output gate), and here the embedding gather, the
 // LayerNorms, bias broadcasts, SiLU, the cross entropy, the sums over rows
