@@ -33,7 +33,8 @@ namespace model {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRowsPerWave = 4;  // rows of a LayerNorm kernel's workgroup per pass (one per wave)
+constexpr int kLnRows = 4;  // rows each wave of the LayerNorm forward normalises together
+constexpr int kRowsPerWave = 4 * kLnRows;  // rows of a LayerNorm forward workgroup (4 waves)
 constexpr int64_t kLnBwdRows = 256;  // rows per workgroup of the LayerNorm backward
 constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -57,38 +58,55 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
     float eps) {
     constexpr int D = 64 * NV;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t row = (int64_t)blockIdx.x * kRowsPerWave + wave_id();
-    if (row >= M) return;
-    float v[NV];
-    float bad = 0.0f;
-    const float* src = a + row * D;
-    if constexpr (EMB) {
-        const int64_t id = ids[row];
-        const bool ok = id >= 0 && id < V;
-        src = a + (ok ? id : 0) * D;
-        bad = ok ? 0.0f : __builtin_nanf("");
-    }
-    float sum = 0.0f;
+    // kLnRows rows per wave, normalised side by side (independent reductions
+    // in flight together).
+    const int64_t row0 = ((int64_t)blockIdx.x * 4 + wave_id()) * kLnRows;
+    float v[kLnRows][NV], m[kLnRows], rstd[kLnRows];
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        v[j] = src[lane + 64 * j] + bad;
-        if (!EMB && r) v[j] += r[row * D + lane + 64 * j];
-        sum += v[j];
-    }
-    const float m = wave_sum(sum) * (1.0f / D);
-    float var = 0.0f;
+    for (int q = 0; q < kLnRows; ++q) {
+        const int64_t row = row0 + q < M ? row0 + q : M - 1;  // tail rows recompute row M-1
+        float bad = 0.0f;
+        const float* src = a + row * D;
+        if constexpr (EMB) {
+            const int64_t id = ids[row];
+            const bool ok = id >= 0 && id < V;
+            src = a + (ok ? id : 0) * D;
+            bad = ok ? 0.0f : __builtin_nanf("");
+        }
 #pragma unroll
-    for (int j = 0; j < NV; ++j) var += (v[j] - m) * (v[j] - m);
-    const float rstd = 1.0f / sqrtf(wave_sum(var) * (1.0f / D) + eps);
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int c = lane + 64 * j;
-        if (s) s[row * D + c] = v[j];
-        y[row * D + c] = (v[j] - m) * rstd * g[c] + b[c];
+        for (int j = 0; j < NV; ++j) {
+            v[q][j] = src[lane + 64 * j] + bad;
+            if (!EMB && r) v[q][j] += r[row * D + lane + 64 * j];
+        }
     }
-    if (lane == 0) {
-        mu[row] = m;
-        rs[row] = rstd;
+#pragma unroll
+    for (int q = 0; q < kLnRows; ++q) {
+        float sum = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) sum += v[q][j];
+        m[q] = wave_sum(sum) * (1.0f / D);
+    }
+#pragma unroll
+    for (int q = 0; q < kLnRows; ++q) {
+        float var = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) var += (v[q][j] - m[q]) * (v[q][j] - m[q]);
+        rstd[q] = 1.0f / sqrtf(wave_sum(var) * (1.0f / D) + eps);
+    }
+#pragma unroll
+    for (int q = 0; q < kLnRows; ++q) {
+        const int64_t row = row0 + q;
+        if (row >= M) break;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int c = lane + 64 * j;
+            if (s) s[row * D + c] = v[q][j];
+            y[row * D + c] = (v[q][j] - m[q]) * rstd[q] * g[c] + b[c];
+        }
+        if (lane == 0) {
+            mu[row] = m[q];
+            rs[row] = rstd[q];
+        }
     }
 }
 
