@@ -77,7 +77,8 @@ enum {
     RECBLR_OP_BACKWARD = 3,
     RECBLR_OP_STEP = 4,
     RECBLR_OP_GATED_FORWARD = 5,
-    RECBLR_OP_GATED_BACKWARD = 6
+    RECBLR_OP_GATED_BACKWARD = 6,
+    RECBLR_OP_SCAN_BACKWARD_METHOD = 7
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -337,6 +338,31 @@ enum { RECBLR_SCAN_CHUNKED = 0, RECBLR_SCAN_SERIAL = 1, RECBLR_SCAN_TREE = 2 };
 int recblr_scan_forward_method(int method, const void* x, const void* z_r, const void* z_i,
                                const float* lambda, void* h, int64_t B, int64_t L, int64_t D,
                                int io, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of the same scan algorithms, for the training side of the
+ * ablation (the table times training epochs): dx, dz_r, dz_i and dLambda of
+ * the gated scan from h0 = 0 (no dL/dh_T, no dh0), given the forward output
+ * h and dh = dL/dh, by one of
+ *   RECBLR_SCAN_CHUNKED  the production kernels (recblr_bdlru_scan_backward);
+ *   RECBLR_SCAN_SERIAL   one thread per channel walks the sequence from
+ *                        t = L - 1 down (one wave per 64 channels);
+ *   RECBLR_SCAN_TREE     the two-tree scan of section 3.3 on the reversed
+ *                        sequence of pairs (alpha_{t+1}, dL/dh_t), padded at
+ *                        its end with the identity (embedding padding seen
+ *                        from the other end); L <= 4096.
+ * The adjoint delta_t = dL/dh_t + alpha_{t+1} delta_{t+1} is derived (the
+ * paper gives the forward only); the gradient formulas are those of
+ * recblr_bdlru_scan_backward.  Arguments as recblr_bdlru_scan_backward
+ * without h0, dhT and dh0; bf16 I/O takes bf16 z and writes bf16 dz.
+ * Workspace: recblr_workspace_size(RECBLR_OP_SCAN_BACKWARD_METHOD, ...) covers
+ * every method.  dLambda sums are in a fixed order (deterministic).
+ * Errors: as recblr_scan_forward_method.
+ */
+int recblr_scan_backward_method(int method, const void* x, const void* z_r, const void* z_i,
+                                const float* lambda, const void* h, const void* dh, void* dx,
+                                void* dz_r, void* dz_i, float* dlambda, int64_t B, int64_t L,
+                                int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Raw first-order recurrence h_t = a_t h_{t-1} + u_t (eq:linrnn with the

@@ -192,6 +192,11 @@ size_t recblr_workspace_size(int op, int64_t B, int64_t L, int64_t D, int io) {
         case RECBLR_OP_STEP: return step_ws(B, D, io);
         case RECBLR_OP_GATED_FORWARD: return gated_layout(B, L, D, io).total;
         case RECBLR_OP_GATED_BACKWARD: return gated_bwd_layout(B, L, D, io).total;
+        case RECBLR_OP_SCAN_BACKWARD_METHOD: {
+            const size_t a = scan_backward_workspace(B, L, D, io_of(io)),
+                         b = scan_backward_method_workspace(B, D);
+            return a > b ? a : b;
+        }
         default: return 0;
     }
 }
@@ -252,6 +257,40 @@ int recblr_scan_forward_method(int method, const void* x, const void* z_r, const
                   nullptr, 0};
     return status_of(method == RECBLR_SCAN_SERIAL ? launch_scan_forward_serial(a, (hipStream_t)stream)
                                                   : launch_scan_forward_tree(a, (hipStream_t)stream));
+}
+
+int recblr_scan_backward_method(int method, const void* x, const void* z_r, const void* z_i,
+                                const float* lambda, const void* h, const void* dh, void* dx,
+                                void* dz_r, void* dz_i, float* dlambda, int64_t B, int64_t L,
+                                int64_t D, int io, void* ws, size_t ws_bytes, void* stream) {
+    if (method == RECBLR_SCAN_CHUNKED)
+        return recblr_bdlru_scan_backward(x, z_r, z_i, lambda, nullptr, h, dh, nullptr, dx, dz_r,
+                                          dz_i, dlambda, nullptr, B, L, D, io, ws, ws_bytes,
+                                          stream);
+    if (method != RECBLR_SCAN_SERIAL && method != RECBLR_SCAN_TREE)
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (method == RECBLR_SCAN_TREE && !tree_scan_supported(L)) return RECBLR_ERR_UNSUPPORTED;
+    if (D == 0) return RECBLR_OK;
+    if (!lambda || !dlambda) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), dl = (size_t)D * 4;
+    if (B > 0 && L > 0 && (!x || !z_r || !z_i || !h || !dh || !dx || !dz_r || !dz_i))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i, h, dh, (const void*)dx, (const void*)dz_r,
+                          (const void*)dz_i})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!aligned(lambda, 4) || !aligned(dlambda, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{dx, n}, {dz_r, n}, {dz_i, n}, {dlambda, dl}},
+                  {{x, n}, {z_r, n}, {z_i, n}, {lambda, dl}, {h, n}, {dh, n}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    if (B == 0 || L == 0) return status_of(launch_fill(dlambda, 0.0f, D, strm));
+    st = check_ws(ws, ws_bytes, scan_backward_method_workspace(B, D));
+    if (st) return st;
+    ScanBwdArgs a{x, z_r, z_i, lambda, nullptr, h, dh, nullptr, dx, dz_r, dz_i, dlambda, nullptr,
+                  B, L, D, io_of(io), io_of(io), ws, ws_bytes};
+    return status_of(launch_scan_backward_method(method == RECBLR_SCAN_TREE, a, strm));
 }
 
 int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,

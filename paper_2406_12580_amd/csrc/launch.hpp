@@ -129,6 +129,12 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream);
 hipError_t launch_scan_forward_serial(const ScanFwdArgs& a, hipStream_t stream);
 hipError_t launch_scan_forward_tree(const ScanFwdArgs& a, hipStream_t stream);
 bool tree_scan_supported(int64_t L);
+// Backward of the same scan variants (h0 = 0, no dL/dh_T, no dh0): the serial
+// walk from t = L - 1 down, or the two-tree scan of the reversed sequence;
+// then the gate-gradient epilogue and dLambda.  a.ws takes
+// scan_backward_method_workspace(B, D) bytes; bf16 I/O uses bf16 z and dz.
+size_t scan_backward_method_workspace(int64_t B, int64_t D);
+hipError_t launch_scan_backward_method(bool tree, const ScanBwdArgs& a, hipStream_t stream);
 
 // Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5).
 // Conv taps are packed as [kConvTaps][D] (zero past K) plus a [D] bias.

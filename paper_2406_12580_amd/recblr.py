@@ -30,14 +30,14 @@ _lib = ctypes.CDLL(LIB_PATH)
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
 (OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP, OP_GATED_FORWARD,
- OP_GATED_BACKWARD) = range(7)
+ OP_GATED_BACKWARD, OP_SCAN_BACKWARD_METHOD) = range(8)
 SCAN_CHUNKED, SCAN_SERIAL, SCAN_TREE = range(3)
 
 EXPORTS = (
     "recblr_status_string", "recblr_workspace_size", "recblr_bdlru_scan_forward",
     "recblr_bdlru_scan_backward", "recblr_bdlru_scan_step", "recblr_bdlru_forward",
     "recblr_bdlru_backward", "recblr_bdlru_step", "recblr_linear_scan_forward",
-    "recblr_scan_forward_method", "recblr_gated_forward", "recblr_bdlru_scan_forward_timed",
+    "recblr_scan_forward_method", "recblr_scan_backward_method", "recblr_gated_forward", "recblr_bdlru_scan_forward_timed",
     "recblr_bdlru_scan_backward_timed", "recblr_gated_backward", "recblr_model_param_count",
     "recblr_model_param_offsets", "recblr_model_workspace_size", "recblr_blas_create",
     "recblr_blas_destroy", "recblr_model_train_step", "recblr_adam_update",
@@ -68,6 +68,8 @@ _SIGS = {
     "recblr_bdlru_step": ([_p] * 8 + [_i64] * 2 + [_int, _p, _sz, _p], _int),
     "recblr_linear_scan_forward": ([_p] * 5 + [_i64] * 3 + [_p], _int),
     "recblr_scan_forward_method": ([_int] + [_p] * 5 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
+    "recblr_scan_backward_method": ([_int] + [_p] * 10 + [_i64] * 3 + [_int, _p, _sz, _p],
+                                    _int),
     "recblr_gated_forward": ([_p] * 4 + [_int] + [_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p],
                              _int),
     "recblr_gated_backward": ([_p] * 4 + [_int] + [_p] * 19 + [_i64] * 3 + [_int, _p, _sz, _p],
@@ -253,6 +255,22 @@ def linear_scan_forward(a, u, h0=None, stream=None):
     _check(recblr_linear_scan_forward(_ptr(a), _ptr(u), _ptr(h0), _ptr(h), _ptr(hT), B, L, D,
                                       _stream(stream)), "recblr_linear_scan_forward")
     return h, hT
+
+
+def scan_backward_method(method, x, zr, zi, lam, h, dh, stream=None):
+    """Gated scan backward (zero initial state, no dL/dh_T) by one of SCAN_CHUNKED,
+    SCAN_SERIAL, SCAN_TREE. Returns dict dx, dzr, dzi (dtype of x), dlambda (float32)."""
+    B, L, D = x.shape
+    io = io_code(x.dtype)
+    out = {"dx": torch.empty_like(x), "dzr": torch.empty_like(x), "dzi": torch.empty_like(x),
+           "dlambda": torch.empty(D, dtype=torch.float32, device=x.device)}
+    ws, nws = _workspace(OP_SCAN_BACKWARD_METHOD, B, L, D, io, x.device)
+    _check(recblr_scan_backward_method(method, _ptr(x), _ptr(zr), _ptr(zi), _ptr(lam), _ptr(h),
+                                       _ptr(dh), _ptr(out["dx"]), _ptr(out["dzr"]),
+                                       _ptr(out["dzi"]), _ptr(out["dlambda"]), B, L, D, io,
+                                       _ptr(ws), nws, _stream(stream)),
+           "recblr_scan_backward_method")
+    return out
 
 
 def scan_forward_method(method, x, zr, zi, lam, stream=None):

@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 21
+    assert len(syms) == 22
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -174,6 +174,23 @@ def test_scan_method_validation(rb):
              None) == rb.ERR_UNSUPPORTED                                # unknown dtype
     assert f(rb.SCAN_TREE, None, None, None, None, None, 0, 3, 4, rb.F32, None, 0,
              None) == rb.OK                                             # empty batch
+
+
+def test_scan_backward_method_validation(rb):
+    """Backward of the ablation's scans: checks run before any launch."""
+    f = rb.recblr_scan_backward_method
+
+    def call(method=rb.SCAN_SERIAL, x=addr(0), dx=addr(6), B=2, L=3, D=4, io=rb.F32, nws=1 << 20):
+        return f(method, x, addr(1), addr(2), addr(3), addr(4), addr(5), dx, addr(7), addr(8),
+                 addr(9), B, L, D, io, addr(10), nws, None)
+    assert call(method=7) == rb.ERR_INVALID_ARGUMENT          # unknown method
+    assert call(method=rb.SCAN_TREE, L=5000) == rb.ERR_UNSUPPORTED  # tree longer than 4096
+    assert call(x=None) == rb.ERR_INVALID_ARGUMENT              # null x
+    assert call(dx=addr(0)) == rb.ERR_INVALID_ARGUMENT          # dx over x
+    assert call(io=5) == rb.ERR_UNSUPPORTED                     # unknown dtype
+    assert call(nws=0) == rb.ERR_WORKSPACE                      # workspace too small
+    need = rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD_METHOD, 2, 3, 4, rb.F32)
+    assert need >= rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, 2, 3, 4, rb.F32)
 
 
 def test_gated_forward_validation(rb):

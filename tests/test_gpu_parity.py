@@ -344,6 +344,22 @@ def test_scan_methods(rb, method, shape, io):
     assert_close(host(h), oh, io, f"{method} h")
 
 
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", ABLATION_SHAPES)
+@pytest.mark.parametrize("method", ["serial", "tree", "chunked"])
+def test_scan_backward_methods(rb, method, shape, io):
+    """Backward of the ablation's scans (zero initial state) against the oracle."""
+    B, L, D = shape
+    inp = dg.scan_inputs(B, L, D, 6200 + B + L + D, io=io, grad=True)
+    m = {"serial": rb.SCAN_SERIAL, "tree": rb.SCAN_TREE, "chunked": rb.SCAN_CHUNKED}[method]
+    X, ZR, ZI, lam = dev(inp.x, io), dev(inp.zr, io), dev(inp.zi, io), dev32(inp.lam)
+    h = rb.scan_forward_method(m, X, ZR, ZI, lam)
+    g = rb.scan_backward_method(m, X, ZR, ZI, lam, h, dev(inp.dh, io))
+    want = oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh)
+    for k in ("dx", "dzr", "dzi", "dlambda"):
+        assert_close(host(g[k]), want[k], io, f"{method} {k}")
+
+
 def test_tree_scan_sequence_padding(rb):
     """Sequence padding: inputs left-padded to a power of two with zero x
     (any z) give the unpadded result on the real positions (zero state)."""
