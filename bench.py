@@ -325,10 +325,13 @@ def model_main(args, torch, dg, rb):
 
 
 def ablation_main(args, torch, dg, rb):
-    """Layer forward (projections + scan) per scan algorithm.
+    """Layer forward, and forward + backward (the training step the paper's table
+    times), per scan algorithm.
 
     proj(len) is measured as recblr_bdlru_forward minus the production scan at
-    that length; each scheme's time is proj(its length) + its scan:
+    that length (and proj_b(len) as recblr_bdlru_backward minus the production
+    scan backward); each scheme's time is the projections at its length plus
+    its scans:
       serial:   proj(L)  + serial scan(L)
       tree_sp:  proj(P)  + tree scan of inputs left-padded to P (sequence padding)
       tree_ep:  proj(L)  + tree scan padding to P inside (embedding padding)
@@ -371,18 +374,42 @@ def ablation_main(args, torch, dg, rb):
         t["serial"] = timed(lambda: rb.scan_forward_method(rb.SCAN_SERIAL, X, ZR, ZI, lam), reps)
         t["tree_sp"] = timed(lambda: rb.scan_forward_method(rb.SCAN_TREE, XP, ZRP, ZIP, lam), reps)
         t["tree_ep"] = timed(lambda: rb.scan_forward_method(rb.SCAN_TREE, X, ZR, ZI, lam), reps)
+        # backward: dL/dh ~ N(0, 1); h from the production forward
+        g = np.random.default_rng(7100 + L).standard_normal((B, L, D)).astype(np.float32)
+        DH, DHP = T(g), T(np.pad(g, padw))
+        H = rb.scan_forward_method(rb.SCAN_CHUNKED, X, ZR, ZI, lam)
+        HP = rb.scan_forward_method(rb.SCAN_CHUNKED, XP, ZRP, ZIP, lam)
+        HL, _ = rb.bdlru_forward(X, Wr, br, Wi, bi, lam)
+        HLP, _ = rb.bdlru_forward(XP, Wr, br, Wi, bi, lam)
+        bwd = lambda m, *a: rb.scan_backward_method(m, *a)
+        t["layer_b_L"] = timed(lambda: rb.bdlru_backward(X, Wr, br, Wi, bi, lam, HL, DH), reps)
+        t["layer_b_P"] = timed(lambda: rb.bdlru_backward(XP, Wr, br, Wi, bi, lam, HLP, DHP), reps)
+        t["b_chunked_L"] = timed(lambda: bwd(rb.SCAN_CHUNKED, X, ZR, ZI, lam, H, DH), reps)
+        t["b_chunked_P"] = timed(lambda: bwd(rb.SCAN_CHUNKED, XP, ZRP, ZIP, lam, HP, DHP), reps)
+        t["b_serial"] = timed(lambda: bwd(rb.SCAN_SERIAL, X, ZR, ZI, lam, H, DH), reps)
+        t["b_tree_sp"] = timed(lambda: bwd(rb.SCAN_TREE, XP, ZRP, ZIP, lam, HP, DHP), reps)
+        t["b_tree_ep"] = timed(lambda: bwd(rb.SCAN_TREE, X, ZR, ZI, lam, H, DH), reps)
         proj_L, proj_P = t["layer_L"] - t["chunked_L"], t["layer_P"] - t["chunked_P"]
+        projb_L, projb_P = t["layer_b_L"] - t["b_chunked_L"], t["layer_b_P"] - t["b_chunked_P"]
         row = {"workload": name, "B": B, "L": L, "padded": P, "D": D,
                "us_scan": {k: round(t[k], 1) for k in ("serial", "tree_sp", "tree_ep", "chunked_L")},
+               "us_scan_backward": {k: round(t["b_" + k], 1)
+                                    for k in ("serial", "tree_sp", "tree_ep", "chunked_L")},
                "us_projection": {"L": round(proj_L, 1), "padded": round(proj_P, 1)},
+               "us_projection_backward": {"L": round(projb_L, 1), "padded": round(projb_P, 1)},
                "us_layer_forward": {"serial": round(proj_L + t["serial"], 1),
                                     "tree_sp": round(proj_P + t["tree_sp"], 1),
                                     "tree_ep": round(proj_L + t["tree_ep"], 1),
-                                    "chunked": round(t["layer_L"], 1)}}
+                                    "chunked": round(t["layer_L"], 1)},
+               "us_layer_train": {
+                   "serial": round(proj_L + projb_L + t["serial"] + t["b_serial"], 1),
+                   "tree_sp": round(proj_P + projb_P + t["tree_sp"] + t["b_tree_sp"], 1),
+                   "tree_ep": round(proj_L + projb_L + t["tree_ep"] + t["b_tree_ep"], 1),
+                   "chunked": round(t["layer_L"] + t["layer_b_L"], 1)}}
         log(json.dumps(row))
         rows.append(row)
-    first = rows[0]["us_layer_forward"]
-    out = {"metric": "BD-LRU layer forward, serial-scan time over chunked-scan time "
+    first = rows[0]["us_layer_train"]
+    out = {"metric": "BD-LRU layer forward + backward, serial-scan time over chunked-scan time "
                      "(efficiency-ablation analogue, ml1m-like)",
            "value": first["serial"] / first["chunked"], "unit": "x", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
