@@ -228,6 +228,9 @@ __global__ __launch_bounds__(256) void conv_bwd_kernel(
         if (t0 >= 3) load_vec<T, VEC>(hx, (rowb + (t0 - 3) * D) * (int64_t)sizeof(T), h3);
         if (t0 >= 2) load_vec<T, VEC>(hx, (rowb + (t0 - 2) * D) * (int64_t)sizeof(T), h2);
         if (t0 >= 1) load_vec<T, VEC>(hx, (rowb + (t0 - 1) * D) * (int64_t)sizeof(T), h1);
+        // Unrolled for fp32 inputs, whose loads then overlap across steps
+        // (c4-shaped backward 1414 -> 1365 us); bf16 measured slower unrolled.
+#pragma unroll(sizeof(T) == 4 ? 4 : 1)
         for (int64_t t = t0; t < end + 3; ++t) {
             float dcv[VEC], x0[VEC];
             if (t < tend) {
