@@ -180,8 +180,13 @@ int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const
                           int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
                           void* stream);
 
-/* Full single step: projections of x_t, then one recurrent step.
- *   x : [B][D] io;  h_prev, h_next : [B][D] float (h_next may == h_prev) */
+/* Full single step: projections of x_t, then one recurrent step
+ * (section 3.2 gates, eq:linrnn), z kept on chip.
+ *   x : [B][D] io;  h_prev, h_next : [B][D] float (h_next may == h_prev)
+ * For bf16 I/O with D in {64, 128, 192, 256} (x, W_r, W_i 16-byte aligned)
+ * persistent workgroups keep W_r and W_i in registers and the workspace is
+ * not touched; other cases use the workspace of
+ * recblr_workspace_size(RECBLR_OP_STEP, ...). */
 int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const void* W_i,
                       const void* b_i, const float* lambda, const float* h_prev, float* h_next,
                       int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
