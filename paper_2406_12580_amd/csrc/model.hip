@@ -132,15 +132,17 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
         ag[j] = ab[j] = 0.0f;
         gc[j] = g[lane + 64 * j];
     }
-    for (int64_t row = r0 + w; row < r1; row += 4) {
+    // Rows w, w + 4, ... of the block, two at a time so that their loads and
+    // reductions overlap; the gamma / beta sums still add rows in order.
+    auto row_grad = [&](int64_t row, float (&xh)[NV], float (&d)[NV], float (&gd)[NV],
+                        float& s1, float& s2) {
         const float* src = s + row * D;
         if constexpr (EMB) {
             const int64_t id = ids[row];
             src = s + (id >= 0 && id < V ? id : 0) * D;
         }
         const float m = mu[row], rstd = rs[row];
-        float xh[NV], d[NV], gd[NV];
-        float s1 = 0.0f, s2 = 0.0f;
+        s1 = s2 = 0.0f;
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             const int c = lane + 64 * j;
@@ -150,13 +152,31 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
             s1 += gd[j];
             s2 += gd[j] * xh[j];
         }
-        const float m1 = wave_sum(s1) * (1.0f / D), m2 = wave_sum(s2) * (1.0f / D);
+    };
+    auto row_out = [&](int64_t row, const float (&xh)[NV], const float (&d)[NV],
+                       const float (&gd)[NV], float m1, float m2) {
+        const float rstd = rs[row];
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             dx[row * D + lane + 64 * j] = rstd * (gd[j] - m1 - xh[j] * m2);
             ag[j] = fmaf(d[j], xh[j], ag[j]);
             ab[j] += d[j];
         }
+    };
+    int64_t row = r0 + w;
+    for (; row + 4 < r1; row += 8) {
+        float xa[NV], da[NV], ga[NV], xb[NV], db[NV], gb[NV], s1a, s2a, s1b, s2b;
+        row_grad(row, xa, da, ga, s1a, s2a);
+        row_grad(row + 4, xb, db, gb, s1b, s2b);
+        const float m1a = wave_sum(s1a) * (1.0f / D), m2a = wave_sum(s2a) * (1.0f / D);
+        const float m1b = wave_sum(s1b) * (1.0f / D), m2b = wave_sum(s2b) * (1.0f / D);
+        row_out(row, xa, da, ga, m1a, m2a);
+        row_out(row + 4, xb, db, gb, m1b, m2b);
+    }
+    if (row < r1) {
+        float xa[NV], da[NV], ga[NV], s1a, s2a;
+        row_grad(row, xa, da, ga, s1a, s2a);
+        row_out(row, xa, da, ga, wave_sum(s1a) * (1.0f / D), wave_sum(s2a) * (1.0f / D));
     }
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
