@@ -46,36 +46,79 @@ __global__ __launch_bounds__(kGateThreads) void conv_silu_kernel(const T* __rest
     store(xp + e, c * sigmoid(c));
 }
 
-// The same with 16-byte loads: V = 16 / sizeof(T) consecutive channels per
-// thread (D % V == 0, 16-byte aligned tensors).
+// The same with 16-byte loads (D % V == 0, 16-byte aligned tensors), each
+// thread on kConvRun consecutive steps of one vector of V = 16 / sizeof(T)
+// channels: every hx row it needs is loaded once and slides
+// through registers (kConvRun + 3 row loads for kConvRun outputs instead of
+// 4 per output).  Threads of a wave take consecutive channel vectors of the
+// same rows.
+constexpr int kConvRun = 4;
 template <typename T, typename TO>
-__global__ __launch_bounds__(kGateThreads) void conv_silu_vec_kernel(
+__global__ __launch_bounds__(kGateThreads) void conv_silu_run_kernel(
     const T* __restrict__ hx, const float* __restrict__ w4, const float* __restrict__ b4,
-    TO* __restrict__ xp, int64_t L, int64_t D, int64_t nvec) {
+    TO* __restrict__ xp, int64_t L, int64_t D, int64_t nthreads) {
     constexpr int V = 16 / sizeof(T);
-    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (q >= nvec) return;
-    const int64_t e = q * V;
-    const int64_t d = e % D, t = (e / D) % L;
-    float c[V];
-#pragma unroll
-    for (int i = 0; i < V; ++i) c[i] = b4[d + i];
-#pragma unroll
-    for (int j = 0; j < kConvTaps; ++j) {
-        if (t - j < 0) break;
-        const uint4 raw = *(const uint4*)(hx + e - j * D);
-        const T* v = (const T*)&raw;
-#pragma unroll
-        for (int i = 0; i < V; ++i) c[i] = fmaf(w4[j * D + d + i], to_f32(v[i]), c[i]);
-    }
     constexpr int VO = 16 / sizeof(TO);  // outputs per 16-byte store
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= nthreads) return;
+    const int64_t dv = D / V, nrun = (L + kConvRun - 1) / kConvRun;
+    const int64_t vec = q % dv, rest = q / dv;
+    const int64_t run = rest % nrun, b = rest / nrun;
+    const int64_t d = vec * V, t0 = run * kConvRun;
+    float w[kConvTaps][V], bias[V];
 #pragma unroll
-    for (int s0 = 0; s0 < V; s0 += VO) {
-        uint4 out;
-        TO* o = (TO*)&out;
+    for (int i = 0; i < V; ++i) {
+        bias[i] = b4[d + i];
 #pragma unroll
-        for (int i = 0; i < VO; ++i) o[i] = from_f32<TO>(c[s0 + i] * sigmoid(c[s0 + i]));
-        *(uint4*)(xp + e + s0) = out;
+        for (int j = 0; j < kConvTaps; ++j) w[j][i] = w4[j * D + d + i];
+    }
+    const T* row0 = hx + b * L * D + d;  // (b, 0, d)
+    // win[j] = hx at step t - j (zero before the sequence start)
+    float win[kConvTaps][V];
+#pragma unroll
+    for (int j = 1; j < kConvTaps; ++j) {
+        const int64_t t = t0 - j;
+        if (t >= 0) {
+            const uint4 raw = *(const uint4*)(row0 + t * D);
+            const T* v = (const T*)&raw;
+#pragma unroll
+            for (int i = 0; i < V; ++i) win[j][i] = to_f32(v[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) win[j][i] = 0.0f;
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < kConvRun; ++s) {
+        const int64_t t = t0 + s;
+        if (t >= L) break;
+        {
+            const uint4 raw = *(const uint4*)(row0 + t * D);
+            const T* v = (const T*)&raw;
+#pragma unroll
+            for (int i = 0; i < V; ++i) win[0][i] = to_f32(v[i]);
+        }
+        float c[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            float acc = bias[i];
+#pragma unroll
+            for (int j = 0; j < kConvTaps; ++j) acc = fmaf(w[j][i], win[j][i], acc);
+            c[i] = acc;
+        }
+        TO* dst = xp + (b * L + t) * D + d;
+#pragma unroll
+        for (int s0 = 0; s0 < V; s0 += VO) {
+            uint4 out;
+            TO* o = (TO*)&out;
+#pragma unroll
+            for (int i = 0; i < VO; ++i) o[i] = from_f32<TO>(c[s0 + i] * sigmoid(c[s0 + i]));
+            *(uint4*)(dst + s0) = out;
+        }
+#pragma unroll
+        for (int j = kConvTaps - 1; j > 0; --j)
+#pragma unroll
+            for (int i = 0; i < V; ++i) win[j][i] = win[j - 1][i];
     }
 }
 
@@ -528,12 +571,13 @@ template <typename T, typename TO>
 hipError_t conv_silu_t(const void* hx, const float* w4, const float* b4, void* xp, int64_t L,
                        int64_t D, int64_t n, hipStream_t stream) {
     constexpr int V = 16 / sizeof(T);
+    if (n == 0) return hipSuccess;
     if (D % V == 0 && ((uintptr_t)hx | (uintptr_t)xp) % 16 == 0) {
-        const int64_t nvec = n / V;
-        hipLaunchKernelGGL((conv_silu_vec_kernel<T, TO>),
-                           dim3((unsigned)((nvec + kGateThreads - 1) / kGateThreads)),
+        const int64_t nthreads = (n / (L * D)) * ((L + kConvRun - 1) / kConvRun) * (D / V);
+        hipLaunchKernelGGL((conv_silu_run_kernel<T, TO>),
+                           dim3((unsigned)((nthreads + kGateThreads - 1) / kGateThreads)),
                            dim3(kGateThreads), 0, stream, (const T*)hx, w4, b4, (TO*)xp, L, D,
-                           nvec);
+                           nthreads);
     } else {
         hipLaunchKernelGGL((conv_silu_kernel<T, TO>),
                            dim3((unsigned)((n + kGateThreads - 1) / kGateThreads)),
