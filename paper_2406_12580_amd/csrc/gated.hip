@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kGateThreads) void conv_silu_kernel(const T* __rest
 // through registers (kConvRun + 3 row loads for kConvRun outputs instead of
 // 4 per output).  Threads of a wave take consecutive channel vectors of the
 // same rows.
-constexpr int kConvRun = 4;
+constexpr int kConvRun = 4;  // 2 and 8 measured slower or no faster on the c4 / c5 shapes
 template <typename T, typename TO>
 __global__ __launch_bounds__(kGateThreads) void conv_silu_run_kernel(
     const T* __restrict__ hx, const float* __restrict__ w4, const float* __restrict__ b4,
