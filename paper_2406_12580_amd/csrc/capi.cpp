@@ -595,7 +595,7 @@ int recblr_bdlru_backward(const void* x, const void* W_r, const void* b_r, const
     }
     const int64_t M = B * L;
     void* pack = at(ws, lay.pack);
-    if (L > 0 && fused_backward_applies(B, L, D, io_of(io), x, pack)) {
+    if (L > 0 && fused_backward_applies(B, L, D, io_of(io), x, h, pack)) {
         // The scan backward recomputes z on the matrix cores (z never reaches HBM).
         if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
             return RECBLR_ERR_HIP;

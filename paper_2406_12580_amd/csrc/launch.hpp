@@ -122,7 +122,7 @@ struct FusedBwdArgs {
     void* ws;
 };
 bool fused_backward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
-                            const void* pack);
+                            const void* h, const void* pack);
 size_t fused_backward_workspace(int64_t B, int64_t L, int64_t D);
 hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream);
 

@@ -941,10 +941,12 @@ static BwdPlan plan_fused_backward(int64_t B, int64_t L, int64_t D) {
 }
 
 bool fused_backward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
-                            const void* pack) {
+                            const void* h, const void* pack) {
     const size_t esz = io_bytes(io);
+    // x and h are staged with 16-byte direct-to-LDS loads (stage_rows): both
+    // must start on a 16-byte boundary, as must the packed weights.
     return B > 0 && L > 0 && D > 0 && D % kWave == 0 &&
-           ((uintptr_t)x | (uintptr_t)pack) % 16 == 0 &&
+           ((uintptr_t)x | (uintptr_t)h | (uintptr_t)pack) % 16 == 0 &&
            (L + fastmm::BM) * D * (int64_t)esz < ((int64_t)1 << 31);
 }
 

@@ -16,6 +16,8 @@ this module raises.  Build it first with ``python -m paper_2406_12580_amd.build`
 from __future__ import annotations
 
 import ctypes
+import functools
+import inspect
 import os
 
 import torch
@@ -125,6 +127,29 @@ def _stream(stream=None):
     return s.cuda_stream
 
 
+def _on_stream(fn):
+    """Run a wrapper with its `stream` argument as torch's current stream.
+
+    The workspace and outputs are then allocated by torch's caching allocator
+    on the stream the kernels are launched on, so the workspace, released when
+    the wrapper returns, is handed out again only to later work on that same
+    stream (which runs after the launched kernels).  Without a `stream`
+    argument nothing changes: torch's current stream is the launch stream.
+    """
+    sig = inspect.signature(fn)
+
+    @functools.wraps(fn)
+    def wrapper(*args, **kwargs):
+        bound = sig.bind(*args, **kwargs)
+        s = bound.arguments.get("stream")
+        if s is None:
+            return fn(*args, **kwargs)
+        bound.arguments["stream"] = None
+        with torch.cuda.stream(s):
+            return fn(*bound.args, **bound.kwargs)
+    return wrapper
+
+
 def _workspace(op: int, B: int, L: int, D: int, io: int, device):
     n = recblr_workspace_size(op, B, L, D, io)
     if n == 0:
@@ -146,6 +171,7 @@ def _io(t, shape, dtype, name):
     return t
 
 
+@_on_stream
 def bdlru_scan_forward(x, zr, zi, lam, h0=None, stream=None):
     """Gated BD-LRU scan from pre-activations. Returns (h [B,L,D] io, hT [B,D] float32)."""
     B, L, D = x.shape
@@ -161,6 +187,7 @@ def bdlru_scan_forward(x, zr, zi, lam, h0=None, stream=None):
     return h, hT
 
 
+@_on_stream
 def bdlru_scan_backward(x, zr, zi, lam, h, dh, h0=None, dhT=None, stream=None):
     """Backward of bdlru_scan_forward. Returns dict dx, dzr, dzi, dlambda, dh0."""
     B, L, D = x.shape
@@ -180,6 +207,7 @@ def bdlru_scan_backward(x, zr, zi, lam, h, dh, h0=None, dhT=None, stream=None):
     return out
 
 
+@_on_stream
 def bdlru_scan_step(x, zr, zi, lam, h_prev, out=None, stream=None):
     """One recurrent step over [B, D]; returns h_next (float32). out may be h_prev."""
     B, D = x.shape
@@ -193,6 +221,7 @@ def bdlru_scan_step(x, zr, zi, lam, h_prev, out=None, stream=None):
     return h_next
 
 
+@_on_stream
 def bdlru_forward(x, Wr, br, Wi, bi, lam, h0=None, stream=None):
     """Full forward with gate projections. Returns (h, hT)."""
     B, L, D = x.shape
@@ -212,6 +241,7 @@ def bdlru_forward(x, Wr, br, Wi, bi, lam, h0=None, stream=None):
     return h, hT
 
 
+@_on_stream
 def bdlru_backward(x, Wr, br, Wi, bi, lam, h, dh, h0=None, dhT=None, stream=None):
     """Full backward. Returns dict dx, dWr, dbr, dWi, dbi, dlambda, dh0."""
     B, L, D = x.shape
@@ -234,6 +264,7 @@ def bdlru_backward(x, Wr, br, Wi, bi, lam, h, dh, h0=None, dhT=None, stream=None
     return out
 
 
+@_on_stream
 def bdlru_step(x, Wr, br, Wi, bi, lam, h_prev, out=None, stream=None):
     """Full single step with gate projections; returns h_next (float32)."""
     B, D = x.shape
@@ -247,6 +278,7 @@ def bdlru_step(x, Wr, br, Wi, bi, lam, h_prev, out=None, stream=None):
     return h_next
 
 
+@_on_stream
 def linear_scan_forward(a, u, h0=None, stream=None):
     """Raw recurrence h_t = a_t h_{t-1} + u_t (float32). Returns (h, hT)."""
     B, L, D = a.shape
@@ -257,6 +289,7 @@ def linear_scan_forward(a, u, h0=None, stream=None):
     return h, hT
 
 
+@_on_stream
 def scan_backward_method(method, x, zr, zi, lam, h, dh, stream=None):
     """Gated scan backward (zero initial state, no dL/dh_T) by one of SCAN_CHUNKED,
     SCAN_SERIAL, SCAN_TREE. Returns dict dx, dzr, dzi (dtype of x), dlambda (float32)."""
@@ -273,6 +306,7 @@ def scan_backward_method(method, x, zr, zi, lam, h, dh, stream=None):
     return out
 
 
+@_on_stream
 def scan_forward_method(method, x, zr, zi, lam, stream=None):
     """Gated scan forward (zero initial state) by one of SCAN_CHUNKED, SCAN_SERIAL,
     SCAN_TREE (the efficiency-ablation variants). Returns h."""
@@ -286,6 +320,7 @@ def scan_forward_method(method, x, zr, zi, lam, stream=None):
     return h
 
 
+@_on_stream
 def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None, keep_h=True,
                   stream=None):
     """Gated recurrent layer core: y = BD-LRU(SiLU(conv(hx))) * SiLU(hz).
@@ -304,6 +339,7 @@ def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None, keep_h=T
     return y, h, hT
 
 
+@_on_stream
 def gated_backward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h, dy, h0=None, dhT=None,
                    stream=None):
     """Backward of gated_forward (h: its BD-LRU output).  Returns a dict with dhx,
@@ -374,6 +410,7 @@ class ModelStep:
         except Exception:
             pass
 
+    @_on_stream
     def train_step(self, params, ids, targets, grads=None, loss=None, stream=None):
         """Loss and gradients (flat, the parameter layout) of one batch."""
         if grads is None:
@@ -387,6 +424,7 @@ class ModelStep:
         return loss, grads
 
 
+@_on_stream
 def adam_update(params, grads, m1, m2, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
                 stream=None):
     _check(recblr_adam_update(_ptr(params), _ptr(grads), _ptr(m1), _ptr(m2), params.numel(),

@@ -22,6 +22,31 @@ def floored_rel_err(got, want):
     return float(np.max(np.abs(got - want) / denom))
 
 
+def error_report(got, want):
+    """Three views of the error of one output tensor: the floored relative
+    error the bar applies to, the same with a floor of 1e-3 rms (close to a
+    plain elementwise relative error wherever |want| is not tiny), and the
+    normwise max|g - o| / max|o|."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    if want.size == 0:
+        return {"floored": 0.0, "tight": 0.0, "normwise": 0.0}
+    diff = np.abs(got - want)
+    rms = float(np.sqrt(np.mean(want * want)))
+    mx = float(np.max(np.abs(want)))
+    return {"floored": float(np.max(diff / (np.abs(want) + rms))) if rms else float(diff.max()),
+            "tight": float(np.max(diff / (np.abs(want) + 1e-3 * rms))) if rms else float(diff.max()),
+            "normwise": float(diff.max() / mx) if mx else float(diff.max())}
+
+
+def report(tag, got, want):
+    """Print the error report of one output (collected from the GPU logs)."""
+    r = error_report(got, want)
+    print(f"ERR {tag}: floored {r['floored']:.2e} tight {r['tight']:.2e} "
+          f"normwise {r['normwise']:.2e}", flush=True)
+    return r
+
+
 def assert_close(got, want, io, name=""):
     err = floored_rel_err(got, want)
     assert np.all(np.isfinite(np.asarray(got, dtype=np.float64))), f"{name}: non-finite output"

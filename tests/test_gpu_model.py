@@ -4,10 +4,13 @@ recblr_adam_update) against the fp64 oracle of oracle/model.py.
 Every gradient tensor is compared with the floored relative error of the
 other parity tests at the fp32 bar (1e-4).
 """
+import os
+import sys
+
 import numpy as np
 import pytest
 
-from helpers import assert_close
+from helpers import assert_close, report
 from oracle import model as om
 from paper_2406_12580_amd import datagen as dg
 
@@ -121,4 +124,38 @@ def test_out_of_range_ids_give_nan_loss(rb):
     loss2, _ = step.train_step(P, torch.from_numpy(ids).cuda(), torch.from_numpy(bad_t).cuda())
     torch.cuda.synchronize()
     assert np.isnan(loss.item()) and np.isnan(loss2.item())
+    step.close()
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "model_ml1m_oracle.npz")
+
+
+def test_model_train_step_ml1m(rb):
+    """The MovieLens-1M training shape the model bench times (batch 2048,
+    length 200, D = 64, E = 2, two layers, 3,416 items): every gradient tensor
+    against the fp64 oracle's, stored by tests/golden/make_model_golden.py
+    (the oracle takes minutes at this size) for the same seeded inputs."""
+    import torch
+    sys.path.insert(0, os.path.dirname(GOLDEN))
+    import make_model_golden as mg
+    dims, named, ids, targets, flat64 = mg.inputs()
+    golden = np.load(GOLDEN, allow_pickle=False)
+    assert str(golden["fingerprint"]) == mg.fingerprint(flat64, ids, targets), \
+        "the seeded inputs changed since the oracle result was stored"
+    rd, P, _ = _device_params(rb, dims, named)
+    step = rb.ModelStep(rd)
+    loss, grads = step.train_step(P, torch.from_numpy(ids).cuda(),
+                                  torch.from_numpy(targets).cuda())
+    torch.cuda.synchronize()
+    print(f"model step {dims}: GPU done", flush=True)
+    g = grads.cpu().numpy()
+    want_loss, want = float(golden["loss"]), golden["grads"].astype(np.float64)
+    assert abs(loss.item() - want_loss) <= 1e-4 * abs(want_loss), (loss.item(), want_loss)
+    lay, _ = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
+    offs = rb.model_param_offsets(rd)
+    for (name, shape, o_ref), o in zip(lay, offs):
+        n = int(np.prod(shape))
+        report(f"model ml1m {name}", g[o:o + n], want[o_ref:o_ref + n])
+        assert_close(g[o:o + n], want[o_ref:o_ref + n], "f32", name)
     step.close()
