@@ -25,10 +25,13 @@ layers, softmax cross entropy, backward, Adam) at the MovieLens-1M training
 shape of the paper (B=2048, T=200, D=64, E=2, 3,416 items); its roofline is
 matrix-multiply flops against the fp32 matrix-core peak.
 Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
-fp64 CPU oracle timed on a bounded sample of the same workload).  With the
-scan API the roofline takes the scan kernel's own duration, from a HIP event
-pair the library records on the launch stream right around that kernel
-(recblr_bdlru_scan_*_timed); the other APIs report it for the whole call.
+fp64 CPU oracle timed on a bounded sample of the same workload).  `value` and
+`ms_per_step` come from K steps timed back to back with no events in between
+(a HIP event costs about 5 us of stream time on each side of what it
+brackets).  With the scan API the roofline takes the scan kernel's own
+duration, from a HIP event pair that the library stamps with that kernel's
+dispatch start and end (recblr_bdlru_scan_*_timed), over K further steps; the
+other APIs report it for the whole call, from an event pass of their own.
 """
 from __future__ import annotations
 
@@ -124,11 +127,61 @@ def cpu_baseline(cfg, api="scan", target_s=10.0):
         total += run(rows)
         passes += 1
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": passes * rows * per_row / total, "unit": "elements/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"fp64 oracle {'layer' if api == 'full' else 'scan'} forward+backward "
-                      f"over {rows} of {cfg.B} batch rows "
-                      f"(L={cfg.L}, D={cfg.D}), {passes} passes, {total:.1f} s"}
+    out = {"value": passes * rows * per_row / total, "unit": "elements/s", "cores": threads,
+           "kind": "oracle",
+           "sample": f"fp64 oracle {'layer' if api == 'full' else 'scan'} forward+backward "
+                     f"over {rows} of {cfg.B} batch rows "
+                     f"(L={cfg.L}, D={cfg.D}), {passes} passes, {total:.1f} s",
+           "cpu_model": cpu_model()}
+    if api == "scan":
+        out["single_thread"] = single_thread_oracle()
+    return out
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo, as lscpu reports it)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+_ONE_THREAD = """
+import sys, time
+sys.path.insert(0, {root!r})
+import oracle
+from paper_2406_12580_amd import datagen as dg
+for name in ("c1", "c2"):
+    cfg = dg.CONFIGS[name]
+    inp = dg.config_inputs(cfg, grad=True)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        oracle.scan_forward(inp.x, inp.zr, inp.zi, inp.lam)
+        oracle.scan_backward(inp.x, inp.zr, inp.zi, inp.lam, inp.dh)
+        n += 1
+        dt = time.perf_counter() - t0
+        if dt > 1.0:
+            break
+    print(name, n * cfg.B * cfg.L * cfg.D / dt, flush=True)
+"""
+
+
+def single_thread_oracle():
+    """fp64 oracle scan forward+backward on one thread (OMP_NUM_THREADS=1, a
+    child process) for the two small workloads, in elements/s."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    res = subprocess.run([sys.executable, "-c", _ONE_THREAD.format(root=ROOT)], env=env,
+                         capture_output=True, text=True, timeout=300)
+    out = {}
+    for line in res.stdout.splitlines():
+        name, v = line.split()
+        out[name] = float(v)
+    return out
 
 
 # Shapes of the paper's efficiency ablation: sequence lengths 200, 100 and 257
@@ -186,8 +239,14 @@ def gated_main(args, torch, dg, rb):
         bwd()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     t0 = time.perf_counter()
+    for k in range(K):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    # call split from a separate, untimed pass with events around the calls
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     for k in range(K):
         ev[k][0].record(s)
         fwd()
@@ -195,7 +254,6 @@ def gated_main(args, torch, dg, rb):
         bwd()
         ev[k][2].record(s)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     t_f = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e-3
     t_b = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
     N = B * L * D
@@ -279,15 +337,15 @@ def model_main(args, torch, dg, rb):
     torch.cuda.synchronize()
     first = loss.item()
     K = args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     t0 = time.perf_counter()
     ev[0].record()
     for k in range(K):
         one()
-        ev[k + 1].record()
+    ev[1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    dts = np.array([ev[0].elapsed_time(ev[1]) / K]) * 1e-3
     tokens = d.B * d.T
     fl = model_flops(d)
     ach = fl / float(np.mean(dts)) / 1e12
@@ -470,16 +528,16 @@ def decode_main(args, torch, dg, rb):
         step(j)
     torch.cuda.synchronize()
     K = args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     stream = torch.cuda.current_stream()
     t0 = time.perf_counter()
     ev[0].record(stream)
     for k in range(K):
         step(args.warmup + k)
-        ev[k + 1].record(stream)
+    ev[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    dts = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(K)]) * 1e-3
+    dts = np.array([ev[0].elapsed_time(ev[1]) / K]) * 1e-3
     N = B * D
     ach = arrays_bytes * N / float(np.mean(dts)) / 1e9
     log(f"step {np.mean(dts)*1e6:.1f} us ({ach:.0f} GB/s)  wall/step {wall/K*1e6:.1f} us")
@@ -637,38 +695,47 @@ def main():
         bwd()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     kernel_ev = None
     if args.api == "scan":
         # torch creates an event on its first record; record each once so that
-        # the raw handles exist before the library records them.
+        # the raw handles exist before the library uses them.
         kernel_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
         for row in kernel_ev:
             for e in row:
                 e.record(stream)
     torch.cuda.synchronize()
+    # Timed region: K steps back to back, no events (an event costs about 5 us
+    # of stream time on each side of the kernel it brackets).
     t0 = time.perf_counter()
     for k in range(K):
-        ev[k][0].record(stream)
-        if kernel_ev is not None:
-            # Every event record costs stream time, so the split between the
-            # calls is the forward kernel's end event (only that kernel runs
-            # after it in the forward call).
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if kernel_ev is not None:
+        # Kernel durations: K more steps in which the library stamps kernel_ev
+        # with the two scan kernels' own start and end times (taken from their
+        # dispatches by hipExtLaunchKernelGGL).
+        for k in range(K):
             r = kernel_ev[k]
             kev[0] = (r[0].cuda_event, r[1].cuda_event)
             kev[1] = (r[2].cuda_event, r[3].cuda_event)
             fwd()
             bwd()
-        else:
-            fwd()
-            ev[k][1].record(stream)
-            bwd()
+        torch.cuda.synchronize()
+        kev[0] = kev[1] = None
+    # Call split, from a separate pass with an event around each call (each
+    # event record costs some stream time, so these passes are not timed).
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    for k in range(K):
+        ev[k][0].record(stream)
+        fwd()
+        ev[k][1].record(stream)
+        bwd()
         ev[k][2].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    mid = [kernel_ev[k][1] if kernel_ev is not None else ev[k][1] for k in range(K)]
-    t_fwd = np.array([ev[k][0].elapsed_time(mid[k]) for k in range(K)]) * 1e-3
-    t_bwd = np.array([mid[k].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
+    t_fwd = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e-3
+    t_bwd = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]) * 1e-3
     step_s = wall / K
     fb_s = float(np.mean(t_fwd + t_bwd))
     fwd_arrays, bwd_arrays = ARRAYS[args.api]
@@ -680,12 +747,13 @@ def main():
     ach = bwd_gbs if dom == "bwd" else fwd_gbs
     kernel_us = None
     if kernel_ev is not None:
-        # Roofline of the dominant kernel on its own duration (the events bracket
-        # only the scan kernel; the call times above include the look-back reset
-        # and the dLambda reduction).
+        # Roofline of the dominant kernel on its own duration (the call times
+        # above include the look-back reset and the dLambda reduction, and the
+        # event packets of their pass).
         k_fwd = np.array([r[0].elapsed_time(r[1]) for r in kernel_ev]) * 1e-3
         k_bwd = np.array([r[2].elapsed_time(r[3]) for r in kernel_ev]) * 1e-3
         kernel_us = {"fwd": float(np.mean(k_fwd)) * 1e6, "bwd": float(np.mean(k_bwd)) * 1e6}
+        dom = "bwd" if kernel_us["bwd"] >= kernel_us["fwd"] else "fwd"
         ach = (bwd_bytes if dom == "bwd" else fwd_bytes) / (kernel_us[dom] * 1e-6) / 1e9
     log(f"fwd {np.mean(t_fwd)*1e6:.1f} us ({fwd_gbs:.0f} GB/s)  bwd {np.mean(t_bwd)*1e6:.1f} us "
         f"({bwd_gbs:.0f} GB/s)  wall/step {step_s*1e6:.1f} us")
@@ -710,7 +778,7 @@ def main():
                                f"forward+backward, {cfg.note}",
                    "B": B, "L": L, "D": D, "io": cfg.io, "elements": N},
         "fwd_elements_per_s": N / float(np.mean(t_fwd)),
-        "fwd_bwd_elements_per_s_events": N / fb_s,
+        "fwd_bwd_elements_per_s_call_events": N / fb_s,
         "us_fwd": float(np.mean(t_fwd)) * 1e6,
         "us_bwd": float(np.mean(t_bwd)) * 1e6,
         "fwd_hbm_gbs": fwd_gbs,

@@ -127,12 +127,15 @@ int recblr_bdlru_scan_backward(const void* x, const void* z_r, const void* z_i,
 /*
  * Measurement variants of the two scans above: the same work, arguments and
  * errors, plus two caller-created HIP events (hipEvent_t; either may be NULL)
- * recorded on `stream` immediately before and after the launch of the scan
- * kernel itself.  The look-back state reset before it and, in the backward,
- * the two dLambda reduction kernels after it fall outside the pair, so the
- * time between the events is that one kernel's duration.  The events are
- * recorded only when the scan kernel is launched (not for B, D or L = 0); a
- * validation error records neither.
+ * that take the start and end times of the scan kernel itself: the kernel is
+ * launched with hipExtLaunchKernelGGL, which stamps the events from the
+ * kernel's dispatch.  The look-back state reset before it and, in the
+ * backward, the dLambda reduction after it fall outside the pair, so the time
+ * between the events is that one kernel's duration.  The events are set only
+ * when the scan kernel is launched (not for B, D or L = 0); a validation error
+ * sets neither.  A launch with events still idles the stream for about 5 us on
+ * each side of the kernel on MI355X, so a loop timed for throughput should
+ * call the plain entry points.
  */
 int recblr_bdlru_scan_forward_timed(const void* x, const void* z_r, const void* z_i,
                                     const float* lambda, const float* h0, void* h, float* hT,

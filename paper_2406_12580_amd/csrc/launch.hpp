@@ -3,6 +3,7 @@
 // launcher enqueues work on `stream` and returns hipGetLastError().
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -53,9 +54,17 @@ struct ScanBwdArgs {
     hipEvent_t ev_end = nullptr;
 };
 
-// Records e on stream unless e is null (the measurement events of the scans).
-inline hipError_t mark_event(hipEvent_t e, hipStream_t stream) {
-    return e ? hipEventRecord(e, stream) : hipSuccess;
+// Launches `kernel` on `stream`.  With measurement events (either may be
+// null) the launch goes through hipExtLaunchKernelGGL, which stamps the
+// events with the kernel's own start and end times from its dispatch.
+template <typename Kernel, typename... Args>
+inline hipError_t launch_measured(Kernel kernel, dim3 grid, dim3 block, hipStream_t stream,
+                                  hipEvent_t ev0, hipEvent_t ev1, Args... args) {
+    if (ev0 || ev1)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev0, ev1, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+    return hipGetLastError();
 }
 
 // Workspace (bytes) the scan launchers need for a given problem.

@@ -844,37 +844,30 @@ size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
     return bwd_layout(B, D, plan_backward(B, L, D, esz, max_vec(esz, lb))).total;
 }
 
-// ev0 / ev1 (may be null) are recorded right before and after the scan kernel.
+// ev0 / ev1 (may be null) take the scan kernel's start and end times.
 template <typename TX, typename TZ, typename Off, int VEC>
 static hipError_t launch_bwd_vec(const BwdParams& P, const BwdPlan& plan, hipStream_t stream,
                                  hipEvent_t ev0, hipEvent_t ev1) {
-    hipError_t e;
     if (!plan.lookback) {
-        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
         // The chain kernel takes one channel per lane (RECBLR_BWD_CHAIN_MAX_VEC).
         if constexpr (VEC != 1) {
             return hipErrorInvalidValue;
         } else {
             const dim3 grid((unsigned)plan.ngroups), block(kChainW * kWave);
             if (chain_steps(P.L) == 5)
-                hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, 5, 1, Off>), grid,
-                                   block, 0, stream, P);
-            else
-                hipLaunchKernelGGL((scan_bwd_chain_kernel<TX, TZ, kChainW, 4, 1, Off>), grid,
-                                   block, 0, stream, P);
+                return launch_measured(scan_bwd_chain_kernel<TX, TZ, kChainW, 5, 1, Off>, grid,
+                                       block, stream, ev0, ev1, P);
+            return launch_measured(scan_bwd_chain_kernel<TX, TZ, kChainW, 4, 1, Off>, grid, block,
+                                   stream, ev0, ev1, P);
         }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        return mark_event(ev1, stream);
     }
-    if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
-    if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
+    hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(kLbW * kWave);
-    hipLaunchKernelGGL((scan_bwd_lookback_kernel<TX, TZ, kLbW,
-                                                 steps_per_wave<lb_elems(sizeof(TX)), VEC>(), VEC,
-                                                 lb_window<VEC>(), Off>),
-                       grid, block, 0, stream, P);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    return mark_event(ev1, stream);
+    return launch_measured(scan_bwd_lookback_kernel<TX, TZ, kLbW,
+                                                    steps_per_wave<lb_elems(sizeof(TX)), VEC>(),
+                                                    VEC, lb_window<VEC>(), Off>,
+                           grid, block, stream, ev0, ev1, P);
 }
 
 template <typename TX, typename TZ>

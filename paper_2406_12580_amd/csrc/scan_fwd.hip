@@ -541,30 +541,23 @@ size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
     return lookback_ws_bytes(plan_forward(B, L, D, esz, max_vec(esz, true)).nseg, B * D);
 }
 
-// ev0 / ev1 (may be null) are recorded right before and after the scan kernel.
+// ev0 / ev1 (may be null) take the scan kernel's start and end times.
 template <typename TX, typename TZ, bool RAW, typename Off, int VEC>
 static hipError_t launch_vec(const FwdParams& P, const FwdPlan& plan, hipStream_t stream,
                              hipEvent_t ev0, hipEvent_t ev1) {
-    hipError_t e;
-    if (!plan.lookback) {
-        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
-        hipLaunchKernelGGL((scan_fwd_chain_kernel<TX, TZ, kChainW,
-                                                  steps_per_wave<kChainE, VEC>(), VEC, RAW, Off>),
-                           dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), 0, stream, P);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        return mark_event(ev1, stream);
-    }
+    if (!plan.lookback)
+        return launch_measured(
+            scan_fwd_chain_kernel<TX, TZ, kChainW, steps_per_wave<kChainE, VEC>(), VEC, RAW, Off>,
+            dim3((unsigned)plan.ngroups), dim3(kChainW * kWave), stream, ev0, ev1, P);
     if constexpr (RAW) {
         return hipErrorInvalidValue;  // the raw scan always runs the chain kernel
     } else {
-        if ((e = lookback_reset(P.lb, plan.nseg * P.nch, stream)) != hipSuccess) return e;
-        if ((e = mark_event(ev0, stream)) != hipSuccess) return e;
-        hipLaunchKernelGGL((scan_fwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(),
-                                                     VEC, lb_window<VEC>(), Off>),
-                           dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), 0,
-                           stream, P);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        return mark_event(ev1, stream);
+        hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
+        if (e != hipSuccess) return e;
+        return launch_measured(
+            scan_fwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(), VEC,
+                                     lb_window<VEC>(), Off>,
+            dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), stream, ev0, ev1, P);
     }
 }
 
