@@ -63,7 +63,9 @@ enum {
     RECBLR_ERR_INVALID_ARGUMENT = -1, /* NULL/misaligned/overlapping pointer, negative size */
     RECBLR_ERR_UNSUPPORTED = -2,      /* unknown dtype or op, size beyond the supported range */
     RECBLR_ERR_WORKSPACE = -3,        /* ws NULL, too small or not 256-byte aligned */
-    RECBLR_ERR_HIP = -4               /* a kernel launch failed (hipGetLastError) */
+    RECBLR_ERR_HIP = -4,              /* a kernel launch failed (hipGetLastError) */
+    RECBLR_ERR_SCRATCH = -5           /* recblr_bdlru_scan_backward_noalloc: the problem needs
+                                         more scratch than the static device buffer holds */
 };
 
 /* Element type of the sequence tensors. */
@@ -148,6 +150,30 @@ int recblr_bdlru_scan_backward_timed(const void* x, const void* z_r, const void*
                                      void* dz_i, float* dlambda, float* dh0, int64_t B,
                                      int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
                                      void* stream, void* ev_begin, void* ev_end);
+
+/*
+ * recblr_bdlru_scan_backward for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same work, arguments, results and errors, with no
+ * workspace argument.  The scratch of its kernels (look-back state words and
+ * ticket, per-tile dLambda partials) is a static device array of 16 MiB
+ * inside the library, one per GPU, held until the process ends; the call
+ * allocates and frees nothing.  The array's address on the current device is
+ * looked up on the first call on that device, so make one call before
+ * capturing a graph.  The kernels clear what must start at zero themselves,
+ * so nothing carries over between calls; but every call on one GPU uses the
+ * same array, so calls that may overlap on one GPU (two streams, two threads)
+ * race and must be serialised by the caller.  Problems whose scratch
+ * (recblr_workspace_size(RECBLR_OP_SCAN_BACKWARD, ...)) exceeds 16 MiB are
+ * rejected with RECBLR_ERR_SCRATCH before anything is enqueued; this covers,
+ * e.g., B*L*D = 2^26 at L = 2048, D = 128 (fp32) and L = 16384, D = 256 (bf16).
+ * The stream must belong to the current device.
+ */
+int recblr_bdlru_scan_backward_noalloc(const void* x, const void* z_r, const void* z_i,
+                                       const float* lambda, const float* h0, const void* h,
+                                       const void* dh, const float* dhT, void* dx, void* dz_r,
+                                       void* dz_i, float* dlambda, float* dh0, int64_t B,
+                                       int64_t L, int64_t D, int io, void* stream);
 
 /*
  * One recurrent step for inference (eq:linrnn applied once; the paper's

@@ -166,6 +166,49 @@ size_t step_ws(int64_t B, int64_t D, int io) {
 
 char* at(void* ws, size_t off) { return (char*)ws + off; }
 
+// The scan backward behind recblr_bdlru_scan_backward(_timed) and
+// recblr_bdlru_scan_backward_noalloc.  With `static_ws` the scratch is the
+// library's static device buffer of the current device (static_scratch);
+// otherwise the caller's ws.  Every argument is validated before anything
+// is enqueued.
+int scan_backward_impl(const void* x, const void* z_r, const void* z_i, const float* lambda,
+                       const float* h0, const void* h, const void* dh, const float* dhT,
+                       void* dx, void* dz_r, void* dz_i, float* dlambda, float* dh0, int64_t B,
+                       int64_t L, int64_t D, int io, void* ws, size_t ws_bytes, bool static_ws,
+                       void* stream, void* ev_begin, void* ev_end) {
+    int st = check_dims(B, L, D, io);
+    if (st) return st;
+    if (D == 0) return RECBLR_OK;
+    if (!lambda || !dlambda) return RECBLR_ERR_INVALID_ARGUMENT;
+    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
+                 dl = (size_t)D * 4;
+    if (B > 0 && L > 0 && (!x || !z_r || !z_i || !h || !dh || !dx || !dz_r || !dz_i))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {x, z_r, z_i, h, dh, (const void*)dx, (const void*)dz_r,
+                          (const void*)dz_i})
+        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
+    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)dhT,
+                          (const void*)dlambda, (const void*)dh0})
+        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
+    if (!disjoint({{dx, n}, {dz_r, n}, {dz_i, n}, {dlambda, dl}, {dh0, s}},
+                  {{x, n}, {z_r, n}, {z_i, n}, {lambda, dl}, {h0, s}, {h, n}, {dh, n},
+                   {dhT, s}}))
+        return RECBLR_ERR_INVALID_ARGUMENT;
+    hipStream_t strm = (hipStream_t)stream;
+    const size_t need = B > 0 ? scan_backward_workspace(B, L, D, io_of(io)) : 0;
+    if (static_ws) {
+        if (need > kStaticScratchBytes) return RECBLR_ERR_SCRATCH;
+        if (need > 0 && static_scratch(&ws, &ws_bytes) != hipSuccess) return RECBLR_ERR_HIP;
+    }
+    if (B == 0) return status_of(launch_fill(dlambda, 0.0f, D, strm));
+    st = check_ws(ws, ws_bytes, need);
+    if (st) return st;
+    ScanBwdArgs a{x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
+                  B, L, D, io_of(io), io_of(io), ws, ws_bytes,
+                  (hipEvent_t)ev_begin, (hipEvent_t)ev_end};
+    return status_of(launch_scan_backward(a, strm));
+}
+
 }  // namespace
 
 extern "C" {
@@ -177,6 +220,8 @@ const char* recblr_status_string(int status) {
         case RECBLR_ERR_UNSUPPORTED: return "unsupported";
         case RECBLR_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
         case RECBLR_ERR_HIP: return "HIP launch failure";
+        case RECBLR_ERR_SCRATCH:
+            return "problem needs more scratch than the library's static device buffer holds";
         default: return "unknown status";
     }
 }
@@ -309,32 +354,17 @@ int recblr_bdlru_scan_backward_timed(const void* x, const void* z_r, const void*
                                      void* dz_i, float* dlambda, float* dh0, int64_t B,
                                      int64_t L, int64_t D, int io, void* ws, size_t ws_bytes,
                                      void* stream, void* ev_begin, void* ev_end) {
-    int st = check_dims(B, L, D, io);
-    if (st) return st;
-    if (D == 0) return RECBLR_OK;
-    if (!lambda || !dlambda) return RECBLR_ERR_INVALID_ARGUMENT;
-    const size_t n = (size_t)(B * L * D) * esz(io), s = (size_t)(B * D) * 4,
-                 dl = (size_t)D * 4;
-    if (B > 0 && L > 0 && (!x || !z_r || !z_i || !h || !dh || !dx || !dz_r || !dz_i))
-        return RECBLR_ERR_INVALID_ARGUMENT;
-    for (const void* p : {x, z_r, z_i, h, dh, (const void*)dx, (const void*)dz_r,
-                          (const void*)dz_i})
-        if (!aligned(p, esz(io))) return RECBLR_ERR_INVALID_ARGUMENT;
-    for (const void* p : {(const void*)lambda, (const void*)h0, (const void*)dhT,
-                          (const void*)dlambda, (const void*)dh0})
-        if (!aligned(p, 4)) return RECBLR_ERR_INVALID_ARGUMENT;
-    if (!disjoint({{dx, n}, {dz_r, n}, {dz_i, n}, {dlambda, dl}, {dh0, s}},
-                  {{x, n}, {z_r, n}, {z_i, n}, {lambda, dl}, {h0, s}, {h, n}, {dh, n},
-                   {dhT, s}}))
-        return RECBLR_ERR_INVALID_ARGUMENT;
-    hipStream_t strm = (hipStream_t)stream;
-    if (B == 0) return status_of(launch_fill(dlambda, 0.0f, D, strm));
-    st = check_ws(ws, ws_bytes, scan_backward_workspace(B, L, D, io_of(io)));
-    if (st) return st;
-    ScanBwdArgs a{x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
-                  B, L, D, io_of(io), io_of(io), ws, ws_bytes,
-                  (hipEvent_t)ev_begin, (hipEvent_t)ev_end};
-    return status_of(launch_scan_backward(a, strm));
+    return scan_backward_impl(x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
+                              B, L, D, io, ws, ws_bytes, false, stream, ev_begin, ev_end);
+}
+
+int recblr_bdlru_scan_backward_noalloc(const void* x, const void* z_r, const void* z_i,
+                                       const float* lambda, const float* h0, const void* h,
+                                       const void* dh, const float* dhT, void* dx, void* dz_r,
+                                       void* dz_i, float* dlambda, float* dh0, int64_t B,
+                                       int64_t L, int64_t D, int io, void* stream) {
+    return scan_backward_impl(x, z_r, z_i, lambda, h0, h, dh, dhT, dx, dz_r, dz_i, dlambda, dh0,
+                              B, L, D, io, nullptr, 0, true, stream, nullptr, nullptr);
 }
 
 int recblr_bdlru_scan_step(const void* x, const void* z_r, const void* z_i,

@@ -67,6 +67,13 @@ inline hipError_t launch_measured(Kernel kernel, dim3 grid, dim3 block, hipStrea
     return hipGetLastError();
 }
 
+// Static scratch of the entry point that allocates nothing
+// (recblr_bdlru_scan_backward_noalloc): a device array of this many bytes,
+// one per GPU, held until the process ends.  static_scratch returns its
+// address on the current device (looked up once per device).
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+hipError_t static_scratch(void** ptr, size_t* bytes);
+
 // Workspace (bytes) the scan launchers need for a given problem.
 size_t scan_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io);
 size_t scan_backward_workspace(int64_t B, int64_t L, int64_t D, IoType io);

@@ -29,7 +29,7 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing; build it with `python -m paper_2406_12580_amd.build`")
 _lib = ctypes.CDLL(LIB_PATH)
 
-OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCRATCH = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
 (OP_SCAN_FORWARD, OP_SCAN_BACKWARD, OP_FORWARD, OP_BACKWARD, OP_STEP, OP_GATED_FORWARD,
  OP_GATED_BACKWARD, OP_SCAN_BACKWARD_METHOD) = range(8)
@@ -43,6 +43,7 @@ EXPORTS = (
     "recblr_bdlru_scan_backward_timed", "recblr_gated_backward", "recblr_model_param_count",
     "recblr_model_param_offsets", "recblr_model_workspace_size", "recblr_blas_create",
     "recblr_blas_destroy", "recblr_model_train_step", "recblr_adam_update",
+    "recblr_bdlru_scan_backward_noalloc",
 )
 
 _p, _i64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
@@ -64,6 +65,7 @@ _SIGS = {
     "recblr_bdlru_scan_forward_timed": ([_p] * 7 + [_i64] * 3 + [_int, _p, _sz, _p, _p, _p], _int),
     "recblr_bdlru_scan_backward_timed": ([_p] * 13 + [_i64] * 3 + [_int, _p, _sz, _p, _p, _p],
                                          _int),
+    "recblr_bdlru_scan_backward_noalloc": ([_p] * 13 + [_i64] * 3 + [_int, _p], _int),
     "recblr_bdlru_scan_step": ([_p] * 6 + [_i64] * 2 + [_int, _p], _int),
     "recblr_bdlru_forward": ([_p] * 9 + [_i64] * 3 + [_int, _p, _sz, _p], _int),
     "recblr_bdlru_backward": ([_p] * 17 + [_i64] * 3 + [_int, _p, _sz, _p], _int),

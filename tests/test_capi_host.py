@@ -28,7 +28,7 @@ def header_symbols():
 def test_header_declares_the_entry_points():
     syms = header_symbols()
     assert "recblr_bdlru_scan_forward" in syms and "recblr_bdlru_backward" in syms
-    assert len(syms) == 22
+    assert len(syms) == 23
 
 
 def test_library_exports_every_declared_symbol(rb):
@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(rb):
 
 
 def test_status_strings(rb):
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         assert rb.recblr_status_string(code)
     assert rb.recblr_status_string(99) == b"unknown status"
 
@@ -257,3 +257,21 @@ def test_model_validation(rb):
     assert rb.recblr_adam_update(addr(0), addr(0), addr(2), addr(3), 10, 1, 1e-3, 0.9, 0.999,
                                  1e-8, None) == rb.ERR_INVALID_ARGUMENT    # grads == params
 
+
+
+def test_noalloc_rejects_problems_beyond_its_static_scratch(rb):
+    """256 x 65536 x 128 fp32 needs ~200 MiB of look-back state and dLambda
+    partials, past the 16 MiB static array: rejected before any HIP call."""
+    B, L, D = 256, 65536, 128
+    assert rb.recblr_workspace_size(rb.OP_SCAN_BACKWARD, B, L, D, rb.F32) > 16 << 20
+    big = 1 << 34  # tensors of 8 GiB: fake addresses 16 GiB apart
+    a = lambda k: (1 << 40) + k * big
+    st = rb.recblr_bdlru_scan_backward_noalloc(a(0), a(1), a(2), a(3), None, a(4), a(5), None,
+                                               a(6), a(7), a(8), a(9), None, B, L, D, rb.F32,
+                                               None)
+    assert st == rb.ERR_SCRATCH
+    # invalid arguments are reported first, as by the workspace entry point
+    st = rb.recblr_bdlru_scan_backward_noalloc(a(0), a(1), a(2), a(3), None, a(4), a(5), None,
+                                               a(0), a(7), a(8), a(9), None, B, L, D, rb.F32,
+                                               None)
+    assert st == rb.ERR_INVALID_ARGUMENT
