@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "librecblr.so")
 SOURCES = ["capi.cpp", "scan_fwd.hip", "scan_bwd.hip", "step.hip", "gemm.hip", "ablation.hip",
-           "gated.hip", "model.hip", "noalloc.hip"]
+           "gated.hip", "model.hip", "noalloc.hip", "fused_fwd.hip"]
 # The prediction layer of the full-model step uses rocBLAS GEMMs.
 LIBS = ["-L/opt/rocm/lib", "-lrocblas"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

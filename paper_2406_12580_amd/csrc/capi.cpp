@@ -87,7 +87,10 @@ FullFwdLayout full_fwd_layout(int64_t B, int64_t L, int64_t D, int io) {
     // fused kernel (D % 64 == 0), whichever the call takes.
     const size_t scan = scan_forward_workspace(B, L, D, io_of(io));
     const size_t fused = D % 64 == 0 ? fused_forward_workspace(B, L, D) : 0;
-    l.total = l.scan + align_up(scan > fused ? scan : fused);
+    const size_t fused2 = fused2_forward_workspace(B, L, D, io_of(io));
+    size_t need = scan > fused ? scan : fused;
+    need = need > fused2 ? need : fused2;
+    l.total = l.scan + align_up(need);
     return l;
 }
 
@@ -414,6 +417,10 @@ int recblr_bdlru_forward(const void* x, const void* W_r, const void* b_r, const 
     void* zr = at(ws, lay.zr);
     void* zi = at(ws, lay.zi);
     void* pack = at(ws, lay.pack);
+    if (L > 0 && fused2_forward_applies(B, L, D, io_of(io), x, W_r, W_i))
+        return status_of(launch_fused2_forward(x, W_r, b_r, W_i, b_i, lambda, h0, h, hT, nullptr,
+                                               nullptr, B, L, D, io_of(io), at(ws, lay.scan),
+                                               strm));
     if (L > 0 && fused_forward_applies(B, L, D, io_of(io), x, pack)) {
         hipError_t e = launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm);
         if (e != hipSuccess) return RECBLR_ERR_HIP;
@@ -469,6 +476,9 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
     // cost that kernel three quarters of its occupancy.
     if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), io_of(io), strm) != hipSuccess)
         return RECBLR_ERR_HIP;
+    if (L > 0 && fused2_forward_applies(B, L, D, io_of(io), xp, W_r, W_i))
+        return status_of(launch_fused2_forward(xp, W_r, b_r, W_i, b_i, lambda, h0, h, hT, hz, y,
+                                               B, L, D, io_of(io), fws + fl.scan, strm));
     if (L > 0 && fused_forward_applies(B, L, D, io_of(io), xp, pack)) {
         if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
             return RECBLR_ERR_HIP;

@@ -110,6 +110,18 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
                                 int64_t B, int64_t L, int64_t D, IoType io, void* ws,
                                 hipStream_t stream);
 
+// Scan forward with the gate projections fused in, weights resident in VGPRs
+// (fused_fwd.hip): D = 128 for fp32 I/O, D = 128 or 256 for bf16 I/O, x, W_r
+// and W_i 16-byte aligned.  With y non-null it stores y = h * SiLU(hz) (and h
+// where h is non-null).  ws: fused2_forward_workspace bytes.
+bool fused2_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
+                            const void* wr, const void* wi);
+size_t fused2_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io);
+hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, const void* wi,
+                                 const void* bi, const float* lambda, const float* h0, void* h,
+                                 float* hT, const void* hz, void* y, int64_t B, int64_t L,
+                                 int64_t D, IoType io, void* ws, hipStream_t stream);
+
 // Scan-algorithm variants for the efficiency ablation (zero initial state;
 // x, z, h share the I/O type): a serial scan (one wave per 64 channels walks
 // the sequence) and the two-tree scan over the power of two >= L with the

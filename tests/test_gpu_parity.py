@@ -223,7 +223,11 @@ def test_full_forward_backward(rb, shape, io):
 # projections inside the look-back scan (tiles of 64 channels x 128 steps);
 # these shapes span several tiles with a ragged last one.  D = 72 takes the
 # path through the separate projection kernels.
-FUSED_FWD = [(1, 1000, 64), (3, 700, 128), (2, 257, 192), (1, 129, 256), (2, 1000, 72)]
+FUSED_FWD = [(1, 1000, 64), (3, 700, 128), (2, 257, 192), (1, 129, 256), (2, 1000, 72),
+             # D = 128 / 256 with W kept in registers: few channel groups take
+             # tiles in ticket order with look-back (above), at least 256 groups
+             # walk their tiles in a chain (below; ragged last tile, L = 1)
+             (256, 100, 128), (512, 1, 128), (128, 77, 256)]
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
@@ -377,7 +381,7 @@ def test_tree_scan_sequence_padding(rb):
 # Few channel groups, L > 128 and D % 64 == 0 take the fused kernel (conv on
 # load, gate on store); the others the unfused path.
 GATED_CASES = [((2, 300, 64), 4), ((1, 700, 128), 2), ((1, 513, 256), 1), ((8, 50, 64), 4),
-               ((2, 300, 72), 3), ((3, 1, 64), 4)]
+               ((2, 300, 72), 3), ((3, 1, 64), 4), ((256, 70, 128), 4)]
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
