@@ -56,7 +56,15 @@ struct BwdParams {
     int64_t L, D, nch;
     int64_t ngroups, nseg;
     LookbackWs lb;
+    unsigned* dl_counters;  // one per 64-channel column group of the dLambda reduction
+    int64_t n_counters;
 };
+
+// Zeroes the dLambda counters (n of them); called by one workgroup of each
+// backward scan kernel, which runs before the reduction.
+__device__ __forceinline__ void zero_counters(unsigned* c, int64_t n) {
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) c[i] = 0u;
+}
 
 template <typename TX, int VEC, typename Off>
 struct BwdLane {
@@ -317,6 +325,7 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(BwdParams P) {
     __shared__ float red[W][kWave][VEC];
     const int lane = threadIdx.x & (kWave - 1);
     const int w = wave_id();
+    if (blockIdx.x == 0) zero_counters(P.dl_counters, P.n_counters);
     BwdLane<TX, VEC, Off> ln;
     ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
     ChannelConst cc[VEC];
@@ -385,6 +394,7 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
     const int64_t g = tile - r * P.ngroups;
     const int64_t s = P.nseg - 1 - r;    // macro-chunk of this tile
+    if (tile == 0) zero_counters(P.dl_counters, P.n_counters);
 
     BwdLane<TX, VEC, Off> ln;
     ln.init(g, lane, P.L, P.D, P.nch);
@@ -634,6 +644,7 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
     const int64_t r = tile / P.ngroups;  // processing order: from the end of the sequence
     const int64_t g = tile - r * P.ngroups;
     const int64_t s = P.nseg - 1 - r;    // tile row along L
+    if (tile == 0) zero_counters(P.dl_counters, P.n_counters);
     const int64_t gpr = P.D / kWave;      // channel groups per batch row
     const int64_t b = g / gpr, cg = g - b * gpr;
     float zr[C], zi[C];
@@ -646,59 +657,76 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
 
 // ------------------------------------------------------------------ dLambda reduction
 // dLambda[d] = sigmoid(Lambda_d) * sum_rows partial[row][d], in double and in a
-// fixed order, in two fence-free launches: block (nb, dg) of the first sums
-// rows [nb*64, nb*64 + 64) of channels [dg*64, dg*64 + 64) into partial2[nb];
-// the second adds the row blocks in order.  (A single launch with a
-// last-block-done counter would need an agent-scope release fence, which on
-// this GPU writes back every dirty line of the L2 right after the scan has
-// filled it with outputs.)
-__global__ __launch_bounds__(256) void dlambda_rows_kernel(const float* __restrict__ partial,
-                                                           double* __restrict__ partial2,
-                                                           int64_t rows, int64_t D) {
+// fixed order, in one launch: block (nb, dg) sums rows [nb*64, nb*64 + 64) of
+// channels [dg*64, dg*64 + 64) into partial2[nb]; the last block of column
+// group dg to finish (a counter per group, zeroed by the scan kernel that
+// wrote the partials) adds the row-block sums in a fixed order, so the result
+// does not depend on which block finishes last.
+__global__ __launch_bounds__(256) void dlambda_kernel(const float* __restrict__ partial,
+                                                      double* __restrict__ partial2,
+                                                      int64_t rows, int64_t D,
+                                                      const float* __restrict__ lam,
+                                                      float* __restrict__ dlambda,
+                                                      unsigned* __restrict__ counters) {
     __shared__ double red[4][kWave];
+    __shared__ int last_sh;
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
     const int64_t d = (int64_t)blockIdx.y * kWave + lane;
     const int64_t nb = blockIdx.x;
     double acc = 0.0;
     if (d < D) {
+        // All loads first (rows past the end read the last row and count as
+        // zero), then the sum in row order.
         const int64_t r0 = nb * kReduceRows + w * (kReduceRows / 4);
+        float v[kReduceRows / 4];
 #pragma unroll
         for (int k = 0; k < kReduceRows / 4; ++k) {
-            const int64_t row = r0 + k;
-            if (row < rows) acc += (double)partial[row * D + d];
+            const int64_t row = r0 + k < rows ? r0 + k : rows - 1;
+            v[k] = partial[row * D + d];
         }
+#pragma unroll
+        for (int k = 0; k < kReduceRows / 4; ++k)
+            if (r0 + k < rows) acc += (double)v[k];
     }
     red[w][lane] = acc;
     __syncthreads();
-    if (w == 0 && d < D)
-        partial2[nb * D + d] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
-}
-
-// dLambda_d = sigmoid(Lambda_d) * sum of the row-block sums, in a fixed order:
-// thread group g of 8 (64 channels per workgroup) sums its contiguous run of
-// row blocks in ascending order, then the 8 runs are added in order.
-constexpr int kFinalGroups = 8;
-__global__ __launch_bounds__(64 * kFinalGroups) void dlambda_final_kernel(
-    const double* __restrict__ partial2, int64_t nblk, const float* __restrict__ lam,
-    float* __restrict__ dlambda, int64_t D) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int g = threadIdx.x / kWave;
-    const int64_t d = (int64_t)blockIdx.x * kWave + lane;
-    const int64_t per = (nblk + kFinalGroups - 1) / kFinalGroups;
-    const int64_t k0 = g * per, k1 = k0 + per < nblk ? k0 + per : nblk;
+    // partial2 and the counter travel as agent-scope atomics, which this GPU
+    // keeps coherent across its L2s (as the look-back state words): each
+    // block's sums are complete in memory (vmcnt(0)) before its counter
+    // increment is issued, and the last block reads them back with atomic
+    // loads.  No release fence, which would write back the whole L2.
+    if (w == 0 && d < D) {
+        const double v = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+        __hip_atomic_store((uint64_t*)(partial2 + nb * D + d), __builtin_bit_cast(uint64_t, v),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        last_sh = __hip_atomic_fetch_add(counters + blockIdx.y, 1u, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
+    __syncthreads();
+    if (!last_sh) return;
+    // Wave w sums its contiguous run of row blocks in ascending order; the
+    // four runs are then added in order.
+    const int64_t nblk = gridDim.x;
+    const int64_t per = (nblk + 3) / 4;
+    const int64_t k0 = w * per, k1 = k0 + per < nblk ? k0 + per : nblk;
     double s = 0.0;
     if (d < D) {
 #pragma unroll 8
-        for (int64_t k = k0; k < k1; ++k) s += partial2[k * D + d];
+        for (int64_t k = k0; k < k1; ++k)
+            s += __builtin_bit_cast(double, __hip_atomic_load((uint64_t*)(partial2 + k * D + d),
+                                                              __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_AGENT));
     }
-    __shared__ double red[kFinalGroups][kWave];
-    red[g][lane] = s;
+    __syncthreads();  // red is reused
+    red[w][lane] = s;
     __syncthreads();
-    if (g != 0 || d >= D) return;
-    double t = red[0][lane];
-#pragma unroll
-    for (int q = 1; q < kFinalGroups; ++q) t += red[q][lane];
+    if (w != 0 || d >= D) return;
+    const double t = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     const double lv = (double)lam[d];
     dlambda[d] = (float)(t / (1.0 + exp(-lv)));
 }
@@ -824,8 +852,10 @@ static int pick_vec_bwd(const ScanBwdArgs& a) {
 
 // Workspace: [look-back states][dLambda partials (nseg rows of B*D)][row-block sums].
 struct BwdLayout {
-    size_t lb, partial, partial2, total;
+    size_t lb, partial, partial2, counters, total;
 };
+
+inline int64_t dlambda_groups(int64_t D) { return (D + kWave - 1) / kWave; }
 
 static BwdLayout bwd_layout(int64_t B, int64_t D, const BwdPlan& p) {
     BwdLayout l;
@@ -834,7 +864,8 @@ static BwdLayout bwd_layout(int64_t B, int64_t D, const BwdPlan& p) {
     l.lb = 0;
     l.partial = p.lookback ? align_up(lookback_ws_bytes(p.nseg, B * D)) : 0;
     l.partial2 = l.partial + align_up((size_t)(rows * D) * sizeof(float));
-    l.total = l.partial2 + align_up((size_t)(nb * D) * sizeof(double));
+    l.counters = l.partial2 + align_up((size_t)(nb * D) * sizeof(double));
+    l.total = l.counters + align_up((size_t)dlambda_groups(D) * sizeof(unsigned));
     return l;
 }
 
@@ -888,17 +919,14 @@ static hipError_t launch_bwd_typed(const BwdParams& P, const BwdPlan& plan, hipS
     return launch_bwd_vec<TX, TZ, uint64_t, 1>(P, plan, stream, ev0, ev1);
 }
 
-// dLambda from the per-tile partials [rows][D]: two fixed-order launches.
+// dLambda from the per-tile partials [rows][D]: one fixed-order launch.
 static hipError_t launch_dlambda(const float* partial, double* partial2, int64_t rows, int64_t D,
-                                 const float* lambda, float* dlambda, hipStream_t stream) {
+                                 const float* lambda, float* dlambda, unsigned* counters,
+                                 hipStream_t stream) {
     const int64_t nblk = (rows + kReduceRows - 1) / kReduceRows;
-    dim3 rgrid((unsigned)nblk, (unsigned)((D + kWave - 1) / kWave));
-    hipLaunchKernelGGL(dlambda_rows_kernel, rgrid, dim3(256), 0, stream, partial, partial2, rows,
-                       D);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(dlambda_final_kernel, dim3((unsigned)((D + kWave - 1) / kWave)),
-                       dim3(kWave * kFinalGroups), 0, stream, partial2, nblk, lambda, dlambda, D);
+    dim3 grid((unsigned)nblk, (unsigned)dlambda_groups(D));
+    hipLaunchKernelGGL(dlambda_kernel, grid, dim3(256), 0, stream, partial, partial2, rows, D,
+                       lambda, dlambda, counters);
     return hipGetLastError();
 }
 
@@ -908,10 +936,12 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
     char* ws = (char*)a.ws;
     float* partial = (float*)(ws + lay.partial);
     double* partial2 = (double*)(ws + lay.partial2);
+    unsigned* counters = (unsigned*)(ws + lay.counters);
     const BwdParams P{a.x,   a.zr,    a.zi,  a.lambda, a.h0, a.h,   a.dh,  a.dhT,
                       a.dx,  a.dzr,   a.dzi, a.dh0,    partial, a.L, a.D,  a.B * a.D,
                       plan.ngroups, plan.nseg,
-                      plan.lookback ? lookback_ws(ws + lay.lb) : LookbackWs{}};
+                      plan.lookback ? lookback_ws(ws + lay.lb) : LookbackWs{},
+                      counters, dlambda_groups(a.D)};
     hipError_t e;
     if (a.io == IoType::kF32)
         e = launch_bwd_typed<float, float>(P, plan, stream, a.ev_begin, a.ev_end);
@@ -919,7 +949,8 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
         e = launch_bwd_typed<bf16, float>(P, plan, stream, a.ev_begin, a.ev_end);
     else e = launch_bwd_typed<bf16, bf16>(P, plan, stream, a.ev_begin, a.ev_end);
     if (e != hipSuccess) return e;
-    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, stream);
+    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, counters,
+                          stream);
 }
 
 // ------------------------------------------------------------------ fused backward
@@ -954,9 +985,11 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
     char* ws = (char*)a.ws;
     float* partial = (float*)(ws + lay.partial);
     double* partial2 = (double*)(ws + lay.partial2);
+    unsigned* counters = (unsigned*)(ws + lay.counters);
     const BwdParams P{a.x,  nullptr, nullptr, a.lambda, a.h0, a.h,   a.dh,  a.dhT,
                       a.dx, a.dzr,   a.dzi,   a.dh0,    partial, a.L, a.D,  a.B * a.D,
-                      plan.ngroups, plan.nseg, lookback_ws(ws + lay.lb)};
+                      plan.ngroups, plan.nseg, lookback_ws(ws + lay.lb),
+                      counters, dlambda_groups(a.D)};
     hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedz::NT);
@@ -981,7 +1014,8 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
                                P, (const __bf16*)a.pack, (const bf16*)a.br, (const bf16*)a.bi);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, stream);
+    return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, counters,
+                          stream);
 }
 
 }  // namespace recblr
