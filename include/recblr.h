@@ -38,7 +38,15 @@
  *  - `ws`/`ws_bytes`: caller-owned device scratch of at least
  *    recblr_workspace_size(...) bytes, 256-byte aligned (NULL is accepted when
  *    that size is 0).  Its contents need no initialisation and are garbage
- *    after the call.  Two calls in flight at once must not share it.
+ *    after the call, with one exception: where recblr_bdlru_scan_forward or
+ *    recblr_bdlru_scan_backward (and their _timed variants) take a nonzero
+ *    workspace, the uint32 at byte offset 4 of ws is a status word that the
+ *    call sets to 0 and that becomes nonzero only if a workgroup's bounded
+ *    wait for another workgroup's state ran out (the affected outputs are
+ *    then NaN): it tells such a NaN apart from one that came with the inputs.
+ *    The waits are bounded for safety; tiles are handed out in an order that
+ *    lets every wait end, so the word stays 0 in normal operation.  Two calls
+ *    in flight at once must not share a workspace.
  *  - Validation happens on the host, before anything is enqueued; a call that
  *    returns an error has enqueued nothing.  Output buffers must not overlap
  *    inputs or each other (recblr_bdlru_scan_step and recblr_bdlru_step allow

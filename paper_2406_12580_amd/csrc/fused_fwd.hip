@@ -79,6 +79,7 @@ struct Params {
     int64_t ngroups, nseg;
     unsigned* counters;  // look-back mode: tile-row tickets, one per group
     uint64_t* states;    // look-back mode: [nseg][nch] state words
+    unsigned* status;    // look-back mode: set when a bounded wait ran out
 };
 
 // 16-byte chunk permutations of the LDS tiles.  A bf16 row (the A operand)
@@ -317,6 +318,21 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
         if (bp) bias = load(bp + cw + (col & 15));
     }
     const ChannelConst cc = channel_const(P.lam[cw + cl]);
+    // LDS byte offsets of this lane's x in a tile (local rows 8 rho + i; block
+    // m adds 32 m rows): the chunk permutation of row 32 m + 8 rho + i is
+    // i | 8 [rho >= 2] for bf16 rows and 4 rho for fp32 rows.
+    int xoff[sizeof(T) == 2 ? 8 : 1];
+    {
+        const int k = cw + cl;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                xoff[i] = (8 * rho + i) * G::kRow + (((k >> 3) ^ (i | (rho >= 2 ? 8 : 0))) << 4) +
+                          (k & 7) * 2;
+        } else {
+            xoff[0] = 8 * rho * G::kRow + (((k >> 2) ^ (4 * rho)) << 4) + (k & 3) * 4;
+        }
+    }
     float carry = P.h0 ? P.h0[chan] : 0.0f;  // chain mode: state before the current tile
 
     const T* xg = (const T*)P.x;
@@ -430,18 +446,26 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
 
         // ---- gates (alpha into acc[m][i], beta' into acc[m][i + 8]) and segments
         Seg run[MB];
+        const int lim = P.L - t0 < TS ? (int)(P.L - t0) : TS;  // valid rows of the tile
 #pragma unroll
         for (int m = 0; m < MB; ++m) {
             Seg sg{1.0f, 0.0f};
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const int r = 32 * m + 8 * rho + i;
-                const float xv = tile_x<T, D>(cur, r, cw + cl);
+                float xv;
+                if constexpr (sizeof(T) == 2)
+                    xv = __uint_as_float((uint32_t)(*(const uint16_t*)(cur + xoff[i] +
+                                                                       32 * m * G::kRow))
+                                         << 16);
+                else
+                    xv = *(const float*)(cur + xoff[0] + (32 * m + i) * G::kRow);
                 float a, u;
                 gate_forward(xv, acc[m][i], acc[m][i + 8], cc, a, u);
-                const bool ok = t0 + r < P.L;
-                a = ok ? a : 1.0f;
-                u = ok ? u : 0.0f;
+                if (lim < TS) {
+                    const bool ok = 32 * m + 8 * rho + i < lim;
+                    a = ok ? a : 1.0f;
+                    u = ok ? u : 0.0f;
+                }
                 acc[m][i] = a;
                 acc[m][i + 8] = u;
                 sg = Seg{a * sg.A, fmaf(a, sg.H, u)};
@@ -481,10 +505,11 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
 #pragma unroll
                 for (int j = 0; j < kWindow; ++j) {
                     const int64_t p = s - 1 - j;
-                    if (p >= 0) wd[j] = wait_ready(P.states + p * P.nch + chan, wd[j]);
+                    if (p >= 0) wd[j] = wait_ready(P.states + p * P.nch + chan, wd[j], P.status);
                 }
                 const int64_t oldest = s - kWindow;
-                cin = fold_window<kWindow>(wd, P.states + (oldest >= 0 ? oldest : 0) * P.nch + chan);
+                cin = fold_window<kWindow>(wd, P.states + (oldest >= 0 ? oldest : 0) * P.nch + chan,
+                                           P.status);
             }
             if (rho == 0) publish(own, pack_inclusive(fmaf(tile.A, cin, tile.H)));
         } else {
@@ -536,7 +561,9 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
     }
 }
 
-// Look-back workspace: [ngroups counters, 256-byte aligned][nseg][nch] state words.
+// Look-back workspace: a 256-byte header (status word at byte 4, as in the
+// other look-back kernels), ngroups tile counters (256-byte aligned), then
+// [nseg][nch] state words.
 struct Plan {
     bool lookback;
     int64_t ngroups, nseg;
@@ -557,9 +584,10 @@ inline size_t counters_bytes(int64_t ngroups) {
 }
 
 __global__ void reset_kernel(unsigned* __restrict__ counters, int64_t ngroups,
-                             uint64_t* __restrict__ states, int64_t n) {
+                             uint64_t* __restrict__ states, int64_t n, unsigned* status) {
     const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if (i0 == 0) *status = 0u;
     for (int64_t i = i0; i < ngroups; i += stride) counters[i] = 0u;
     for (int64_t i = i0; i < n; i += stride) states[i] = ~0ull;
 }
@@ -605,7 +633,7 @@ size_t fused2_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
     if (B <= 0 || L <= 0 || D <= 0 || D % 128 != 0) return 0;
     const fv2::Plan p = fv2::plan(B, L, D, fv2::waves_of(io));
     if (!p.lookback) return 0;
-    return fv2::counters_bytes(p.ngroups) + (size_t)(p.nseg * B * D) * sizeof(uint64_t);
+    return 256 + fv2::counters_bytes(p.ngroups) + (size_t)(p.nseg * B * D) * sizeof(uint64_t);
 }
 
 hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, const void* wi,
@@ -614,15 +642,16 @@ hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, 
                                  int64_t D, IoType io, void* ws, hipStream_t stream) {
     const fv2::Plan pl = fv2::plan(B, L, D, fv2::waves_of(io));
     fv2::Params P{x, wr, wi, br, bi, lambda, h0, h, hT, hz, y, L, D, B * D, pl.ngroups, pl.nseg,
-                  nullptr, nullptr};
+                  nullptr, nullptr, nullptr};
     if (pl.lookback) {
-        P.counters = (unsigned*)ws;
-        P.states = (uint64_t*)((char*)ws + fv2::counters_bytes(pl.ngroups));
+        P.status = (unsigned*)((char*)ws + kStatusOffset);
+        P.counters = (unsigned*)((char*)ws + 256);
+        P.states = (uint64_t*)((char*)ws + 256 + fv2::counters_bytes(pl.ngroups));
         const int64_t n = pl.nseg * B * D;
         int64_t blocks = (n + 255) / 256;
         blocks = blocks > 1024 ? 1024 : (blocks < 1 ? 1 : blocks);
         hipLaunchKernelGGL(fv2::reset_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                           P.counters, pl.ngroups, P.states, n);
+                           P.counters, pl.ngroups, P.states, n, P.status);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -1,21 +1,35 @@
+// Matrix-core products of the library (gfx950).
+//
 // Gate projections of the BD-LRU (RecBLR, arXiv 2406.12580, section 3.2):
 //   z_r = x W_r^T + b_r,  z_i = x W_i^T + b_i            (forward)
 //   dx += dz_r W_r + dz_i W_i                            (backward, data)
 //   dW_r = dz_r^T x, dW_i = dz_i^T x, db = sum_rows dz   (backward, weights)
-// One tiled kernel serves all three products through operand accessors; the
-// two gates are handled as one concatenated operand of width 2D.  x and the
-// weights use the I/O type; z and dz are fp32 scratch (rounding them to bf16
-// would cost about 1e-2 of relative accuracy in dW).
+// with the two gates handled as one concatenated operand of width 2D.  x and
+// the weights use the I/O type; z and dz are fp32 scratch (rounding them to
+// bf16 would cost about 1e-2 of relative accuracy in dW).
 //
-// Tiling: a 256-thread workgroup (4 waves) computes a 64 x 64 tile of C = A B
-// on the matrix cores; each wave owns a 32 x 32 quarter as 2 x 2 MFMA blocks of
-// 16 x 16 (v_mfma_f32_16x16x4_f32, or v_mfma_f32_16x16x32_bf16 when both
-// operands are bf16 inputs), accumulating in fp32.  K-slices of A and B are
-// staged through LDS in a K-contiguous layout; each operand is read from
-// global memory in the order that is contiguous for it.  The weight-gradient
-// product reduces over all B*L rows and is split across workgroups
-// (split-K); its fp32 partial tiles are summed afterwards in a fixed order,
-// so results are deterministic.
+// Two engines:
+//  * fastmm (namespace below, staging in mfma_tile.hpp), taken for every
+//    shape with D % 8 == 0 and 16-byte-aligned operands: a 256-thread
+//    workgroup owns a 128 x 128 output tile, each wave a 64 x 64 quarter as
+//    4 x 4 blocks of v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  K-slices
+//    of 64 are fetched through buffer resources as 16-byte quads one slice
+//    ahead (pinned with a scheduling barrier), fp32 operands split into bf16
+//    hi and lo planes (a product becomes hi*hi + hi*lo + lo*hi), and stored to
+//    LDS K-contiguous with a chunk swizzle that keeps fragment reads
+//    conflict-free.  Tiles are numbered so that each XCD owns a contiguous run
+//    of row blocks (their column tiles share that XCD's L2).  The weight
+//    gradient is split over rows into about two workgroups per CU, its fp32
+//    partials summed afterwards in a fixed order (deterministic), db summed
+//    from the same staged dz rows.  The same engine packs the weights for the
+//    fused scans (pack_group_kernel) and runs the decode step's product
+//    (step_kernel), and its fp32 linear32 / wgrad kernels serve the model
+//    step's linear layers.
+//  * the generic kernels (proj_*_kernel), for D % 8 != 0 or unaligned
+//    operands: 64 x 64 tiles, each wave a 32 x 32 quarter as 2 x 2 blocks of
+//    v_mfma_f32_16x16x4_f32 (or 16x16x32_bf16 when both operands are bf16
+//    inputs), one element per load, split-K weight gradient with a
+//    fixed-order sum.
 #include <initializer_list>
 #include <type_traits>
 

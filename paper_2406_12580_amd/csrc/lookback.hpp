@@ -17,7 +17,9 @@
 // Tiles are handed out in ticket order (an atomic counter), so the tile a
 // workgroup waits on was taken by a workgroup that is already running and
 // publishes its aggregate without waiting on anyone: the wait always ends.
-// Spins are still bounded; an exhausted bound yields NaN instead of a hang.
+// Spins are still bounded; an exhausted bound yields NaN instead of a hang
+// and sets a status word in the workspace header, so that the caller can tell
+// it from a NaN that came with the inputs.
 #pragma once
 
 #include "device_common.hpp"
@@ -60,12 +62,20 @@ __device__ __forceinline__ uint64_t peek(const uint64_t* p) {
                              __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Records in the workspace status word that a bounded wait ran out.
+__device__ __forceinline__ void flag_exhausted(unsigned* status) {
+    if (status) __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Wait until the word at p is ready (bounded); returns it, or a NaN inclusive
-// word if the bound runs out.
-__device__ __forceinline__ uint64_t wait_ready(const uint64_t* p, uint64_t w) {
+// word (and sets *status) if the bound runs out.
+__device__ __forceinline__ uint64_t wait_ready(const uint64_t* p, uint64_t w, unsigned* status) {
     int spins = 0;
     while (!word_ready(w)) {
-        if (++spins > kSpinLimit) return pack_inclusive(__uint_as_float(0x7FC00000u));
+        if (++spins > kSpinLimit) {
+            flag_exhausted(status);
+            return pack_inclusive(__uint_as_float(0x7FC00000u));
+        }
         __builtin_amdgcn_s_sleep(1);
         w = peek(p);
     }
@@ -78,7 +88,8 @@ __device__ __forceinline__ uint64_t wait_ready(const uint64_t* p, uint64_t w) {
 // inclusive, waits (bounded) for tile r-N's inclusive state at `oldest`.
 // Unrolled with selects: no dynamic indexing, no branches but the wait.
 template <int N>
-__device__ __forceinline__ float fold_window(uint64_t (&wd)[N], const uint64_t* oldest) {
+__device__ __forceinline__ float fold_window(uint64_t (&wd)[N], const uint64_t* oldest,
+                                             unsigned* status) {
     int nearest = N;
 #pragma unroll
     for (int i = N - 1; i >= 0; --i)
@@ -91,6 +102,7 @@ __device__ __forceinline__ float fold_window(uint64_t (&wd)[N], const uint64_t* 
         int spins = 0;
         while (!word_inclusive(w)) {
             if (++spins > kSpinLimit) {
+                flag_exhausted(status);
                 w = pack_inclusive(__uint_as_float(0x7FC00000u));
                 break;
             }
@@ -132,7 +144,8 @@ template <int W, int VEC, int K>
 __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ states, int64_t nch,
                                                int64_t c0, int64_t r, const float (&init)[VEC],
                                                uint64_t (&win_sh)[W * K][kWave][VEC],
-                                               float (&carry_sh)[kWave][VEC], int w, int lane) {
+                                               float (&carry_sh)[kWave][VEC], int w, int lane,
+                                               unsigned* status) {
     // Issue all K*VEC loads of the window first, then wait on any not ready.
     uint64_t wv[K][VEC];
 #pragma unroll
@@ -147,7 +160,7 @@ __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ stat
         const int64_t p = r - 1 - (int64_t)w * K - j;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
-            if (p >= 0) wv[j][k] = wait_ready(states + p * nch + c0 + k, wv[j][k]);
+            if (p >= 0) wv[j][k] = wait_ready(states + p * nch + c0 + k, wv[j][k], status);
             win_sh[w * K + j][lane][k] = wv[j][k];
         }
     }
@@ -158,24 +171,28 @@ __device__ __forceinline__ void lookback_carry(const uint64_t* __restrict__ stat
             uint64_t wd[W * K];
 #pragma unroll
             for (int i = 0; i < W * K; ++i) wd[i] = win_sh[i][lane][k];
-            carry_sh[lane][k] = fold_window<W * K>(wd, states + (r - W * K) * nch + c0 + k);
+            carry_sh[lane][k] = fold_window<W * K>(wd, states + (r - W * K) * nch + c0 + k, status);
         }
     }
 }
 
-// Fills the state words with "not ready" and zeroes the ticket counter
-// (internal linkage: every translation unit launches its own copy).
+// Fills the state words with "not ready" and zeroes the ticket counter and
+// the status word (internal linkage: every translation unit launches its own
+// copy).
 static __global__ void lookback_init_kernel(uint64_t* __restrict__ states, int64_t n,
                                             unsigned* __restrict__ ticket) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i == 0) *ticket = 0u;
+    if (i < 2) ticket[i] = 0u;  // ticket, status
     for (int64_t k = i; k < n; k += (int64_t)gridDim.x * blockDim.x) states[k] = ~0ull;
 }
 
 // Workspace of a look-back launch: a 256-byte header holding the ticket
-// counter, then one state word per (tile, channel).
+// counter (byte 0) and the status word (byte 4: nonzero once a bounded wait
+// ran out), then one state word per (tile, channel).
+constexpr size_t kStatusOffset = 4;
 struct LookbackWs {
     unsigned* ticket;
+    unsigned* status;
     uint64_t* states;
 };
 
@@ -184,7 +201,8 @@ inline size_t lookback_ws_bytes(int64_t nseg, int64_t nch) {
 }
 
 inline LookbackWs lookback_ws(void* ws) {
-    return LookbackWs{(unsigned*)ws, (uint64_t*)((char*)ws + 256)};
+    return LookbackWs{(unsigned*)ws, (unsigned*)((char*)ws + kStatusOffset),
+                      (uint64_t*)((char*)ws + 256)};
 }
 
 inline hipError_t lookback_reset(const LookbackWs& w, int64_t n, hipStream_t stream) {

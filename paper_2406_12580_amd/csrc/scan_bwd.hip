@@ -325,7 +325,10 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_chain_kernel(BwdParams P) {
     __shared__ float red[W][kWave][VEC];
     const int lane = threadIdx.x & (kWave - 1);
     const int w = wave_id();
-    if (blockIdx.x == 0) zero_counters(P.dl_counters, P.n_counters);
+    if (blockIdx.x == 0) {
+        zero_counters(P.dl_counters, P.n_counters);
+        if (threadIdx.x == 0 && P.lb.status) *P.lb.status = 0u;  // no waits in this kernel
+    }
     BwdLane<TX, VEC, Off> ln;
     ln.init(blockIdx.x, lane, P.L, P.D, P.nch);
     ChannelConst cc[VEC];
@@ -452,7 +455,8 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
 #pragma unroll
             for (int k = 0; k < VEC; ++k) publish(own + k, pack_aggregate(tot[k]));
         }
-        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, r, zero, win_sh, carry_sh, w, lane);
+        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, r, zero, win_sh, carry_sh, w, lane,
+                           P.lb.status);
         if (w == 0 && ln.valid) {
 #pragma unroll
             for (int k = 0; k < VEC; ++k)
@@ -582,7 +586,8 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
         }
     } else {
         if (w == 0 && ln.valid) publish(own, pack_aggregate(tot));
-        lookback_carry<W, 1, K>(P.lb.states, P.nch, ln.c0, r, dhTv, win_sh, carry_sh, w, lane);
+        lookback_carry<W, 1, K>(P.lb.states, P.nch, ln.c0, r, dhTv, win_sh, carry_sh, w, lane,
+                           P.lb.status);
         if (w == 0 && ln.valid)
             publish(own, pack_inclusive(fmaf(tot.A, carry_sh[lane][0], tot.H)));
     }
@@ -861,8 +866,8 @@ static BwdLayout bwd_layout(int64_t B, int64_t D, const BwdPlan& p) {
     BwdLayout l;
     const int64_t rows = p.nseg * B;
     const int64_t nb = (rows + kReduceRows - 1) / kReduceRows;
-    l.lb = 0;
-    l.partial = p.lookback ? align_up(lookback_ws_bytes(p.nseg, B * D)) : 0;
+    l.lb = 0;  // the header (ticket, status word) is there in both modes
+    l.partial = align_up(p.lookback ? lookback_ws_bytes(p.nseg, B * D) : 256);
     l.partial2 = l.partial + align_up((size_t)(rows * D) * sizeof(float));
     l.counters = l.partial2 + align_up((size_t)(nb * D) * sizeof(double));
     l.total = l.counters + align_up((size_t)dlambda_groups(D) * sizeof(unsigned));
@@ -940,7 +945,8 @@ hipError_t launch_scan_backward(const ScanBwdArgs& a, hipStream_t stream) {
     const BwdParams P{a.x,   a.zr,    a.zi,  a.lambda, a.h0, a.h,   a.dh,  a.dhT,
                       a.dx,  a.dzr,   a.dzi, a.dh0,    partial, a.L, a.D,  a.B * a.D,
                       plan.ngroups, plan.nseg,
-                      plan.lookback ? lookback_ws(ws + lay.lb) : LookbackWs{},
+                      plan.lookback ? lookback_ws(ws + lay.lb)
+                                    : LookbackWs{nullptr, lookback_ws(ws + lay.lb).status, nullptr},
                       counters, dlambda_groups(a.D)};
     hipError_t e;
     if (a.io == IoType::kF32)

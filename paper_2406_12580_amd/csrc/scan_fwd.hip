@@ -306,7 +306,8 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
 #pragma unroll
             for (int k = 0; k < VEC; ++k) publish(own + k, pack_aggregate(tot[k]));
         }
-        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, s, h0v, win_sh, carry_sh, w, lane);
+        lookback_carry<W, VEC, K>(P.lb.states, P.nch, ln.c0, s, h0v, win_sh, carry_sh, w, lane,
+                           P.lb.status);
         if (w == 0 && ln.valid) {
 #pragma unroll
             for (int k = 0; k < VEC; ++k)
@@ -421,7 +422,8 @@ scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
         }
     } else {
         if (w == 0 && ln.valid) publish(own, pack_aggregate(tot));
-        lookback_carry<W, 1, K>(P.lb.states, P.nch, ln.c0, s, h0v, win_sh, carry_sh, w, lane);
+        lookback_carry<W, 1, K>(P.lb.states, P.nch, ln.c0, s, h0v, win_sh, carry_sh, w, lane,
+                           P.lb.status);
         if (w == 0 && ln.valid)
             publish(own, pack_inclusive(fmaf(tot.A, carry_sh[lane][0], tot.H)));
     }
