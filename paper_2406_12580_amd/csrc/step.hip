@@ -4,7 +4,7 @@
 // Purely elementwise and bound by HBM bandwidth.  Each thread handles 8
 // consecutive elements (one 16-byte bf16 load or two 16-byte fp32 loads per
 // operand); the per-channel constants of softplus(Lambda) are built once per
-// workgroup in LDS and the grid strides over the [B, D] array.
+// workgroup in LDS.
 #include <type_traits>
 #include <utility>
 
@@ -45,6 +45,9 @@ struct Vec8<bf16> {
 };
 
 // Vector path: n and D multiples of 8, every pointer 16-byte aligned, D <= table size.
+// One group of 8 elements per thread and no grid-stride loop: every thread
+// issues its loads at once (a grid-stride loop over fewer workgroups measured
+// 42-43 us against 40-40.5 us at 65536 x 256, bf16 with fp32 state).
 template <typename T, typename TZ>
 __global__ __launch_bounds__(kStepThreads) void step_vec_kernel(
     const T* __restrict__ x, const TZ* __restrict__ zr, const TZ* __restrict__ zi,
@@ -52,9 +55,8 @@ __global__ __launch_bounds__(kStepThreads) void step_vec_kernel(
     __shared__ ChannelConst table[kStepMaxTable];
     for (int64_t d = threadIdx.x; d < D; d += blockDim.x) table[d] = channel_const(lam[d]);
     __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x * kStepVec;
-    for (int64_t e0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStepVec; e0 < n;
-         e0 += stride) {
+    const int64_t e0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kStepVec;
+    if (e0 < n) {
         Vec8<T> vx;
         Vec8<TZ> vr, vi;
         vx.load(x + e0);
@@ -100,8 +102,7 @@ static hipError_t launch_step_t(const void* x, const void* zr, const void* zi, c
     const bool vec = (D % kStepVec == 0) && D <= kStepMaxTable && aligned16(x) &&
                      aligned16(zr) && aligned16(zi) && aligned16(h_prev) && aligned16(h_next);
     if (vec) {
-        int64_t blocks = (n / kStepVec + kStepThreads - 1) / kStepThreads;
-        if (blocks > 2048) blocks = 2048;
+        const int64_t blocks = (n / kStepVec + kStepThreads - 1) / kStepThreads;
         hipLaunchKernelGGL((step_vec_kernel<T, TZ>), dim3((unsigned)blocks), dim3(kStepThreads),
                            0, stream, (const T*)x, (const TZ*)zr, (const TZ*)zi, lam, h_prev,
                            h_next, n, D);

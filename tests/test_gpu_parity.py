@@ -227,7 +227,10 @@ FUSED_FWD = [(1, 1000, 64), (3, 700, 128), (2, 257, 192), (1, 129, 256), (2, 100
              # D = 128 / 256 with W kept in registers: few channel groups take
              # tiles in ticket order with look-back (above), at least 256 groups
              # walk their tiles in a chain (below; ragged last tile, L = 1)
-             (256, 100, 128), (512, 1, 128), (128, 77, 256)]
+             (256, 100, 128), (512, 1, 128), (128, 77, 256),
+             # many tiles per group: the workgroups' tickets run several tiles
+             # ahead of the one they work on
+             (2, 4100, 256), (5, 3000, 128)]
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
