@@ -157,7 +157,8 @@ __global__ __launch_bounds__(kGateThreads) void gate_out_vec_kernel(const T* __r
 __device__ __forceinline__ float dsilu(float v, float s) { return s * fmaf(v, 1.0f - s, 1.0f); }
 
 // dh = dy SiLU(hz) and dhz = dy h SiLU'(hz), one element per thread; dh is
-// stored as TG (fp32 when it feeds an fp32 backward).
+// stored as TG (fp32 when it feeds an fp32 backward), or not at all when dh
+// is null (the fused scan then forms it on load).
 template <typename T, typename TG>
 __global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(
     const T* __restrict__ dy, const T* __restrict__ hz, const T* __restrict__ h,
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_kernel(
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n) return;
     const float g = load(hz + e), s = sigmoid(g), gy = load(dy + e);
-    store(dh + e, gy * (g * s));
+    if (dh) store(dh + e, gy * (g * s));
     store(dhz + e, gy * load(h + e) * dsilu(g, s));
 }
 
@@ -192,13 +193,15 @@ __global__ __launch_bounds__(kGateThreads) void gate_bwd_vec_kernel(
         b[i] = from_f32<T>(gy * to_f32(vh[i]) * dsilu(g, s));
     }
     constexpr int VG = 16 / sizeof(TG);
+    if (dh) {
 #pragma unroll
-    for (int s0 = 0; s0 < V; s0 += VG) {
-        uint4 o1;
-        TG* a = (TG*)&o1;
+        for (int s0 = 0; s0 < V; s0 += VG) {
+            uint4 o1;
+            TG* a = (TG*)&o1;
 #pragma unroll
-        for (int i = 0; i < VG; ++i) a[i] = from_f32<TG>(g1[s0 + i]);
-        *(uint4*)(dh + q * V + s0) = o1;
+            for (int i = 0; i < VG; ++i) a[i] = from_f32<TG>(g1[s0 + i]);
+            *(uint4*)(dh + q * V + s0) = o1;
+        }
     }
     *(uint4*)(dhz + q * V) = o2;
 }

@@ -200,13 +200,13 @@ __global__ __launch_bounds__(kThreads) void proj_fwd_kernel(const T* x, const T*
     });
 }
 
-template <typename T>
+template <typename T, typename TD = T>
 __global__ __launch_bounds__(kThreads) void proj_dx_kernel(const float* dzr, const float* dzi,
-                                                           const T* wr, const T* wi, T* dx,
+                                                           const T* wr, const T* wi, TD* dx,
                                                            int64_t M, int64_t D) {
     DxOps<T> ops{dzr, dzi, wr, wi, D};
     mfma_tile<false>(ops, M, D, 0, 2 * D, [&](int64_t i, int64_t n, float v) {
-        T* p = dx + i * D + n;
+        TD* p = dx + i * D + n;
         store(p, load(p) + v);  // dx already holds the direct term delta * beta
     });
 }
@@ -620,11 +620,11 @@ struct DxEpi {
 
 // One 128 x 128 tile of dx per workgroup: dx += [dz_r | dz_i] Wcat, with the
 // two dz halves at dzr and dzr + hoff bytes and pack holding Wcat^T planes.
-template <typename T>
+template <typename T, typename TD = T>
 __global__ __launch_bounds__(256, 2) void dx_kernel(const float* dzr, uint32_t hoff,
-                                                    const __bf16* pack, T* dx, int64_t M,
+                                                    const __bf16* pack, TD* dx, int64_t M,
                                                     int64_t D) {
-    constexpr bool F32 = sizeof(T) == 4;
+    constexpr bool F32 = sizeof(T) == 4;  // fp32 weights: two bf16 planes
     using OpA = Operand<kF32, true, true>;
     using OpB = Operand<F32 ? kPack2 : kPack1, true>;
     __shared__ __attribute__((aligned(16))) char smem[lds_bytes<OpA::kPlanes, OpB::kPlanes>()];
@@ -635,7 +635,7 @@ __global__ __launch_bounds__(256, 2) void dx_kernel(const float* dzr, uint32_t h
     const OpA a{resource(dzr, hoff + (uint32_t)(M * D * 4)), (uint32_t)(D * 4), (uint32_t)D, hoff,
                 0};
     const OpB b{resource(pack, OpB::kPlanes * plane), (uint32_t)(2 * D * 2), 0, 0, plane};
-    const DxEpi<T> epi{dx, M, D};
+    const DxEpi<TD> epi{dx, M, D};
     tile(a, b, (t / ntn) * BM, (t % ntn) * BN, 0, 2 * D, epi, smem);
 }
 
@@ -1148,8 +1148,9 @@ hipError_t launch_project_forward(const void* x, const void* wr, const void* br,
 
 hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const void* wr,
                                         const void* wi, void* dx, int64_t M, int64_t D,
-                                        IoType io, void* pack, hipStream_t stream) {
+                                        IoType io, void* pack, hipStream_t stream, bool dx_f32) {
     if (M == 0 || D == 0) return hipSuccess;
+    dx_f32 = dx_f32 && io == IoType::kBf16;
     const int64_t hoff = pair_offset(dzr, dzi, M * D * 4, fastmm::BM * D * 4);
     if (D % 8 == 0 && hoff >= 0 && aligned16({dzr, dx, pack})) {
         hipError_t e = launch_pack(wr, wi, D, io, true, pack, stream);
@@ -1160,6 +1161,10 @@ hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const 
             hipLaunchKernelGGL(fastmm::dx_kernel<float>, dim3(fastmm::grid_of(tiles)), dim3(256),
                                0, stream, (const float*)dzr, (uint32_t)hoff, (const __bf16*)pack,
                                (float*)dx, M, D);
+        else if (dx_f32)
+            hipLaunchKernelGGL((fastmm::dx_kernel<bf16, float>), dim3(fastmm::grid_of(tiles)),
+                               dim3(256), 0, stream, (const float*)dzr, (uint32_t)hoff,
+                               (const __bf16*)pack, (float*)dx, M, D);
         else
             hipLaunchKernelGGL(fastmm::dx_kernel<bf16>, dim3(fastmm::grid_of(tiles)), dim3(256),
                                0, stream, (const float*)dzr, (uint32_t)hoff, (const __bf16*)pack,
@@ -1170,6 +1175,10 @@ hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const 
         hipLaunchKernelGGL(proj_dx_kernel<float>, tiles(M, D), dim3(kThreads), 0, stream,
                            (const float*)dzr, (const float*)dzi, (const float*)wr,
                            (const float*)wi, (float*)dx, M, D);
+    else if (dx_f32)
+        hipLaunchKernelGGL((proj_dx_kernel<bf16, float>), tiles(M, D), dim3(kThreads), 0, stream,
+                           (const float*)dzr, (const float*)dzi, (const bf16*)wr, (const bf16*)wi,
+                           (float*)dx, M, D);
     else
         hipLaunchKernelGGL(proj_dx_kernel<bf16>, tiles(M, D), dim3(kThreads), 0, stream,
                            (const float*)dzr, (const float*)dzi, (const bf16*)wr, (const bf16*)wi,

@@ -19,10 +19,12 @@ hipError_t launch_project_forward(const void* x, const void* wr, const void* br,
                                   const void* bi, void* zr, void* zi, int64_t M, int64_t D,
                                   IoType io, void* pack, hipStream_t stream);
 
-// dx += dz_r W_r + dz_i W_i (dx holds the direct term on entry).
+// dx += dz_r W_r + dz_i W_i (dx holds the direct term on entry); dx is in the
+// I/O type, or fp32 when dx_f32 is set.
 hipError_t launch_project_backward_data(const void* dzr, const void* dzi, const void* wr,
                                         const void* wi, void* dx, int64_t M, int64_t D,
-                                        IoType io, void* pack, hipStream_t stream);
+                                        IoType io, void* pack, hipStream_t stream,
+                                        bool dx_f32 = false);
 
 // dW_r, dW_i = dz^T x and db_r, db_i = column sums of dz; uses
 // project_dw_workspace(M, D) bytes of scratch at `ws`.

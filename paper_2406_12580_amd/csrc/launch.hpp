@@ -148,6 +148,13 @@ struct FusedBwdArgs {
     int64_t B, L, D;
     IoType io;
     void* ws;
+    // Output gate of the gated layer: when gy is set, dh is formed on load as
+    // gy SiLU(gz) (fp32) instead of being read (dh is then unused).
+    const void* gy = nullptr;
+    const void* gz = nullptr;
+    // fp32 x with h (and gy, gz) in bf16: the gated layer's bf16 backward,
+    // which keeps x' and the gradients in fp32.
+    bool h_bf16 = false;
 };
 bool fused_backward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
                             const void* h, const void* pack);
@@ -176,8 +183,8 @@ hipError_t launch_conv_silu(const void* hx, const float* w4, const float* b4, vo
 // y = h * SiLU(hz) over n elements.
 hipError_t launch_gate_out(const void* h, const void* hz, void* y, int64_t n, IoType io,
                            hipStream_t stream);
-// Output gate backward: dh = dy * SiLU(hz) (stored as dh_io), dhz = dy * h *
-// SiLU'(hz) (I/O type).
+// Output gate backward: dh = dy * SiLU(hz) (stored as dh_io; skipped when dh
+// is null), dhz = dy * h * SiLU'(hz) (I/O type).
 hipError_t launch_gate_backward(const void* dy, const void* hz, const void* h, void* dh,
                                 void* dhz, int64_t n, IoType io, IoType dh_io,
                                 hipStream_t stream);

@@ -58,6 +58,10 @@ struct BwdParams {
     LookbackWs lb;
     unsigned* dl_counters;  // one per 64-channel column group of the dLambda reduction
     int64_t n_counters;
+    // Fused kernel only: when gy is set, dh is not read but formed on load
+    // as dh_t = gy_t SiLU(gz_t) (the output gate of the gated layer), in fp32.
+    const void* gy = nullptr;
+    const void* gz = nullptr;
 };
 
 // Zeroes the dLambda counters (n of them); called by one workgroup of each
@@ -521,7 +525,14 @@ __device__ __forceinline__ float lds_elem(const char* base, int idx) {
 // point, the same tile measured 376 against 366 µs for 256 x 2048 x 128 fp32
 // and 215-222 against 220-223 µs for 16 x 16384 x 256 bf16, so the scan
 // keeps its own kernels.)
-template <typename T, typename TZ, int W, int C, int K, typename Off>
+// Element offset of one tensor from that of another with a different element
+// size (same [B][L][D] index).
+template <typename TA, typename TB, typename Off>
+__device__ __forceinline__ Off elem_offset(Off off_a) {
+    return sizeof(TA) == sizeof(TB) ? off_a : off_a / (Off)sizeof(TA) * (Off)sizeof(TB);
+}
+
+template <typename T, typename TH, typename TD, typename TZ, int W, int C, int K, typename Off>
 __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int64_t g, int64_t b,
                                              int64_t cg, const float (&zr)[C],
                                              const float (&zi)[C], char* stage,
@@ -543,15 +554,27 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
     constexpr int kStaged = C * kWave * (int)sizeof(T);  // one tensor's rows of a wave
     char* const xs = stage + w * 2 * kStaged;
     char* const hs = xs + kStaged;
+    static_assert(sizeof(TH) <= sizeof(T), "the staged h rows fit the x rows' room");
     stage_rows<T, C>((const T*)P.x, b, P.L, P.D, cg * kWave, tw, 0, xs, lane);
-    stage_rows<T, C>((const T*)P.h, b, P.L, P.D, cg * kWave, tw, -1, hs, lane);
+    stage_rows<TH, C>((const TH*)P.h, b, P.L, P.D, cg * kWave, tw, -1, hs, lane);
     float gv[C];
+    if (P.gy) {
 #pragma unroll
-    for (int j = 0; j < C; ++j) {
-        const int64_t t = tw + j < P.L ? tw + j : P.L - 1;
-        float v[1];
-        load_vec<T, 1>((const T*)P.dh, ln.at(t), v);
-        gv[j] = v[0];
+        for (int j = 0; j < C; ++j) {
+            const int64_t t = tw + j < P.L ? tw + j : P.L - 1;
+            float y[1], z[1];
+            load_vec<TH, 1>((const TH*)P.gy, elem_offset<T, TH>(ln.at(t)), y);
+            load_vec<TH, 1>((const TH*)P.gz, elem_offset<T, TH>(ln.at(t)), z);
+            gv[j] = y[0] * (z[0] * sigmoid(z[0]));
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            const int64_t t = tw + j < P.L ? tw + j : P.L - 1;
+            float v[1];
+            load_vec<T, 1>((const T*)P.dh, ln.at(t), v);
+            gv[j] = v[0];
+        }
     }
     float rr[C], al[C];
 #pragma unroll
@@ -606,7 +629,7 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
         const float mm = one_minus_exp_neg(rj * cc[0].two_s, a);
         const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
         const float sq = mm * rs;  // sqrt(1 - alpha^2)
-        const float hprev = !full && t == 0 ? h0v[0] : lds_elem<T>(hs, j * kWave + lane);
+        const float hprev = !full && t == 0 ? h0v[0] : lds_elem<TH>(hs, j * kWave + lane);
         const float g_alpha = delta * hprev;
         const float g_beta = delta * lds_elem<T>(xs, j * kWave + lane);
         const float g1 = -a * g_alpha;
@@ -618,7 +641,7 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
         eps = a * delta;
         if (ln.valid) {
             const Off off = ln.at(t);
-            store_vec<T, 1>((T*)P.dx, off, dxv);
+            store_vec<TD, 1>((TD*)P.dx, z_offset<T, TD>(off), dxv);
             store_vec<TZ, 1>((TZ*)P.dzr, z_offset<T, TZ>(off), dzrv);
             store_vec<TZ, 1>((TZ*)P.dzi, z_offset<T, TZ>(off), dziv);
             if (!full && t == 0 && P.dh0) P.dh0[ln.c0] = eps;
@@ -627,7 +650,7 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
     write_partial<W, 1>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
 }
 
-template <typename T, int K, typename Off>
+template <typename T, typename TH, int K, typename Off>
 __global__ __launch_bounds__(fusedz::NT, 4) void
 scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi) {
     constexpr int W = fusedz::W, C = fusedz::C;
@@ -656,7 +679,7 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
     fusedz::tile_z<T>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, s * W * C, smem, tid, w,
                       lane, zr, zi);
     __syncthreads();  // every wave holds its z: the product's LDS is free
-    bwd_eps_tile<T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh, carry_sh, red,
+    bwd_eps_tile<T, TH, T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh, carry_sh, red,
                                          w, lane);
 }
 
@@ -995,29 +1018,40 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
     const BwdParams P{a.x,  nullptr, nullptr, a.lambda, a.h0, a.h,   a.dh,  a.dhT,
                       a.dx, a.dzr,   a.dzi,   a.dh0,    partial, a.L, a.D,  a.B * a.D,
                       plan.ngroups, plan.nseg, lookback_ws(ws + lay.lb),
-                      counters, dlambda_groups(a.D)};
+                      counters, dlambda_groups(a.D), a.gy, a.gz};
     hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedz::NT);
     const size_t esz = io_bytes(a.io);
     const bool small = (uint64_t)(a.B * a.L * a.D) * 4 < (1ull << 32);
     constexpr int K = lb_window<1>();
-    if (esz == 4) {
+    if (esz == 4 && !a.h_bf16) {
         if (small)
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, K, uint32_t>), grid, block, 0,
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, float, K, uint32_t>), grid, block, 0,
                                stream, P, (const __bf16*)a.pack, (const float*)a.br,
                                (const float*)a.bi);
         else
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, K, uint64_t>), grid, block, 0,
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, float, K, uint64_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
+                               (const float*)a.bi);
+    } else if (a.h_bf16) {
+        if (small)
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint32_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
+                               (const float*)a.bi);
+        else
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint64_t>), grid, block, 0,
                                stream, P, (const __bf16*)a.pack, (const float*)a.br,
                                (const float*)a.bi);
     } else {
         if (small)
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, K, uint32_t>), grid, block, 0, stream,
-                               P, (const __bf16*)a.pack, (const bf16*)a.br, (const bf16*)a.bi);
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, bf16, K, uint32_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const bf16*)a.br,
+                               (const bf16*)a.bi);
         else
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, K, uint64_t>), grid, block, 0, stream,
-                               P, (const __bf16*)a.pack, (const bf16*)a.br, (const bf16*)a.bi);
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, bf16, K, uint64_t>), grid, block, 0,
+                               stream, P, (const __bf16*)a.pack, (const bf16*)a.br,
+                               (const bf16*)a.bi);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_dlambda(partial, partial2, plan.nseg * a.B, a.D, a.lambda, a.dlambda, counters,
