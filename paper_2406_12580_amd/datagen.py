@@ -241,12 +241,35 @@ def model_params(dims: ModelDims, seed: int) -> dict:
     return p
 
 
-def model_batch(dims: ModelDims, seed: int):
+def model_batch(dims: ModelDims, seed: int, min_len: int | None = None, pad_id: int = 0):
     """Item ids [B][T] and next-item targets [B] (int32), drawn with Zipf(1)
-    popularity over the V items (item v has weight 1 / (v + 1))."""
+    popularity over the V items (item v has weight 1 / (v + 1)).
+
+    With min_len given, the batch holds short sequences instead: row b has a
+    length l_b ~ U{min_len, ..., T}, its first T - l_b positions hold pad_id
+    (left padding) and its items and target are drawn, with the same Zipf
+    weights, from the V - 1 ids other than pad_id."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    pr = 1.0 / np.arange(1, dims.V + 1, dtype=np.float64)
+    if min_len is None:
+        pr = 1.0 / np.arange(1, dims.V + 1, dtype=np.float64)
+        pr /= pr.sum()
+        ids = rng.choice(dims.V, size=(dims.B, dims.T), p=pr).astype(np.int32)
+        targets = rng.choice(dims.V, size=dims.B, p=pr).astype(np.int32)
+        return ids, targets
+    if not 1 <= min_len <= dims.T or not 0 <= pad_id < dims.V:
+        raise ValueError("need 1 <= min_len <= T and 0 <= pad_id < V")
+    items = np.array([v for v in range(dims.V) if v != pad_id])
+    pr = 1.0 / np.arange(1, dims.V, dtype=np.float64)
     pr /= pr.sum()
-    ids = rng.choice(dims.V, size=(dims.B, dims.T), p=pr).astype(np.int32)
-    targets = rng.choice(dims.V, size=dims.B, p=pr).astype(np.int32)
+    lengths = rng.integers(min_len, dims.T, size=dims.B, endpoint=True)
+    ids = items[rng.choice(dims.V - 1, size=(dims.B, dims.T), p=pr)].astype(np.int32)
+    ids[np.arange(dims.T)[None, :] < (dims.T - lengths)[:, None]] = pad_id
+    targets = items[rng.choice(dims.V - 1, size=dims.B, p=pr)].astype(np.int32)
     return ids, targets
+
+
+def ml1m_min_len(T: int = 200, mean_len: float = 165.5) -> int:
+    """Shortest length of the MovieLens-1M length mix: U{m, ..., T} has mean
+    (m + T) / 2, so m = 2 * 165.5 - 200 = 131 gives the dataset's average
+    length of 165.5 (table tab:dataset) under the maximum length 200."""
+    return int(round(2 * mean_len - T))
