@@ -22,8 +22,9 @@ and backward (causal conv + SiLU, BD-LRU with projections, SiLU output gate;
 recblr_gated_forward / recblr_gated_backward) on the workload.  --api model
 times a full 2-layer RecBLR training step (embedding, behaviour-modelling
 layers, softmax cross entropy, backward, Adam) at the MovieLens-1M training
-shape of the paper (B=2048, T=200, D=64, E=2, 3,416 items); its roofline is
-matrix-multiply flops against the fp32 matrix-core peak.
+shape of the paper (B=2048, T=200, D=64, E=2, 3,416 items) with its setting
+of dropout 0.2 and rows of the dataset's length mix, left-padded; its
+roofline is matrix-multiply flops against the fp32 matrix-core peak.
 Prints ONE JSON line (metric, value, roofline of the dominant kernel, and the
 fp64 CPU oracle timed on a bounded sample of the same workload).  `value` and
 `ms_per_step` come from K steps timed back to back with no events in between
@@ -311,9 +312,12 @@ def model_main(args, torch, dg, rb):
     training shape."""
     d = dg.MODEL_CONFIGS[args.workload or "ml1m"]
     dev = torch.device("cuda:0")
-    log(f"model {d}")
+    # the paper's MovieLens-1M setting: dropout 0.2 (its dropout study) and
+    # rows of the dataset's length mix, left-padded with id 0
+    p_drop, pad, min_len = args.dropout, 0, dg.ml1m_min_len(d.T)
+    log(f"model {d}, dropout {p_drop}, lengths U{{{min_len}..{d.T}}} left-padded")
     named = dg.model_params(d, 1)
-    ids, targets = dg.model_batch(d, 2)
+    ids, targets = dg.model_batch(d, 2, min_len=min_len, pad_id=pad)
     rd = rb.model_dims(d.B, d.T, d.D, d.E, d.V, d.layers, d.K, d.eps)
     offs = rb.model_param_offsets(rd)
     # model_params lists the tensors in the documented parameter order
@@ -329,7 +333,8 @@ def model_main(args, torch, dg, rb):
     n = [0]
 
     def one():
-        step.train_step(P, I, Tg, G, loss)
+        # a new Philox offset per step: new dropout masks every step
+        step.train_step(P, I, Tg, G, loss, dropout=p_drop, seed=2406, offset=n[0], pad_id=pad)
         n[0] += 1
         rb.adam_update(P, G, M1, M2, n[0])
     for _ in range(args.warmup):
@@ -354,10 +359,12 @@ def model_main(args, torch, dg, rb):
            "value": tokens * K / wall, "unit": "tokens/s", "n_gpus": 1, "steps": K,
            "warmup": args.warmup, "ms_per_step": wall / K * 1e3, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-           "data": "synthetic (Zipf item ids, seeded random-init weights)",
+           "data": "synthetic (Zipf item ids, row lengths U{%d..%d} left-padded with id 0, "
+                   "seeded random-init weights)" % (min_len, d.T),
            "config": {"workload": f"{args.workload or 'ml1m'}: 2-layer RecBLR, MovieLens-1M "
                                   "training shape", "B": d.B, "T": d.T, "D": d.D, "E": d.E,
-                      "V": d.V, "layers": d.layers, "K": d.K},
+                      "V": d.V, "layers": d.layers, "K": d.K, "dropout": p_drop,
+                      "real_item_fraction": round(float((ids != pad).mean()), 4)},
            "loss_first_last": [first, loss.item()],
            "roofline": {"bound": "mfma", "kernel": "model_step (matrix-multiply flops)",
                         "achieved": ach, "peak": 157.3, "unit": "TFLOP/s", "frac": ach / 157.3,
@@ -371,7 +378,8 @@ def model_main(args, torch, dg, rb):
         for name, shape, o in lay:
             f64[o:o + int(np.prod(shape))] = named[name].ravel()
         while time.perf_counter() - t0 < 10.0:
-            om.train_step(f64, ids[:rows], targets[:rows], d.D, d.E, d.V, d.layers, d.K, d.eps)
+            om.train_step(f64, ids[:rows], targets[:rows], d.D, d.E, d.V, d.layers, d.K, d.eps,
+                          dropout=p_drop, seed=2406, offset=passes, pad_id=pad)
             passes += 1
         total = time.perf_counter() - t0
         threads = torch.get_num_threads()
@@ -588,6 +596,8 @@ def main():
     ap.add_argument("--api", choices=["scan", "full", "step", "scan_step", "ablation", "gated",
                                       "model"], default="scan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dropout", type=float, default=0.2,
+                    help="--api model: drop probability (the paper's MovieLens-1M rate)")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MIB",
                     help="only run K plain device copies of MIB MiB (calibrates HBM counters)")
     args = ap.parse_args()

@@ -284,17 +284,21 @@ int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
 /*
  * Full RecBLR model: one training step of the paper's model (sections 2 and
  * 3.1), as a model-level harness around the BD-LRU path:
- *   H = LayerNorm(E[ids])                               (eq:layernorm; no positions)
+ *   H = LayerNorm(Dropout(E[ids]))                      (eq:layernorm; no positions)
  *   `layers` times (behaviour-modelling layer):
- *     H1 = LayerNorm(H + GRL(H))     GRL: Algorithm alg:gated_recurrent with
+ *     H1 = LayerNorm(H + Dropout(GRL(H)))  GRL: Algorithm alg:gated_recurrent with
  *          Hx, Hz = H Wx^T + bx, H Wz^T + bz (D -> E*D), the gated layer core of
  *          recblr_gated_forward (h0 = 0), output projection Wo (E*D -> D)
- *     H  = LayerNorm(H1 + PFFN(H1))  PFFN = SiLU(H1 W1^T + b1) W2^T + b2 (eq. PFFN)
+ *     H  = LayerNorm(H1 + Dropout(PFFN(H1)))
+ *          PFFN = SiLU(H1 W1^T + b1) W2^T + b2 (eq. PFFN)
  *   logits = h_T E^T over the V items (h_T: each row's last step);
  *   loss = mean over rows of the cross entropy of softmax(logits) with targets.
  * Readings (the paper leaves them open): residual + LayerNorm after each
- * sub-layer, dropout as the identity, the cross entropy of the next item at
- * the last step.  The linear layers of the behaviour-modelling layers run on
+ * sub-layer, dropout on the embedding and on each sub-layer's output before
+ * its residual sum (section 3.1 lists dropout without placing it), the cross
+ * entropy of the next item at the last step.  Positions holding the padding
+ * id (recblr_model_step_opts) enter as the zero vector: left padding with
+ * zeros (section 3.3).  The linear layers of the behaviour-modelling layers run on
  * this library's matrix-core kernels (fp32 products for the forward and the
  * data gradients; bias, SiLU and its derivative fused in); the prediction
  * layer's products are rocBLAS fp32 GEMMs; all other steps run in this
@@ -330,6 +334,31 @@ int64_t recblr_model_param_offsets(const recblr_model_dims* m, int64_t* offsets,
  * layer, backward scratch, the sort of the item ids); 0 if unsupported. */
 size_t recblr_model_workspace_size(const recblr_model_dims* m);
 
+/*
+ * Per-step options of recblr_model_train_step (NULL: no dropout, no padding).
+ *
+ * Dropout is inverted dropout with drop probability `dropout`: an element is
+ * kept or zeroed and kept elements are scaled by 1 / (1 - dropout) (float).
+ * Its masks come from Philox4x64-10 (Salmon, Moraes, Dror and Shaw, SC 2011),
+ * so any implementation can draw them: element e (row-major over [B][T][D])
+ * of dropout site s (0 the embedding, 1 + 2l layer l's gated recurrent
+ * output, 2 + 2l layer l's PFFN output) takes the 32-bit word e mod 8 (the
+ * low half of each 64-bit output word first) of Philox4x64-10 at counter
+ * (floor(e / 8), s, 0, 0) under key (seed, offset), and is dropped when that
+ * word is below floor(dropout * 2^32).  The backward uses the same masks.
+ * A caller that wants new masks each step changes offset (e.g. the step count).
+ *
+ * pad_id marks left padding: a position holding it enters as the zero vector
+ * (its lookup sends no gradient to E) and is otherwise processed like any
+ * other position; the prediction softmax still runs over all V ids.
+ */
+typedef struct {
+    float dropout;   /* drop probability, 0 <= dropout < 1; 0 turns dropout off */
+    int32_t pad_id;  /* padding id in [0, V), or -1 for none */
+    uint64_t seed;   /* Philox key, word 0 */
+    uint64_t offset; /* Philox key, word 1 */
+} recblr_model_step_opts;
+
 /* rocBLAS handle for the model step's prediction-layer GEMMs: created and
  * destroyed by the caller (creation allocates rocBLAS' own state; the step
  * itself allocates nothing).  A handle serves one stream at a time. */
@@ -338,19 +367,22 @@ int recblr_blas_destroy(void* handle);
 
 /*
  * Forward and backward of one batch:
+ *   opts : dropout and padding (may be NULL: neither);
  *   params : flat float parameters (256-byte aligned);  ids : [B][T] int32 item
  *   ids;  targets : [B] int32 next items;  grads : flat float, the layout of
  *   params (padding zero);  loss : one float.
  * Every sum over rows is taken in a fixed order (double), so loss and
- * gradients repeat bitwise for a given rocBLAS handle and GPU.  An id or
- * target outside [0, V) makes the loss NaN (nothing is read out of bounds).
+ * gradients repeat bitwise for a given rocBLAS handle, GPU and opts.  An id
+ * or target outside [0, V) makes the loss NaN (nothing is read out of bounds).
  * Errors: INVALID_ARGUMENT for a NULL pointer or misaligned buffer or
- * overlapping outputs; UNSUPPORTED for dimensions outside the ranges above;
- * WORKSPACE; HIP for a failed launch or GEMM.
+ * overlapping outputs, a dropout outside [0, 1) or a pad_id outside
+ * [-1, V); UNSUPPORTED for dimensions outside the ranges above; WORKSPACE;
+ * HIP for a failed launch or GEMM.
  */
-int recblr_model_train_step(const recblr_model_dims* m, const float* params, const int32_t* ids,
-                            const int32_t* targets, float* grads, float* loss, void* ws,
-                            size_t ws_bytes, void* blas, void* stream);
+int recblr_model_train_step(const recblr_model_dims* m, const recblr_model_step_opts* opts,
+                            const float* params, const int32_t* ids, const int32_t* targets,
+                            float* grads, float* loss, void* ws, size_t ws_bytes, void* blas,
+                            void* stream);
 
 /*
  * Adam (Kingma and Ba, Algorithm 1) over n floats, in place: step is the

@@ -787,11 +787,23 @@ int recblr_blas_destroy(void* handle) {
                : RECBLR_ERR_HIP;
 }
 
-int recblr_model_train_step(const recblr_model_dims* m, const float* params, const int32_t* ids,
-                            const int32_t* targets, float* grads, float* loss, void* ws,
-                            size_t ws_bytes, void* blas, void* stream) {
+int recblr_model_train_step(const recblr_model_dims* m, const recblr_model_step_opts* opts,
+                            const float* params, const int32_t* ids, const int32_t* targets,
+                            float* grads, float* loss, void* ws, size_t ws_bytes, void* blas,
+                            void* stream) {
     if (!m) return RECBLR_ERR_INVALID_ARGUMENT;
     if (!model_dims_ok(m)) return RECBLR_ERR_UNSUPPORTED;
+    model::StepOpts o;
+    if (opts) {
+        // NaN fails both comparisons
+        if (!(opts->dropout >= 0.0f && opts->dropout < 1.0f) || opts->pad_id < -1 ||
+            opts->pad_id >= m->V)
+            return RECBLR_ERR_INVALID_ARGUMENT;
+        o.dropout = opts->dropout;
+        o.seed = opts->seed;
+        o.offset = opts->offset;
+        o.pad_id = opts->pad_id;
+    }
     if (!params || !ids || !targets || !grads || !loss || !blas)
         return RECBLR_ERR_INVALID_ARGUMENT;
     if (!aligned(params, kWsAlign) || !aligned(grads, kWsAlign) || !aligned(ids, 4) ||
@@ -809,7 +821,7 @@ int recblr_model_train_step(const recblr_model_dims* m, const float* params, con
     if (st) return st;
     if (!disjoint({{ws, need}}, {{params, np}, {ids, ni}, {targets, nt}, {grads, np}, {loss, 4}}))
         return RECBLR_ERR_INVALID_ARGUMENT;
-    return model::train_step(d, params, ids, targets, grads, loss, ws, (rocblas_handle)blas,
+    return model::train_step(d, o, params, ids, targets, grads, loss, ws, (rocblas_handle)blas,
                              (hipStream_t)stream);
 }
 

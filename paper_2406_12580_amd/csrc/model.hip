@@ -15,7 +15,8 @@
 // LayerNorms, bias broadcasts, SiLU, the cross entropy, the sums over rows
 // for bias and LayerNorm gradients (fixed order, double), the embedding
 // gradient (positions sorted by item, then summed per item in position
-// order) and Adam.  Dropout is the identity.
+// order), the dropout masks (one bit per element from a counter-based
+// generator, applied inside the LayerNorm kernels) and Adam.
 #include <hip/hip_runtime.h>
 #include <rocblas/rocblas.h>
 
@@ -45,17 +46,92 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// ------------------------------------------------------------------ dropout masks
+// Philox4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+// easy as 1, 2, 3", SC 2011), in place on the counter c under key (k0, k1):
+// ten rounds, each multiplying words 0 and 2 by the round multipliers and
+// mixing the product halves with words 1 and 3 and the key; the key is
+// bumped by the Weyl constants between rounds.
+// The 128-bit product a * b as four 32 x 32 -> 64-bit multiply-adds (each
+// one v_mad_u64_u32; no partial sum overflows 64 bits).
+__device__ __forceinline__ void mul128(uint64_t a, uint64_t b, uint64_t& lo, uint64_t& hi) {
+    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+    const uint64_t p00 = (uint64_t)a0 * b0;
+    const uint64_t t1 = (uint64_t)a0 * b1 + (p00 >> 32);
+    const uint64_t t2 = (uint64_t)a1 * b0 + (uint32_t)t1;
+    hi = (uint64_t)a1 * b1 + ((t1 >> 32) + (t2 >> 32));
+    lo = (t2 << 32) | (uint32_t)p00;
+}
+
+__device__ __forceinline__ void philox4x64_10(uint64_t (&c)[4], uint64_t k0, uint64_t k1) {
+    constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
+    constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += kW0;
+            k1 += kW1;
+        }
+        uint64_t lo0, hi0, lo1, hi1;
+        mul128(kM0, c[0], lo0, hi0);
+        mul128(kM1, c[2], lo1, hi1);
+        const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+}
+
+// Keep bits of `sites` dropout sites of `words` 32-bit words each: bit b of
+// word w of site s is element e = 32 w + b of that site, taken from 32-bit
+// word e mod 8 (low half of each 64-bit output first) of Philox4x64-10 at
+// counter (e / 8, s, 0, 0) under key (seed, offset); the element is kept when
+// that word is at least thr = floor(p 2^32).  One thread per mask word.
+__global__ __launch_bounds__(kThreads) void dropout_mask_kernel(uint32_t* __restrict__ mask,
+                                                                int64_t words, int64_t total,
+                                                                uint32_t thr, uint64_t seed,
+                                                                uint64_t offset) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= total) return;
+    const int64_t site = i / words, w = i - site * words;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        uint64_t c[4] = {(uint64_t)(w * 4 + q), (uint64_t)site, 0ull, 0ull};
+        philox4x64_10(c, seed, offset);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            bits |= (uint32_t)((uint32_t)c[j] >= thr) << (8 * q + 2 * j);
+            bits |= (uint32_t)((uint32_t)(c[j] >> 32) >= thr) << (8 * q + 2 * j + 1);
+        }
+    }
+    mask[i] = bits;
+}
+
+// v after dropout: v * scale if element e of the site is kept, else 0; the
+// identity when keep is null (no dropout).
+__device__ __forceinline__ float dropped(const uint32_t* __restrict__ keep, int64_t e, float v,
+                                         float scale) {
+    if (!keep) return v;
+    return (keep[e >> 5] >> (e & 31)) & 1u ? v * scale : 0.0f;
+}
+
 // ------------------------------------------------------------------ LayerNorm
 // y = (v - mean) / sqrt(var + eps) * g + b over rows of D = 64 * NV features,
-// one wave per row (lane holds features lane + 64 j).  v = a + r (r may be
-// null: no residual) and, if s is not null, v is stored for the backward.
-// EMB: v is row ids[row] of the embedding a (an id outside [0, V) gives NaN).
+// one wave per row (lane holds features lane + 64 j).  v = drop(a) + r (r may
+// be null: no residual) and, if s is not null, v is stored for the backward.
+// EMB: v is drop(row ids[row] of the embedding a), or drop(0) where the id is
+// the padding id `pad`; an id outside [0, V) gives NaN.  drop: dropout with
+// the keep bits `keep` (null: none) and scale 1 / (1 - p), element index
+// row * D + feature.
 template <int NV, bool EMB>
 __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
     const float* __restrict__ a, const float* __restrict__ r, const int* __restrict__ ids,
     const float* __restrict__ g, const float* __restrict__ b, float* __restrict__ s,
     float* __restrict__ y, float* __restrict__ mu, float* __restrict__ rs, int64_t M, int64_t V,
-    float eps) {
+    float eps, const uint32_t* __restrict__ keep, float scale, int pad) {
     constexpr int D = 64 * NV;
     const int lane = threadIdx.x & (kWave - 1);
     // kLnRows rows per wave, normalised side by side (independent reductions
@@ -66,17 +142,20 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
     for (int q = 0; q < kLnRows; ++q) {
         const int64_t row = row0 + q < M ? row0 + q : M - 1;  // tail rows recompute row M-1
         float bad = 0.0f;
+        bool padded = false;
         const float* src = a + row * D;
         if constexpr (EMB) {
             const int64_t id = ids[row];
             const bool ok = id >= 0 && id < V;
             src = a + (ok ? id : 0) * D;
             bad = ok ? 0.0f : __builtin_nanf("");
+            padded = pad >= 0 && id == pad;
         }
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-            v[q][j] = src[lane + 64 * j] + bad;
-            if (!EMB && r) v[q][j] += r[row * D + lane + 64 * j];
+            const int c = lane + 64 * j;
+            v[q][j] = dropped(keep, row * D + c, padded ? 0.0f : src[c], scale) + bad;
+            if (!EMB && r) v[q][j] += r[row * D + c];
         }
     }
 #pragma unroll
@@ -110,8 +189,12 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
     }
 }
 
-// LayerNorm backward: dx = rstd (gd - mean(gd) - xh mean(gd xh)), gd = dy g,
-// xh = (v - mean) rstd with v from s (or the embedding rows by id).  The
+// LayerNorm backward: dv = rstd (gd - mean(gd) - xh mean(gd xh)), gd = dy g,
+// xh = (v - mean) rstd with v from s (or, EMB, recomputed from the embedding
+// rows by id, the padding id and the keep bits as in the forward).  Non-EMB:
+// dx = dv (the residual's gradient) and, if dxm is not null, dxm = dv through
+// the dropout (the sub-layer output's gradient).  EMB: dx = dv through the
+// dropout, 0 at padded positions (the gradient of the looked-up rows).  The
 // workgroup handles rows [blk * kLnBwdRows, + kLnBwdRows), wave w the rows
 // w, w + 4, ...; the sums of dy xh and dy over its rows are added in wave
 // order and written to pg[blk], pb[blk] (summed over workgroups later).
@@ -120,7 +203,8 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     const float* __restrict__ dy, const float* __restrict__ s, const int* __restrict__ ids,
     const float* __restrict__ mu, const float* __restrict__ rs, const float* __restrict__ g,
     float* __restrict__ dx, float* __restrict__ pg, float* __restrict__ pb, int64_t M,
-    int64_t V) {
+    int64_t V, const uint32_t* __restrict__ keep, float scale, int pad,
+    float* __restrict__ dxm) {
     constexpr int D = 64 * NV;
     __shared__ float red[4][2][D];
     const int lane = threadIdx.x & (kWave - 1), w = wave_id();
@@ -134,9 +218,14 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     }
     // Rows w, w + 4, ... of the block, two at a time so that their loads and
     // reductions overlap; the gamma / beta sums still add rows in order.
+    auto padded_row = [&](int64_t row) {
+        if constexpr (EMB) return pad >= 0 && ids[row] == pad;
+        return false;
+    };
     auto row_grad = [&](int64_t row, float (&xh)[NV], float (&d)[NV], float (&gd)[NV],
                         float& s1, float& s2) {
         const float* src = s + row * D;
+        const bool padded = padded_row(row);
         if constexpr (EMB) {
             const int64_t id = ids[row];
             src = s + (id >= 0 && id < V ? id : 0) * D;
@@ -146,7 +235,9 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             const int c = lane + 64 * j;
-            xh[j] = (src[c] - m) * rstd;
+            const float v = EMB ? dropped(keep, row * D + c, padded ? 0.0f : src[c], scale)
+                                : src[c];
+            xh[j] = (v - m) * rstd;
             d[j] = dy[row * D + c];
             gd[j] = d[j] * gc[j];
             s1 += gd[j];
@@ -156,9 +247,17 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     auto row_out = [&](int64_t row, const float (&xh)[NV], const float (&d)[NV],
                        const float (&gd)[NV], float m1, float m2) {
         const float rstd = rs[row];
+        const bool padded = padded_row(row);
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-            dx[row * D + lane + 64 * j] = rstd * (gd[j] - m1 - xh[j] * m2);
+            const int64_t e = row * D + lane + 64 * j;
+            const float dv = rstd * (gd[j] - m1 - xh[j] * m2);
+            if constexpr (EMB) {
+                dx[e] = padded ? 0.0f : dropped(keep, e, dv, scale);
+            } else {
+                dx[e] = dv;
+                if (dxm) dxm[e] = dropped(keep, e, dv, scale);
+            }
             ag[j] = fmaf(d[j], xh[j], ag[j]);
             ab[j] += d[j];
         }
@@ -275,13 +374,22 @@ __global__ __launch_bounds__(kThreads) void ce_kernel(const float* __restrict__ 
     if (threadIdx.x == 0) lossb[b] = ok ? logf(se) + mx - l[t] : __builtin_nanf("");
 }
 
-// loss = sum_b loss_b / B, in order, in double.
-__global__ void loss_final_kernel(const float* __restrict__ lossb, int64_t B,
-                                  float* __restrict__ loss) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+// loss = sum_b loss_b / B in double, in a fixed order: thread t adds rows
+// t, t + 256, ... in turn, then the 256 partials are added in a fixed tree
+// (one workgroup of kThreads).
+__global__ __launch_bounds__(kThreads) void loss_final_kernel(const float* __restrict__ lossb,
+                                                              int64_t B,
+                                                              float* __restrict__ loss) {
+    __shared__ double sh[kThreads];
     double acc = 0.0;
-    for (int64_t b = 0; b < B; ++b) acc += (double)lossb[b];
-    *loss = (float)(acc / (double)B);
+    for (int64_t b = threadIdx.x; b < B; b += kThreads) acc += (double)lossb[b];
+    sh[threadIdx.x] = acc;
+    __syncthreads();
+    for (int o = kThreads / 2; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = (float)(sh[0] / (double)B);
 }
 
 // ------------------------------------------------------------------ embedding gradient
@@ -368,7 +476,24 @@ __global__ __launch_bounds__(kThreads) void emb_piece_kernel(
     float acc[NV];
 #pragma unroll
     for (int j = 0; j < NV; ++j) acc[j] = 0.0f;
-    for (int64_t i = start; i < end; ++i) {
+    // kBatch positions' rows loaded together, then added in position order
+    constexpr int kBatch = 8;
+    int64_t i = start;
+    for (; i + kBatch <= end; i += kBatch) {
+        int64_t r[kBatch];
+        float v[kBatch][NV];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q) r[q] = pos_sorted[i + q];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) v[q][j] = dx[r[q] * D + lane + 64 * j];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) acc[j] += v[q][j];
+    }
+    for (; i < end; ++i) {
         const int64_t r = pos_sorted[i];
 #pragma unroll
         for (int j = 0; j < NV; ++j) acc[j] += dx[r * D + lane + 64 * j];
@@ -388,7 +513,22 @@ __global__ __launch_bounds__(kThreads) void emb_item_kernel(const int64_t* __res
     float acc[NV];
 #pragma unroll
     for (int j = 0; j < NV; ++j) acc[j] = 0.0f;
-    for (int64_t p = poff[v]; p < poff[v + 1]; ++p)
+    // kBatch pieces loaded together, then added in piece order
+    constexpr int kBatch = 8;
+    const int64_t p1 = poff[v + 1];
+    int64_t p = poff[v];
+    for (; p + kBatch <= p1; p += kBatch) {
+        float x[kBatch][NV];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) x[q][j] = part[(p + q) * D + lane + 64 * j];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) acc[j] += x[q][j];
+    }
+    for (; p < p1; ++p)
 #pragma unroll
         for (int j = 0; j < NV; ++j) acc[j] += part[p * D + lane + 64 * j];
 #pragma unroll
@@ -455,12 +595,18 @@ int64_t param_offsets(const Dims& d, int64_t* off) {
 // ------------------------------------------------------------------ workspace
 struct Layout {
     size_t H, Hx, Hz, hb, y, s1, H1, A, P, s2, stats, emb_stats, logits, dlogits, lossb;
-    size_t X, Y, dP, dY, dHx, dHz, lnp, dwp, wt, colsum, emb_lo, emb_hi, emb_np, emb_poff, emb_part;
+    size_t X, Y, Z, dP, dY, dHx, dHz, lnp, dwp, wt, colsum, emb_lo, emb_hi, emb_np, emb_poff,
+        emb_part, mask;
     size_t ids_s, pos, pos_s, sort_tmp, gated, total;
     size_t sort_bytes, gated_bytes;
 };
 
 constexpr int64_t kDwChunk = 4096;  // rows per partial of a weight gradient
+
+// Dropout sites (the embedding, then two per layer) and 32-bit keep words per
+// site (B T D is a multiple of 64).
+int64_t mask_sites(const Dims& d) { return 1 + 2 * d.layers; }
+int64_t mask_words(const Dims& d) { return d.B * d.T * d.D / 32; }
 
 Layout layout(const Dims& d) {
     const int64_t M = d.B * d.T, D = d.D, ED = d.E * d.D, F = 4 * d.D, L = d.layers;
@@ -489,6 +635,7 @@ Layout layout(const Dims& d) {
     w.lossb = take((size_t)d.B * f);
     w.X = take((size_t)(M * D) * f);
     w.Y = take((size_t)(M * D) * f);
+    w.Z = take((size_t)(M * D) * f);            // a sub-layer output's gradient (dropout)
     w.dP = take((size_t)(M * F) * f);
     w.dY = take((size_t)(M * ED) * f);
     w.dHx = take((size_t)(M * ED) * f);
@@ -522,6 +669,7 @@ Layout layout(const Dims& d) {
     w.emb_np = take((size_t)(d.V + 1) * sizeof(int64_t));
     w.emb_poff = take((size_t)(d.V + 1) * sizeof(int64_t));
     w.emb_part = take((size_t)(max_pieces * D) * f);
+    w.mask = take((size_t)(mask_sites(d) * mask_words(d)) * sizeof(uint32_t));
     w.ids_s = take((size_t)M * sizeof(unsigned));
     w.pos = take((size_t)M * sizeof(int));
     w.pos_s = take((size_t)M * sizeof(int));
@@ -652,44 +800,55 @@ bool linear_wgrad(Ctx& c, const float* X, const float* dY, float* dW, float* db,
     return bias_grad(c, dY, M, N, db) && weight_grad(c, X, K, dY, N, dW, M, N, K);
 }
 
+// Dropout of one site: its keep bits (null: no dropout), 1 / (1 - p), and the
+// padding id (embedding site only; -1: none).
+struct Drop {
+    const uint32_t* keep = nullptr;
+    float scale = 1.0f;
+    int pad = -1;
+};
+
 template <int NV>
 bool ln_fwd(Ctx& c, const float* a, const float* r, const int* ids, const float* g,
             const float* b, float* s, float* y, float* mu, float* rs, int64_t M, int64_t V,
-            float eps) {
+            float eps, Drop dr) {
     const dim3 grid(blocks_for(M, kRowsPerWave));
     if (ids)
         hipLaunchKernelGGL((ln_fwd_kernel<NV, true>), grid, dim3(kThreads), 0, c.stream, a, r,
-                           ids, g, b, s, y, mu, rs, M, V, eps);
+                           ids, g, b, s, y, mu, rs, M, V, eps, dr.keep, dr.scale, dr.pad);
     else
         hipLaunchKernelGGL((ln_fwd_kernel<NV, false>), grid, dim3(kThreads), 0, c.stream, a, r,
-                           ids, g, b, s, y, mu, rs, M, V, eps);
+                           ids, g, b, s, y, mu, rs, M, V, eps, dr.keep, dr.scale, dr.pad);
     return hipGetLastError() == hipSuccess;
 }
 
-// LayerNorm backward; gamma / beta gradients into dg, db.
+// LayerNorm backward; gamma / beta gradients into dg, db; dxm (non-embedding,
+// may be null) the gradient of the dropped-out sub-layer output.
 template <int NV>
 bool ln_bwd(Ctx& c, const float* dy, const float* s, const int* ids, const float* mu,
             const float* rs, const float* g, float* dx, float* dg, float* db, int64_t M,
-            int64_t V) {
+            int64_t V, Drop dr, float* dxm = nullptr) {
     constexpr int D = 64 * NV;
     const int64_t nblk = (M + kLnBwdRows - 1) / kLnBwdRows;
     float* pg = (float*)(c.ws + c.w.lnp);
     float* pb = pg + nblk * D;
     if (ids)
         hipLaunchKernelGGL((ln_bwd_kernel<NV, true>), dim3((unsigned)nblk), dim3(kThreads), 0,
-                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V);
+                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V, dr.keep, dr.scale,
+                           dr.pad, dxm);
     else
         hipLaunchKernelGGL((ln_bwd_kernel<NV, false>), dim3((unsigned)nblk), dim3(kThreads), 0,
-                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V);
+                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V, dr.keep, dr.scale,
+                           dr.pad, dxm);
     if (hipGetLastError() != hipSuccess) return false;
     return launch_colsum(pg, nblk, D, dg, c.ws + c.w.colsum, c.stream) == hipSuccess &&
            launch_colsum(pb, nblk, D, db, c.ws + c.w.colsum, c.stream) == hipSuccess;
 }
 
 template <int NV>
-int train_step_t(const Dims& d, const float* params, const int* ids, const int* targets,
-                 float* grads, float* loss, char* ws, const Layout& w, rocblas_handle blas,
-                 hipStream_t stream) {
+int train_step_t(const Dims& d, const StepOpts& o, const float* params, const int* ids,
+                 const int* targets, float* grads, float* loss, char* ws, const Layout& w,
+                 rocblas_handle blas, hipStream_t stream) {
     Ctx c{blas, stream, ws, w};
     const int64_t B = d.B, T = d.T, M = B * T, D = d.D, ED = d.E * d.D, F = 4 * d.D, V = d.V;
     const int64_t nt = tensor_count(d);
@@ -718,9 +877,31 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         if ((st_ = (x)) != RECBLR_OK) return st_; \
     } while (0)
 
+    // ---- dropout masks: every site's keep bits, drawn once for the step
+    const bool dropout = o.dropout > 0.0f;
+    const int64_t mwords = mask_words(d);
+    uint32_t* mask = (uint32_t*)(ws + w.mask);
+    auto site = [&](int64_t k, int pad = -1) {
+        Drop dr;
+        dr.pad = pad;
+        if (dropout) {
+            dr.keep = mask + k * mwords;
+            dr.scale = 1.0f / (1.0f - o.dropout);
+        }
+        return dr;
+    };
+    if (dropout) {
+        const int64_t total = mask_sites(d) * mwords;
+        const uint32_t thr = (uint32_t)floor((double)o.dropout * 4294967296.0);
+        hipLaunchKernelGGL(dropout_mask_kernel, dim3(blocks_for(total)), dim3(kThreads), 0,
+                           stream, mask, mwords, total, thr, o.seed, o.offset);
+        CHECK(hipGetLastError() == hipSuccess);
+    }
+    float* Z = buf(w.Z);
+
     // ---- forward
     CHECK(ln_fwd<NV>(c, E, nullptr, ids, params + off[1], params + off[2], nullptr, Hl(0), mu0,
-                     rs0, M, V, d.eps));
+                     rs0, M, V, d.eps, site(0, o.pad_id)));
     for (int64_t l = 0; l < d.layers; ++l) {
         float *Hx = per(w.Hx, l, ED), *Hz = per(w.Hz, l, ED), *hb = per(w.hb, l, ED),
               *y = per(w.y, l, ED), *s1 = per(w.s1, l, D), *H1 = per(w.H1, l, D),
@@ -734,11 +915,11 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         // O = y Wo^T + bo goes to s1, then s1 += H and H1 = LN(s1).
         CHECK(linear_fwd(c, y, P(l, kWo), P(l, kbo), s1, M, D, ED));
         CHECK(ln_fwd<NV>(c, s1, Hl(l), nullptr, P(l, kLn1g), P(l, kLn1b), s1, H1, stat(l, 0),
-                         stat(l, 1), M, V, d.eps));
+                         stat(l, 1), M, V, d.eps, site(1 + 2 * l)));
         CHECK(linear_fwd(c, H1, P(l, kW1), P(l, kb1), A, M, F, D, Pp));  // Pp = SiLU(A)
         CHECK(linear_fwd(c, Pp, P(l, kW2), P(l, kb2), s2, M, D, F));
         CHECK(ln_fwd<NV>(c, s2, H1, nullptr, P(l, kLn2g), P(l, kLn2b), s2, Hl(l + 1),
-                         stat(l, 2), stat(l, 3), M, V, d.eps));
+                         stat(l, 2), stat(l, 3), M, V, d.eps, site(2 + 2 * l)));
     }
     // prediction: logits = h_T E^T with h_T the last step of every row
     const float* hT = Hl(d.layers) + (T - 1) * D;
@@ -748,7 +929,8 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
     hipLaunchKernelGGL(ce_kernel, dim3((unsigned)B), dim3(kThreads), 0, stream, logits, targets, B,
                        V, dlogits, buf(w.lossb));
     CHECK(hipGetLastError() == hipSuccess);
-    hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(64), 0, stream, buf(w.lossb), B, loss);
+    hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(kThreads), 0, stream, buf(w.lossb), B,
+                       loss);
     CHECK(hipGetLastError() == hipSuccess);
 
     // ---- backward
@@ -764,21 +946,25 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
         float *Hx = per(w.Hx, l, ED), *Hz = per(w.Hz, l, ED), *hb = per(w.hb, l, ED),
               *y = per(w.y, l, ED), *s1 = per(w.s1, l, D), *H1 = per(w.H1, l, D),
               *A = per(w.A, l, F), *Pp = per(w.P, l, F), *s2 = per(w.s2, l, D);
-        // LN2: Y (dH2) -> X (ds2 = dQ, and the residual part of dH1)
+        // LN2: Y (dH2) -> X (ds2: the residual part of dH1) and dQ (ds2 through
+        // the dropout, in Z; X itself without dropout)
+        float* dQ = dropout ? Z : X;
         CHECK(ln_bwd<NV>(c, Y, s2, nullptr, stat(l, 2), stat(l, 3), P(l, kLn2g), X, G(l, kLn2g),
-                         G(l, kLn2b), M, V));
+                         G(l, kLn2b), M, V, site(2 + 2 * l), dropout ? Z : nullptr));
         // PFFN: Q = P W2^T + b2, P = SiLU(A), A = H1 W1^T + b1
-        CHECK(linear_wgrad(c, Pp, X, G(l, kW2), G(l, kb2), M, D, F));
+        CHECK(linear_wgrad(c, Pp, dQ, G(l, kW2), G(l, kb2), M, D, F));
         // dP = (dQ W2) * SiLU'(A)
-        CHECK(linear_dgrad(c, X, P(l, kW2), dP, M, D, F, LinearMode::kSiluGrad, A));
+        CHECK(linear_dgrad(c, dQ, P(l, kW2), dP, M, D, F, LinearMode::kSiluGrad, A));
         CHECK(linear_wgrad(c, H1, dP, G(l, kW1), G(l, kb1), M, F, D));
         CHECK(linear_dgrad(c, dP, P(l, kW1), X, M, F, D, LinearMode::kAccumulate));  // X = dH1
-        // LN1: X (dH1) -> Y (ds1 = dO, and the residual part of dH)
+        // LN1: X (dH1) -> Y (ds1: the residual part of dH) and dO (ds1 through
+        // the dropout, in Z; Y itself without dropout)
+        float* dO = dropout ? Z : Y;
         CHECK(ln_bwd<NV>(c, X, s1, nullptr, stat(l, 0), stat(l, 1), P(l, kLn1g), Y, G(l, kLn1g),
-                         G(l, kLn1b), M, V));
+                         G(l, kLn1b), M, V, site(1 + 2 * l), dropout ? Z : nullptr));
         // O = y Wo^T + bo
-        CHECK(linear_wgrad(c, y, Y, G(l, kWo), G(l, kbo), M, D, ED));
-        CHECK(linear_dgrad(c, Y, P(l, kWo), dY, M, D, ED, LinearMode::kStore));
+        CHECK(linear_wgrad(c, y, dO, G(l, kWo), G(l, kbo), M, D, ED));
+        CHECK(linear_dgrad(c, dO, P(l, kWo), dY, M, D, ED, LinearMode::kStore));
         CHECK_ST(recblr_gated_backward(Hx, Hz, P(l, kConvW), P(l, kConvB), d.K, P(l, kWr),
                                        P(l, kbr), P(l, kWi), P(l, kbi), P(l, kLam), nullptr, hb,
                                        dY, nullptr, dHx, dHz, G(l, kConvW), G(l, kConvB),
@@ -793,7 +979,7 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
     }
     // embedding LayerNorm, then the input side of dE: rows summed per item
     CHECK(ln_bwd<NV>(c, Y, E, ids, mu0, rs0, params + off[1], X, grads + off[1], grads + off[2], M,
-                     V));
+                     V, site(0, o.pad_id)));
     unsigned* ids_s = (unsigned*)(ws + w.ids_s);
     int* pos = (int*)(ws + w.pos);
     int* pos_s = (int*)(ws + w.pos_s);
@@ -827,16 +1013,18 @@ int train_step_t(const Dims& d, const float* params, const int* ids, const int* 
 
 }  // namespace
 
-int train_step(const Dims& d, const float* params, const int* ids, const int* targets,
-               float* grads, float* loss, void* ws, rocblas_handle blas, hipStream_t stream) {
+int train_step(const Dims& d, const StepOpts& o, const float* params, const int* ids,
+               const int* targets, float* grads, float* loss, void* ws, rocblas_handle blas,
+               hipStream_t stream) {
     const Layout w = layout(d);
     // Padding between tensors is zero in the gradient.
     if (launch_fill(grads, 0.0f, param_offsets(d, nullptr), stream) != hipSuccess)
         return RECBLR_ERR_HIP;
+    char* wsb = (char*)ws;
     switch (d.D / 64) {
-        case 1: return train_step_t<1>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
-        case 2: return train_step_t<2>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
-        case 4: return train_step_t<4>(d, params, ids, targets, grads, loss, (char*)ws, w, blas, stream);
+        case 1: return train_step_t<1>(d, o, params, ids, targets, grads, loss, wsb, w, blas, stream);
+        case 2: return train_step_t<2>(d, o, params, ids, targets, grads, loss, wsb, w, blas, stream);
+        case 4: return train_step_t<4>(d, o, params, ids, targets, grads, loss, wsb, w, blas, stream);
         default: return RECBLR_ERR_UNSUPPORTED;
     }
 }

@@ -17,6 +17,14 @@ struct Dims {
     float eps;
 };
 
+// Dropout and padding of one step: drop probability (0: off), Philox key
+// (seed, offset), padding id (-1: none).
+struct StepOpts {
+    float dropout = 0.0f;
+    uint64_t seed = 0, offset = 0;
+    int pad_id = -1;
+};
+
 // Tensors of one behaviour-modelling layer, in parameter order.
 enum LayerTensor {
     kWx, kbx, kWz, kbz, kConvW, kConvB, kWr, kbr, kWi, kbi, kLam,
@@ -31,8 +39,9 @@ int64_t tensor_count(const Dims& d);
 int64_t param_offsets(const Dims& d, int64_t* off);
 // Workspace bytes of train_step (0 if the sort's scratch size is unavailable).
 size_t workspace_size(const Dims& d);
-int train_step(const Dims& d, const float* params, const int* ids, const int* targets,
-               float* grads, float* loss, void* ws, rocblas_handle blas, hipStream_t stream);
+int train_step(const Dims& d, const StepOpts& o, const float* params, const int* ids,
+               const int* targets, float* grads, float* loss, void* ws, rocblas_handle blas,
+               hipStream_t stream);
 hipError_t adam(float* p, const float* g, float* m1, float* m2, int64_t n, int64_t step, float lr,
                 float b1, float b2, float eps, hipStream_t stream);
 

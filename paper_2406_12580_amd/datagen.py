@@ -268,8 +268,9 @@ def model_batch(dims: ModelDims, seed: int, min_len: int | None = None, pad_id: 
     return ids, targets
 
 
-def ml1m_min_len(T: int = 200, mean_len: float = 165.5) -> int:
+def ml1m_min_len(T: int = 200) -> int:
     """Shortest length of the MovieLens-1M length mix: U{m, ..., T} has mean
     (m + T) / 2, so m = 2 * 165.5 - 200 = 131 gives the dataset's average
-    length of 165.5 (table tab:dataset) under the maximum length 200."""
-    return int(round(2 * mean_len - T))
+    length of 165.5 (table tab:dataset) under the maximum length 200; other
+    T keep the ratio of mean to maximum length (m = 0.655 T)."""
+    return max(1, int(round(T * (2 * 165.5 / 200 - 1))))

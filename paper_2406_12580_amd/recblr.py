@@ -56,7 +56,14 @@ class ModelDims(ctypes.Structure):
                 ("layers", _i64), ("K", _int), ("ln_eps", _f)]
 
 
+class ModelStepOpts(ctypes.Structure):
+    """recblr_model_step_opts."""
+    _fields_ = [("dropout", _f), ("pad_id", ctypes.c_int32), ("seed", ctypes.c_uint64),
+                ("offset", ctypes.c_uint64)]
+
+
 _pd = ctypes.POINTER(ModelDims)
+_po = ctypes.POINTER(ModelStepOpts)
 _SIGS = {
     "recblr_status_string": ([_int], ctypes.c_char_p),
     "recblr_workspace_size": ([_int, _i64, _i64, _i64, _int], _sz),
@@ -83,7 +90,7 @@ _SIGS = {
     "recblr_model_workspace_size": ([_pd], _sz),
     "recblr_blas_create": ([ctypes.POINTER(_p)], _int),
     "recblr_blas_destroy": ([_p], _int),
-    "recblr_model_train_step": ([_pd] + [_p] * 6 + [_sz, _p, _p], _int),
+    "recblr_model_train_step": ([_pd, _po] + [_p] * 6 + [_sz, _p, _p], _int),
     "recblr_adam_update": ([_p] * 4 + [_i64, _i64, _f, _f, _f, _f, _p], _int),
 }
 for _name, (_args, _res) in _SIGS.items():
@@ -413,15 +420,20 @@ class ModelStep:
             pass
 
     @_on_stream
-    def train_step(self, params, ids, targets, grads=None, loss=None, stream=None):
-        """Loss and gradients (flat, the parameter layout) of one batch."""
+    def train_step(self, params, ids, targets, grads=None, loss=None, dropout=0.0, seed=0,
+                   offset=0, pad_id=-1, stream=None):
+        """Loss and gradients (flat, the parameter layout) of one batch; dropout
+        with drop probability `dropout` and Philox key (seed, offset), left
+        padding with id pad_id (-1: none)."""
         if grads is None:
             grads = torch.empty_like(params)
         if loss is None:
             loss = torch.empty(1, dtype=torch.float32, device=params.device)
-        _check(recblr_model_train_step(ctypes.byref(self.dims), _ptr(params), _ptr(ids),
-                                       _ptr(targets), _ptr(grads), _ptr(loss), _ptr(self.ws),
-                                       self.ws.numel(), self.blas, _stream(stream)),
+        opts = ModelStepOpts(dropout, pad_id, seed, offset)
+        _check(recblr_model_train_step(ctypes.byref(self.dims), ctypes.byref(opts), _ptr(params),
+                                       _ptr(ids), _ptr(targets), _ptr(grads), _ptr(loss),
+                                       _ptr(self.ws), self.ws.numel(), self.blas,
+                                       _stream(stream)),
                "recblr_model_train_step")
         return loss, grads
 

@@ -245,13 +245,18 @@ def test_model_validation(rb):
     assert rb.recblr_model_param_count(rb.model_dims(2, 3, 64, K=5)) == 0
     assert rb.recblr_model_param_count(rb.model_dims(2, 3, 64, E=17)) == 0   # E*D > 1024
     assert rb.recblr_model_param_offsets(rb.model_dims(0, 3, 64), None, 0) == -1
-    step = lambda m, params=addr(0), ids=addr(1), grads=addr(3), ws=addr(5), nws=1 << 40: \
-        rb.recblr_model_train_step(ctypes.byref(m), params, ids, addr(2), grads, addr(4), ws, nws,
-                                   addr(6), None)
+    def step(m, params=addr(0), ids=addr(1), grads=addr(3), ws=addr(5), nws=1 << 40,
+             opts=None):
+        o = ctypes.byref(opts) if opts is not None else None
+        return rb.recblr_model_train_step(ctypes.byref(m), o, params, ids, addr(2), grads,
+                                          addr(4), ws, nws, addr(6), None)
     assert step(rb.model_dims(2, 3, 48)) == rb.ERR_UNSUPPORTED
     assert step(ok, params=None) == rb.ERR_INVALID_ARGUMENT
     assert step(ok, params=addr(0) + 4) == rb.ERR_INVALID_ARGUMENT          # not 256-aligned
     assert step(ok, grads=addr(0)) == rb.ERR_INVALID_ARGUMENT               # grads over params
+    # dropout outside [0, 1) (NaN included) and a padding id outside [-1, V)
+    for p, pad in ((1.0, -1), (-0.1, -1), (float("nan"), -1), (0.2, -2), (0.2, ok.V)):
+        assert step(ok, opts=rb.ModelStepOpts(p, pad, 0, 0)) == rb.ERR_INVALID_ARGUMENT, (p, pad)
     assert rb.recblr_adam_update(addr(0), addr(1), addr(2), addr(3), 10, 0, 1e-3, 0.9, 0.999,
                                  1e-8, None) == rb.ERR_INVALID_ARGUMENT    # step < 1
     assert rb.recblr_adam_update(addr(0), addr(0), addr(2), addr(3), 10, 1, 1e-3, 0.9, 0.999,

@@ -44,6 +44,19 @@ def _device_params(rb, dims, named):
     return rd, torch.from_numpy(flat).cuda(), flat
 
 
+# Dropout and padding: (dims, shortest row length or None for full rows,
+# drop probability, padding id, Philox seed, Philox offset).
+DROP_CASES = [
+    (dg.MODEL_CONFIGS["ml1m-small"], 5, 0.2, 0, 7, 3),
+    (dg.ModelDims(B=2, T=5, D=128, E=1, V=37, layers=1, K=2, eps=1e-5), None, 0.1, -1, 1, 0),
+    (dg.ModelDims(B=3, T=70, D=64, E=3, V=300, layers=3, K=4, eps=1e-6), 1, 0.5, 0,
+     2 ** 40 + 1, 2 ** 63),
+    (dg.ModelDims(B=2, T=9, D=256, E=1, V=40, layers=1, K=3, eps=1e-5), 2, 0.3, 0, 5, 6),
+    (dg.ModelDims(B=5, T=33, D=64, E=2, V=90, layers=2, K=4, eps=1e-5), 3, 0.0, 0, 0, 0),
+    (dg.ModelDims(B=64, T=130, D=64, E=2, V=500, layers=1, K=4), 20, 0.2, 0, 11, 12),
+]
+
+
 def _oracle_flat(dims, named):
     lay, total = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
     flat = np.zeros(total)
@@ -82,6 +95,51 @@ def test_model_train_step(rb, case):
     for (name, shape, _), o in zip(lay, offs):
         mask[o:o + int(np.prod(shape))] = False
     assert not g[mask].any()
+    step.close()
+
+
+def _check_against_oracle(rb, rd, dims, g, loss, want_loss, want, tag=""):
+    assert abs(loss - want_loss) <= 1e-4 * abs(want_loss), (loss, want_loss)
+    lay, _ = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
+    offs = rb.model_param_offsets(rd)
+    for (name, shape, o_ref), o in zip(lay, offs):
+        n = int(np.prod(shape))
+        if tag:
+            report(f"{tag} {name}", g[o:o + n], want[o_ref:o_ref + n])
+        assert_close(g[o:o + n], want[o_ref:o_ref + n], "f32", name)
+
+
+@pytest.mark.parametrize("case", range(len(DROP_CASES)))
+def test_model_train_step_dropout_padding(rb, case):
+    """Dropout (masks from the counter-based generator, drawn on the GPU) and
+    left-padded rows: every gradient against the oracle's, bitwise repeats for
+    one key, new masks for a new offset."""
+    import torch
+    dims, min_len, p, pad, seed, offset = DROP_CASES[case]
+    named = dg.model_params(dims, 900 + case)
+    if min_len is None:
+        ids, targets = dg.model_batch(dims, 950 + case)
+    else:
+        ids, targets = dg.model_batch(dims, 950 + case, min_len=min_len, pad_id=pad)
+        assert (ids == pad).any()
+    rd, P, _ = _device_params(rb, dims, named)
+    step = rb.ModelStep(rd)
+    I, Tg = torch.from_numpy(ids).cuda(), torch.from_numpy(targets).cuda()
+    kw = dict(dropout=p, seed=seed, offset=offset, pad_id=pad)
+    loss, grads = step.train_step(P, I, Tg, **kw)
+    loss2, grads2 = step.train_step(P, I, Tg, **kw)
+    loss3, grads3 = step.train_step(P, I, Tg, **dict(kw, offset=offset + 1))
+    torch.cuda.synchronize()
+    print(f"model step {dims} {kw}: GPU done", flush=True)
+    g = grads.cpu().numpy()
+    assert np.array_equal(g.view(np.uint32), grads2.cpu().numpy().view(np.uint32))
+    assert loss.item() == loss2.item()
+    if p > 0:
+        assert not np.array_equal(g, grads3.cpu().numpy()), "a new offset must draw new masks"
+    flat, _ = _oracle_flat(dims, named)
+    want_loss, want = om.train_step(flat, ids, targets, dims.D, dims.E, dims.V, dims.layers,
+                                    dims.K, dims.eps, **kw)
+    _check_against_oracle(rb, rd, dims, g, loss.item(), want_loss, want)
     step.close()
 
 
@@ -131,31 +189,28 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
                       "model_ml1m_oracle.npz")
 
 
-def test_model_train_step_ml1m(rb):
+@pytest.mark.parametrize("variant", ["ml1m", "ml1m-dropout"])
+def test_model_train_step_ml1m(rb, variant):
     """The MovieLens-1M training shape the model bench times (batch 2048,
-    length 200, D = 64, E = 2, two layers, 3,416 items): every gradient tensor
-    against the fp64 oracle's, stored by tests/golden/make_model_golden.py
-    (the oracle takes minutes at this size) for the same seeded inputs."""
+    length 200, D = 64, E = 2, two layers, 3,416 items), with full-length rows
+    and no dropout, and with the dataset's length mix (left-padded) and
+    dropout 0.2: every gradient tensor against the fp64 oracle's, stored by
+    tests/golden/make_model_golden.py (the oracle takes minutes at this size)
+    for the same seeded inputs."""
     import torch
     sys.path.insert(0, os.path.dirname(GOLDEN))
     import make_model_golden as mg
-    dims, named, ids, targets, flat64 = mg.inputs()
-    golden = np.load(GOLDEN, allow_pickle=False)
-    assert str(golden["fingerprint"]) == mg.fingerprint(flat64, ids, targets), \
+    dims, named, ids, targets, flat64 = mg.inputs(variant)
+    opts = mg.options(variant)
+    golden = np.load(mg.path(variant), allow_pickle=False)
+    assert str(golden["fingerprint"]) == mg.fingerprint(flat64, ids, targets, opts), \
         "the seeded inputs changed since the oracle result was stored"
     rd, P, _ = _device_params(rb, dims, named)
     step = rb.ModelStep(rd)
     loss, grads = step.train_step(P, torch.from_numpy(ids).cuda(),
-                                  torch.from_numpy(targets).cuda())
+                                  torch.from_numpy(targets).cuda(), **opts)
     torch.cuda.synchronize()
-    print(f"model step {dims}: GPU done", flush=True)
-    g = grads.cpu().numpy()
-    want_loss, want = float(golden["loss"]), golden["grads"].astype(np.float64)
-    assert abs(loss.item() - want_loss) <= 1e-4 * abs(want_loss), (loss.item(), want_loss)
-    lay, _ = om.layout(dims.D, dims.E, dims.V, dims.layers, dims.K)
-    offs = rb.model_param_offsets(rd)
-    for (name, shape, o_ref), o in zip(lay, offs):
-        n = int(np.prod(shape))
-        report(f"model ml1m {name}", g[o:o + n], want[o_ref:o_ref + n])
-        assert_close(g[o:o + n], want[o_ref:o_ref + n], "f32", name)
+    print(f"model step {dims} {opts}: GPU done", flush=True)
+    _check_against_oracle(rb, rd, dims, grads.cpu().numpy(), loss.item(), float(golden["loss"]),
+                          golden["grads"].astype(np.float64), tag=f"model {variant}")
     step.close()
