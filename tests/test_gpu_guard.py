@@ -347,12 +347,15 @@ def test_guard_linear_scan(rb):
 
 
 def test_guard_model_step(rb):
-    """The model step's gradients and loss, and Adam's in-place updates."""
+    """The model step's gradients and loss (with dropout and left-padded rows,
+    so the mask and dropout-gradient regions of the workspace are used), and
+    Adam's in-place updates."""
     import ctypes
     import torch
     dims = dg.ModelDims(B=64, T=130, D=64, E=2, V=500, layers=2, K=4)
     named = dg.model_params(dims, 9700)
-    ids, targets = dg.model_batch(dims, 9701)
+    ids, targets = dg.model_batch(dims, 9701, min_len=10, pad_id=0)
+    opts = rb.ModelStepOpts(0.3, 0, 77, 5)
     rd = rb.model_dims(dims.B, dims.T, dims.D, dims.E, dims.V, dims.layers, dims.K, dims.eps)
     offs = rb.model_param_offsets(rd)
     n = rb.recblr_model_param_count(rd)
@@ -365,10 +368,11 @@ def test_guard_model_step(rb):
     G, loss = Guarded((n,), torch.float32), Guarded((1,), torch.float32)
     nws = rb.recblr_model_workspace_size(ctypes.byref(rd))
     ws = Guarded((nws,), torch.uint8)
-    st = rb.recblr_model_train_step(ctypes.byref(rd), P.data_ptr(), I.data_ptr(), Tg.data_ptr(),
-                                    G.ptr, loss.ptr, ws.ptr, nws, step.blas, _stream())
+    st = rb.recblr_model_train_step(ctypes.byref(rd), ctypes.byref(opts), P.data_ptr(),
+                                    I.data_ptr(), Tg.data_ptr(), G.ptr, loss.ptr, ws.ptr, nws,
+                                    step.blas, _stream())
     assert st == 0, st
-    rloss, rG = step.train_step(P, I, Tg)
+    rloss, rG = step.train_step(P, I, Tg, dropout=0.3, seed=77, offset=5, pad_id=0)
     # Adam in place on guarded copies of the parameters and moments.
     params, m1, m2 = (Guarded((n,), torch.float32) for _ in range(3))
     params.t.copy_(P)
