@@ -561,38 +561,53 @@ int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
     if (launch_pack_conv(conv_w, conv_b, K, D, w4, b4, strm) != hipSuccess) return RECBLR_ERR_HIP;
     if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), IoType::kF32, strm) != hipSuccess)
         return RECBLR_ERR_HIP;
-    if (io == RECBLR_BF16) {
-        // fp32 x' and gradients, bf16 h read as stored, and the output gate
-        // folded into the fused scan: dh = dy SiLU(hz) formed in fp32 on load
-        // (x' or dh rounded to bf16 would move dW by up to 1.5% and dhx by
-        // 1.3%; h is exact in bf16).
+    {
+        // The output gate folded into the fused scan: dh = dy SiLU(hz) formed
+        // in fp32 on load (dh never reaches memory) and, for fp32 I/O,
+        // dhz = dy h SiLU'(hz) stored by the same pass.  x' and the gradients
+        // stay fp32; for bf16 I/O h, dy, hz are read as stored (x' or dh
+        // rounded to bf16 would move dW by up to 1.5% and dhx by 1.3%; h is
+        // exact in bf16).
         void* lws = at(ws, lay.full);
         const FullBwdLayout fl = full_bwd_layout(B, L, D, RECBLR_F32);
         void* pack = at(lws, fl.pack);
         if (fused_backward_applies(B, L, D, IoType::kF32, xp, h, pack)) {
+            const bool bf = io == RECBLR_BF16;
             float* wt = (float*)at(ws, lay.wts);
-            const float* br32 = b_r ? wt + 2 * D * D : nullptr;
-            const float* bi32 = b_i ? wt + 2 * D * D + D : nullptr;
+            const void *wr32 = W_r, *wi32 = W_i, *br32 = b_r, *bi32 = b_i;
+            if (bf) {
+                // the scan recomputes z from fp32 x' with fp32 weights
+                if (launch_widen(W_r, wt, D * D, strm) != hipSuccess ||
+                    launch_widen(W_i, wt + D * D, D * D, strm) != hipSuccess ||
+                    (b_r && launch_widen(b_r, wt + 2 * D * D, D, strm) != hipSuccess) ||
+                    (b_i && launch_widen(b_i, wt + 2 * D * D + D, D, strm) != hipSuccess))
+                    return RECBLR_ERR_HIP;
+                wr32 = wt;
+                wi32 = wt + D * D;
+                br32 = b_r ? wt + 2 * D * D : nullptr;
+                bi32 = b_i ? wt + 2 * D * D + D : nullptr;
+            }
             void* dzr = at(lws, fl.dzr);
             void* dzi = at(lws, fl.dzi);
-            if (launch_gate_backward(dy, hz, h, nullptr, dhz, n_el, IoType::kBf16,
-                                     IoType::kBf16, strm) != hipSuccess ||
-                launch_widen(W_r, wt, D * D, strm) != hipSuccess ||
-                launch_widen(W_i, wt + D * D, D * D, strm) != hipSuccess ||
-                (b_r && launch_widen(b_r, wt + 2 * D * D, D, strm) != hipSuccess) ||
-                (b_i && launch_widen(b_i, wt + 2 * D * D + D, D, strm) != hipSuccess) ||
-                launch_pack_groups(wt, wt + D * D, D, IoType::kF32, pack, strm) != hipSuccess)
+            // bf16: dhz = dy h SiLU'(hz) in a pass of its own (reading dy, hz, h
+            // as stored), which measured faster than folding it into the scan.
+            if ((bf && launch_gate_backward(dy, hz, h, nullptr, dhz, n_el, IoType::kBf16,
+                                            IoType::kBf16, strm) != hipSuccess) ||
+                launch_pack_groups(wr32, wi32, D, IoType::kF32, pack, strm) != hipSuccess)
                 return RECBLR_ERR_HIP;
             FusedBwdArgs fa{xp,        pack,      br32,    bi32,        lambda, h0, h, nullptr,
                             dhT,       dxp,       (float*)dzr, (float*)dzi, dlambda, dh0,
                             B,         L,         D,       IoType::kF32, at(lws, fl.scan)};
             fa.gy = dy;
             fa.gz = hz;
-            fa.h_bf16 = true;
+            fa.gdz = bf ? nullptr : dhz;
+            fa.h_bf16 = bf;
             if (launch_fused_backward(fa, strm) != hipSuccess) return RECBLR_ERR_HIP;
-            // dx' += dz W with the bf16 weights as given (one operand plane).
-            if (launch_project_backward_data(dzr, dzi, W_r, W_i, dxp, B * L, D, IoType::kBf16,
-                                             pack, strm, true) != hipSuccess ||
+            // dx' += dz W (for bf16 I/O with the bf16 weights as given: one
+            // operand plane), then dW from fp32 x'.
+            if (launch_project_backward_data(dzr, dzi, W_r, W_i, dxp, B * L, D,
+                                             bf ? IoType::kBf16 : IoType::kF32, pack, strm,
+                                             bf) != hipSuccess ||
                 launch_project_backward_weights(dzr, dzi, xp, dW_r, db_r, dW_i, db_i, B * L, D,
                                                 IoType::kF32, at(lws, fl.dw), strm) != hipSuccess)
                 return RECBLR_ERR_HIP;

@@ -148,10 +148,15 @@ struct FusedBwdArgs {
     int64_t B, L, D;
     IoType io;
     void* ws;
-    // Output gate of the gated layer: when gy is set, dh is formed on load as
-    // gy SiLU(gz) (fp32) instead of being read (dh is then unused).
+    // Output gate of the gated layer (fp32 x only): when gy is set, dh is
+    // formed on load as gy SiLU(gz) (fp32) instead of being read (dh is then
+    // unused), and, with fp32 h, if gdz is set, the gate input's gradient
+    // gy h SiLU'(gz) is stored there (h's layout).  Folding that gradient in
+    // for bf16 h measured slower than its own pass (one extra store and load
+    // per element in the scan against a 108 us pass at 16 x 16384 x 256).
     const void* gy = nullptr;
     const void* gz = nullptr;
+    void* gdz = nullptr;
     // fp32 x with h (and gy, gz) in bf16: the gated layer's bf16 backward,
     // which keeps x' and the gradients in fp32.
     bool h_bf16 = false;

@@ -58,10 +58,13 @@ struct BwdParams {
     LookbackWs lb;
     unsigned* dl_counters;  // one per 64-channel column group of the dLambda reduction
     int64_t n_counters;
-    // Fused kernel only: when gy is set, dh is not read but formed on load
-    // as dh_t = gy_t SiLU(gz_t) (the output gate of the gated layer), in fp32.
+    // Fused kernel only, fp32 x: when gy is set, dh is not read but formed on
+    // load as dh_t = gy_t SiLU(gz_t) (the output gate of the gated layer), in
+    // fp32; with fp32 h, if gdz is set too, the gate input's gradient
+    // gy_t h_t SiLU'(gz_t) is stored there (same layout as h).
     const void* gy = nullptr;
     const void* gz = nullptr;
+    void* gdz = nullptr;
 };
 
 // Zeroes the dLambda counters (n of them); called by one workgroup of each
@@ -558,14 +561,35 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
     stage_rows<T, C>((const T*)P.x, b, P.L, P.D, cg * kWave, tw, 0, xs, lane);
     stage_rows<TH, C>((const TH*)P.h, b, P.L, P.D, cg * kWave, tw, -1, hs, lane);
     float gv[C];
-    if (P.gy) {
+    // The output gate is folded in only with fp32 x (the gated layer's x');
+    // the host passes no gy otherwise.
+    if (sizeof(T) == 4 && P.gy) {
+        // dh_t = y_t SiLU(z_t) and, with gdz (fp32 h only), dz_t = y_t h_t
+        // SiLU'(z_t), SiLU'(v) = s (1 + v (1 - s)), s = sigmoid(v).  h_t is
+        // loaded beside dy and hz (the same lines as the staged rows h_{t-1},
+        // mostly from the cache); every load is issued before the first store
+        // (a store could alias a later load's tensor and would hold it).
+        float dzv[C];
+        const bool gdz = sizeof(TH) == 4 && P.gdz;
 #pragma unroll
         for (int j = 0; j < C; ++j) {
             const int64_t t = tw + j < P.L ? tw + j : P.L - 1;
-            float y[1], z[1];
-            load_vec<TH, 1>((const TH*)P.gy, elem_offset<T, TH>(ln.at(t)), y);
-            load_vec<TH, 1>((const TH*)P.gz, elem_offset<T, TH>(ln.at(t)), z);
-            gv[j] = y[0] * (z[0] * sigmoid(z[0]));
+            const Off off = elem_offset<T, TH>(ln.at(t));
+            float y[1], z[1], hv[1] = {0.0f};
+            load_vec<TH, 1>((const TH*)P.gy, off, y);
+            load_vec<TH, 1>((const TH*)P.gz, off, z);
+            if (gdz) load_vec<TH, 1>((const TH*)P.h, off, hv);
+            const float sg = sigmoid(z[0]);
+            gv[j] = y[0] * (z[0] * sg);
+            dzv[j] = y[0] * hv[0] * (sg * fmaf(z[0], 1.0f - sg, 1.0f));
+        }
+        if (gdz && ln.valid) {
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                const float dz[1] = {dzv[j]};
+                if (full || tw + j < P.L)
+                    store_vec<TH, 1>((TH*)P.gdz, elem_offset<T, TH>(ln.at(tw + j)), dz);
+            }
         }
     } else {
 #pragma unroll
@@ -1009,6 +1033,8 @@ size_t fused_backward_workspace(int64_t B, int64_t L, int64_t D) {
 }
 
 hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
+    // the output gate is folded into the fp32-x kernels only
+    if (a.gy && io_bytes(a.io) != 4) return hipErrorInvalidValue;
     const BwdPlan plan = plan_fused_backward(a.B, a.L, a.D);
     const BwdLayout lay = bwd_layout(a.B, a.D, plan);
     char* ws = (char*)a.ws;
@@ -1018,7 +1044,7 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
     const BwdParams P{a.x,  nullptr, nullptr, a.lambda, a.h0, a.h,   a.dh,  a.dhT,
                       a.dx, a.dzr,   a.dzi,   a.dh0,    partial, a.L, a.D,  a.B * a.D,
                       plan.ngroups, plan.nseg, lookback_ws(ws + lay.lb),
-                      counters, dlambda_groups(a.D), a.gy, a.gz};
+                      counters, dlambda_groups(a.D), a.gy, a.gz, a.gdz};
     hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(plan.ngroups * plan.nseg)), block(fusedz::NT);
