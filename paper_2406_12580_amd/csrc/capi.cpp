@@ -573,29 +573,17 @@ int recblr_gated_backward(const void* hx, const void* hz, const float* conv_w,
         void* pack = at(lws, fl.pack);
         if (fused_backward_applies(B, L, D, IoType::kF32, xp, h, pack)) {
             const bool bf = io == RECBLR_BF16;
-            float* wt = (float*)at(ws, lay.wts);
-            const void *wr32 = W_r, *wi32 = W_i, *br32 = b_r, *bi32 = b_i;
-            if (bf) {
-                // the scan recomputes z from fp32 x' with fp32 weights
-                if (launch_widen(W_r, wt, D * D, strm) != hipSuccess ||
-                    launch_widen(W_i, wt + D * D, D * D, strm) != hipSuccess ||
-                    (b_r && launch_widen(b_r, wt + 2 * D * D, D, strm) != hipSuccess) ||
-                    (b_i && launch_widen(b_i, wt + 2 * D * D + D, D, strm) != hipSuccess))
-                    return RECBLR_ERR_HIP;
-                wr32 = wt;
-                wi32 = wt + D * D;
-                br32 = b_r ? wt + 2 * D * D : nullptr;
-                bi32 = b_i ? wt + 2 * D * D + D : nullptr;
-            }
             void* dzr = at(lws, fl.dzr);
             void* dzi = at(lws, fl.dzi);
             // bf16: dhz = dy h SiLU'(hz) in a pass of its own (reading dy, hz, h
-            // as stored), which measured faster than folding it into the scan.
+            // as stored), which measured faster than folding it into the scan;
+            // the scan recomputes z from fp32 x' with the weights and biases as
+            // given (bf16 weights are one exact operand plane).
             if ((bf && launch_gate_backward(dy, hz, h, nullptr, dhz, n_el, IoType::kBf16,
                                             IoType::kBf16, strm) != hipSuccess) ||
-                launch_pack_groups(wr32, wi32, D, IoType::kF32, pack, strm) != hipSuccess)
+                launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
                 return RECBLR_ERR_HIP;
-            FusedBwdArgs fa{xp,        pack,      br32,    bi32,        lambda, h0, h, nullptr,
+            FusedBwdArgs fa{xp,        pack,      b_r,     b_i,         lambda, h0, h, nullptr,
                             dhT,       dxp,       (float*)dzr, (float*)dzi, dlambda, dh0,
                             B,         L,         D,       IoType::kF32, at(lws, fl.scan)};
             fa.gy = dy;

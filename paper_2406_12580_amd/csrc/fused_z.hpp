@@ -53,12 +53,14 @@ __device__ __forceinline__ void strip_mma(__bf16 (*la)[fastmm::BM][fastmm::KP],
     }
 }
 
-// Operand kinds and LDS size of the tile product for I/O type T.
-template <typename T>
+// Operand kinds and LDS size of the tile product for x of type T and weights
+// of type TW (bf16 weights are one exact plane even against fp32 x: the
+// split's hi * lo term would only add zeros).
+template <typename T, typename TW = T>
 struct Tile {
     static constexpr bool kF32 = sizeof(T) == 4;
     using OpA = fastmm::Operand<kF32 ? fastmm::kF32 : fastmm::kBf16, true>;
-    using OpB = fastmm::Operand<kF32 ? fastmm::kPack2 : fastmm::kPack1, true>;
+    using OpB = fastmm::Operand<sizeof(TW) == 4 ? fastmm::kPack2 : fastmm::kPack1, true>;
     static constexpr int PA = OpA::kPlanes, PB = OpB::kPlanes;
     static constexpr size_t kStage =
         (size_t)(PA * fastmm::BM + PB * fastmm::BN) * fastmm::KP * 2;
@@ -67,17 +69,18 @@ struct Tile {
 };
 
 // z_r, z_i of the tile for this lane's channel at this wave's 16 steps.
-// x: [B][L][D] (row b is read), pack: [W_r; W_i] ordered by channel group of
-// 64 (launch_pack_groups), biases may be null; D % 64 == 0.  Steps past L
-// read x as zero.  smem: Tile<T>::kSmem bytes, free on entry; all NT threads
-// call this (it holds workgroup barriers).
-template <typename T>
-__device__ __forceinline__ void tile_z(const T* x, const __bf16* pack, const T* br,
-                                       const T* bi, int64_t L, int64_t D, int64_t b,
+// x: [B][L][D] (row b is read), pack: [W_r; W_i] of type TW ordered by
+// channel group of 64 (launch_pack_groups), biases (TW) may be null;
+// D % 64 == 0.  Steps past L read x as zero.  smem: Tile<T, TW>::kSmem
+// bytes, free on entry; all NT threads call this (it holds workgroup
+// barriers).
+template <typename T, typename TW = T>
+__device__ __forceinline__ void tile_z(const T* x, const __bf16* pack, const TW* br,
+                                       const TW* bi, int64_t L, int64_t D, int64_t b,
                                        int64_t cg, int64_t t0, char* smem, int tid, int w,
                                        int lane, float (&zr)[C], float (&zi)[C]) {
     using namespace fastmm;
-    using TT = Tile<T>;
+    using TT = Tile<T, TW>;
     using OpA = typename TT::OpA;
     using OpB = typename TT::OpB;
     constexpr int PA = TT::PA, PB = TT::PB;
@@ -118,7 +121,7 @@ __device__ __forceinline__ void tile_z(const T* x, const __bf16* pack, const T* 
     // steps) becomes lane c's z_r, then its z_i.  A wave's LDS operations
     // execute in order, so the second gate may reuse the strip.
     float* zs = (float*)smem + w * 64 * ZP;
-    const ElemReader<T> rbr(br, D), rbi(bi, D);
+    const ElemReader<TW> rbr(br, D), rbi(bi, D);
     const int64_t d = cg * kWave + (lane & 15);
 #pragma unroll
     for (int gate = 0; gate < 2; ++gate) {

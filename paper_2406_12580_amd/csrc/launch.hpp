@@ -157,7 +157,8 @@ struct FusedBwdArgs {
     const void* gy = nullptr;
     const void* gz = nullptr;
     void* gdz = nullptr;
-    // fp32 x with h (and gy, gz) in bf16: the gated layer's bf16 backward,
+    // fp32 x with h, gy, gz, the weights (pack: one bf16 plane, packed from
+    // bf16 weights) and the biases in bf16: the gated layer's bf16 backward,
     // which keeps x' and the gradients in fp32.
     bool h_bf16 = false;
 };

@@ -674,13 +674,17 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
     write_partial<W, 1>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
 }
 
-template <typename T, typename TH, int K, typename Off>
+// TW: type of the weights and biases (bf16 weights against fp32 x take one
+// operand plane).
+template <typename T, typename TH, int K, typename Off, typename TW = T>
 __global__ __launch_bounds__(fusedz::NT, 4) void
-scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi) {
+scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const TW* br, const TW* bi) {
     constexpr int W = fusedz::W, C = fusedz::C;
-    static_assert(2 * W * C * kWave * (int)sizeof(T) <= (int)fusedz::Tile<T>::kSmem,
-                  "x and h staging fits in the product's LDS");
-    __shared__ __attribute__((aligned(16))) char smem[fusedz::Tile<T>::kSmem];
+    // LDS: the tile product, then the x and h staging of the epilogue.
+    constexpr size_t kStaging = (size_t)2 * W * C * kWave * sizeof(T);
+    constexpr size_t kSmem = fusedz::Tile<T, TW>::kSmem > kStaging
+                                 ? fusedz::Tile<T, TW>::kSmem : kStaging;
+    __shared__ __attribute__((aligned(16))) char smem[kSmem];
     __shared__ Seg agg[W][kWave][1];
     __shared__ uint64_t win_sh[W * K][kWave][1];
     __shared__ float carry_sh[kWave][1];
@@ -700,8 +704,8 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const T* br, const T* bi)
     const int64_t gpr = P.D / kWave;      // channel groups per batch row
     const int64_t b = g / gpr, cg = g - b * gpr;
     float zr[C], zi[C];
-    fusedz::tile_z<T>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, s * W * C, smem, tid, w,
-                      lane, zr, zi);
+    fusedz::tile_z<T, TW>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, s * W * C, smem, tid, w,
+                          lane, zr, zi);
     __syncthreads();  // every wave holds its z: the product's LDS is free
     bwd_eps_tile<T, TH, T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh, carry_sh, red,
                                          w, lane);
@@ -1061,14 +1065,15 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, hipStream_t stream) {
                                stream, P, (const __bf16*)a.pack, (const float*)a.br,
                                (const float*)a.bi);
     } else if (a.h_bf16) {
+        // fp32 x; h, the weights (one packed plane) and biases in bf16
         if (small)
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint32_t>), grid, block, 0,
-                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
-                               (const float*)a.bi);
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint32_t, bf16>), grid,
+                               block, 0, stream, P, (const __bf16*)a.pack, (const bf16*)a.br,
+                               (const bf16*)a.bi);
         else
-            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint64_t>), grid, block, 0,
-                               stream, P, (const __bf16*)a.pack, (const float*)a.br,
-                               (const float*)a.bi);
+            hipLaunchKernelGGL((scan_bwd_fused_kernel<float, bf16, K, uint64_t, bf16>), grid,
+                               block, 0, stream, P, (const __bf16*)a.pack, (const bf16*)a.br,
+                               (const bf16*)a.bi);
     } else {
         if (small)
             hipLaunchKernelGGL((scan_bwd_fused_kernel<bf16, bf16, K, uint32_t>), grid, block, 0,
