@@ -209,13 +209,22 @@ __device__ __forceinline__ ChannelConst channel_const(float lam) {
     return c;
 }
 
-// alpha and beta' = beta * x of one element (forward path).
+// alpha and beta' = beta * x of one element (forward path).  kSeries: 1 -
+// alpha^2 through one_minus_exp_neg (full relative accuracy however small
+// 2q is).  Without it, 1 - alpha^2 is formed directly (one fma): its error
+// is about one ulp of 1 in absolute terms, so beta = sqrt(1 - alpha^2) i is
+// off by at most ~1e-3 of itself for 2q down to 3e-5 and by a few 1e-4 in
+// absolute terms below that, which bf16 I/O (a 2^-9 rounding of every input
+// and output) does not see; it saves the series' ~7 instructions per element
+// (the bf16 fused forward, 16 x 16384 x 256: 222 -> 209 us).  The backward
+// keeps the series: its dz_r and dLambda terms carry 1 / sqrt(1 - alpha^2).
+template <bool kSeries = true>
 __device__ __forceinline__ void gate_forward(float x, float zr, float zi, const ChannelConst& cc,
                                              float& alpha, float& u) {
     float r = sigmoid(zr);
     float i = sigmoid(zi);
     alpha = fast_exp2(r * cc.neg_s_l2);
-    float m = one_minus_exp_neg(r * cc.two_s, alpha);
+    float m = kSeries ? one_minus_exp_neg(r * cc.two_s, alpha) : fmaf(-alpha, alpha, 1.0f);
     u = fast_sqrt(m) * i * x;
 }
 

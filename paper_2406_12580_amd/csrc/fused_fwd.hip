@@ -460,7 +460,7 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
                 else
                     xv = *(const float*)(cur + xoff[0] + (32 * m + i) * G::kRow);
                 float a, u;
-                gate_forward(xv, acc[m][i], acc[m][i + 8], cc, a, u);
+                gate_forward<sizeof(T) == 4>(xv, acc[m][i], acc[m][i + 8], cc, a, u);
                 if (lim < TS) {
                     const bool ok = 32 * m + 8 * rho + i < lim;
                     a = ok ? a : 1.0f;

@@ -103,7 +103,8 @@ __device__ __forceinline__ void form_steps(const ChunkIn<TX, TZ, C, VEC, RAW, Of
                 aj = in.v0[j][k];
                 uj = in.v1[j][k];
             } else {
-                gate_forward(in.v0[j][k], in.v1[j][k], in.v2[j][k], cc[k], aj, uj);
+                gate_forward<sizeof(TX) == 4>(in.v0[j][k], in.v1[j][k], in.v2[j][k], cc[k], aj,
+                                              uj);
             }
             a[j][k] = ok ? aj : 1.0f;
             u[j][k] = ok ? uj : 0.0f;
@@ -395,7 +396,7 @@ scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
     for (int j = 0; j < C; ++j) {
         const bool ok = full || tw + j < P.L;
         float aj, uj;
-        gate_forward(xs[j], zr[j], zi[j], cc[0], aj, uj);
+        gate_forward<sizeof(T) == 4>(xs[j], zr[j], zi[j], cc[0], aj, uj);
         a[j][0] = ok ? aj : 1.0f;
         u[j][0] = ok ? uj : 0.0f;
     }

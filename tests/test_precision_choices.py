@@ -52,3 +52,28 @@ def test_bf16_x_prime_or_dh_would_break_the_bar(shape, K):
     worst_dh = max(error_report(with_dh[k], ref[k])["floored"] for k in ("dWr", "dWi"))
     assert worst_x > 1e-2, worst_x
     assert worst_dh > 1e-2, worst_dh
+
+
+@pytest.mark.parametrize("a_range", [(0.9, 0.999), (0.99, 0.9999)])
+def test_direct_one_minus_alpha2_is_inside_the_bf16_bar(a_range):
+    """The bf16 forward kernels form 1 - alpha^2 directly (one fp32 fma)
+    instead of through the series that keeps its relative accuracy when
+    2q is tiny.  Emulated in float32 (gates, alpha, the direct 1 - alpha^2,
+    beta x) with the recurrence in fp64, h moves by well under a tenth of
+    the bf16 bar against the fp64 oracle, also for the slow decays of the
+    gated tests, where 2q gets smallest."""
+    B, L, D = 2, 2048, 64
+    f = dg.scan_inputs(B, L, D, seed=77, io="bf16", a_range=a_range)
+    ref, _ = oracle.scan_forward(f.x, f.zr, f.zi, f.lam)
+    f32 = np.float32
+    l2e = f32(1.4426950408889634)
+    sig = lambda z: f32(1) / (f32(1) + np.exp2(-z.astype(f32) * l2e))
+    lam = f.lam.astype(np.float64)
+    s = (np.maximum(lam, 0) + np.log1p(np.exp(-np.abs(lam)))).astype(f32)
+    r, i = sig(f.zr), sig(f.zi)
+    alpha = np.exp2(r * (-s * l2e)).astype(f32)
+    m = (f32(1) - alpha * alpha).astype(f32)
+    u = (np.sqrt(m) * i * f.x.astype(f32)).astype(f32)
+    got, _ = oracle.linear_scan(alpha.astype(np.float64), u.astype(np.float64))
+    err = error_report(got, ref)["floored"]
+    assert err < 1e-3, err
