@@ -468,12 +468,17 @@ scan_fwd_fused_kernel(FwdParams P, const __bf16* pack, const T* br, const T* bi,
 #ifndef RECBLR_FWD_LB_E
 #define RECBLR_FWD_LB_E 16
 #endif
-// Channels per lane at most, per kernel (measured best on MI355X).
+// Channels per lane at most, per kernel (measured best on MI355X): the
+// look-back kernel takes two bf16 channels per lane (4-byte accesses; a
+// 2-byte access per lane streams about 10% slower) and one fp32 channel.
 #ifndef RECBLR_FWD_CHAIN_MAX_VEC
 #define RECBLR_FWD_CHAIN_MAX_VEC 4
 #endif
 #ifndef RECBLR_FWD_LB_MAX_VEC
-#define RECBLR_FWD_LB_MAX_VEC 1
+#define RECBLR_FWD_LB_MAX_VEC 2
+#endif
+#ifndef RECBLR_FWD_LB_MAX_VEC_F32
+#define RECBLR_FWD_LB_MAX_VEC_F32 1
 #endif
 constexpr int kChainW = RECBLR_FWD_CHAIN_W, kChainE = RECBLR_FWD_CHAIN_E;
 constexpr int kLbW = RECBLR_FWD_LB_W, kLbE = RECBLR_FWD_LB_E;
@@ -485,8 +490,13 @@ template <int VEC>
 constexpr int lb_window() { return RECBLR_FWD_LB_WORDS / VEC > 0 ? RECBLR_FWD_LB_WORDS / VEC : 1; }
 template <int E, int VEC>
 constexpr int steps_per_wave() { return E / VEC > 0 ? E / VEC : 1; }
-// Steps of one look-back tile for a given VEC.
-constexpr int64_t lb_tile_steps(int vec) { return (int64_t)kLbW * (kLbE / vec > 0 ? kLbE / vec : 1); }
+// Look-back tiles keep kLbE steps per wave whatever VEC is (two channels per
+// lane double the tile's channels, not its length): fewer tile rows along L
+// keep the chain of inclusive states short.
+template <int VEC>
+constexpr int lb_steps_per_wave() { return kLbE; }
+// Steps of one look-back tile.
+constexpr int64_t lb_tile_steps(int) { return (int64_t)kLbW * kLbE; }
 // The chain kernel is used when its workgroups alone fill the GPU.
 // The chain kernel is used when its workgroups alone fill the GPU (one
 // workgroup per compute unit at least); lanes then take as many channels as
@@ -495,7 +505,9 @@ constexpr int64_t kChainMinGroups = 256;
 // Largest channels-per-lane of a kernel for an element size (8-byte accesses
 // per lane at most).
 constexpr int max_vec(size_t esz, bool lookback, int64_t nch = INT64_MAX) {
-    const int cap = lookback ? RECBLR_FWD_LB_MAX_VEC : RECBLR_FWD_CHAIN_MAX_VEC;
+    const int cap = !lookback ? RECBLR_FWD_CHAIN_MAX_VEC
+                    : esz == 4 ? RECBLR_FWD_LB_MAX_VEC_F32
+                               : RECBLR_FWD_LB_MAX_VEC;
     int v = (int)(8 / esz) < cap ? (int)(8 / esz) : cap;
     while (v > 1 && !lookback && nch / (kWave * v) < kChainMinGroups) v /= 2;
     return v;
@@ -558,7 +570,7 @@ static hipError_t launch_vec(const FwdParams& P, const FwdPlan& plan, hipStream_
         hipError_t e = lookback_reset(P.lb, plan.nseg * P.nch, stream);
         if (e != hipSuccess) return e;
         return launch_measured(
-            scan_fwd_lookback_kernel<TX, TZ, kLbW, steps_per_wave<kLbE, VEC>(), VEC,
+            scan_fwd_lookback_kernel<TX, TZ, kLbW, lb_steps_per_wave<VEC>(), VEC,
                                      lb_window<VEC>(), Off>,
             dim3((unsigned)(plan.ngroups * plan.nseg)), dim3(kLbW * kWave), stream, ev0, ev1, P);
     }
