@@ -312,11 +312,10 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
             wf[kk] = *(const b8*)(wsrc + k0);
         }
     }
-    float bias = 0.0f;
-    {
-        const T* bp = (const T*)(col < 16 ? P.br : P.bi);
-        if (bp) bias = load(bp + cw + (col & 15));
-    }
+    // Biases of this lane's channel cw + cl (after the swap below a lane holds
+    // z_r and z_i of one channel), folded into the sigmoids' exponents.
+    const float nbr = P.br ? -load((const T*)P.br + cw + cl) * kLog2e : 0.0f;
+    const float nbi = P.bi ? -load((const T*)P.bi + cw + cl) * kLog2e : 0.0f;
     const ChannelConst cc = channel_const(P.lam[cw + cl]);
     // LDS byte offsets of this lane's x in a tile (local rows 8 rho + i; block
     // m adds 32 m rows): the chunk permutation of row 32 m + 8 rho + i is
@@ -406,12 +405,12 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
             abuf = planes;
         }
 
-        // ---- z = x W^T + b for 64 steps x this wave's 32 columns
+        // ---- z = x W^T for 64 steps x this wave's 32 columns (b comes with the gates)
         f16v acc[MB];
 #pragma unroll
         for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[m][v] = bias;
+            for (int v = 0; v < 16; ++v) acc[m][v] = 0.0f;
         {
             const int R = lane & 31;
 #pragma unroll
@@ -444,34 +443,44 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
                 acc[m][i + 8] = zi;
             }
 
-        // ---- gates (alpha into acc[m][i], beta' into acc[m][i + 8]) and segments
+        // ---- gates (alpha into acc[m][i], beta' into acc[m][i + 8]) and segments.
+        // Only the last tile can hold rows past L (they become the identity);
+        // the full tiles take a path without the per-element masks.
         Seg run[MB];
         const int lim = P.L - t0 < TS ? (int)(P.L - t0) : TS;  // valid rows of the tile
+        auto gates = [&](auto full_tag) {
+            constexpr bool kFull = decltype(full_tag)::value;
 #pragma unroll
-        for (int m = 0; m < MB; ++m) {
-            Seg sg{1.0f, 0.0f};
+            for (int m = 0; m < MB; ++m) {
+                Seg sg{1.0f, 0.0f};
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                float xv;
-                if constexpr (sizeof(T) == 2)
-                    xv = __uint_as_float((uint32_t)(*(const uint16_t*)(cur + xoff[i] +
-                                                                       32 * m * G::kRow))
-                                         << 16);
-                else
-                    xv = *(const float*)(cur + xoff[0] + (32 * m + i) * G::kRow);
-                float a, u;
-                gate_forward<sizeof(T) == 4>(xv, acc[m][i], acc[m][i + 8], cc, a, u);
-                if (lim < TS) {
-                    const bool ok = 32 * m + 8 * rho + i < lim;
-                    a = ok ? a : 1.0f;
-                    u = ok ? u : 0.0f;
+                for (int i = 0; i < 8; ++i) {
+                    float xv;
+                    if constexpr (sizeof(T) == 2)
+                        xv = __uint_as_float((uint32_t)(*(const uint16_t*)(cur + xoff[i] +
+                                                                           32 * m * G::kRow))
+                                             << 16);
+                    else
+                        xv = *(const float*)(cur + xoff[0] + (32 * m + i) * G::kRow);
+                    float a, u;
+                    gate_forward_biased<sizeof(T) == 4>(xv, acc[m][i], acc[m][i + 8], nbr, nbi,
+                                                        cc, a, u);
+                    if constexpr (!kFull) {
+                        const bool ok = 32 * m + 8 * rho + i < lim;
+                        a = ok ? a : 1.0f;
+                        u = ok ? u : 0.0f;
+                    }
+                    acc[m][i] = a;
+                    acc[m][i + 8] = u;
+                    sg = Seg{a * sg.A, fmaf(a, sg.H, u)};
                 }
-                acc[m][i] = a;
-                acc[m][i + 8] = u;
-                sg = Seg{a * sg.A, fmaf(a, sg.H, u)};
+                run[m] = sg;
             }
-            run[m] = sg;
-        }
+        };
+        if (lim == TS)
+            gates(std::true_type{});
+        else
+            gates(std::false_type{});
         // ---- the four runs of a block: exclusive prefix and block total
         Seg excl[MB], tot[MB];
 #pragma unroll
