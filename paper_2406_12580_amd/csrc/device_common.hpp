@@ -228,20 +228,6 @@ __device__ __forceinline__ void gate_forward(float x, float zr, float zi, const 
     u = fast_sqrt(m) * i * x;
 }
 
-// gate_forward on pre-activations that still lack their biases: the exponent
-// of each sigmoid is formed as fma(z, -log2 e, nb) with nb = -b log2 e, so
-// adding the bias costs no instruction (z + b is never rounded on its own).
-template <bool kSeries = true>
-__device__ __forceinline__ void gate_forward_biased(float x, float zr, float zi, float nbr,
-                                                    float nbi, const ChannelConst& cc,
-                                                    float& alpha, float& u) {
-    float r = fast_rcp(1.0f + fast_exp2(fmaf(zr, -kLog2e, nbr)));
-    float i = fast_rcp(1.0f + fast_exp2(fmaf(zi, -kLog2e, nbi)));
-    alpha = fast_exp2(r * cc.neg_s_l2);
-    float m = kSeries ? one_minus_exp_neg(r * cc.two_s, alpha) : fmaf(-alpha, alpha, 1.0f);
-    u = fast_sqrt(m) * i * x;
-}
-
 // (A, H) pair of the scan operator: a segment maps a state h to A h + H.
 // Composing an earlier segment e with a later segment l gives
 // (A_l A_e, A_l H_e + H_l) (section 3.3, operator "bullet").

@@ -200,6 +200,20 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t b
 
 __device__ __forceinline__ float silu(float c) { return c * sigmoid(c); }
 
+// gate_forward on pre-activations that still lack their biases: the exponent
+// of each sigmoid is formed as fma(z, -log2 e, nb) with nb = -b log2 e, so
+// adding the bias costs no instruction (z + b is never rounded on its own).
+template <bool kSeries = true>
+__device__ __forceinline__ void gate_forward_biased(float x, float zr, float zi, float nbr,
+                                                    float nbi, const ChannelConst& cc,
+                                                    float& alpha, float& u) {
+    float r = fast_rcp(1.0f + fast_exp2(fmaf(zr, -kLog2e, nbr)));
+    float i = fast_rcp(1.0f + fast_exp2(fmaf(zi, -kLog2e, nbi)));
+    alpha = fast_exp2(r * cc.neg_s_l2);
+    float m = kSeries ? one_minus_exp_neg(r * cc.two_s, alpha) : fmaf(-alpha, alpha, 1.0f);
+    u = fast_sqrt(m) * i * x;
+}
+
 // Workgroup barrier for LDS hand-offs that leaves vector-memory operations in
 // flight: __syncthreads() carries a release fence, which waits for every
 // outstanding load and store of the wave (the direct-to-LDS prefetch of the
