@@ -535,7 +535,8 @@ __device__ __forceinline__ Off elem_offset(Off off_a) {
     return sizeof(TA) == sizeof(TB) ? off_a : off_a / (Off)sizeof(TA) * (Off)sizeof(TB);
 }
 
-template <typename T, typename TH, typename TD, typename TZ, int W, int C, int K, typename Off>
+template <bool FULL, typename T, typename TH, typename TD, typename TZ, int W, int C, int K,
+          typename Off>
 __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int64_t g, int64_t b,
                                              int64_t cg, const float (&zr)[C],
                                              const float (&zi)[C], char* stage,
@@ -551,7 +552,9 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
     float h0v[1], dhTv[1];
     bwd_lane_consts<1>(P, ln.c0, ln.d0, cc, h0v, dhTv);
     const int64_t tw = t0 + (int64_t)w * C;
-    const bool full = s > 0 && (s + 1) * W * C <= P.L;  // workgroup-uniform
+    // FULL: a tile with s > 0 and every step before L (no masks, h_{t-1} of
+    // every step from the staged rows); the caller branches on it uniformly.
+    constexpr bool full = FULL;
     // x and h_{t-1} are only needed in the epilogue: they wait in LDS, not in
     // registers.
     constexpr int kStaged = C * kWave * (int)sizeof(T);  // one tensor's rows of a wave
@@ -707,8 +710,12 @@ scan_bwd_fused_kernel(BwdParams P, const __bf16* pack, const TW* br, const TW* b
     fusedz::tile_z<T, TW>((const T*)P.x, pack, br, bi, P.L, P.D, b, cg, s * W * C, smem, tid, w,
                           lane, zr, zi);
     __syncthreads();  // every wave holds its z: the product's LDS is free
-    bwd_eps_tile<T, TH, T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh, carry_sh, red,
-                                         w, lane);
+    if (s > 0 && (s + 1) * W * C <= P.L)
+        bwd_eps_tile<true, T, TH, T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh,
+                                                          carry_sh, red, w, lane);
+    else
+        bwd_eps_tile<false, T, TH, T, float, W, C, K, Off>(P, r, g, b, cg, zr, zi, smem, agg, win_sh,
+                                                           carry_sh, red, w, lane);
 }
 
 // ------------------------------------------------------------------ dLambda reduction
