@@ -61,13 +61,13 @@ ARRAYS = {"scan": (4, 8), "full": (2, 4)}
 # valid only for the kernel sources they were taken on: the sha256 prefix of
 # the listed files must match, else the traffic is reported as null.
 TRAFFIC = {
-    ("c4", "scan_bwd"): {"bytes": 2187192659, "sha": "dac093dab1b0800d",
+    ("c4", "scan_bwd"): {"bytes": 2186809344, "sha": "e69a30050e64190c",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c4", "scan_fwd"): {"bytes": 1074250560, "sha": "fd5a570ddb8d6780",
+    ("c4", "scan_fwd"): {"bytes": 1074241536, "sha": "5450919d02e895fb",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c5", "scan_bwd"): {"bytes": 1120554054, "sha": "dac093dab1b0800d",
+    ("c5", "scan_bwd"): {"bytes": 1120487424, "sha": "e69a30050e64190c",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c5", "scan_fwd"): {"bytes": 571180019, "sha": "fd5a570ddb8d6780",
+    ("c5", "scan_fwd"): {"bytes": 582594560, "sha": "5450919d02e895fb",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
 }
 
