@@ -239,10 +239,12 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
  *   hx, hz, y : [B][L][D] io;  h : [B][L][D] io or NULL (the BD-LRU output,
  *   kept for a backward);  conv_w : [D][K] float;  conv_b : [D] float or NULL;
  *   W_r, b_r, W_i, b_i, lambda, h0, hT : as recblr_bdlru_forward.
- * Workspace: recblr_workspace_size(RECBLR_OP_GATED_FORWARD, ...).  x' is
- * formed by one streaming kernel; where the scan forward with the
- * projections fused in applies (few channel groups, D % 64 == 0) it reads x'
- * and stores y directly (neither z nor h needs to reach memory).
+ * Workspace: recblr_workspace_size(RECBLR_OP_GATED_FORWARD, ...).  Where the
+ * weights-resident fused forward applies (D = 128 fp32 or bf16, D = 256 bf16,
+ * 16-byte aligned hx and weights) one kernel does the three lines: x' is
+ * formed on load from hx rows staged in LDS, z on the matrix cores, and y is
+ * stored directly (neither x', z nor h needs to reach memory).  Elsewhere x'
+ * is formed by one streaming kernel first.
  * Errors: UNSUPPORTED for K outside 1..4 or D > 1024; otherwise as
  * recblr_bdlru_forward.
  */

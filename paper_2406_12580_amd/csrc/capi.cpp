@@ -471,14 +471,14 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
     char* fws = at(ws, lay.full);
     void* pack = fws + fl.pack;
     void* xp = at(ws, lay.xp);
-    // x' = SiLU(conv(hx)) is formed once, in a streaming kernel: doing it on
-    // the fly inside the fused scan kernel (its tap loads held in registers)
-    // cost that kernel three quarters of its occupancy.
+    // Where the weights-resident fused forward applies, x' = SiLU(conv(hx)) is
+    // formed on load, from hx rows staged in LDS (with the three before each
+    // tile); elsewhere once, by a streaming kernel.
+    if (L > 0 && fused2_forward_applies(B, L, D, io_of(io), hx, W_r, W_i))
+        return status_of(launch_fused2_forward(hx, W_r, b_r, W_i, b_i, lambda, h0, h, hT, hz, y,
+                                               B, L, D, io_of(io), fws + fl.scan, strm, w4, b4));
     if (launch_conv_silu(hx, w4, b4, xp, B, L, D, io_of(io), io_of(io), strm) != hipSuccess)
         return RECBLR_ERR_HIP;
-    if (L > 0 && fused2_forward_applies(B, L, D, io_of(io), xp, W_r, W_i))
-        return status_of(launch_fused2_forward(xp, W_r, b_r, W_i, b_i, lambda, h0, h, hT, hz, y,
-                                               B, L, D, io_of(io), fws + fl.scan, strm));
     if (L > 0 && fused_forward_applies(B, L, D, io_of(io), xp, pack)) {
         if (launch_pack_groups(W_r, W_i, D, io_of(io), pack, strm) != hipSuccess)
             return RECBLR_ERR_HIP;

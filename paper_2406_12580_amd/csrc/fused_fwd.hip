@@ -75,6 +75,8 @@ struct Params {
     float* hT;        // [B][D] or null
     const void* hz;   // gated: [B][L][D] I/O type
     void* y;          // gated: [B][L][D] I/O type
+    const float* cw4;  // conv on load: taps [4][D] (zero past K); x then holds hx
+    const float* cb4;  // conv on load: bias [D]
     int64_t L, D, nch;    // nch = B * D
     int64_t ngroups, nseg;
     unsigned* counters;  // look-back mode: tile-row tickets, one per group
@@ -170,6 +172,115 @@ __device__ __forceinline__ void split_tile(const char* raw, char* planes, int ti
     }
 }
 
+// ---- causal conv + SiLU on load (gated layer core, Algorithm alg:gated_recurrent
+// line 3): the tile's hx rows and the three rows before them are staged raw,
+// x' = SiLU(b + sum_{j<4} w_j hx_{t-j}) is formed from them into the x tile
+// (the layout stage_tile gives), and the products and the scan read it from
+// there as from a staged x tile.
+template <typename T, int D>
+struct ConvGeo {
+    using G = Geo<T, D>;
+    static constexpr int kRows = TS + 3;             // the tile's rows and the 3 before
+    static constexpr int kHx = kRows * G::kRow;       // one staged hx tile
+    static constexpr int kChunks = kHx / 16;
+    static constexpr int kPerWave = kChunks / G::kNW;  // 16-byte chunks per wave
+    static constexpr int kLoads = (kPerWave + kWave - 1) / kWave;  // loads per wave (the last partial)
+    static constexpr int kTaps = 5 * D * 4;           // [4][D] taps then [D] bias, fp32
+    static constexpr int kBase = G::kTile + G::kPlanes + G::kHTile + kTaps;
+    static constexpr int kLimit = 160 * 1024 - 1024;  // dynamic LDS (static slots aside)
+    static constexpr int kBufs = kBase + 2 * kHx <= kLimit ? 2 : 1;  // hx tiles in LDS
+    static constexpr int kSmem = kBase + kBufs * kHx;
+    static constexpr int kCpr = G::kRow / 16;         // 16-byte chunks per row
+    static constexpr int kRpg = TS * kCpr / G::NT;    // conv: rows per thread
+    static_assert(kPerWave * G::kNW == kChunks, "hx chunks split evenly over the waves");
+    static_assert(kRpg * G::NT == TS * kCpr, "conv rows split evenly over the threads");
+    static_assert(kSmem <= kLimit, "LDS");
+    static_assert(kConvTaps == 4, "three halo rows before the tile");
+};
+
+// Issues the direct-to-LDS loads of one hx tile: rows t0 - 3 .. t0 + TS - 1 of
+// batch row b (clamped to [0, L - 1]; rows before 0 are zeroed by conv_tile),
+// stored row after row.  Every wave issues ConvGeo::kLoads loads (the last
+// with some lanes off), so vector-memory wait counts stay exact.
+template <typename T, int D>
+__device__ __forceinline__ void stage_hx(const T* hx, int64_t b, int64_t L, int64_t t0, char* buf,
+                                         int lane, int w) {
+    using CG = ConvGeo<T, D>;
+    using G = Geo<T, D>;
+#pragma unroll
+    for (int q = 0; q < CG::kLoads; ++q) {
+        const int c = q * kWave + lane;  // chunk within this wave's share
+        if (c < CG::kPerWave) {
+            const int o = w * CG::kPerWave + c;
+            const int r = o / CG::kCpr, j = o % CG::kCpr;
+            int64_t t = t0 - 3 + r;
+            t = t < 0 ? 0 : (t < L ? t : L - 1);
+            const char* gp = (const char*)hx + ((b * L + t) * D) * G::kEsz + j * 16;
+            __builtin_amdgcn_global_load_lds((const glb_void*)gp,
+                                             (lds_void*)(buf + (w * CG::kPerWave + q * kWave) * 16),
+                                             16, 0, 0);
+        }
+    }
+}
+
+// x' of the tile from its staged hx rows: thread tid takes chunk tid % kCpr
+// (V channels) of rows (tid / kCpr) kRpg .. + kRpg - 1, with the taps and bias
+// of those channels from the LDS table.  The sum runs over j = 0 .. 3 in that
+// order from the bias, as the streaming conv kernel does.
+template <typename T, int D>
+__device__ __forceinline__ void conv_tile(const char* hxb, const float* taps, char* xt, int64_t t0,
+                                          int tid) {
+    using CG = ConvGeo<T, D>;
+    using G = Geo<T, D>;
+    constexpr int V = 16 / (int)sizeof(T);
+    constexpr int R = CG::kRpg;
+    const int j = tid % CG::kCpr, r0 = (tid / CG::kCpr) * R;
+    float wt[kConvTaps][V], bv[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        bv[v] = taps[kConvTaps * D + j * V + v];
+#pragma unroll
+        for (int k = 0; k < kConvTaps; ++k) wt[k][v] = taps[k * D + j * V + v];
+    }
+    float win[R + 3][V];
+#pragma unroll
+    for (int i = 0; i < R + 3; ++i) {
+        const u4v raw = *(const u4v*)(hxb + (r0 + i) * G::kRow + j * 16);
+        const bool live = t0 - 3 + r0 + i >= 0;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            float f;
+            if constexpr (sizeof(T) == 2)
+                f = (v & 1) ? bf16_hi(raw[v >> 1]) : bf16_lo(raw[v >> 1]);
+            else
+                f = __uint_as_float(raw[v]);
+            win[i][v] = live ? f : 0.0f;
+        }
+    }
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) {
+        const int r = r0 + rr;
+        float xo[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            float c = bv[v];
+#pragma unroll
+            for (int k = 0; k < kConvTaps; ++k) c = fmaf(wt[k][v], win[rr + 3 - k][v], c);
+            xo[v] = c * sigmoid(c);
+        }
+        u4v out;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[e] = bf16_pair(xo[2 * e], xo[2 * e + 1]);
+            *(u4v*)(xt + r * G::kRow + ((j ^ swz16(r)) << 4)) = out;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[e] = __float_as_uint(xo[e]);
+            *(u4v*)(xt + r * G::kRow + ((j ^ swz32(r)) << 4)) = out;
+        }
+    }
+}
+
 __device__ __forceinline__ float sw_bits(uint32_t v) { return __uint_as_float(v); }
 
 // v_permlane16_swap of two accumulators: even 16-lane rows keep a and get
@@ -260,16 +371,24 @@ __device__ __forceinline__ u4v gate_chunk(u4v hv, u4v zv) {
     return out;
 }
 
-template <typename T, int D, bool GATED, bool LOOKBACK>
+// CONV (gated only): x holds hx and x' = SiLU(conv(hx)) is formed on load.
+template <typename T, int D, bool GATED, bool LOOKBACK, bool CONV = false>
 __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
     using G = Geo<T, D>;
+    using CG = ConvGeo<T, D>;
     constexpr int NT = G::NT, CH = G::CH;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int64_t slot_sh[2];
+    // LDS: two x tiles (double buffer), the bf16 operand planes (fp32 I/O),
+    // the h tile; with CONV one x' tile, the planes, the h tile, the conv
+    // taps and one or two staged hx tiles.
     char* const xbuf0 = smem;
-    char* const xbuf1 = smem + G::kTile;
-    char* const planes = smem + 2 * G::kTile;
+    char* const xbuf1 = CONV ? smem : smem + G::kTile;
+    char* const planes = smem + (CONV ? 1 : 2) * G::kTile;
     char* const hst = planes + G::kPlanes;
+    float* const taps = (float*)(hst + G::kHTile);
+    char* const hxbuf0 = hst + G::kHTile + CG::kTaps;
+    char* const hxbuf1 = CG::kBufs == 2 ? hxbuf0 + CG::kHx : hxbuf0;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -359,13 +478,26 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
              GATED ? row_bytes : 0u);
     u4v hz_load[GATED ? G::kSt : 1], hz_store[GATED ? G::kSt : 1];
 
-    stage_tile<T, D>(xg, b, P.L, s_cur * TS, xbuf0, tid, w);
+    if constexpr (CONV) {
+        // the taps table, visible after the loop's first barrier
+        for (int i = tid; i < 5 * D; i += NT)
+            taps[i] = i < kConvTaps * D ? P.cw4[i] : P.cb4[i - kConvTaps * D];
+        stage_hx<T, D>(xg, b, P.L, s_cur * TS, hxbuf0, lane, w);
+    } else {
+        stage_tile<T, D>(xg, b, P.L, s_cur * TS, xbuf0, tid, w);
+    }
 
     int64_t s_prev = -1;  // tile whose h waits in the LDS h tile
     constexpr int kHz = GATED ? G::kSt : 0;  // hz loads per thread per tile
+    // Loads of the next tile issued at the top of an iteration (x, or hx with
+    // two hx buffers; a single hx buffer is refilled after the conv instead).
+    constexpr bool kEarly = !CONV || CG::kBufs == 2;
+    constexpr int kNextLoads = CONV ? CG::kLoads : G::kLoads;
     for (int64_t it = 0;; ++it) {
         char* const cur = (it & 1) ? xbuf1 : xbuf0;
         char* const nxt = (it & 1) ? xbuf0 : xbuf1;
+        char* const hxcur = (it & 1) ? hxbuf1 : hxbuf0;
+        char* const hxnxt = (it & 1) ? hxbuf0 : hxbuf1;
         lds_barrier();  // all waves are done with the previous tile: nxt is free, hst is full
         const bool has_next = s_next < P.nseg;
         unsigned ticket = 0;
@@ -377,7 +509,12 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
 #pragma unroll
             for (int q = 0; q < G::kSt; ++q) hz_store[q] = hz_load[q];
         }
-        if (has_next) stage_tile<T, D>(xg, b, P.L, s_next * TS, nxt, tid, w);
+        if (kEarly && has_next) {
+            if constexpr (CONV)
+                stage_hx<T, D>(xg, b, P.L, s_next * TS, hxnxt, lane, w);
+            else
+                stage_tile<T, D>(xg, b, P.L, s_next * TS, nxt, tid, w);
+        }
         if constexpr (GATED) {
             // hz of the current tile, used when its h leaves (next iteration).
 #pragma unroll
@@ -386,9 +523,9 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
                     zr_, chunk_offset<T, D>(s_cur * TS, cg, q, tid), 0, 0);
         }
         // Everything but the loads just issued has landed: the current tile's
-        // x rows (issued one iteration ago) among it.
-        if (has_next)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::kLoads + kHz));
+        // x (or hx) rows, issued one iteration ago, among it.
+        if (kEarly && has_next)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(kNextLoads + kHz));
         else
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(kHz));
         // ---- the previous tile's h (and y) leave in 16-byte row chunks
@@ -412,6 +549,11 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
         lds_barrier();  // the current tile is in LDS for every wave; the h tile is free
         const int64_t s = s_cur;
         const int64_t t0 = s * TS;
+        if constexpr (CONV) {
+            conv_tile<T, D>(hxcur, taps, cur, t0, tid);
+            lds_barrier();  // x' is in LDS for every wave; hxcur is free
+            if (!kEarly && has_next) stage_hx<T, D>(xg, b, P.L, s_next * TS, hxbuf0, lane, w);
+        }
         const char* abuf = cur;
         if constexpr (G::kF32) {
             split_tile<D, NT>(cur, planes, tid);
@@ -615,10 +757,10 @@ __global__ void reset_kernel(unsigned* __restrict__ counters, int64_t ngroups,
     for (int64_t i = i0; i < n; i += stride) states[i] = ~0ull;
 }
 
-template <typename T, int D, bool GATED, bool LOOKBACK>
+template <typename T, int D, bool GATED, bool LOOKBACK, bool CONV>
 hipError_t launch(const Params& P, int grid, hipStream_t stream) {
-    auto kern = fused_fwd_kernel<T, D, GATED, LOOKBACK>;
-    constexpr int smem = Geo<T, D>::kSmem, nt = Geo<T, D>::NT;
+    auto kern = fused_fwd_kernel<T, D, GATED, LOOKBACK, CONV>;
+    constexpr int smem = CONV ? ConvGeo<T, D>::kSmem : Geo<T, D>::kSmem, nt = Geo<T, D>::NT;
     static const hipError_t attr =
         hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
     if (attr != hipSuccess) return attr;
@@ -626,9 +768,9 @@ hipError_t launch(const Params& P, int grid, hipStream_t stream) {
     return hipGetLastError();
 }
 
-template <typename T, int D, bool GATED>
+template <typename T, int D, bool GATED, bool CONV = false>
 hipError_t launch_mode(const Params& P, const Plan& pl, hipStream_t stream) {
-    if (!pl.lookback) return launch<T, D, GATED, false>(P, (int)pl.ngroups, stream);
+    if (!pl.lookback) return launch<T, D, GATED, false, CONV>(P, (int)pl.ngroups, stream);
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -638,7 +780,7 @@ hipError_t launch_mode(const Params& P, const Plan& pl, hipStream_t stream) {
     const int64_t slots = (int64_t)cus * (8 / Geo<T, D>::kNW);
     int64_t per = (slots + pl.ngroups - 1) / pl.ngroups;
     if (per > pl.nseg) per = pl.nseg;
-    return launch<T, D, GATED, true>(P, (int)(pl.ngroups * per), stream);
+    return launch<T, D, GATED, true, CONV>(P, (int)(pl.ngroups * per), stream);
 }
 
 }  // namespace fv2
@@ -662,10 +804,11 @@ size_t fused2_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io) {
 hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, const void* wi,
                                  const void* bi, const float* lambda, const float* h0, void* h,
                                  float* hT, const void* hz, void* y, int64_t B, int64_t L,
-                                 int64_t D, IoType io, void* ws, hipStream_t stream) {
+                                 int64_t D, IoType io, void* ws, hipStream_t stream,
+                                 const float* w4, const float* b4) {
     const fv2::Plan pl = fv2::plan(B, L, D, fv2::waves_of(io));
-    fv2::Params P{x, wr, wi, br, bi, lambda, h0, h, hT, hz, y, L, D, B * D, pl.ngroups, pl.nseg,
-                  nullptr, nullptr, nullptr};
+    fv2::Params P{x,  wr,        wi,  br,  bi,  lambda, h0, h, hT, hz, y, w4, b4, L, D, B * D,
+                  pl.ngroups, pl.nseg, nullptr, nullptr, nullptr};
     if (pl.lookback) {
         P.status = (unsigned*)((char*)ws + kStatusOffset);
         P.counters = (unsigned*)((char*)ws + 256);
@@ -679,6 +822,12 @@ hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, 
         if (e != hipSuccess) return e;
     }
     const bool gated = y != nullptr;
+    if (w4 && (!gated || !b4)) return hipErrorInvalidValue;  // conv on load: gated layer only
+    if (w4) {
+        if (io == IoType::kF32) return fv2::launch_mode<float, 128, true, true>(P, pl, stream);
+        if (D == 128) return fv2::launch_mode<bf16, 128, true, true>(P, pl, stream);
+        return fv2::launch_mode<bf16, 256, true, true>(P, pl, stream);
+    }
     if (io == IoType::kF32)
         return gated ? fv2::launch_mode<float, 128, true>(P, pl, stream)
                      : fv2::launch_mode<float, 128, false>(P, pl, stream);

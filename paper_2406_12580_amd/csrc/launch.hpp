@@ -117,10 +117,13 @@ hipError_t launch_fused_forward(const void* x, const void* pack, const void* br,
 bool fused2_forward_applies(int64_t B, int64_t L, int64_t D, IoType io, const void* x,
                             const void* wr, const void* wi);
 size_t fused2_forward_workspace(int64_t B, int64_t L, int64_t D, IoType io);
+// With conv taps (w4 [4][D] and b4 [D], as launch_pack_conv packs them; gated
+// only) x is hx and x' = SiLU(conv(hx)) is formed on load.
 hipError_t launch_fused2_forward(const void* x, const void* wr, const void* br, const void* wi,
                                  const void* bi, const float* lambda, const float* h0, void* h,
                                  float* hT, const void* hz, void* y, int64_t B, int64_t L,
-                                 int64_t D, IoType io, void* ws, hipStream_t stream);
+                                 int64_t D, IoType io, void* ws, hipStream_t stream,
+                                 const float* w4 = nullptr, const float* b4 = nullptr);
 
 // Scan-algorithm variants for the efficiency ablation (zero initial state;
 // x, z, h share the I/O type): a serial scan (one wave per 64 channels walks
