@@ -455,6 +455,37 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const double* __restr
     out[col] = (float)acc;
 }
 
+// Column sums of a short matrix (rows <= kColsumGroups, the split partials of
+// the weight gradients and the LayerNorm parameter gradients) in one launch:
+// the four waves of a workgroup take four consecutive row ranges of the same
+// 64 columns, each summed in row order in double (8 loads in flight), and the
+// four range sums are added in range order.
+__global__ __launch_bounds__(256) void colsum_short_kernel(const float* __restrict__ src,
+                                                           int64_t rows, int64_t cols,
+                                                           float* __restrict__ out) {
+    __shared__ double sh[4][64];
+    const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t per = (rows + 3) / 4;
+    const int64_t r0 = q * per, r1 = r0 + per < rows ? r0 + per : rows;
+    double acc = 0.0;
+    if (c < cols) {
+        int64_t r = r0;
+        for (; r + 8 <= r1; r += 8) {
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = src[(r + k) * cols + c];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) acc += (double)v[k];
+        }
+        for (; r < r1; ++r) acc += (double)src[r * cols + c];
+    }
+    sh[q][lane] = acc;
+    __syncthreads();
+    if (q == 0 && c < cols)
+        out[c] = (float)(((sh[0][lane] + sh[1][lane]) + sh[2][lane]) + sh[3][lane]);
+}
+
 size_t colsum_workspace(int64_t rows, int64_t cols) {
     const int64_t g = rows < kColsumGroups ? (rows > 0 ? rows : 1) : kColsumGroups;
     return (size_t)(g * cols) * sizeof(double);
@@ -464,7 +495,12 @@ hipError_t launch_colsum(const float* src, int64_t rows, int64_t cols, float* ou
                          hipStream_t stream) {
     if (cols == 0) return hipSuccess;
     if (rows == 0) return launch_fill(out, 0.0f, cols, stream);
-    const int64_t groups = rows < kColsumGroups ? rows : kColsumGroups;
+    if (rows <= kColsumGroups) {
+        hipLaunchKernelGGL(colsum_short_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0,
+                           stream, src, rows, cols, out);
+        return hipGetLastError();
+    }
+    const int64_t groups = kColsumGroups;
     const int64_t per = (rows + groups - 1) / groups;
     double* part = (double*)ws;
     hipLaunchKernelGGL(colsum_part_kernel, dim3((unsigned)groups, (unsigned)((cols + 255) / 256)),
