@@ -706,56 +706,130 @@ __device__ __forceinline__ void store_slice32(float (*lds)[KP32], int tid, const
     for (int j = 0; j < NQ; ++j) *(f4*)&lds[(tid >> 4) + 16 * j][4 * (tid & 15)] = r[j];
 }
 
+// JN: 16-column blocks per wave (4: 64 x 64 per wave, 128 x 128 tiles; 2:
+// 64 x 32 per wave, 128 x 64 tiles for outputs at most 64 wide).
+template <int JN = 4>
 __device__ __forceinline__ void mma_slice32(float (*la)[KP32], float (*lb)[KP32],
-                                            f4 (&acc)[4][4], int wm, int wn, int fr, int g) {
+                                            f4 (&acc)[4][JN], int wm, int wn, int fr, int g) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        f4 fa[4], fb[4];
+        f4 fa[4], fb[JN];
 #pragma unroll
         for (int i = 0; i < 4; ++i) fa[i] = *(const f4*)&la[wm * 64 + 16 * i + fr][16 * g + 4 * c];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) fb[j] = *(const f4*)&lb[wn * 64 + 16 * j + fr][16 * g + 4 * c];
+        for (int j = 0; j < JN; ++j)
+            fb[j] = *(const f4*)&lb[wn * 16 * JN + 16 * j + fr][16 * g + 4 * c];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < JN; ++j)
                     acc[i][j] =
                         __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][e], fb[j][e], acc[i][j], 0, 0, 0);
     }
 }
 
+// The B operand of a 128 x 64 tile: rows n0 .. n0 + 63, four quads per thread
+// (quad j: row tid / 16 + 16 j, k = 4 (tid % 16) .. + 3; zeros past N or K).
+struct NarrowB {
+    uint32_t fixed;
+    __device__ NarrowB(const Operand<kF32, true>& op, int64_t n0, int tid)
+        : fixed(op.row_off(n0 + (tid >> 4))) {}
+    __device__ void fetch(const Operand<kF32, true>& op, int64_t k0, int64_t k_end, int tid,
+                          f4 (&r)[NQ / 2]) const {
+        const int64_t k = k0 + 4 * (tid & 15);
+        const uint32_t base = fixed + (k < k_end ? op.col_off(k) : kOOB);
+        const uint32_t step = 16 * op.pitch;
+#pragma unroll
+        for (int j = 0; j < NQ / 2; ++j) r[j] = op.load(base + j * step);
+    }
+};
+
+// Epilogue of a wave's 64 x 32 block (JN = 2): as tile_epilogue, with each
+// lane handed two rows (8 apart) of four columns per 16-row strip; the
+// epilogue's other two row slots point past M.
+__device__ __forceinline__ void strip_rows_narrow(int64_t m0w, int i, int lane, int64_t M,
+                                                  int64_t (&m)[4]) {
+    m[0] = m0w + i * 16 + (lane >> 3);
+    m[1] = m[0] + 8;
+    m[2] = m[3] = M;
+}
+
+template <class Epi>
+__device__ __forceinline__ void tile_epilogue_narrow(const f4 (&acc)[4][2], char* smem,
+                                                     int64_t m0w, int64_t n0w, const Epi& epi,
+                                                     typename Epi::pre_t pre) {
+    const int lane = threadIdx.x & 63;
+    float* buf = (float*)smem + (threadIdx.x >> 6) * 16 * EP;
+    const int64_t n = n0w + 4 * (lane & 7);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                buf[(4 * (lane >> 4) + v) * EP + j * 16 + (lane & 15)] = acc[i][j][v];
+        __syncthreads();
+        int64_t m[4];
+        strip_rows_narrow(m0w, i, lane, epi.M, m);
+        f4 val[4];
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+            val[q] = *(const f4*)&buf[(8 * q + (lane >> 3)) * EP + 4 * (lane & 7)];
+        val[2] = val[3] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (Epi::kStripLoads) {
+            typename Epi::pre_t next{};
+            if (i < 3) {
+                int64_t mn[4];
+                strip_rows_narrow(m0w, i + 1, lane, epi.M, mn);
+                epi.load(mn, n, next);
+            }
+            epi.run(m, n, val, pre);
+            pre = next;
+        } else {
+            epi.run(m, n, val, pre);
+        }
+        __syncthreads();
+    }
+}
+
 // One output tile at (m0, n0): the sum over k in [0, K) of A(m, k) B(n, k),
 // handed to epi.
-template <class Epi>
+template <int JN, class Epi>
 __device__ __forceinline__ void tile32(const Operand<kF32, true>& a, const Operand<kF32, true>& b,
                                        int64_t m0, int64_t n0, int64_t K, const Epi& epi,
                                        char* smem) {
     using Op = Operand<kF32, true>;
+    constexpr int QB = JN == 4 ? NQ : NQ / 2;  // B quads per thread
     float (*la)[KP32] = (float (*)[KP32])smem;
     float (*lb)[KP32] = (float (*)[KP32])(smem + (size_t)BM * KP32 * sizeof(float));
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int wm = wv >> 1, wn = wv & 1, fr = lane & 15, g = lane >> 4;
-    const int64_t m0w = m0 + wm * 64, n0w = n0 + wn * 64;
+    const int64_t m0w = m0 + wm * 64, n0w = n0 + wn * 16 * JN;
     const int64_t nsl = (K + BK - 1) / BK;
     const Stager<Op> sa(a, m0, tid);
-    const Stager<Op> sb(b, n0, tid);
-    f4 ra[NQ], rb[NQ];
-    f4 acc[4][4];
+    using SB = typename std::conditional<JN == 4, Stager<Op>, NarrowB>::type;
+    const SB sb(b, n0, tid);
+    f4 ra[NQ], rb[QB];
+    f4 acc[4][JN];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < JN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     typename Epi::pre_t pre{};
     int64_t mr[4];
-    strip_rows(m0w, 0, lane, mr);
-    const int64_t ne = n0w + 4 * (lane & 15);
+    if constexpr (JN == 4)
+        strip_rows(m0w, 0, lane, mr);
+    else
+        strip_rows_narrow(m0w, 0, lane, epi.M, mr);
+    const int64_t ne = n0w + (JN == 4 ? 4 * (lane & 15) : 4 * (lane & 7));
     sa.fetch(a, 0, K, tid, ra);
     sb.fetch(b, 0, K, tid, rb);
     for (int64_t sl = 0; sl < nsl; ++sl) {
         store_slice32(la, tid, ra);
-        store_slice32(lb, tid, rb);
+#pragma unroll
+        for (int j = 0; j < QB; ++j) *(f4*)&lb[(tid >> 4) + 16 * j][4 * (tid & 15)] = rb[j];
         __syncthreads();
         if (sl + 1 < nsl) {
             sa.fetch(a, (sl + 1) * BK, K, tid, ra);
@@ -765,10 +839,13 @@ __device__ __forceinline__ void tile32(const Operand<kF32, true>& a, const Opera
         }
         // Keep the loads ahead of the MFMAs (see tile()).
         __builtin_amdgcn_sched_barrier(0);
-        mma_slice32(la, lb, acc, wm, wn, fr, g);
+        mma_slice32<JN>(la, lb, acc, wm, wn, fr, g);
         __syncthreads();
     }
-    tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+    if constexpr (JN == 4)
+        tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+    else
+        tile_epilogue_narrow(acc, smem, m0w, n0w, epi, pre);
 }
 
 // Epilogues of the linear layers' products C (M x N, row-major outputs).
@@ -837,17 +914,21 @@ struct LinEpi {
 };
 
 // Y[M][N] (epilogue MODE) of C = A B^T: A[M][K], B[N][K], both row-major.
-template <int MODE>
+// JN = 2 (N <= 64): 128 x 64 tiles, so that no half-empty 128-column tile is
+// multiplied.
+template <int MODE, int JN = 4>
 __global__ __launch_bounds__(256, 2) void linear32_kernel(const float* a, const float* b,
                                                           LinEpi<MODE> epi, int64_t K) {
-    __shared__ __attribute__((aligned(16))) char smem[kLds32 > kEpiBytes ? kLds32 : kEpiBytes];
+    constexpr size_t kLds = (size_t)(BM + 32 * JN) * KP32 * sizeof(float);
+    __shared__ __attribute__((aligned(16))) char smem[kLds > kEpiBytes ? kLds : kEpiBytes];
     const int64_t M = epi.M, N = epi.N;
-    const int64_t ntn = (N + BN - 1) / BN;
+    constexpr int kBNt = 32 * JN;
+    const int64_t ntn = (N + kBNt - 1) / kBNt;
     const int64_t t = xcd_tile(((M + BM - 1) / BM) * ntn);
     if (t < 0) return;
     const Operand<kF32, true> oa{resource(a, (uint32_t)(M * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
     const Operand<kF32, true> ob{resource(b, (uint32_t)(N * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
-    tile32(oa, ob, (t / ntn) * BM, (t % ntn) * BN, K, epi, smem);
+    tile32<JN>(oa, ob, (t / ntn) * BM, (t % ntn) * kBNt, K, epi, smem);
 }
 
 // out[K][N] = in[N][K] (the data gradient's weight operand, once per call).
@@ -1306,12 +1387,27 @@ bool wgrad_fast_ok(std::initializer_list<const void*> ptrs, int64_t M, int64_t N
            (M + fastmm::BM) * (N > K ? N : K) * 4 < kFastLimit;
 }
 
+namespace {
+// Tiles of a linear-layer product with output width N: 128 x 64 when N <= 64.
+int64_t linear_tiles(int64_t M, int64_t N) {
+    const int64_t bn = N <= 64 ? 64 : fastmm::BN;
+    return ((M + fastmm::BM - 1) / fastmm::BM) * ((N + bn - 1) / bn);
+}
+template <int MODE>
+void launch_lin32(const float* a, const float* b, const fastmm::LinEpi<MODE>& e, int64_t K,
+                  hipStream_t stream) {
+    const dim3 grid(fastmm::grid_of(linear_tiles(e.M, e.N))), block(256);
+    if (e.N <= 64)
+        hipLaunchKernelGGL((fastmm::linear32_kernel<MODE, 2>), grid, block, 0, stream, a, b, e, K);
+    else
+        hipLaunchKernelGGL((fastmm::linear32_kernel<MODE, 4>), grid, block, 0, stream, a, b, e, K);
+}
+}  // namespace
+
 hipError_t launch_linear_fwd32(const float* x, const float* w, const float* bias, float* y,
                                float* act, int64_t M, int64_t N, int64_t K, hipStream_t stream) {
-    const int64_t t = ((M + fastmm::BM - 1) / fastmm::BM) * ((N + fastmm::BN - 1) / fastmm::BN);
     const fastmm::LinEpi<fastmm::kLinStore> e{y, bias, act, nullptr, M, N};
-    hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinStore>, dim3(fastmm::grid_of(t)),
-                       dim3(256), 0, stream, x, w, e, K);
+    launch_lin32(x, w, e, K, stream);
     return hipGetLastError();
 }
 
@@ -1323,27 +1419,19 @@ hipError_t launch_linear_dgrad32(const float* dy, const float* w, float* dx, Lin
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     // dX[M][K] = dY[M][N] W^T[K][N]^T: output width K, contraction N.
-    const int64_t t = ((M + fastmm::BM - 1) / fastmm::BM) * ((K + fastmm::BN - 1) / fastmm::BN);
-    const dim3 grid(fastmm::grid_of(t)), block(256);
     switch (mode) {
-        case LinearMode::kStore: {
-            const fastmm::LinEpi<fastmm::kLinStore> e{dx, nullptr, nullptr, nullptr, M, K};
-            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinStore>, grid, block, 0, stream,
-                               dy, wt, e, N);
+        case LinearMode::kStore:
+            launch_lin32(dy, wt, fastmm::LinEpi<fastmm::kLinStore>{dx, nullptr, nullptr, nullptr, M, K},
+                         N, stream);
             break;
-        }
-        case LinearMode::kAccumulate: {
-            const fastmm::LinEpi<fastmm::kLinAcc> e{dx, nullptr, nullptr, nullptr, M, K};
-            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinAcc>, grid, block, 0, stream,
-                               dy, wt, e, N);
+        case LinearMode::kAccumulate:
+            launch_lin32(dy, wt, fastmm::LinEpi<fastmm::kLinAcc>{dx, nullptr, nullptr, nullptr, M, K},
+                         N, stream);
             break;
-        }
-        case LinearMode::kSiluGrad: {
-            const fastmm::LinEpi<fastmm::kLinSiluGrad> e{dx, nullptr, nullptr, aux, M, K};
-            hipLaunchKernelGGL(fastmm::linear32_kernel<fastmm::kLinSiluGrad>, grid, block, 0,
-                               stream, dy, wt, e, N);
+        case LinearMode::kSiluGrad:
+            launch_lin32(dy, wt, fastmm::LinEpi<fastmm::kLinSiluGrad>{dx, nullptr, nullptr, aux, M, K},
+                         N, stream);
             break;
-        }
     }
     return hipGetLastError();
 }
