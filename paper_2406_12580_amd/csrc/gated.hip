@@ -401,7 +401,7 @@ hipError_t gate_backward_t(const void* dy, const void* hz, const void* h, void* 
 // workgroup (b, tile) adds rows [b * R, b * R + R) of up to 256 columns; its
 // 256 threads are J = 256 / tc row lanes of tc columns, lane j adding rows
 // j, j + J, ... in double, and the J lanes are then added in lane order.
-// Stage 2 adds the G workgroup sums of each column in order.
+// Stage 2 adds the G workgroup sums of each column (colsum_short_kernel).
 constexpr int kColsumGroups = 512;
 __global__ __launch_bounds__(256) void colsum_part_kernel(const float* __restrict__ src,
                                                           double* __restrict__ part,
@@ -437,30 +437,13 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const float* __restric
     }
 }
 
-__global__ __launch_bounds__(256) void colsum_final_kernel(const double* __restrict__ part,
-                                                           int64_t groups, int64_t cols,
-                                                           float* __restrict__ out) {
-    const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (col >= cols) return;
-    double acc = 0.0;
-    int64_t r = 0;
-    for (; r + 8 <= groups; r += 8) {  // 8 loads in flight, added in order
-        double v[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] = part[(r + q) * cols + col];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc += v[q];
-    }
-    for (; r < groups; ++r) acc += part[r * cols + col];
-    out[col] = (float)acc;
-}
-
 // Column sums of a short matrix (rows <= kColsumGroups, the split partials of
 // the weight gradients and the LayerNorm parameter gradients) in one launch:
 // the four waves of a workgroup take four consecutive row ranges of the same
 // 64 columns, each summed in row order in double (8 loads in flight), and the
 // four range sums are added in range order.
-__global__ __launch_bounds__(256) void colsum_short_kernel(const float* __restrict__ src,
+template <typename TS>
+__global__ __launch_bounds__(256) void colsum_short_kernel(const TS* __restrict__ src,
                                                            int64_t rows, int64_t cols,
                                                            float* __restrict__ out) {
     __shared__ double sh[4][64];
@@ -472,7 +455,7 @@ __global__ __launch_bounds__(256) void colsum_short_kernel(const float* __restri
     if (c < cols) {
         int64_t r = r0;
         for (; r + 8 <= r1; r += 8) {
-            float v[8];
+            TS v[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) v[k] = src[(r + k) * cols + c];
 #pragma unroll
@@ -496,8 +479,8 @@ hipError_t launch_colsum(const float* src, int64_t rows, int64_t cols, float* ou
     if (cols == 0) return hipSuccess;
     if (rows == 0) return launch_fill(out, 0.0f, cols, stream);
     if (rows <= kColsumGroups) {
-        hipLaunchKernelGGL(colsum_short_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0,
-                           stream, src, rows, cols, out);
+        hipLaunchKernelGGL(colsum_short_kernel<float>, dim3((unsigned)((cols + 63) / 64)),
+                           dim3(256), 0, stream, src, rows, cols, out);
         return hipGetLastError();
     }
     const int64_t groups = kColsumGroups;
@@ -507,8 +490,9 @@ hipError_t launch_colsum(const float* src, int64_t rows, int64_t cols, float* ou
                        dim3(256), 0, stream, src, part, rows, cols, per);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0,
-                       stream, part, groups, cols, out);
+    // Stage 2: the group sums of each column, as a short matrix of doubles.
+    hipLaunchKernelGGL(colsum_short_kernel<double>, dim3((unsigned)((cols + 63) / 64)), dim3(256),
+                       0, stream, part, groups, cols, out);
     return hipGetLastError();
 }
 
