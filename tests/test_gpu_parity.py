@@ -381,10 +381,14 @@ def test_tree_scan_sequence_padding(rb):
 
 
 # ------------------------------------------------------------------ gated recurrent layer core
-# Few channel groups, L > 128 and D % 64 == 0 take the fused kernel (conv on
-# load, gate on store); the others the unfused path.
+# D = 128 (fp32, bf16) and D = 256 (bf16) take the weights-resident fused
+# kernel with the conv on load (look-back mode with few channel groups, chain
+# mode with 256); other D % 64 == 0 shapes the tile kernel, the rest the
+# unfused path.  The D = 128 / 256 cases with L below the conv's 3-row halo,
+# a last tile of one row and K = 3 exercise the staged halo of the conv.
 GATED_CASES = [((2, 300, 64), 4), ((1, 700, 128), 2), ((1, 513, 256), 1), ((8, 50, 64), 4),
-               ((2, 300, 72), 3), ((3, 1, 64), 4), ((256, 70, 128), 4)]
+               ((2, 300, 72), 3), ((3, 1, 64), 4), ((256, 70, 128), 4), ((2, 2, 128), 3),
+               ((1, 65, 256), 4), ((4, 130, 128), 3), ((3, 1, 256), 2)]
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
