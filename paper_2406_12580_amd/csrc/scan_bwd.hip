@@ -197,8 +197,14 @@ __device__ __forceinline__ void local_reverse(const BwdIn<TX, TZ, C, VEC, Off>& 
 }
 
 // Run the chunk backwards from delta (the adjoint right after the chunk) and
-// apply the gate-gradient epilogue to every step before L.
-template <bool FULL, typename TX, typename TZ, int C, int VEC, typename Off, bool KEEP>
+// apply the gate-gradient epilogue to every step before L.  GROUPED: the
+// gradient terms share dLoss/dq = -alpha g_alpha + g_beta i alpha^2 /
+// sqrt(1 - alpha^2) (dLambda adds r dLoss/dq, dz_r = s r (1 - r) dLoss/dq),
+// four vector instructions fewer per element; the look-back kernels take it
+// (256 x 2048 x 128 fp32 backward 362-365 -> 358 us), while the chain kernel
+// keeps the two terms apart (with the grouped form its 2048 x 200 x 64
+// backward measured 154-157 against 148-151 us).
+template <bool FULL, bool GROUPED, typename TX, typename TZ, int C, int VEC, typename Off, bool KEEP>
 __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, VEC, Off>& ln,
                                          const BwdIn<TX, TZ, C, VEC, Off>& in,
                                          const BwdSteps<C, VEC, KEEP>& st,
@@ -214,10 +220,11 @@ __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, V
             delta[k] = fmaf(pj.A, delta[k], pj.H);
             const float r = st.r[j][k], al = st.al[j][k];
             const float i = sigmoid(in.zi[j][k]);
-            const float q = r * cc[k].s;
             const float mm = one_minus_exp_neg(r * cc[k].two_s, al);
             const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
             const float sq = mm * rs;  // sqrt(1 - alpha^2)
+            if constexpr (!GROUPED) {
+            const float q = r * cc[k].s;
             const float g_alpha = delta[k] * in.hp[j][k];
             const float g_beta = delta[k] * in.x[j][k];
             const float g1 = -al * g_alpha;
@@ -226,6 +233,16 @@ __device__ __forceinline__ void emit_bwd(const BwdParams& P, const BwdLane<TX, V
             dxv[k] = delta[k] * sq * i;
             dzrv[k] = fmaf(g1, q, g2 * (q * rs)) * (1.0f - r);
             dziv[k] = g_beta * sq * i * (1.0f - i);
+            } else {
+            const float g_alpha = delta[k] * in.hp[j][k];
+            const float gbi = delta[k] * in.x[j][k] * i;  // dLoss/dbeta * i
+            // dLoss/dq = -alpha g_alpha + g_beta i alpha^2 / sqrt(1 - alpha^2)
+            const float gq = fmaf(gbi * (al * al), rs, -al * g_alpha);
+            if (FULL || t < P.L) dsum[k] = fmaf(gq, r, dsum[k]);
+            dxv[k] = delta[k] * (sq * i);
+            dzrv[k] = gq * (cc[k].s * fmaf(-r, r, r));  // dq/dz_r = s r (1 - r)
+            dziv[k] = gbi * sq * (1.0f - i);
+            }
         }
         if (ln.valid && (FULL || t < P.L)) {
             const Off off = ln.at(t);
@@ -305,7 +322,7 @@ __device__ __forceinline__ void chain_bwd_step(const BwdParams& P, const BwdLane
     }
 #pragma unroll
     for (int k = 0; k < VEC; ++k) cout[k] = delta[k];
-    emit_bwd<FULL>(P, ln, cur, st, cc, tw, delta, dsum);
+    emit_bwd<FULL, false>(P, ln, cur, st, cc, tw, delta, dsum);
     // Carry out of the macro-chunk, towards earlier steps.
 #pragma unroll
     for (int q = W - 1; q >= 0; --q) {
@@ -474,8 +491,8 @@ __global__ __launch_bounds__(W* kWave) void scan_bwd_lookback_kernel(BwdParams P
     float delta[VEC];
 #pragma unroll
     for (int k = 0; k < VEC; ++k) delta[k] = fmaf(pre[k].A, carry_sh[lane][k], pre[k].H);
-    if (full) emit_bwd<true>(P, ln, in, st, cc, tw, delta, dsum);
-    else emit_bwd<false>(P, ln, in, st, cc, tw, delta, dsum);
+    if (full) emit_bwd<true, true>(P, ln, in, st, cc, tw, delta, dsum);
+    else emit_bwd<false, true>(P, ln, in, st, cc, tw, delta, dsum);
     write_partial<W, VEC>(red, dsum, P.partial + s * P.nch + ln.c0, ln.valid, w, lane);
 }
 
@@ -652,19 +669,17 @@ __device__ __forceinline__ void bwd_eps_tile(const BwdParams& P, int64_t r, int6
         const float delta = gv[j] + eps;
         const float rj = rr[j], a = al[j];
         const float i = sigmoid(zi[j]);
-        const float q = rj * cc[0].s;
         const float mm = one_minus_exp_neg(rj * cc[0].two_s, a);
         const float rs = mm > 0.0f ? fast_rsq(mm) : 0.0f;
         const float sq = mm * rs;  // sqrt(1 - alpha^2)
         const float hprev = !full && t == 0 ? h0v[0] : lds_elem<TH>(hs, j * kWave + lane);
         const float g_alpha = delta * hprev;
-        const float g_beta = delta * lds_elem<T>(xs, j * kWave + lane);
-        const float g1 = -a * g_alpha;
-        const float g2 = g_beta * i * a * a;
-        dsum[0] = fmaf(g1, rj, fmaf(g2, rj * rs, dsum[0]));
-        const float dxv[1] = {delta * sq * i};
-        const float dzrv[1] = {fmaf(g1, q, g2 * (q * rs)) * (1.0f - rj)};
-        const float dziv[1] = {g_beta * sq * i * (1.0f - i)};
+        const float gbi = delta * lds_elem<T>(xs, j * kWave + lane) * i;  // dLoss/dbeta * i
+        const float gq = fmaf(gbi * (a * a), rs, -a * g_alpha);       // dLoss/dq
+        dsum[0] = fmaf(gq, rj, dsum[0]);
+        const float dxv[1] = {delta * (sq * i)};
+        const float dzrv[1] = {gq * (cc[0].s * fmaf(-rj, rj, rj))};
+        const float dziv[1] = {gbi * sq * (1.0f - i)};
         eps = a * delta;
         if (ln.valid) {
             const Off off = ln.at(t);
