@@ -35,6 +35,7 @@
 #include "device_common.hpp"
 #include "launch.hpp"
 #include "lookback.hpp"
+#include "mfma_tile.hpp"
 
 namespace recblr {
 namespace fv2 {
@@ -163,12 +164,11 @@ __device__ __forceinline__ void split_tile(const char* raw, char* planes, int ti
         const int r = o / cpr, jb = o % cpr;
         const f4 v0 = *(const f4*)(raw + r * (D * 4) + (((2 * jb) ^ swz32(r)) << 4));
         const f4 v1 = *(const f4*)(raw + r * (D * 4) + (((2 * jb + 1) ^ swz32(r)) << 4));
-        const f8 v = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-        const b8 hi = __builtin_convertvector(v, b8);
-        const b8 lo = __builtin_convertvector(v - __builtin_convertvector(hi, f8), b8);
+        const fastmm::u2v p0 = fastmm::split2(v0[0], v0[1]), p1 = fastmm::split2(v0[2], v0[3]);
+        const fastmm::u2v p2 = fastmm::split2(v1[0], v1[1]), p3 = fastmm::split2(v1[2], v1[3]);
         const int pos = r * (D * 2) + ((jb ^ swz16(r)) << 4);
-        *(b8*)(planes + pos) = hi;
-        *(b8*)(planes + TS * D * 2 + pos) = lo;
+        *(u4v*)(planes + pos) = u4v{p0.x, p1.x, p2.x, p3.x};
+        *(u4v*)(planes + TS * D * 2 + pos) = u4v{p0.y, p1.y, p2.y, p3.y};
     }
 }
 

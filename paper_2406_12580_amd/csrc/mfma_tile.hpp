@@ -58,6 +58,16 @@ __device__ __forceinline__ uint32_t bits16(u2v v, int c) {
     return (c & 1) ? w >> 16 : w & 0xffffu;
 }
 
+// {hi, lo}: hi = bf16(a) and lo = bf16(a - hi), and the same for b, as
+// packed bf16 pairs (round to nearest even).  hi's halves are widened back
+// by a shift and a mask; written as a conversion of the vector, the
+// compiler converts every value a second time on its own to widen it (4
+// instructions per value instead of 3).
+__device__ __forceinline__ u2v split2(float a, float b) {
+    const uint32_t hi = bf16_pair(a, b);
+    return u2v{hi, bf16_pair(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u))};
+}
+
 // Kinds of operand data.
 enum Kind {
     kF32,    // fp32 values, split into hi and lo planes on the way to LDS
@@ -186,10 +196,9 @@ __device__ __forceinline__ void store_slice(__bf16 (*lds)[BM][KP], int tid,
             const int row = (tid >> 4) + (NT / 16) * j, col = lds_col(row, 4 * (tid & 15));
             if constexpr (KIND == kF32) {
                 const f4 v = r[j];
-                const b4 hi = __builtin_convertvector(v, b4);
-                *(b4*)&lds[0][row][col] = hi;
-                *(b4*)&lds[1][row][col] =
-                    __builtin_convertvector(v - __builtin_convertvector(hi, f4), b4);
+                const u2v p = split2(v[0], v[1]), q = split2(v[2], v[3]);
+                *(u2v*)&lds[0][row][col] = u2v{p.x, q.x};
+                *(u2v*)&lds[1][row][col] = u2v{p.y, q.y};
             } else if constexpr (KIND == kPack2) {
                 *(u2v*)&lds[0][row][col] = r[j].p[0];
                 *(u2v*)&lds[1][row][col] = r[j].p[1];
@@ -213,13 +222,15 @@ __device__ __forceinline__ void store_slice(__bf16 (*lds)[BM][KP], int tid,
                     w[j] = bits16(r[2 * j], c) | (bits16(r[2 * j + 1], c) << 16);
                 *(typename PK::bits*)&lds[0][row][col] = *(const typename PK::bits*)w;
             } else {
-                typename PK::fv v;
+                uint32_t hi[NQ / 2], lo[NQ / 2];
 #pragma unroll
-                for (int j = 0; j < NQ; ++j) v[j] = r[j][c];
-                const typename PK::bv hi = __builtin_convertvector(v, typename PK::bv);
-                *(typename PK::bv*)&lds[0][row][col] = hi;
-                *(typename PK::bv*)&lds[1][row][col] = __builtin_convertvector(
-                    v - __builtin_convertvector(hi, typename PK::fv), typename PK::bv);
+                for (int j = 0; j < NQ / 2; ++j) {
+                    const u2v p = split2(r[2 * j][c], r[2 * j + 1][c]);
+                    hi[j] = p.x;
+                    lo[j] = p.y;
+                }
+                *(typename PK::bits*)&lds[0][row][col] = *(const typename PK::bits*)hi;
+                *(typename PK::bits*)&lds[1][row][col] = *(const typename PK::bits*)lo;
             }
         }
     }

@@ -35,16 +35,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kLnRows = 4;  // rows each wave of the LayerNorm forward normalises together
-constexpr int kRowsPerWave = 4 * kLnRows;  // rows of a LayerNorm forward workgroup (4 waves)
 constexpr int64_t kLnBwdRows = 256;  // rows per workgroup of the LayerNorm backward
 constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
 
 // ------------------------------------------------------------------ dropout masks
 // Philox4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
@@ -110,79 +103,106 @@ __global__ __launch_bounds__(kThreads) void dropout_mask_kernel(uint32_t* __rest
     mask[i] = bits;
 }
 
-// v after dropout: v * scale if element e of the site is kept, else 0; the
-// identity when keep is null (no dropout).
-__device__ __forceinline__ float dropped(const uint32_t* __restrict__ keep, int64_t e, float v,
-                                         float scale) {
-    if (!keep) return v;
-    return (keep[e >> 5] >> (e & 31)) & 1u ? v * scale : 0.0f;
+// ------------------------------------------------------------------ LayerNorm
+// Four consecutive features per lane (16-byte accesses): a row of D = 64 NV
+// features spans G = 16 NV lanes and one wave access covers 64 / G rows.
+template <int NV>
+struct LnGeo {
+    static constexpr int D = 64 * NV;
+    static constexpr int G = 16 * NV;     // lanes per row
+    static constexpr int RPA = 64 / G;    // rows per wave access
+};
+
+// Sum over the G lanes of a row (xor butterfly inside aligned groups of G).
+template <int G>
+__device__ __forceinline__ float row_sum(float v) {
+#pragma unroll
+    for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
 }
 
-// ------------------------------------------------------------------ LayerNorm
-// y = (v - mean) / sqrt(var + eps) * g + b over rows of D = 64 * NV features,
-// one wave per row (lane holds features lane + 64 j).  v = drop(a) + r (r may
-// be null: no residual) and, if s is not null, v is stored for the backward.
-// EMB: v is drop(row ids[row] of the embedding a), or drop(0) where the id is
-// the padding id `pad`; an id outside [0, V) gives NaN.  drop: dropout with
-// the keep bits `keep` (null: none) and scale 1 / (1 - p), element index
-// row * D + feature.
+__device__ __forceinline__ float4 ld4(const float* p) { return *(const float4*)p; }
+__device__ __forceinline__ void st4(float* p, float4 v) { *(float4*)p = v; }
+__device__ __forceinline__ float el(const float4& v, int i) {
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+// Elements e .. e + 3 of v after dropout (e a multiple of 4: their keep bits
+// are bits e % 32 .. + 3 of one word): v * scale where kept, else 0; the
+// identity when keep is null (no dropout).
+__device__ __forceinline__ float4 drop4(const uint32_t* __restrict__ keep, int64_t e, float4 v,
+                                        float scale) {
+    if (!keep) return v;
+    const uint32_t k = keep[e >> 5] >> (e & 31);
+    return float4{(k & 1u) ? v.x * scale : 0.0f, (k & 2u) ? v.y * scale : 0.0f,
+                  (k & 4u) ? v.z * scale : 0.0f, (k & 8u) ? v.w * scale : 0.0f};
+}
+
+// y = (v - mean) / sqrt(var + eps) * g + b over rows of D = 64 * NV features.
+// v = drop(a) + r (r may be null: no residual) and, if s is not null, v is
+// stored for the backward (s may be a: in place).  EMB: v is drop(row
+// ids[row] of the embedding a), or drop(0) where the id is the padding id
+// `pad`; an id outside [0, V) gives NaN.  drop: dropout with the keep bits
+// `keep` (null: none) and scale 1 / (1 - p), element index row * D +
+// feature.  Each wave normalises kLnRows accesses of RPA rows side by side
+// (independent reductions in flight together).
 template <int NV, bool EMB>
 __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
-    const float* __restrict__ a, const float* __restrict__ r, const int* __restrict__ ids,
-    const float* __restrict__ g, const float* __restrict__ b, float* __restrict__ s,
-    float* __restrict__ y, float* __restrict__ mu, float* __restrict__ rs, int64_t M, int64_t V,
-    float eps, const uint32_t* __restrict__ keep, float scale, int pad) {
-    constexpr int D = 64 * NV;
+    const float* a, const float* r, const int* __restrict__ ids,
+    const float* __restrict__ g, const float* __restrict__ b, float* s, float* __restrict__ y,
+    float* __restrict__ mu, float* __restrict__ rs, int64_t M, int64_t V, float eps,
+    const uint32_t* __restrict__ keep, float scale, int pad) {
+    using Geo = LnGeo<NV>;
+    constexpr int D = Geo::D, G = Geo::G, RPA = Geo::RPA;
     const int lane = threadIdx.x & (kWave - 1);
-    // kLnRows rows per wave, normalised side by side (independent reductions
-    // in flight together).
-    const int64_t row0 = ((int64_t)blockIdx.x * 4 + wave_id()) * kLnRows;
-    float v[kLnRows][NV], m[kLnRows], rstd[kLnRows];
+    const int sub = lane / G, c = 4 * (lane % G);
+    const int64_t row0 = ((int64_t)blockIdx.x * 4 + wave_id()) * (kLnRows * RPA) + sub;
+    float4 v[kLnRows];
+    float m[kLnRows], rstd[kLnRows];
 #pragma unroll
     for (int q = 0; q < kLnRows; ++q) {
-        const int64_t row = row0 + q < M ? row0 + q : M - 1;  // tail rows recompute row M-1
-        float bad = 0.0f;
-        bool padded = false;
-        const float* src = a + row * D;
+        const int64_t rq = row0 + q * RPA;
+        const int64_t row = rq < M ? rq : M - 1;  // tail rows recompute row M-1
+        const int64_t e = row * D + c;
         if constexpr (EMB) {
             const int64_t id = ids[row];
             const bool ok = id >= 0 && id < V;
-            src = a + (ok ? id : 0) * D;
-            bad = ok ? 0.0f : __builtin_nanf("");
-            padded = pad >= 0 && id == pad;
+            const bool padded = pad >= 0 && id == pad;
+            const float bad = ok ? 0.0f : __builtin_nanf("");
+            float4 t = padded ? float4{0.0f, 0.0f, 0.0f, 0.0f} : ld4(a + (ok ? id : 0) * D + c);
+            t = drop4(keep, e, t, scale);
+            v[q] = float4{t.x + bad, t.y + bad, t.z + bad, t.w + bad};
+        } else {
+            float4 t = drop4(keep, e, ld4(a + e), scale);
+            if (r) {
+                const float4 u = ld4(r + e);
+                t = float4{t.x + u.x, t.y + u.y, t.z + u.z, t.w + u.w};
+            }
+            v[q] = t;
         }
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int c = lane + 64 * j;
-            v[q][j] = dropped(keep, row * D + c, padded ? 0.0f : src[c], scale) + bad;
-            if (!EMB && r) v[q][j] += r[row * D + c];
-        }
     }
 #pragma unroll
-    for (int q = 0; q < kLnRows; ++q) {
-        float sum = 0.0f;
+    for (int q = 0; q < kLnRows; ++q)
+        m[q] = row_sum<G>((v[q].x + v[q].y) + (v[q].z + v[q].w)) * (1.0f / D);
 #pragma unroll
-        for (int j = 0; j < NV; ++j) sum += v[q][j];
-        m[q] = wave_sum(sum) * (1.0f / D);
+    for (int q = 0; q < kLnRows; ++q) {
+        const float dx0 = v[q].x - m[q], dx1 = v[q].y - m[q], dx2 = v[q].z - m[q],
+                    dx3 = v[q].w - m[q];
+        const float var = (dx0 * dx0 + dx1 * dx1) + (dx2 * dx2 + dx3 * dx3);
+        rstd[q] = 1.0f / sqrtf(row_sum<G>(var) * (1.0f / D) + eps);
     }
+    const float4 gc = ld4(g + c), bc = ld4(b + c);
 #pragma unroll
     for (int q = 0; q < kLnRows; ++q) {
-        float var = 0.0f;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) var += (v[q][j] - m[q]) * (v[q][j] - m[q]);
-        rstd[q] = 1.0f / sqrtf(wave_sum(var) * (1.0f / D) + eps);
-    }
-#pragma unroll
-    for (int q = 0; q < kLnRows; ++q) {
-        const int64_t row = row0 + q;
+        const int64_t row = row0 + q * RPA;
         if (row >= M) break;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int c = lane + 64 * j;
-            if (s) s[row * D + c] = v[q][j];
-            y[row * D + c] = (v[q][j] - m[q]) * rstd[q] * g[c] + b[c];
-        }
-        if (lane == 0) {
+        const int64_t e = row * D + c;
+        if (s) st4(s + e, v[q]);
+        st4(y + e, float4{(v[q].x - m[q]) * rstd[q] * gc.x + bc.x,
+                          (v[q].y - m[q]) * rstd[q] * gc.y + bc.y,
+                          (v[q].z - m[q]) * rstd[q] * gc.z + bc.z,
+                          (v[q].w - m[q]) * rstd[q] * gc.w + bc.w});
+        if (c == 0) {
             mu[row] = m[q];
             rs[row] = rstd[q];
         }
@@ -195,9 +215,11 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
 // dx = dv (the residual's gradient) and, if dxm is not null, dxm = dv through
 // the dropout (the sub-layer output's gradient).  EMB: dx = dv through the
 // dropout, 0 at padded positions (the gradient of the looked-up rows).  The
-// workgroup handles rows [blk * kLnBwdRows, + kLnBwdRows), wave w the rows
-// w, w + 4, ...; the sums of dy xh and dy over its rows are added in wave
-// order and written to pg[blk], pb[blk] (summed over workgroups later).
+// workgroup handles rows [blk * kLnBwdRows, + kLnBwdRows) in wave accesses of
+// RPA rows (wave w takes accesses w, w + 4, ...); each lane sums dy xh and dy
+// of its four features over its rows in order, then the RPA row slots of a
+// wave and the four waves are added in a fixed order into pg[blk], pb[blk]
+// (summed over workgroups later).
 template <int NV, bool EMB>
 __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     const float* __restrict__ dy, const float* __restrict__ s, const int* __restrict__ ids,
@@ -205,91 +227,105 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     float* __restrict__ dx, float* __restrict__ pg, float* __restrict__ pb, int64_t M,
     int64_t V, const uint32_t* __restrict__ keep, float scale, int pad,
     float* __restrict__ dxm) {
-    constexpr int D = 64 * NV;
-    __shared__ float red[4][2][D];
+    using Geo = LnGeo<NV>;
+    constexpr int D = Geo::D, G = Geo::G, RPA = Geo::RPA;
+    __shared__ float4 red[4][2][D / 4];
     const int lane = threadIdx.x & (kWave - 1), w = wave_id();
+    const int sub = lane / G, c = 4 * (lane % G);
     const int64_t r0 = (int64_t)blockIdx.x * kLnBwdRows;
     const int64_t r1 = r0 + kLnBwdRows < M ? r0 + kLnBwdRows : M;
-    float ag[NV], ab[NV], gc[NV];
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        ag[j] = ab[j] = 0.0f;
-        gc[j] = g[lane + 64 * j];
-    }
-    // Rows w, w + 4, ... of the block, two at a time so that their loads and
-    // reductions overlap; the gamma / beta sums still add rows in order.
+    float4 ag{0.0f, 0.0f, 0.0f, 0.0f}, ab{0.0f, 0.0f, 0.0f, 0.0f};
+    const float4 gc = ld4(g + c);
     auto padded_row = [&](int64_t row) {
         if constexpr (EMB) return pad >= 0 && ids[row] == pad;
         return false;
     };
-    auto row_grad = [&](int64_t row, float (&xh)[NV], float (&d)[NV], float (&gd)[NV],
-                        float& s1, float& s2) {
-        const float* src = s + row * D;
-        const bool padded = padded_row(row);
+    struct RowIn {
+        float4 xh, d, gd;
+        float s1, s2;
+    };
+    auto row_grad = [&](int64_t row, RowIn& o) {
+        const int64_t e = row * D + c;
+        float4 v;
         if constexpr (EMB) {
             const int64_t id = ids[row];
-            src = s + (id >= 0 && id < V ? id : 0) * D;
+            const bool padded = pad >= 0 && id == pad;
+            v = padded ? float4{0.0f, 0.0f, 0.0f, 0.0f}
+                       : ld4(s + (id >= 0 && id < V ? id : 0) * D + c);
+            v = drop4(keep, e, v, scale);
+        } else {
+            v = ld4(s + e);
         }
         const float m = mu[row], rstd = rs[row];
-        s1 = s2 = 0.0f;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int c = lane + 64 * j;
-            const float v = EMB ? dropped(keep, row * D + c, padded ? 0.0f : src[c], scale)
-                                : src[c];
-            xh[j] = (v - m) * rstd;
-            d[j] = dy[row * D + c];
-            gd[j] = d[j] * gc[j];
-            s1 += gd[j];
-            s2 += gd[j] * xh[j];
-        }
+        o.xh = float4{(v.x - m) * rstd, (v.y - m) * rstd, (v.z - m) * rstd, (v.w - m) * rstd};
+        o.d = ld4(dy + e);
+        o.gd = float4{o.d.x * gc.x, o.d.y * gc.y, o.d.z * gc.z, o.d.w * gc.w};
+        o.s1 = (o.gd.x + o.gd.y) + (o.gd.z + o.gd.w);
+        o.s2 = (o.gd.x * o.xh.x + o.gd.y * o.xh.y) + (o.gd.z * o.xh.z + o.gd.w * o.xh.w);
     };
-    auto row_out = [&](int64_t row, const float (&xh)[NV], const float (&d)[NV],
-                       const float (&gd)[NV], float m1, float m2) {
+    auto row_out = [&](int64_t row, const RowIn& o, float m1, float m2) {
         const float rstd = rs[row];
-        const bool padded = padded_row(row);
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int64_t e = row * D + lane + 64 * j;
-            const float dv = rstd * (gd[j] - m1 - xh[j] * m2);
-            if constexpr (EMB) {
-                dx[e] = padded ? 0.0f : dropped(keep, e, dv, scale);
-            } else {
-                dx[e] = dv;
-                if (dxm) dxm[e] = dropped(keep, e, dv, scale);
-            }
-            ag[j] = fmaf(d[j], xh[j], ag[j]);
-            ab[j] += d[j];
+        const int64_t e = row * D + c;
+        const float4 dv{rstd * (o.gd.x - m1 - o.xh.x * m2), rstd * (o.gd.y - m1 - o.xh.y * m2),
+                        rstd * (o.gd.z - m1 - o.xh.z * m2), rstd * (o.gd.w - m1 - o.xh.w * m2)};
+        if constexpr (EMB) {
+            st4(dx + e, padded_row(row) ? float4{0.0f, 0.0f, 0.0f, 0.0f}
+                                        : drop4(keep, e, dv, scale));
+        } else {
+            st4(dx + e, dv);
+            if (dxm) st4(dxm + e, drop4(keep, e, dv, scale));
         }
+        ag = float4{fmaf(o.d.x, o.xh.x, ag.x), fmaf(o.d.y, o.xh.y, ag.y),
+                    fmaf(o.d.z, o.xh.z, ag.z), fmaf(o.d.w, o.xh.w, ag.w)};
+        ab = float4{ab.x + o.d.x, ab.y + o.d.y, ab.z + o.d.z, ab.w + o.d.w};
     };
-    int64_t row = r0 + w;
-    for (; row + 4 < r1; row += 8) {
-        float xa[NV], da[NV], ga[NV], xb[NV], db[NV], gb[NV], s1a, s2a, s1b, s2b;
-        row_grad(row, xa, da, ga, s1a, s2a);
-        row_grad(row + 4, xb, db, gb, s1b, s2b);
-        const float m1a = wave_sum(s1a) * (1.0f / D), m2a = wave_sum(s2a) * (1.0f / D);
-        const float m1b = wave_sum(s1b) * (1.0f / D), m2b = wave_sum(s2b) * (1.0f / D);
-        row_out(row, xa, da, ga, m1a, m2a);
-        row_out(row + 4, xb, db, gb, m1b, m2b);
+    // Accesses w, w + 4, ... of the block, two at a time so that their loads
+    // and reductions overlap; rows past r1 are skipped (all RPA rows of an
+    // access are in range or not, per lane).
+    int64_t row = r0 + (int64_t)w * RPA + sub;
+    constexpr int64_t kStep = 4 * RPA;
+    for (; row + kStep < r1; row += 2 * kStep) {
+        RowIn ia, ib;
+        row_grad(row, ia);
+        row_grad(row + kStep, ib);
+        const float m1a = row_sum<G>(ia.s1) * (1.0f / D), m2a = row_sum<G>(ia.s2) * (1.0f / D);
+        const float m1b = row_sum<G>(ib.s1) * (1.0f / D), m2b = row_sum<G>(ib.s2) * (1.0f / D);
+        row_out(row, ia, m1a, m2a);
+        row_out(row + kStep, ib, m1b, m2b);
     }
-    if (row < r1) {
-        float xa[NV], da[NV], ga[NV], s1a, s2a;
-        row_grad(row, xa, da, ga, s1a, s2a);
-        row_out(row, xa, da, ga, wave_sum(s1a) * (1.0f / D), wave_sum(s2a) * (1.0f / D));
+    {
+        // The last access: rows before r1 only.  The sums are taken by every
+        // lane of the wave (the shuffles need all of them); out-of-range rows
+        // read row r1 - 1 and store nothing.
+        const bool in = row < r1;
+        RowIn ia;
+        row_grad(in ? row : r1 - 1, ia);
+        const float m1a = row_sum<G>(ia.s1) * (1.0f / D), m2a = row_sum<G>(ia.s2) * (1.0f / D);
+        if (in) row_out(row, ia, m1a, m2a);
     }
+    // The RPA row slots of the wave (lanes G apart), then the four waves.
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        red[w][0][lane + 64 * j] = ag[j];
-        red[w][1][lane + 64 * j] = ab[j];
+    for (int o = G; o < kWave; o <<= 1) {
+        ag = float4{ag.x + __shfl_xor(ag.x, o), ag.y + __shfl_xor(ag.y, o),
+                    ag.z + __shfl_xor(ag.z, o), ag.w + __shfl_xor(ag.w, o)};
+        ab = float4{ab.x + __shfl_xor(ab.x, o), ab.y + __shfl_xor(ab.y, o),
+                    ab.z + __shfl_xor(ab.z, o), ab.w + __shfl_xor(ab.w, o)};
+    }
+    if (sub == 0) {
+        red[w][0][c / 4] = ag;
+        red[w][1][c / 4] = ab;
     }
     __syncthreads();
-    if (w == 0) {
+    if (w == 0 && sub == 0) {
+        float4 tg = red[0][0][c / 4], tb = red[0][1][c / 4];
 #pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int c = lane + 64 * j;
-            pg[blockIdx.x * D + c] = ((red[0][0][c] + red[1][0][c]) + red[2][0][c]) + red[3][0][c];
-            pb[blockIdx.x * D + c] = ((red[0][1][c] + red[1][1][c]) + red[2][1][c]) + red[3][1][c];
+        for (int q = 1; q < 4; ++q) {
+            const float4 ug = red[q][0][c / 4], ub = red[q][1][c / 4];
+            tg = float4{tg.x + ug.x, tg.y + ug.y, tg.z + ug.z, tg.w + ug.w};
+            tb = float4{tb.x + ub.x, tb.y + ub.y, tb.z + ub.z, tb.w + ub.w};
         }
+        st4(pg + blockIdx.x * D + c, tg);
+        st4(pb + blockIdx.x * D + c, tb);
     }
 }
 
@@ -812,7 +848,7 @@ template <int NV>
 bool ln_fwd(Ctx& c, const float* a, const float* r, const int* ids, const float* g,
             const float* b, float* s, float* y, float* mu, float* rs, int64_t M, int64_t V,
             float eps, Drop dr) {
-    const dim3 grid(blocks_for(M, kRowsPerWave));
+    const dim3 grid(blocks_for(M, 4 * kLnRows * LnGeo<NV>::RPA));
     if (ids)
         hipLaunchKernelGGL((ln_fwd_kernel<NV, true>), grid, dim3(kThreads), 0, c.stream, a, r,
                            ids, g, b, s, y, mu, rs, M, V, eps, dr.keep, dr.scale, dr.pad);
