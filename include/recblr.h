@@ -229,13 +229,14 @@ int recblr_bdlru_step(const void* x, const void* W_r, const void* b_r, const voi
                       int64_t B, int64_t D, int io, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+ * Gated recurrent layer core (Algorithm alg:gated_recurrent):
  *   x'_t = SiLU(conv_b + sum_{j<K} conv_w[d][j] hx_{t-j})   causal, depthwise
  *   h    = BD-LRU(x') with z = x' W^T + b                  (as recblr_bdlru_forward)
  *   y_t  = h_t * SiLU(hz_t)
  * The kernel size is not stated in the paper; 1 <= K <= 4, and hx before step
- * 0 counts as zero.  The linear layers around this core (Algorithm lines 1,
- * 2 and 6) are plain GEMMs outside the library.
+ * 0 counts as zero.  The linear layers around this core in the same
+ * algorithm (the input projections to hx and hz, the output projection) are
+ * plain GEMMs outside the library.
  *   hx, hz, y : [B][L][D] io;  h : [B][L][D] io or NULL (the BD-LRU output,
  *   kept for a backward);  conv_w : [D][K] float;  conv_b : [D] float or NULL;
  *   W_r, b_r, W_i, b_i, lambda, h0, hT : as recblr_bdlru_forward.
@@ -256,7 +257,7 @@ int recblr_gated_forward(const void* hx, const void* hz, const float* conv_w,
 
 /*
  * Backward of recblr_gated_forward.  The paper gives no backward pass; this is
- * the exact chain rule through Algorithm alg:gated_recurrent, lines 3 to 5:
+ * the exact chain rule through the core of Algorithm alg:gated_recurrent:
  *   dh    = dy (x) SiLU(hz)                     (dhT adds on the final state)
  *   dhz   = dy (x) h (x) SiLU'(hz)
  *   dx', dW_r, db_r, dW_i, db_i, dlambda, dh0   as recblr_bdlru_backward at x'

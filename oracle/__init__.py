@@ -160,7 +160,7 @@ def step(x, Wr, br, Wi, bi, lam, h_prev):
 
 
 def gated_forward(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0=None):
-    """Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+    """Gated recurrent layer core (Algorithm alg:gated_recurrent):
     x' = SiLU(causal depthwise Conv1d(hx)), h = BD-LRU(x'), y = h * SiLU(hz).
     conv_w is [D][K]. Returns (y, h, hT)."""
     hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam, h0 = map(

@@ -152,7 +152,8 @@ def _softplus(v):
 
 
 def gated_core(hx, hz, conv_w, conv_b, Wr, br, Wi, bi, lam):
-    """Algorithm alg:gated_recurrent, lines 3 to 5, with h_0 = 0 (torch tensors)."""
+    """The core of Algorithm alg:gated_recurrent (causal conv + SiLU, BD-LRU,
+    output gate), with h_0 = 0 (torch tensors)."""
     B, T, C = hx.shape
     K = conv_w.shape[1]
     c = conv_b.expand(B, T, C).clone()

@@ -25,7 +25,7 @@
  *     it is the same number, without the cancellation of 1 - alpha*alpha.
  *   - The backward pass is the exact adjoint of the forward recurrence
  *     (derived here; the paper gives no backward formulas).
- *   - Gated recurrent layer (Algorithm alg:gated_recurrent, lines 3 to 5):
+ *   - Gated recurrent layer core (Algorithm alg:gated_recurrent):
  *     the causal Conv1d is depthwise with K taps and a bias per channel,
  *     c_t[d] = b[d] + sum_{j<K} w[d][j] hx_{t-j}[d] with hx_{t<0} = 0 (the
  *     kernel size is not stated); x' = SiLU(c) feeds both the gate
@@ -261,7 +261,7 @@ void oracle_backward(int64_t B, int64_t L, int64_t D, const double* x, const dou
 }
 
 /*
- * Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5):
+ * Gated recurrent layer core (Algorithm alg:gated_recurrent):
  *   x'_t = SiLU(conv_b + sum_{j<K} conv_w[.][j] * hx_{t-j})   (causal, depthwise)
  *   h    = BD-LRU(x') with z = x' W^T + b                    (section 3.2)
  *   y_t  = h_t * SiLU(hz_t)

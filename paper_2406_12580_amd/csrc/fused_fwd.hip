@@ -3,7 +3,8 @@
 // z_r = W_r x_t + b_r and z_i = W_i x_t + b_i, are formed on the matrix cores
 // right where the BD-LRU scan (eq:linrnn, evaluated with the operator of
 // section 3.3) consumes them, so z never reaches HBM: the kernel reads x and
-// writes h (or y = h * SiLU(hz), Algorithm alg:gated_recurrent line 5).
+// writes h (or y = h * SiLU(hz), the output gate of Algorithm
+// alg:gated_recurrent).
 //
 // Work decomposition.  A channel group is 128 consecutive channels of one
 // batch row; a tile is 64 steps of a group.  A workgroup of 8 waves owns one
@@ -172,8 +173,8 @@ __device__ __forceinline__ void split_tile(const char* raw, char* planes, int ti
     }
 }
 
-// ---- causal conv + SiLU on load (gated layer core, Algorithm alg:gated_recurrent
-// line 3): the tile's hx rows and the three rows before them are staged raw,
+// ---- causal conv + SiLU on load (the gated layer core's input step, Algorithm
+// alg:gated_recurrent): the tile's hx rows and the three rows before them are staged raw,
 // x' = SiLU(b + sum_{j<4} w_j hx_{t-j}) is formed from them into the x tile
 // (the layout stage_tile gives), and the products and the scan read it from
 // there as from a staged x tile.

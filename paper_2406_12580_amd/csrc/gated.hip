@@ -1,5 +1,5 @@
 // Gated recurrent layer core of RecBLR (arXiv 2406.12580, Algorithm
-// alg:gated_recurrent, lines 3 to 5) outside the fused scan: the causal
+// alg:gated_recurrent: conv + SiLU, BD-LRU, output gate) outside the fused scan: the causal
 // depthwise Conv1d + SiLU that forms the BD-LRU input, and the output gate
 // y = h * SiLU(hz).  The scan kernel with the projections fused in applies
 // the gate on the fly; these kernels serve the shapes it does not cover.

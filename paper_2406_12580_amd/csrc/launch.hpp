@@ -180,7 +180,8 @@ bool tree_scan_supported(int64_t L);
 size_t scan_backward_method_workspace(int64_t B, int64_t D);
 hipError_t launch_scan_backward_method(bool tree, const ScanBwdArgs& a, hipStream_t stream);
 
-// Gated recurrent layer core (Algorithm alg:gated_recurrent, lines 3 to 5).
+// Gated recurrent layer core (Algorithm alg:gated_recurrent: the causal conv
+// + SiLU, the BD-LRU and the output gate).
 // Conv taps are packed as [kConvTaps][D] (zero past K) plus a [D] bias.
 constexpr int kConvTaps = 4;
 hipError_t launch_pack_conv(const float* w, const float* b, int K, int64_t D, float* w4,

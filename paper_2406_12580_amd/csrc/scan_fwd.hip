@@ -334,7 +334,7 @@ __global__ __launch_bounds__(W* kWave) void scan_fwd_lookback_kernel(FwdParams P
 // layout, and the scan proceeds as in the look-back kernel.  z never reaches
 // HBM: the kernel reads x and writes h.
 namespace fusedfwd {
-// Gated-layer output (Algorithm alg:gated_recurrent, line 5): with GATED the
+// Gated-layer output (the output gate of Algorithm alg:gated_recurrent): with GATED the
 // kernel stores y = h * SiLU(hz) (and h only where asked for).
 struct GatedArgs {
     const void* hz;  // [B][L][D], I/O type

@@ -481,7 +481,7 @@ def test_golden_small_case_regression():
 
 
 # ------------------------------------------------------------------ gated recurrent layer core
-# Algorithm alg:gated_recurrent, lines 3 to 5: x' = SiLU(Conv1d(hx)), BD-LRU, y = h * SiLU(hz).
+# Algorithm alg:gated_recurrent, its core: x' = SiLU(Conv1d(hx)), BD-LRU, y = h * SiLU(hz).
 
 def _gated_case(B, L, D, K, seed):
     rng = np.random.default_rng(seed)

@@ -1,8 +1,8 @@
-"""Why the gated layer's bf16 backward keeps x' and dh in fp32 (CPU, fp64
-oracle only).
+"""Why the bf16 backward paths keep some intermediates in fp32 (CPU, fp64
+oracle only): the gated layer's x' and dh, and the layer's dz.
 
 The gated layer feeds x' = SiLU(conv(hx)) into the BD-LRU and scales its
-output by SiLU(hz) (Algorithm alg:gated_recurrent, lines 3 to 5); its
+output by SiLU(hz) (Algorithm alg:gated_recurrent); its
 backward therefore runs the BD-LRU adjoint on x' with dh = dy SiLU(hz).
 Rounding either of them to bf16 before that adjoint, even with everything
 else exact, moves the weight gradients past the bf16 tolerance (1e-2,
@@ -77,3 +77,27 @@ def test_direct_one_minus_alpha2_is_inside_the_bf16_bar(a_range):
     got, _ = oracle.linear_scan(alpha.astype(np.float64), u.astype(np.float64))
     err = error_report(got, ref)["floored"]
     assert err < 1e-3, err
+
+
+def test_bf16_dz_would_eat_most_of_the_bar():
+    """The layer backward writes dz_r, dz_i in fp32 for the weight and data
+    gradient products, also with bf16 I/O.  In bf16 they would halve that
+    traffic, but rounding dz alone (everything else exact, the direct term of
+    dx rounded to bf16 as the GPU stores it) moves dW_r or dW_i by more than
+    half of the bf16 bar (1e-2, floored relative) on this shape."""
+    B, L, D = 1, 513, 256
+    f = dg.full_inputs(B, L, D, 4402, io="bf16", a_range=(0.99, 0.9999), bias=True, h0=True,
+                       grad=True, dhT=True)
+    want = oracle.backward(f.x, f.Wr, f.br, f.Wi, f.bi, f.lam, f.dh, f.h0, f.dhT)
+    zr = oracle.project(f.x, f.Wr, f.br)
+    zi = oracle.project(f.x, f.Wi, f.bi)
+    sb = oracle.scan_backward(f.x, zr, zi, f.lam, f.dh, f.h0, f.dhT)
+    x = f.x.astype(np.float64).reshape(-1, D)
+    worst = {}
+    for tag, rz in (("fp32", lambda a: a.astype(np.float32).astype(np.float64)), ("bf16", _bf16)):
+        dzr = rz(sb["dzr"]).reshape(-1, D)
+        dzi = rz(sb["dzi"]).reshape(-1, D)
+        worst[tag] = max(error_report(dzr.T @ x, want["dWr"])["floored"],
+                         error_report(dzi.T @ x, want["dWi"])["floored"])
+    assert worst["fp32"] < 1e-5, worst
+    assert worst["bf16"] > 5e-3, worst
