@@ -63,11 +63,11 @@ ARRAYS = {"scan": (4, 8), "full": (2, 4)}
 TRAFFIC = {
     ("c4", "scan_bwd"): {"bytes": 2186777600, "sha": "0208a2897c4c00c7",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c4", "scan_fwd"): {"bytes": 1074241536, "sha": "5450919d02e895fb",
+    ("c4", "scan_fwd"): {"bytes": 1074241536, "sha": "a62592a42f205fc1",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
     ("c5", "scan_bwd"): {"bytes": 1120493568, "sha": "0208a2897c4c00c7",
                          "sources": ["scan_bwd.hip", "device_common.hpp", "lookback.hpp"]},
-    ("c5", "scan_fwd"): {"bytes": 582594560, "sha": "5450919d02e895fb",
+    ("c5", "scan_fwd"): {"bytes": 582594560, "sha": "a62592a42f205fc1",
                          "sources": ["scan_fwd.hip", "device_common.hpp", "lookback.hpp"]},
 }
 
