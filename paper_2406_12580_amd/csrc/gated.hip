@@ -344,6 +344,207 @@ __global__ __launch_bounds__(256) void conv_bwd_kernel(
     }
 }
 
+// The same conv backward, software-pipelined: a lane's steps t0 .. end + 2
+// run in blocks of kConvBlk, the loads of block j + 1 issued before the
+// stores of block j (vector memory operations complete in issue order, so a
+// load issued after a store is waited for together with it).  Every block
+// issues the same operations: loads through per-row buffer resources at
+// rows clamped to tend - 1 (values past tend taken as zero), stores of dhx
+// at an offset past the resource where they must not land (the chunk's
+// first three steps, steps past end + 2, idle lanes); the compiler's
+// vector-memory wait counts are then exact.  Steps are processed in the
+// order and with the arithmetic of conv_bwd_kernel, so the results are the
+// same bit for bit.  Taken when a batch row of hx spans less than 2 GiB.
+constexpr int kConvBlk = 4;
+constexpr uint32_t kConvOOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t conv_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void conv_bload(__amdgpu_buffer_rsrc_t r, uint32_t off,
+                                           float (&out)[VEC]) {
+    static_assert(VEC == 1 || VEC == 4, "one or four channels per lane");
+    if constexpr (sizeof(T) == 4) {
+        if constexpr (VEC == 4) {
+            typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+            const u4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) out[k] = __uint_as_float(v[k]);
+        } else {
+            out[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+        }
+    } else {
+        if constexpr (VEC == 4) {
+            typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+            const u2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+            out[0] = bf16_lo(v[0]);
+            out[1] = bf16_hi(v[0]);
+            out[2] = bf16_lo(v[1]);
+            out[3] = bf16_hi(v[1]);
+        } else {
+            out[0] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)
+                                     << 16);
+        }
+    }
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void conv_bstore(__amdgpu_buffer_rsrc_t r, uint32_t off,
+                                            const float (&in)[VEC]) {
+    if constexpr (sizeof(T) == 4) {
+        if constexpr (VEC == 4) {
+            typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+            const u4 v = {__float_as_uint(in[0]), __float_as_uint(in[1]), __float_as_uint(in[2]),
+                          __float_as_uint(in[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 0);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(in[0]), r, off, 0, 0);
+        }
+    } else {
+        if constexpr (VEC == 4) {
+            typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+            const u2 v = {bf16_pair(in[0], in[1]), bf16_pair(in[2], in[3])};
+            __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b16((unsigned short)from_f32<bf16>(in[0]).bits, r,
+                                                  off, 0, 0);
+        }
+    }
+}
+
+template <typename T, typename TG, int VEC>
+__global__ __launch_bounds__(256) void conv_bwd_piped_kernel(
+    const T* __restrict__ hx, const TG* __restrict__ dxp, const float* __restrict__ w4,
+    const float* __restrict__ b4, T* __restrict__ dhx, float* __restrict__ partial, int64_t L,
+    int64_t D, int64_t groups) {
+    constexpr int S = kConvBlk;
+    __shared__ float red[4][kConvRowCols][kWave][VEC];
+    const int lane = threadIdx.x & (kWave - 1), w = wave_id();
+    const int64_t b = blockIdx.x / groups, cg = blockIdx.x - b * groups;
+    const int64_t d0 = ((int64_t)blockIdx.y * kWave + lane) * VEC;
+    const bool valid = d0 < D;
+    const int64_t dc0 = valid ? d0 : 0;  // idle lanes shadow channel 0 and store nothing
+    const int64_t t0 = (4 * cg + w) * kConvChunk;
+    const int64_t end = t0 + kConvChunk < L ? t0 + kConvChunk : L;  // may be <= t0
+    const int64_t tend = end + 3 < L ? end + 3 : L;
+    float wt[kConvTaps][VEC], bias[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        bias[k] = b4[dc0 + k];
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) wt[j][k] = w4[j * D + dc0 + k];
+    }
+    const uint32_t row_elems = (uint32_t)(L * D);
+    const __amdgpu_buffer_rsrc_t rx = conv_rsrc(hx + b * L * D, row_elems * (uint32_t)sizeof(T));
+    const __amdgpu_buffer_rsrc_t rg =
+        conv_rsrc(dxp + b * L * D, row_elems * (uint32_t)sizeof(TG));
+    const __amdgpu_buffer_rsrc_t ro = conv_rsrc(dhx + b * L * D, row_elems * (uint32_t)sizeof(T));
+    auto elem = [&](int64_t t) -> uint32_t { return (uint32_t)(t * D + dc0); };
+    float h1[VEC], h2[VEC], h3[VEC];           // hx at t-1, t-2, t-3
+    float e0[VEC], e1[VEC], e2[VEC], e3[VEC];  // dc at t, t-1, t-2, t-3
+    float sw[kConvTaps][VEC], sb[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+        h1[k] = h2[k] = h3[k] = 0.0f;
+        e0[k] = e1[k] = e2[k] = e3[k] = 0.0f;
+        sb[k] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) sw[j][k] = 0.0f;
+    }
+    if (t0 < end) {
+        if (t0 >= 3) conv_bload<T, VEC>(rx, elem(t0 - 3) * (uint32_t)sizeof(T), h3);
+        if (t0 >= 2) conv_bload<T, VEC>(rx, elem(t0 - 2) * (uint32_t)sizeof(T), h2);
+        if (t0 >= 1) conv_bload<T, VEC>(rx, elem(t0 - 1) * (uint32_t)sizeof(T), h1);
+        const int64_t tstop = end + 3;
+        const int nb = (int)((tstop - t0 + S - 1) / S);
+        auto load_blk = [&](int64_t tb, float (&xv)[S][VEC], float (&gv)[S][VEC]) {
+#pragma unroll
+            for (int i = 0; i < S; ++i) {
+                const int64_t t = tb + i < tend ? tb + i : tend - 1;
+                conv_bload<T, VEC>(rx, elem(t) * (uint32_t)sizeof(T), xv[i]);
+                conv_bload<TG, VEC>(rg, elem(t) * (uint32_t)sizeof(TG), gv[i]);
+            }
+        };
+        auto proc_blk = [&](int64_t tb, const float (&xv)[S][VEC], const float (&gv)[S][VEC]) {
+#pragma unroll
+            for (int i = 0; i < S; ++i) {
+                const int64_t t = tb + i;
+                float dcv[VEC], x0[VEC];
+                if (t < tend) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) {
+                        x0[k] = xv[i][k];
+                        float c = bias[k];
+                        c = fmaf(wt[0][k], x0[k], c);
+                        c = fmaf(wt[1][k], h1[k], c);
+                        c = fmaf(wt[2][k], h2[k], c);
+                        c = fmaf(wt[3][k], h3[k], c);
+                        dcv[k] = gv[i][k] * dsilu(c, sigmoid(c));
+                    }
+                    if (t < end) {
+#pragma unroll
+                        for (int k = 0; k < VEC; ++k) {
+                            sb[k] += dcv[k];
+                            sw[0][k] = fmaf(dcv[k], x0[k], sw[0][k]);
+                            sw[1][k] = fmaf(dcv[k], h1[k], sw[1][k]);
+                            sw[2][k] = fmaf(dcv[k], h2[k], sw[2][k]);
+                            sw[3][k] = fmaf(dcv[k], h3[k], sw[3][k]);
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) dcv[k] = x0[k] = 0.0f;
+                }
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    e3[k] = e2[k];
+                    e2[k] = e1[k];
+                    e1[k] = e0[k];
+                    e0[k] = dcv[k];
+                    h3[k] = h2[k];
+                    h2[k] = h1[k];
+                    h1[k] = x0[k];
+                }
+                float o[VEC];
+#pragma unroll
+                for (int k = 0; k < VEC; ++k)
+                    o[k] = fmaf(wt[0][k], e3[k],
+                                fmaf(wt[1][k], e2[k], fmaf(wt[2][k], e1[k], wt[3][k] * e0[k])));
+                const bool keep = valid && t - 3 >= t0 && t < tstop;
+                conv_bstore<T, VEC>(ro, keep ? elem(t - 3) * (uint32_t)sizeof(T) : kConvOOB, o);
+            }
+        };
+        float xa[S][VEC], ga[S][VEC], xb[S][VEC], gb[S][VEC];
+        load_blk(t0, xa, ga);
+        for (int j = 0; j < nb; j += 2) {
+            load_blk(t0 + (int64_t)(j + 1) * S, xb, gb);
+            proc_blk(t0 + (int64_t)j * S, xa, ga);
+            if (j + 1 >= nb) break;
+            load_blk(t0 + (int64_t)(j + 2) * S, xa, ga);
+            proc_blk(t0 + (int64_t)(j + 1) * S, xb, gb);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j) red[w][j][lane][k] = sw[j][k];
+        red[w][kConvTaps][lane][k] = sb[k];
+    }
+    __syncthreads();
+    if (w == 0 && valid) {
+        float* row = partial + (int64_t)blockIdx.x * kConvRowCols * D + dc0;
+#pragma unroll
+        for (int j = 0; j < kConvRowCols; ++j)
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+                row[j * D + k] = red[0][j][lane][k] + red[1][j][lane][k] + red[2][j][lane][k] +
+                                 red[3][j][lane][k];
+    }
+}
+
 // Column sums of partial[rows][cols] in a fixed order, in double: block
 // (nb, cb) adds rows [nb * 64, nb * 64 + 64) of columns [cb * 256, + 256).
 constexpr int kColRows = 64;
@@ -544,8 +745,13 @@ template <typename T, typename TG, int VEC>
 void conv_backward_t(dim3 grid, const void* hx, const void* dxp, const float* w4, const float* b4,
                      void* dhx, float* partial, int64_t L, int64_t D, int64_t groups,
                      hipStream_t stream) {
-    hipLaunchKernelGGL((conv_bwd_kernel<T, TG, VEC>), grid, dim3(256), 0, stream, (const T*)hx,
-                       (const TG*)dxp, w4, b4, (T*)dhx, partial, L, D, groups);
+    // The pipelined kernel addresses a batch row with 32-bit offsets.
+    if (L * D * (int64_t)(sizeof(T) > sizeof(TG) ? sizeof(T) : sizeof(TG)) < ((int64_t)1 << 31))
+        hipLaunchKernelGGL((conv_bwd_piped_kernel<T, TG, VEC>), grid, dim3(256), 0, stream,
+                           (const T*)hx, (const TG*)dxp, w4, b4, (T*)dhx, partial, L, D, groups);
+    else
+        hipLaunchKernelGGL((conv_bwd_kernel<T, TG, VEC>), grid, dim3(256), 0, stream,
+                           (const T*)hx, (const TG*)dxp, w4, b4, (T*)dhx, partial, L, D, groups);
 }
 }  // namespace
 
