@@ -931,6 +931,77 @@ __global__ __launch_bounds__(256, 2) void linear32_kernel(const float* a, const 
     tile32<JN>(oa, ob, (t / ntn) * BM, (t % ntn) * kBNt, K, epi, smem);
 }
 
+// The same products for K <= BK (one slice), in persistent workgroups: the
+// grid is a fixed number of workgroups (a multiple of the column tiles);
+// workgroup w keeps the B slice of column tile w % ntn in LDS for the whole
+// launch and walks row tiles w / ntn, + G / ntn, ..., the next tile's A
+// slice fetched into registers during the current tile's MFMAs and its
+// epilogue, so that a tile's load, products and stores overlap those of its
+// neighbours.  Each tile's arithmetic is that of linear32_kernel (same
+// fragments, same order), so the results are the same bit for bit.
+template <int MODE, int JN = 4>
+__global__ __launch_bounds__(256, 2) void linear32p_kernel(const float* a, const float* b,
+                                                           LinEpi<MODE> epi, int64_t K) {
+    constexpr int kBNt = 32 * JN;
+    constexpr int QB = JN == 4 ? NQ : NQ / 2;  // B quads per thread
+    // A slice (also the epilogue's strips), then the resident B slice.
+    constexpr size_t kA = (size_t)BM * KP32 * sizeof(float);
+    constexpr size_t kAreg = kA > kEpiBytes ? kA : kEpiBytes;
+    __shared__ __attribute__((aligned(16))) char smem[kAreg + (size_t)kBNt * KP32 * sizeof(float)];
+    using Op = Operand<kF32, true>;
+    const int64_t M = epi.M, N = epi.N;
+    const int64_t ntn = (N + kBNt - 1) / kBNt, ntm = (M + BM - 1) / BM;
+    const int64_t cn = blockIdx.x % ntn, stride = gridDim.x / ntn;
+    int64_t tm = blockIdx.x / ntn;
+    if (tm >= ntm) return;
+    float (*la)[KP32] = (float (*)[KP32])smem;
+    float (*lb)[KP32] = (float (*)[KP32])(smem + kAreg);
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1, fr = lane & 15, g = lane >> 4;
+    const Op oa{resource(a, (uint32_t)(M * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
+    const Op ob{resource(b, (uint32_t)(N * K * 4)), (uint32_t)(K * 4), 0, 0, 0};
+    const int64_t n0 = cn * kBNt, n0w = n0 + wn * 16 * JN;
+    const int64_t ne = n0w + (JN == 4 ? 4 * (lane & 15) : 4 * (lane & 7));
+    {
+        using SB = typename std::conditional<JN == 4, Stager<Op>, NarrowB>::type;
+        const SB sb(ob, n0, tid);
+        f4 rb[QB];
+        sb.fetch(ob, 0, K, tid, rb);
+#pragma unroll
+        for (int j = 0; j < QB; ++j) *(f4*)&lb[(tid >> 4) + 16 * j][4 * (tid & 15)] = rb[j];
+    }
+    f4 ra[NQ];
+    Stager<Op>(oa, tm * BM, tid).fetch(oa, 0, K, tid, ra);
+    for (;;) {
+        const int64_t m0 = tm * BM, m0w = m0 + wm * 64;
+        store_slice32(la, tid, ra);
+        __syncthreads();  // this tile's A and (first pass) the B slice are in LDS
+        const int64_t tn = tm + stride;
+        if (tn < ntm) Stager<Op>(oa, tn * BM, tid).fetch(oa, 0, K, tid, ra);
+        typename LinEpi<MODE>::pre_t pre{};
+        int64_t mr[4];
+        if constexpr (JN == 4)
+            strip_rows(m0w, 0, lane, mr);
+        else
+            strip_rows_narrow(m0w, 0, lane, M, mr);
+        epi.load(mr, ne, pre);
+        __builtin_amdgcn_sched_barrier(0);
+        f4 acc[4][JN];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < JN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        mma_slice32<JN>(la, lb, acc, wm, wn, fr, g);
+        __syncthreads();  // la is free for the epilogue's strips
+        if constexpr (JN == 4)
+            tile_epilogue(acc, smem, m0w, n0w, epi, pre);
+        else
+            tile_epilogue_narrow(acc, smem, m0w, n0w, epi, pre);
+        tm = tn;
+        if (tm >= ntm) break;
+    }
+}
+
 // out[K][N] = in[N][K] (the data gradient's weight operand, once per call).
 __global__ __launch_bounds__(256) void transpose_kernel(const float* in, float* out, int64_t N,
                                                         int64_t K) {
@@ -1393,10 +1464,36 @@ int64_t linear_tiles(int64_t M, int64_t N) {
     const int64_t bn = N <= 64 ? 64 : fastmm::BN;
     return ((M + fastmm::BM - 1) / fastmm::BM) * ((N + bn - 1) / bn);
 }
+// Compute units of the current device (256 if the query fails).
+int device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+        cus = 256;
+    return cus;
+}
+
 template <int MODE>
 void launch_lin32(const float* a, const float* b, const fastmm::LinEpi<MODE>& e, int64_t K,
                   hipStream_t stream) {
-    const dim3 grid(fastmm::grid_of(linear_tiles(e.M, e.N))), block(256);
+    const dim3 block(256);
+    const int64_t tiles = linear_tiles(e.M, e.N);
+    if (K <= fastmm::BK) {
+        // Persistent: two workgroups per CU, a multiple of the column tiles.
+        const int64_t ntn = tiles / ((e.M + fastmm::BM - 1) / fastmm::BM);
+        int64_t g = 2 * (int64_t)device_cus();
+        g = g / ntn * ntn;
+        if (g > tiles) g = tiles;
+        if (g < ntn) g = ntn;
+        const dim3 grid((unsigned)g);
+        if (e.N <= 64)
+            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 2>), grid, block, 0, stream, a, b, e, K);
+        else
+            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 4>), grid, block, 0, stream, a, b, e, K);
+        return;
+    }
+    const dim3 grid(fastmm::grid_of(tiles));
     if (e.N <= 64)
         hipLaunchKernelGGL((fastmm::linear32_kernel<MODE, 2>), grid, block, 0, stream, a, b, e, K);
     else
