@@ -931,23 +931,29 @@ __global__ __launch_bounds__(256, 2) void linear32_kernel(const float* a, const 
     tile32<JN>(oa, ob, (t / ntn) * BM, (t % ntn) * kBNt, K, epi, smem);
 }
 
-// The same products for K <= BK (one slice), in persistent workgroups: the
-// grid is a fixed number of workgroups (a multiple of the column tiles);
-// workgroup w keeps the B slice of column tile w % ntn in LDS for the whole
-// launch and walks row tiles w / ntn, + G / ntn, ..., the next tile's A
-// slice fetched into registers during the current tile's MFMAs and its
-// epilogue, so that a tile's load, products and stores overlap those of its
-// neighbours.  Each tile's arithmetic is that of linear32_kernel (same
-// fragments, same order), so the results are the same bit for bit.
-template <int MODE, int JN = 4>
-__global__ __launch_bounds__(256, 2) void linear32p_kernel(const float* a, const float* b,
-                                                           LinEpi<MODE> epi, int64_t K) {
+// The same products for K <= KS * BK, in persistent workgroups: the grid is
+// a fixed number of workgroups (a multiple of the column tiles); workgroup w
+// keeps the KS B slices of column tile w % ntn in LDS for the whole launch
+// and walks row tiles w / ntn, + G / ntn, ..., each A slice fetched into
+// registers during the previous slice's MFMAs (the next tile's first slice
+// during the current tile's last slice and epilogue), so that a tile's
+// loads, products and stores overlap those of its neighbours.  Each tile's
+// arithmetic is that of linear32_kernel (same fragments, same slice order),
+// so the results are the same bit for bit.  Two workgroups per CU while the
+// B slices take at most 128 LDS rows (KS = 1 at 128 columns, KS <= 2 at 64).
+template <int JN, int KS>
+constexpr int lin32p_occupancy() { return KS * 32 * JN <= 128 ? 2 : 1; }
+
+template <int MODE, int JN, int KS>
+__global__ __launch_bounds__(256, (lin32p_occupancy<JN, KS>())) void linear32p_kernel(
+    const float* a, const float* b, LinEpi<MODE> epi, int64_t K) {
     constexpr int kBNt = 32 * JN;
     constexpr int QB = JN == 4 ? NQ : NQ / 2;  // B quads per thread
-    // A slice (also the epilogue's strips), then the resident B slice.
+    // A slice (also the epilogue's strips), then the resident B slices.
     constexpr size_t kA = (size_t)BM * KP32 * sizeof(float);
     constexpr size_t kAreg = kA > kEpiBytes ? kA : kEpiBytes;
-    __shared__ __attribute__((aligned(16))) char smem[kAreg + (size_t)kBNt * KP32 * sizeof(float)];
+    __shared__ __attribute__((aligned(16))) char
+        smem[kAreg + (size_t)KS * kBNt * KP32 * sizeof(float)];
     using Op = Operand<kF32, true>;
     const int64_t M = epi.M, N = epi.N;
     const int64_t ntn = (N + kBNt - 1) / kBNt, ntm = (M + BM - 1) / BM;
@@ -965,34 +971,44 @@ __global__ __launch_bounds__(256, 2) void linear32p_kernel(const float* a, const
     {
         using SB = typename std::conditional<JN == 4, Stager<Op>, NarrowB>::type;
         const SB sb(ob, n0, tid);
-        f4 rb[QB];
-        sb.fetch(ob, 0, K, tid, rb);
 #pragma unroll
-        for (int j = 0; j < QB; ++j) *(f4*)&lb[(tid >> 4) + 16 * j][4 * (tid & 15)] = rb[j];
+        for (int sl = 0; sl < KS; ++sl) {
+            f4 rb[QB];
+            sb.fetch(ob, sl * BK, K, tid, rb);
+#pragma unroll
+            for (int j = 0; j < QB; ++j)
+                *(f4*)&lb[sl * kBNt + (tid >> 4) + 16 * j][4 * (tid & 15)] = rb[j];
+        }
     }
     f4 ra[NQ];
     Stager<Op>(oa, tm * BM, tid).fetch(oa, 0, K, tid, ra);
     for (;;) {
         const int64_t m0 = tm * BM, m0w = m0 + wm * 64;
-        store_slice32(la, tid, ra);
-        __syncthreads();  // this tile's A and (first pass) the B slice are in LDS
         const int64_t tn = tm + stride;
-        if (tn < ntm) Stager<Op>(oa, tn * BM, tid).fetch(oa, 0, K, tid, ra);
         typename LinEpi<MODE>::pre_t pre{};
         int64_t mr[4];
         if constexpr (JN == 4)
             strip_rows(m0w, 0, lane, mr);
         else
             strip_rows_narrow(m0w, 0, lane, M, mr);
-        epi.load(mr, ne, pre);
-        __builtin_amdgcn_sched_barrier(0);
         f4 acc[4][JN];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < JN; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-        mma_slice32<JN>(la, lb, acc, wm, wn, fr, g);
-        __syncthreads();  // la is free for the epilogue's strips
+#pragma unroll
+        for (int sl = 0; sl < KS; ++sl) {
+            store_slice32(la, tid, ra);
+            __syncthreads();  // this slice of A and (first pass) the B slices are in LDS
+            if (sl + 1 < KS)
+                Stager<Op>(oa, m0, tid).fetch(oa, (sl + 1) * BK, K, tid, ra);
+            else if (tn < ntm)
+                Stager<Op>(oa, tn * BM, tid).fetch(oa, 0, K, tid, ra);
+            if (sl + 1 == KS) epi.load(mr, ne, pre);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_slice32<JN>(la, lb + sl * kBNt, acc, wm, wn, fr, g);
+            __syncthreads();  // la is free (for the next slice or the epilogue's strips)
+        }
         if constexpr (JN == 4)
             tile_epilogue(acc, smem, m0w, n0w, epi, pre);
         else
@@ -1479,18 +1495,24 @@ void launch_lin32(const float* a, const float* b, const fastmm::LinEpi<MODE>& e,
                   hipStream_t stream) {
     const dim3 block(256);
     const int64_t tiles = linear_tiles(e.M, e.N);
-    if (K <= fastmm::BK) {
-        // Persistent: two workgroups per CU, a multiple of the column tiles.
+    // Persistent workgroups where the B slices stay in LDS: K <= 64, or
+    // K <= 128 with outputs at most 64 wide.
+    // (Four slices at K = 256, one workgroup per CU for the LDS they take,
+    // measured slower than the tile kernel: 159-162 against 147-155 us.)
+    const int ks = K <= fastmm::BK ? 1 : (K <= 2 * fastmm::BK && e.N <= 64 ? 2 : 0);
+    if (ks > 0) {
         const int64_t ntn = tiles / ((e.M + fastmm::BM - 1) / fastmm::BM);
         int64_t g = 2 * (int64_t)device_cus();
         g = g / ntn * ntn;
         if (g > tiles) g = tiles;
         if (g < ntn) g = ntn;
         const dim3 grid((unsigned)g);
-        if (e.N <= 64)
-            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 2>), grid, block, 0, stream, a, b, e, K);
+        if (e.N <= 64 && ks == 2)
+            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 2, 2>), grid, block, 0, stream, a, b, e, K);
+        else if (e.N <= 64)
+            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 2, 1>), grid, block, 0, stream, a, b, e, K);
         else
-            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 4>), grid, block, 0, stream, a, b, e, K);
+            hipLaunchKernelGGL((fastmm::linear32p_kernel<MODE, 4, 1>), grid, block, 0, stream, a, b, e, K);
         return;
     }
     const dim3 grid(fastmm::grid_of(tiles));
