@@ -1497,8 +1497,10 @@ void launch_lin32(const float* a, const float* b, const fastmm::LinEpi<MODE>& e,
     const int64_t tiles = linear_tiles(e.M, e.N);
     // Persistent workgroups where the B slices stay in LDS: K <= 64, or
     // K <= 128 with outputs at most 64 wide.
-    // (Four slices at K = 256, one workgroup per CU for the LDS they take,
-    // measured slower than the tile kernel: 159-162 against 147-155 us.)
+    // (At K = 256 four slices in LDS need one workgroup per CU, 159-162
+    // against 147-155 us on the tile kernel; the B fragments held in
+    // registers instead, 128 VGPRs per wave, spill and measured 143-163
+    // against 149-157 us.)
     const int ks = K <= fastmm::BK ? 1 : (K <= 2 * fastmm::BK && e.N <= 64 ? 2 : 0);
     if (ks > 0) {
         const int64_t ntn = tiles / ((e.M + fastmm::BM - 1) / fastmm::BM);
