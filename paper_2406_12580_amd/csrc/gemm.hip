@@ -1500,7 +1500,9 @@ void launch_lin32(const float* a, const float* b, const fastmm::LinEpi<MODE>& e,
     // (At K = 256 four slices in LDS need one workgroup per CU, 159-162
     // against 147-155 us on the tile kernel; the B fragments held in
     // registers instead, 128 VGPRs per wave, spill and measured 143-163
-    // against 149-157 us.)
+    // against 149-157 us; one 8-wave workgroup whose two halves share the
+    // resident slices and walk alternate row tiles, 158-179 against
+    // 148-157 us: the halves run in lockstep and do not overlap.)
     const int ks = K <= fastmm::BK ? 1 : (K <= 2 * fastmm::BK && e.N <= 64 ? 2 : 0);
     if (ks > 0) {
         const int64_t ntn = tiles / ((e.M + fastmm::BM - 1) / fastmm::BM);
