@@ -214,13 +214,14 @@ __global__ __launch_bounds__(kThreads) void ln_fwd_kernel(
 // rows by id, the padding id and the keep bits as in the forward).  Non-EMB:
 // dx = dv (the residual's gradient) and, if dxm is not null, dxm = dv through
 // the dropout (the sub-layer output's gradient).  EMB: dx = dv through the
-// dropout, 0 at padded positions (the gradient of the looked-up rows).  The
+// dropout, 0 at padded positions (the gradient of the looked-up rows).
+// DROP: keep bits given (and, non-EMB, dxm with them); without, neither.  The
 // workgroup handles rows [blk * kLnBwdRows, + kLnBwdRows) in wave accesses of
 // RPA rows (wave w takes accesses w, w + 4, ...); each lane sums dy xh and dy
 // of its four features over its rows in order, then the RPA row slots of a
 // wave and the four waves are added in a fixed order into pg[blk], pb[blk]
 // (summed over workgroups later).
-template <int NV, bool EMB>
+template <int NV, bool EMB, bool DROP>
 __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     const float* __restrict__ dy, const float* __restrict__ s, const int* __restrict__ ids,
     const float* __restrict__ mu, const float* __restrict__ rs, const float* __restrict__ g,
@@ -236,58 +237,94 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
     const int64_t r1 = r0 + kLnBwdRows < M ? r0 + kLnBwdRows : M;
     float4 ag{0.0f, 0.0f, 0.0f, 0.0f}, ab{0.0f, 0.0f, 0.0f, 0.0f};
     const float4 gc = ld4(g + c);
-    auto padded_row = [&](int64_t row) {
-        if constexpr (EMB) return pad >= 0 && ids[row] == pad;
-        return false;
+    // A row's inputs (the normalised value's source, dy, the row statistics
+    // and the keep bits of the lane's four elements), all read before the
+    // stores that use them: vector memory operations complete in issue
+    // order, so a read issued after a store is waited for together with it.
+    struct RowRaw {
+        float4 v, d;
+        float m, rstd;
+        uint32_t kw;
+        bool padded;
     };
     struct RowIn {
         float4 xh, d, gd;
-        float s1, s2;
+        float s1, s2, rstd;
+        uint32_t kw;
+        bool padded;
     };
-    auto row_grad = [&](int64_t row, RowIn& o) {
+    auto drop_bits = [&](uint32_t k, float4 v) -> float4 {
+        if constexpr (!DROP) return v;
+        return float4{(k & 1u) ? v.x * scale : 0.0f, (k & 2u) ? v.y * scale : 0.0f,
+                      (k & 4u) ? v.z * scale : 0.0f, (k & 8u) ? v.w * scale : 0.0f};
+    };
+    auto row_load = [&](int64_t row, RowRaw& r) {
         const int64_t e = row * D + c;
-        float4 v;
         if constexpr (EMB) {
             const int64_t id = ids[row];
-            const bool padded = pad >= 0 && id == pad;
-            v = padded ? float4{0.0f, 0.0f, 0.0f, 0.0f}
-                       : ld4(s + (id >= 0 && id < V ? id : 0) * D + c);
-            v = drop4(keep, e, v, scale);
+            r.padded = pad >= 0 && id == pad;
+            r.v = r.padded ? float4{0.0f, 0.0f, 0.0f, 0.0f}
+                           : ld4(s + (id >= 0 && id < V ? id : 0) * D + c);
         } else {
-            v = ld4(s + e);
+            r.padded = false;
+            r.v = ld4(s + e);
         }
-        const float m = mu[row], rstd = rs[row];
+        if constexpr (DROP)
+            r.kw = keep[e >> 5] >> (e & 31);
+        else
+            r.kw = 0xFu;
+        r.m = mu[row];
+        r.rstd = rs[row];
+        r.d = ld4(dy + e);
+    };
+    auto row_grad = [&](const RowRaw& r, RowIn& o) {
+        const float4 v = EMB ? drop_bits(r.kw, r.v) : r.v;
+        const float m = r.m, rstd = r.rstd;
         o.xh = float4{(v.x - m) * rstd, (v.y - m) * rstd, (v.z - m) * rstd, (v.w - m) * rstd};
-        o.d = ld4(dy + e);
+        o.d = r.d;
         o.gd = float4{o.d.x * gc.x, o.d.y * gc.y, o.d.z * gc.z, o.d.w * gc.w};
         o.s1 = (o.gd.x + o.gd.y) + (o.gd.z + o.gd.w);
         o.s2 = (o.gd.x * o.xh.x + o.gd.y * o.xh.y) + (o.gd.z * o.xh.z + o.gd.w * o.xh.w);
+        o.rstd = rstd;
+        o.kw = r.kw;
+        o.padded = r.padded;
     };
     auto row_out = [&](int64_t row, const RowIn& o, float m1, float m2) {
-        const float rstd = rs[row];
+        const float rstd = o.rstd;
         const int64_t e = row * D + c;
         const float4 dv{rstd * (o.gd.x - m1 - o.xh.x * m2), rstd * (o.gd.y - m1 - o.xh.y * m2),
                         rstd * (o.gd.z - m1 - o.xh.z * m2), rstd * (o.gd.w - m1 - o.xh.w * m2)};
         if constexpr (EMB) {
-            st4(dx + e, padded_row(row) ? float4{0.0f, 0.0f, 0.0f, 0.0f}
-                                        : drop4(keep, e, dv, scale));
+            st4(dx + e, o.padded ? float4{0.0f, 0.0f, 0.0f, 0.0f} : drop_bits(o.kw, dv));
         } else {
             st4(dx + e, dv);
-            if (dxm) st4(dxm + e, drop4(keep, e, dv, scale));
+            if constexpr (DROP) st4(dxm + e, drop_bits(o.kw, dv));
         }
         ag = float4{fmaf(o.d.x, o.xh.x, ag.x), fmaf(o.d.y, o.xh.y, ag.y),
                     fmaf(o.d.z, o.xh.z, ag.z), fmaf(o.d.w, o.xh.w, ag.w)};
         ab = float4{ab.x + o.d.x, ab.y + o.d.y, ab.z + o.d.z, ab.w + o.d.w};
     };
     // Accesses w, w + 4, ... of the block, two at a time so that their loads
-    // and reductions overlap; rows past r1 are skipped (all RPA rows of an
-    // access are in range or not, per lane).
+    // and reductions overlap, the next pair's inputs read before this pair's
+    // stores; rows past r1 are skipped (all RPA rows of an access are in
+    // range or not, per lane).
     int64_t row = r0 + (int64_t)w * RPA + sub;
     constexpr int64_t kStep = 4 * RPA;
+    RowRaw xa, xb;
+    if (row + kStep < r1) {
+        row_load(row, xa);
+        row_load(row + kStep, xb);
+    }
     for (; row + kStep < r1; row += 2 * kStep) {
         RowIn ia, ib;
-        row_grad(row, ia);
-        row_grad(row + kStep, ib);
+        row_grad(xa, ia);
+        row_grad(xb, ib);
+        // (rows clamped to r1 - 1 past the block, read but unused: the loop
+        // then issues the same memory operations every pass, so the
+        // compiler's wait counts stay exact)
+        const int64_t nr = row + 2 * kStep;
+        row_load(nr < r1 ? nr : r1 - 1, xa);
+        row_load(nr + kStep < r1 ? nr + kStep : r1 - 1, xb);
         const float m1a = row_sum<G>(ia.s1) * (1.0f / D), m2a = row_sum<G>(ia.s2) * (1.0f / D);
         const float m1b = row_sum<G>(ib.s1) * (1.0f / D), m2b = row_sum<G>(ib.s2) * (1.0f / D);
         row_out(row, ia, m1a, m2a);
@@ -298,8 +335,10 @@ __global__ __launch_bounds__(kThreads) void ln_bwd_kernel(
         // lane of the wave (the shuffles need all of them); out-of-range rows
         // read row r1 - 1 and store nothing.
         const bool in = row < r1;
+        RowRaw xr;
+        row_load(in ? row : r1 - 1, xr);
         RowIn ia;
-        row_grad(in ? row : r1 - 1, ia);
+        row_grad(xr, ia);
         const float m1a = row_sum<G>(ia.s1) * (1.0f / D), m2a = row_sum<G>(ia.s2) * (1.0f / D);
         if (in) row_out(row, ia, m1a, m2a);
     }
@@ -868,14 +907,20 @@ bool ln_bwd(Ctx& c, const float* dy, const float* s, const int* ids, const float
     const int64_t nblk = (M + kLnBwdRows - 1) / kLnBwdRows;
     float* pg = (float*)(c.ws + c.w.lnp);
     float* pb = pg + nblk * D;
+    // The kernel reads the keep bits and writes dxm together (non-EMB).
+    const bool drop = dr.keep != nullptr;
+    if (!ids && drop != (dxm != nullptr)) return false;
+    auto run = [&](auto emb, auto dp) {
+        hipLaunchKernelGGL((ln_bwd_kernel<NV, decltype(emb)::value, decltype(dp)::value>),
+                           dim3((unsigned)nblk), dim3(kThreads), 0, c.stream, dy, s, ids, mu, rs,
+                           g, dx, pg, pb, M, V, dr.keep, dr.scale, dr.pad, dxm);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
     if (ids)
-        hipLaunchKernelGGL((ln_bwd_kernel<NV, true>), dim3((unsigned)nblk), dim3(kThreads), 0,
-                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V, dr.keep, dr.scale,
-                           dr.pad, dxm);
+        drop ? run(T_{}, T_{}) : run(T_{}, F_{});
     else
-        hipLaunchKernelGGL((ln_bwd_kernel<NV, false>), dim3((unsigned)nblk), dim3(kThreads), 0,
-                           c.stream, dy, s, ids, mu, rs, g, dx, pg, pb, M, V, dr.keep, dr.scale,
-                           dr.pad, dxm);
+        drop ? run(F_{}, T_{}) : run(F_{}, F_{});
     if (hipGetLastError() != hipSuccess) return false;
     return launch_colsum(pg, nblk, D, dg, c.ws + c.w.colsum, c.stream) == hipSuccess &&
            launch_colsum(pb, nblk, D, db, c.ws + c.w.colsum, c.stream) == hipSuccess;
