@@ -44,6 +44,11 @@ namespace fv2 {
 constexpr int TS = 64;             // steps per tile
 constexpr int MB = TS / 32;        // 32-step MFMA blocks per tile
 constexpr int kWindow = 8;         // look-back window, tiles
+// Cache policy of the h / y stores: nontemporal (written once and read
+// again only by a later backward; gated forward 291 -> 277 us at
+// 256 x 2048 x 128, 308-314 -> 304 us at 16 x 16384 x 256, the plain
+// layer forward unchanged).
+constexpr int kOutCP = 2;
 // Chain mode from this many channel groups on: one workgroup per group, and
 // at least one workgroup per compute unit (two per unit for 4-wave groups).
 constexpr int64_t chain_groups(int nw) { return 256 * 8 / nw; }
@@ -539,9 +544,9 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
                 const uint32_t off = chunk_offset<T, D>(s_prev * TS, cg, q, tid);
                 if constexpr (GATED) {
                     __builtin_amdgcn_raw_buffer_store_b128(gate_chunk<T>(hv, hz_store[q]), yr, off,
-                                                           0, 0);
+                                                           0, kOutCP);
                 }
-                __builtin_amdgcn_raw_buffer_store_b128(hv, hr, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(hv, hr, off, 0, kOutCP);
             }
         }
         if constexpr (LOOKBACK) {
@@ -720,9 +725,9 @@ __global__ __launch_bounds__(threads<T>(), 2) void fused_fwd_kernel(Params P) {
             const uint32_t off = chunk_offset<T, D>(s_prev * TS, cg, q, tid);
             if constexpr (GATED) {
                 __builtin_amdgcn_raw_buffer_store_b128(gate_chunk<T>(hv, hz_load[q]), yr, off, 0,
-                                                       0);
+                                                       kOutCP);
             }
-            __builtin_amdgcn_raw_buffer_store_b128(hv, hr, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(hv, hr, off, 0, kOutCP);
         }
     }
 }
